@@ -1,0 +1,190 @@
+"""Oracle: top-1 selection, greedy acceptance, commit and KV rollback.
+
+TEST INFRASTRUCTURE ONLY (see ``oracle/__init__``).
+
+The fused step
+--------------
+The paper's serving round uses two forwards: a draft forward over
+``[x0, [M] x B]`` and a causal verify forward over ``[a0, d_1..d_B]``
+(appendix "Self-Speculative Decoding and KV-Cache Update").  The step
+implemented here carries both in one forward of ``n_causal + n_mask`` rows:
+
+* causal rows r = 0..n_causal-1 take ``[x0, d_1, ..., d_{n_causal-1}]`` and
+  row r predicts position ``L + r + 1`` (shifted prediction: the logit at
+  position p-1 gives token p; Method "Joint AR-Diffusion Training", and the
+  appendix's "Direct Block-Diffusion Decoding").  So ``a_j = top1(row j-1)``.
+* mask rows r = n_causal..R-1 take ``[M]`` and their top-1 tokens form the
+  next draft: ``d'_j = top1(row n_causal + j - 1)``, j = 1..W, where W is the
+  draft width (n_causal - 1 in the fused step).  A window without mask rows
+  (plain AR) leaves the draft unchanged.  Which draft to carry after a
+  partial acceptance is not fixed by the paper (its round always redrafts
+  from the true boundary); reusing the mask rows unconditionally is this
+  implementation's reading, and its content is parity unpinned beyond
+  oracle == GPU and the invariants that hold for any draft.
+
+Acceptance (Method "Self-Speculative Decoding"; appendix item Accept): A is
+the length of the longest prefix with ``d_j == a_j``; with n_causal verify
+rows the drafts that can be checked are d_1..d_{n_causal-1}, so
+``0 <= A <= n_causal - 1``.  The step commits ``d_1..d_A`` and ``a_{A+1}``
+(the verifier's own prediction), i.e. 1..n_causal tokens.
+
+Cache update (appendix item Cache update): the causal KV of x0 and the
+accepted drafts is kept, so ``L' = L + A + 1``; every other slot written by
+the window, in particular every mask-row slot, is rolled back.  The new
+boundary is the last committed token (item Next round).  A stop condition
+(EOS or the output budget) truncates the committed run at that token and
+freezes the sequence (item Next round, last sentence).
+
+Top-1 rule: the maximum logit wins; among equal maxima the lowest vocabulary
+index wins; -0.0 and +0.0 are equal.  Non-finite logits are an error.
+
+Pages (a reading: the paper does not describe a paged cache).  Every
+sequence holds exactly ``ceil((L + R) / page_size)`` pages so that the next
+window's slots exist.  After a commit, sequences that need fewer pages push
+their surplus logical pages onto the free stack (sequences in order, each
+from its highest logical page down); then sequences that need more pop pages
+from the top of the stack (sequences in order, logical pages ascending).  If
+the pops cannot be served, or a table would exceed ``max_pages``, nothing is
+committed and the error word records why (1 = pool exhausted,
+2 = max_pages exceeded).
+"""
+from __future__ import annotations
+
+import numpy as np
+
+ERR_POOL_EXHAUSTED = 1
+ERR_MAX_PAGES = 2
+ERR_NONFINITE = 4
+
+
+def top1(row: np.ndarray) -> int:
+    """Index of the largest value, lowest index among ties.
+
+    numpy's argmax returns the first maximal index, and its comparisons treat
+    -0.0 == +0.0.  Values must be finite.
+    """
+    if not np.all(np.isfinite(row)):
+        raise ValueError("non-finite logit")
+    return int(np.argmax(row))
+
+
+def top1_rows(logits: np.ndarray) -> np.ndarray:
+    """top1 over the last axis for every leading index; returns int32."""
+    lead = logits.shape[:-1]
+    flat = logits.reshape(-1, logits.shape[-1])
+    out = np.empty(flat.shape[0], dtype=np.int32)
+    for i in range(flat.shape[0]):
+        out[i] = top1(flat[i])
+    return out.reshape(lead)
+
+
+def accept_length(a: np.ndarray, d: np.ndarray) -> int:
+    """Longest k such that d_j == a_j for every j <= k (1-based j).
+
+    ``a[j-1]`` is a_j and ``d[j-1]`` is d_j; only positions present in d count.
+    """
+    k = 0
+    for j in range(1, d.shape[0] + 1):
+        if d[j - 1] != a[j - 1]:
+            break
+        k = j
+    return k
+
+
+def accept(argmax: np.ndarray, draft: np.ndarray, n_causal: int) -> np.ndarray:
+    """A_s for every sequence.  argmax [S, R] (row r's top-1), draft [S, n_causal-1]."""
+    S = argmax.shape[0]
+    A = np.zeros(S, dtype=np.int32)
+    for s in range(S):
+        a = argmax[s, :n_causal]               # a_1..a_{n_causal}
+        A[s] = accept_length(a, draft[s, :n_causal - 1])
+    return A
+
+
+def committed_run(argmax_row: np.ndarray, draft_row: np.ndarray, A: int) -> list:
+    """The tokens a step commits before any stop rule: d_1..d_A then a_{A+1}."""
+    return [int(draft_row[j - 1]) for j in range(1, A + 1)] + [int(argmax_row[A])]
+
+
+def kv_commit(st, accept_len: np.ndarray, argmax: np.ndarray, n_causal: int, n_mask: int,
+              eos_id: int = -1, max_new: int | None = None, page_size: int = 16) -> int:
+    """Apply one step's commit to ``st`` (a synth.PagedState-like object) in place.
+
+    Returns the error word (0 on success; on error ``st`` is unchanged).
+    """
+    S = st.kv_len.shape[0]
+    R = n_causal + n_mask
+    W = st.draft.shape[1]
+    if n_mask > 0 and n_mask < W:
+        raise ValueError("mask rows must cover the draft width")
+    if max_new is None:
+        max_new = st.out_tokens.shape[1]
+    max_new = min(max_new, st.out_tokens.shape[1])
+
+    new_len = st.kv_len.copy()
+    new_bound = st.boundary.copy()
+    new_draft = st.draft.copy()
+    new_fin = st.finished.copy()
+    runs = [[] for _ in range(S)]
+    for s in range(S):
+        if st.finished[s]:
+            continue
+        run = committed_run(argmax[s], st.draft[s], int(accept_len[s]))
+        kept = []
+        stop = False
+        for tok in run:
+            if st.out_count[s] + len(kept) >= max_new:
+                stop = True
+                break
+            kept.append(tok)
+            if eos_id >= 0 and tok == eos_id:
+                stop = True
+                break
+        if st.out_count[s] + len(kept) >= max_new:
+            stop = True
+        runs[s] = kept
+        new_len[s] = st.kv_len[s] + len(kept)
+        if kept:
+            new_bound[s] = kept[-1]
+        if n_mask > 0:
+            W = st.draft.shape[1]
+            new_draft[s] = argmax[s, n_causal:n_causal + W]
+        new_fin[s] = 1 if stop else 0
+
+    need = np.array([(int(new_len[s]) + R + page_size - 1) // page_size for s in range(S)],
+                    dtype=np.int64)
+    err = 0
+    if np.any(need > st.max_pages):
+        err |= ERR_MAX_PAGES
+    pushes = int(sum(max(int(st.num_pages[s]) - int(need[s]), 0) for s in range(S)))
+    pops = int(sum(max(int(need[s]) - int(st.num_pages[s]), 0) for s in range(S)))
+    if pops > st.free_top + pushes:
+        err |= ERR_POOL_EXHAUSTED
+    if err:
+        return err
+
+    # pushes: sequences in order, surplus logical pages from the highest down
+    top = st.free_top
+    for s in range(S):
+        for i in range(int(st.num_pages[s]) - 1, int(need[s]) - 1, -1):
+            st.free_stack[top] = st.page_table[s, i]
+            st.page_table[s, i] = -1
+            top += 1
+    # pops: sequences in order, missing logical pages ascending
+    for s in range(S):
+        for i in range(int(st.num_pages[s]), int(need[s])):
+            top -= 1
+            st.page_table[s, i] = st.free_stack[top]
+            st.free_stack[top] = -1
+    st.free_top = top
+    st.num_pages[:] = need
+
+    for s in range(S):
+        for tok in runs[s]:
+            st.out_tokens[s, st.out_count[s]] = tok
+            st.out_count[s] += 1
+    st.kv_len[:] = new_len
+    st.boundary[:] = new_bound
+    st.draft[:] = new_draft
+    st.finished[:] = new_fin
+    return 0
