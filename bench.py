@@ -1,0 +1,239 @@
+#!/usr/bin/env python3
+"""Benchmark: committed tokens/s of the fused draft-verify step on one MI355X.
+
+Workload (long-document stress, bf16): 64 sequences with committed KV lengths
+uniform in [4096, 16384], 16 query / 4 KV heads, head_dim 128, block B=32
+(32 causal verify rows + 32 mask rows = 64 window rows per sequence), 16-token
+pages scattered in a shared pool, vocabulary 65536 with logits ~N(0, 4), and
+drafts that equal the verifier's top-1 with probability 0.95.  Inputs are
+seeded synthetic arrays, resident in HBM before timing starts.
+
+One step = restore the pristine integer state (one device copy) ->
+attn_hybrid_block (append window K/V + hybrid-mask attention) ->
+argmax_accept (vocab top-1 + longest accepted prefix) -> kv_commit (commit +
+KV rollback).  This is a single-layer step: the metric is committed tokens/s
+of that step, not of a full model forward.
+
+Prints one JSON line.  `roofline` is for the attention kernel (the dominant
+one), from HIP events recorded on the stream the library launches on;
+`cpu_baseline` times the float64 oracle on a bounded sample of the same
+workload on this host.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+COUNTERS = os.path.join(ROOT, "profiles", "attn_long_document_counters.json")
+ATTN_SOURCES = [os.path.join(ROOT, "paper_2609_26638_amd", "csrc", f)
+                for f in ("attn.hip", "dvs_common.h")]
+
+
+def attn_source_hash() -> str:
+    h = hashlib.sha256()
+    for f in ATTN_SOURCES:
+        h.update(open(f, "rb").read())
+    return h.hexdigest()[:16]
+
+
+def attn_algorithmic_bytes(kv_len, S, R, Hq, Hkv, D, b=2) -> int:
+    """HBM bytes one attention launch must move: the cache once per KV head,
+    the window K/V read and appended, Q read, O written, the page table."""
+    kv = int(sum(int(L) for L in kv_len)) * Hkv * D * 2 * b
+    window = 2 * S * R * Hkv * D * 2 * b
+    qo = 2 * S * R * Hq * D * b
+    pages = int(sum((int(L) + 15) // 16 for L in kv_len)) * 4
+    return kv + window + qo + pages
+
+
+def cpu_baseline(ai, li, n_seq: int):
+    """The oracle, as it stands, on the first n_seq sequences of the workload:
+    full-window attention, top-1 over the vocabulary, acceptance and commit.
+    Returns (committed tokens/s, cores, sample description, seconds)."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+    from oracle import attention as oa
+    from oracle import decode as od
+    from paper_2609_26638_amd import synth
+
+    B = ai.n_causal
+    seqs = list(range(n_seq))
+    samples = [(s, r, h) for s in seqs for r in range(ai.R) for h in range(ai.Hq)]
+    q = synth.bf16_to_f64(ai.q[:n_seq])
+    kn = synth.bf16_to_f64(ai.k_new[:n_seq])
+    vn = synth.bf16_to_f64(ai.v_new[:n_seq])
+    st = ai.state.copy()
+    sub = synth.PagedState(
+        kv_len=st.kv_len[:n_seq].copy(), page_table=st.page_table[:n_seq].copy(),
+        num_pages=st.num_pages[:n_seq].copy(), free_stack=st.free_stack.copy(),
+        free_top=st.free_top, boundary=st.boundary[:n_seq].copy(), draft=st.draft[:n_seq].copy(),
+        out_tokens=np.full((n_seq, 256), -1, np.int32), out_count=np.zeros(n_seq, np.int32),
+        finished=np.zeros(n_seq, np.int32), pool_pages=st.pool_pages, max_pages=st.max_pages)
+    t0 = time.perf_counter()
+    oa.attn_sampled(q, kn, vn, ai.k_pool, ai.v_pool, sub.page_table, sub.kv_len, B, ai.n_mask,
+                    ai.scale, samples, decode=synth.bf16_to_f64)
+    am = od.top1_rows(synth.bf16_to_f64(li.logits[:n_seq]))
+    A = od.accept(am, sub.draft, B)
+    err = od.kv_commit(sub, A, am, B, ai.n_mask)
+    dt = time.perf_counter() - t0
+    assert err == 0
+    tokens = int(sub.out_count.sum())
+    threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    desc = (f"first {n_seq} of {ai.S} sequences (KV {int(sub.kv_len.min())}.."
+            f"{int(ai.state.kv_len[:n_seq].max())}), all {ai.R} rows x {ai.Hq} heads, "
+            f"{tokens} committed tokens, {dt:.1f} s")
+    return tokens / dt, threads, desc, dt
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=30)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--chunk-keys", type=int, default=0, help="attention key chunk (0 = auto)")
+    ap.add_argument("--cpu-seqs", type=int, default=16, help="oracle sample size (sequences)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(json.dumps({"error": "this benchmark runs on exactly one GPU: the draft-verify "
+                                   "step shards by sequence with no exchange, so a multi-GPU "
+                                   "figure is the one-GPU figure times N and is not measured",
+                          "n_gpus": args.gpus}))
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    from paper_2609_26638_amd import dvs, synth
+
+    if not torch.cuda.is_available():
+        print(json.dumps({"error": "no GPU visible"}))
+        sys.exit(1)
+    dvs.lib()   # fail loudly if the HIP library is missing
+
+    t_gen = time.perf_counter()
+    ai, li = synth.long_document_inputs()
+    t_gen = time.perf_counter() - t_gen
+    S, R, B, Hq, Hkv, D = ai.S, ai.R, ai.n_causal, ai.Hq, ai.Hkv, ai.D
+    V = li.logits.shape[-1]
+
+    def dev(a):
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).cuda()
+
+    q, kn, vn = dev(ai.q), dev(ai.k_new), dev(ai.v_new)
+    kp, vp = dev(ai.k_pool), dev(ai.v_pool)
+    logits = dev(li.logits)
+    host_state = ai.state.copy()
+    host_state.out_tokens = np.full((S, 256), -1, np.int32)
+    pristine = dvs.DeviceState(host_state)
+    st = dvs.DeviceState(host_state)
+    out = torch.empty_like(q)
+    am = torch.empty((S, R), dtype=torch.int32, device="cuda")
+    acc = torch.empty((S,), dtype=torch.int32, device="cuda")
+    ws = dvs.Workspace(dvs.attn_workspace_bytes(S, B, B, Hq, Hkv, D, host_state.max_pages,
+                                                args.chunk_keys))
+    torch.cuda.synchronize()
+
+    stages = ("restore", "attn", "argmax", "commit")
+
+    def step(ev=None):
+        def rec(k, i):
+            if ev is not None:
+                ev[k][i].record()
+        rec("restore", 0)
+        st.copy_from(pristine)
+        rec("restore", 1); rec("attn", 0)
+        dvs.attn_hybrid_block(q, kn, vn, kp, vp, st.page_table, st.kv_len, B, B, ai.scale,
+                              out=out, err=st.err, workspace=ws, chunk_keys=args.chunk_keys)
+        rec("attn", 1); rec("argmax", 0)
+        dvs.argmax_accept(logits, B, st.draft, argmax_out=am, accept_len=acc, err=st.err)
+        rec("argmax", 1); rec("commit", 0)
+        dvs.kv_commit(st, acc, am, B, B)
+        rec("commit", 1)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    err = int(st.err.item())
+    if err:
+        print(json.dumps({"error": f"device error word {err}"}))
+        sys.exit(1)
+    tokens_per_step = int((st.out_count - pristine.out_count).sum().item())
+    accept_mean = float(acc.float().mean().item())
+
+    # timed region: exactly K steps; per-step, per-stage HIP events on the
+    # stream the library launches on (torch's current stream), read afterwards
+    evs = [{k: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+            for k in stages} for _ in range(args.steps)]
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0.record()
+    for i in range(args.steps):
+        step(evs[i])
+    t1.record()
+    torch.cuda.synchronize()
+    ms_nosync = t0.elapsed_time(t1) / args.steps
+    stage_ms = {k: sum(e[k][0].elapsed_time(e[k][1]) for e in evs) / args.steps for k in stages}
+    if int(st.err.item()):
+        print(json.dumps({"error": f"device error word {int(st.err.item())}"}))
+        sys.exit(1)
+
+    value = tokens_per_step / (ms_nosync / 1e3)
+    attn_bytes = attn_algorithmic_bytes(ai.state.kv_len, S, R, Hq, Hkv, D)
+    attn_gbs = attn_bytes / (stage_ms["attn"] / 1e3) / 1e9
+    traffic = None
+    if os.path.exists(COUNTERS):
+        c = json.load(open(COUNTERS))
+        if c.get("src_hash") == attn_source_hash():
+            traffic = c.get("bytes_per_launch")
+
+    line = {
+        "metric": "committed tokens/sec per GPU for draft-verify step; KV-attn HBM GB/s vs peak",
+        "value": round(value, 1),
+        "unit": "committed tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_nosync, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded; KV/Q ~N(0,1), logits ~N(0,4), drafts match top-1 w.p. 0.95)",
+        "config": {
+            "workload": "long-document stress: 64 sequences, KV U[4096,16384], 16q/4kv heads, "
+                        "head_dim 128, B=32 (64 window rows), 16-token scattered pages, "
+                        "vocab 65536; single-layer step",
+            "sequences": S, "block": B, "window_rows": R, "vocab": V,
+            "kv_tokens": int(ai.state.kv_len.sum()), "chunk_keys": args.chunk_keys,
+        },
+        "roofline": {
+            "bound": "hbm", "achieved": round(attn_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": round(attn_gbs / HBM_PEAK_GBS, 4), "traffic": traffic,
+            "kernel": "attn_bf16_kernel<128,4,2>", "algorithmic_bytes": attn_bytes,
+            "avg_ms": round(stage_ms["attn"], 4),
+        },
+        "breakdown_ms": {k: round(v, 4) for k, v in stage_ms.items()},
+        "tokens_per_step": tokens_per_step,
+        "accept_mean": round(accept_mean, 3),
+        "input_gen_s": round(t_gen, 1),
+    }
+    if not args.no_cpu_baseline:
+        rate, cores, desc, _ = cpu_baseline(ai, li, args.cpu_seqs)
+        line["cpu_baseline"] = {"value": round(rate, 2), "unit": "committed tokens/s",
+                                "cores": cores, "kind": "oracle", "sample": desc}
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

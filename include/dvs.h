@@ -1,0 +1,178 @@
+/*
+ * dvs.h - C ABI of the self-speculative draft-verify step for MI355X (gfx950).
+ *
+ * One step of self-speculative decoding (method section "Self-Speculative
+ * Decoding" and the appendix "Self-Speculative Decoding and KV-Cache
+ * Update") carried out in a single forward of R = n_causal + n_mask window
+ * rows per sequence:
+ *
+ *   causal rows  r = 0..n_causal-1 : inputs [x0, d_1..d_{n_causal-1}],
+ *                                     token-level causal attention (verify);
+ *   mask rows    r = n_causal..R-1 : the mask token [M], attending to the
+ *                                     whole cache, every causal row and,
+ *                                     bidirectionally, the whole mask block
+ *                                     (block diffusion draft; Preliminaries
+ *                                     "Block Diffusion").
+ *
+ * The hot path is attn_hybrid_block -> argmax_accept -> kv_commit;
+ * draft_verify_step runs a whole decoder forward plus those stages.
+ *
+ * Conventions for every entry point
+ *   - All array arguments are DEVICE pointers owned by the caller.  The
+ *     library never allocates or frees device memory in these calls; scratch
+ *     space is passed in as `workspace` and sized by the *_workspace_bytes
+ *     queries.  Arrays are dense, row-major, with the shapes given below.
+ *   - `stream` is a hipStream_t (NULL = the null stream).  Every call only
+ *     enqueues work on it and returns without synchronising.
+ *   - Return value: DVS_OK, or a negative DVS_E* code when the host-side
+ *     argument check fails (then nothing is launched) or a launch fails.
+ *     dvs_last_error() gives a message for the calling thread.
+ *   - Conditions that only the device can see (bad page ids, pool
+ *     exhaustion, non-finite logits, ...) OR a DVS_ERR_* bit into the
+ *     caller's int32 `err_word` (device memory, never cleared by the
+ *     library); the affected sequences are left unmodified.
+ *   - Page size is fixed at 16 tokens.  KV pools are laid out
+ *     [num_pool_pages, Hkv, 16, D]; logical position p of sequence s lives in
+ *     page page_table[s * max_pages + p / 16], slot p % 16.
+ *   - dtype: DVS_F32 (float) or DVS_BF16 (bfloat16 storage, fp32 accumulate).
+ */
+#ifndef DVS_H
+#define DVS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define DVS_OK 0
+#define DVS_EINVAL (-1)        /* bad pointer, shape or parameter          */
+#define DVS_EUNSUPPORTED (-2)  /* valid but not implemented (D, dtype, ...) */
+#define DVS_EHIP (-3)          /* a HIP launch or query failed             */
+#define DVS_EWORKSPACE (-4)    /* workspace missing or too small           */
+
+#define DVS_F32 0
+#define DVS_BF16 1
+
+#define DVS_ERR_POOL_EXHAUSTED 1  /* commit needed more free pages than exist */
+#define DVS_ERR_MAX_PAGES 2       /* a sequence would exceed max_pages        */
+#define DVS_ERR_NONFINITE 4       /* a logit was NaN or infinite              */
+#define DVS_ERR_BAD_PAGE 8        /* a page id outside [0, num_pool_pages)    */
+
+#define DVS_PAGE_SIZE 16
+
+int dvs_version(void);
+const char* dvs_last_error(void);
+
+/* ------------------------------------------------------------------------
+ * attn_hybrid_block
+ *
+ * Appends the window's K/V to the cache, then computes block-causal (hybrid)
+ * masked softmax attention for every window row (Preliminaries "Block
+ * Diffusion": causal across blocks, bidirectional within the block; Method
+ * "Joint AR-Diffusion Training": a corrupted block sees the preceding clean
+ * blocks and itself; appendix items Draft forward / Verify forward).
+ *
+ * For sequence s with committed length L = kv_len[s], window row r sits at
+ * position L + r and sees key position k iff
+ *     k <= L + r            for r <  n_causal   (token-level causal),
+ *     k <= L + R - 1        for r >= n_causal   (cache + whole window).
+ * out[s,r,h,:] = sum_k softmax_k(softmax_scale * <q[s,r,h], K_k>) V_k over the
+ * visible keys, with query head h reading KV head h / (Hq / Hkv).
+ *
+ *   q       [S, R, Hq, D]     window queries (after any position encoding)
+ *   k_new   [S, R, Hkv, D]    window keys, written to positions [L, L+R)
+ *   v_new   [S, R, Hkv, D]    window values, written likewise
+ *   k_pool, v_pool [num_pool_pages, Hkv, 16, D]  paged cache (updated)
+ *   page_table [S, max_pages] int32, kv_len [S] int32 (read only)
+ *   out     [S, R, Hq, D]     attention output, same dtype as q
+ *   chunk_keys   key-range split per workgroup (multiple of 64; 0 = auto).
+ *                Chunks start at absolute positions that are multiples of it,
+ *                so a row's arithmetic does not depend on the other rows.
+ *   err_word     int32 device word (may be NULL): DVS_ERR_MAX_PAGES if
+ *                L + R > max_pages * 16, DVS_ERR_BAD_PAGE for a page id
+ *                outside the pool; such sequences are skipped.
+ *   workspace    >= dvs_attn_workspace_bytes(...) bytes of device memory.
+ *                Its first 4 * S * Hkv * ceil(R*Hq/Hkv / 256) bytes are
+ *                counters that must be zero before the first call (e.g.
+ *                cleared once at allocation); every call leaves them zero.
+ *                Calls that share a workspace must not overlap in time.
+ * Requirements: Hq % Hkv == 0, D in {64, 96, 128}, R >= 1, S >= 1, all
+ * pointers non-NULL (except err_word), softmax_scale > 0.
+ * ---------------------------------------------------------------------- */
+size_t dvs_attn_workspace_bytes(int32_t S, int32_t n_causal, int32_t n_mask, int32_t Hq,
+                                int32_t Hkv, int32_t D, int32_t max_pages, int32_t chunk_keys,
+                                int32_t dtype);
+
+int attn_hybrid_block(const void* q, const void* k_new, const void* v_new, void* k_pool,
+                      void* v_pool, const int32_t* page_table, const int32_t* kv_len,
+                      int32_t S, int32_t n_causal, int32_t n_mask, int32_t Hq, int32_t Hkv,
+                      int32_t D, int32_t max_pages, int32_t num_pool_pages,
+                      float softmax_scale, int32_t dtype, int32_t chunk_keys, void* out,
+                      int32_t* err_word, void* workspace, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * argmax_accept
+ *
+ * Top-1 over the vocabulary for every window row, then greedy acceptance
+ * (method "Self-Speculative Decoding"; appendix item Accept):
+ *   argmax_out[s, r] = index of the largest logits[s, r, :]; among equal
+ *                      maxima the lowest index; -0.0 equals +0.0;
+ *   a_j = argmax_out[s, j-1]  (row j-1 predicts the token after it);
+ *   accept_len[s] = A = largest k <= n_causal-1 with draft[s, j-1] == a_j
+ *                   for every j <= k.
+ *
+ *   logits   [S, R, V]  DVS_F32 or DVS_BF16
+ *   draft    [S, draft_width] int32; draft_width >= n_causal - 1
+ *   argmax_out [S, R] int32, accept_len [S] int32 (written)
+ *   err_word  DVS_ERR_NONFINITE if any logit is NaN/Inf (the argmax of such
+ *             a row is still written, by bit-pattern order).  May be NULL.
+ * Requirements: 1 <= n_causal <= R, V >= 1.
+ * ---------------------------------------------------------------------- */
+int argmax_accept(const void* logits, int32_t dtype, int32_t S, int32_t R, int32_t V,
+                  int32_t n_causal, const int32_t* draft, int32_t draft_width,
+                  int32_t* argmax_out, int32_t* accept_len, int32_t* err_word, void* stream);
+
+/* ------------------------------------------------------------------------
+ * kv_commit
+ *
+ * Commit and KV rollback for one step (appendix items Accept, Cache update,
+ * Next round).  For every sequence s with finished[s] == 0:
+ *   run      = d_1..d_A, a_{A+1}   (A = accept_len[s], a_j = argmax[s, j-1]);
+ *   kept     = run truncated after the first eos_id (inclusive; eos_id < 0 =
+ *              none) and at max_new total output tokens; k = |kept| >= 1;
+ *   out_tokens[s, out_count[s] ...] += kept;  out_count[s] += k;
+ *   kv_len[s] += k  (KV of x0 and the accepted drafts is kept; every other
+ *                    window slot, including all mask-row slots, is dropped);
+ *   boundary[s] = last kept token;
+ *   draft[s, j-1] = argmax[s, n_causal + j - 1], j = 1..draft_width, when
+ *                   n_mask > 0 (requires n_mask >= draft_width);
+ *   finished[s] = 1 when EOS was kept or max_new was reached.
+ * Finished sequences are left unchanged.  Afterwards every sequence holds
+ * exactly ceil((kv_len + R) / 16) pages: surplus pages are pushed onto the
+ * free stack (sequences in order, highest logical page first), then missing
+ * pages are popped from its top (sequences in order, logical pages
+ * ascending); freed table entries become -1.  If the pops exceed the free
+ * pages, or a table would exceed max_pages, NOTHING is changed and
+ * DVS_ERR_POOL_EXHAUSTED / DVS_ERR_MAX_PAGES is ORed into err_word.
+ *
+ *   accept_len [S], argmax [S, R] (read)
+ *   kv_len [S], page_table [S, max_pages], num_pages [S],
+ *   free_stack [num_pool_pages], free_top [1], boundary [S],
+ *   draft [S, draft_width], out_tokens [S, max_new], out_count [S],
+ *   finished [S]  (all int32, read and written)
+ * Requirements: 1 <= S <= 1024, 1 <= n_causal, 0 <= n_mask.
+ * ---------------------------------------------------------------------- */
+int kv_commit(int32_t S, int32_t n_causal, int32_t n_mask, const int32_t* accept_len,
+              const int32_t* argmax, int32_t* kv_len, int32_t* page_table, int32_t* num_pages,
+              int32_t max_pages, int32_t* free_stack, int32_t* free_top, int32_t num_pool_pages,
+              int32_t* boundary, int32_t* draft, int32_t draft_width, int32_t* out_tokens,
+              int32_t* out_count, int32_t max_new, int32_t eos_id, int32_t* finished,
+              int32_t* err_word, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DVS_H */

@@ -41,25 +41,36 @@ def visible_hi(L: int, n_causal: int, n_mask: int) -> np.ndarray:
     return hi
 
 
-def gather_cache(pool: np.ndarray, page_row: np.ndarray, L: int, page_size: int) -> np.ndarray:
+def gather_cache(pool: np.ndarray, page_row: np.ndarray, L: int, page_size: int,
+                 slot_last: bool = False, decode=None) -> np.ndarray:
     """Dense [L, Hkv, D] view of a sequence's first L cached positions.
 
     Logical position p lives in physical page ``page_row[p // page_size]`` at
-    slot ``p % page_size``; the pool is laid out [pages, Hkv, page_size, D].
+    slot ``p % page_size``.  K pools are laid out [pages, Hkv, page_size, D];
+    V pools (``slot_last``) are laid out [pages, Hkv, D, page_size].
+    ``decode`` (optional) maps stored elements to float64, e.g. bf16 bit
+    patterns, so a large pool need not be expanded as a whole.
     """
-    Hkv, D = pool.shape[1], pool.shape[3]
+    Hkv = pool.shape[1]
+    D = pool.shape[2] if slot_last else pool.shape[3]
     out = np.empty((L, Hkv, D), dtype=np.float64)
     for p in range(L):
-        out[p] = pool[page_row[p // page_size], :, p % page_size, :]
+        page, slot = page_row[p // page_size], p % page_size
+        v = pool[page, :, :, slot] if slot_last else pool[page, :, slot, :]
+        out[p] = v if decode is None else decode(v)
     return out
 
 
 def append_block(pool: np.ndarray, page_row: np.ndarray, L: int, block: np.ndarray,
-                 page_size: int) -> None:
+                 page_size: int, slot_last: bool = False) -> None:
     """Write the window's R rows of K (or V), [R, Hkv, D], at positions [L, L+R)."""
     for r in range(block.shape[0]):
         p = L + r
-        pool[page_row[p // page_size], :, p % page_size, :] = block[r]
+        page, slot = page_row[p // page_size], p % page_size
+        if slot_last:
+            pool[page, :, :, slot] = block[r]
+        else:
+            pool[page, :, slot, :] = block[r]
 
 
 def attend_rows(q: np.ndarray, keys: np.ndarray, vals: np.ndarray, hi: np.ndarray,
@@ -93,7 +104,8 @@ def attn_hybrid_block(q, k_new, v_new, k_pool, v_pool, page_table, kv_len,
     """Append the window's K/V to the pools, then attend with the hybrid mask.
 
     All float inputs are float64 arrays: q [S,R,Hq,D], k_new/v_new [S,R,Hkv,D],
-    pools [P,Hkv,page_size,D] (modified in place by the append).
+    k_pool [P,Hkv,page_size,D], v_pool [P,Hkv,D,page_size] (both modified in
+    place by the append).
     Returns out [S,R,Hq,D] (rows of sequences not in ``seqs`` are left zero).
     """
     S, R = q.shape[0], q.shape[1]
@@ -102,19 +114,21 @@ def attn_hybrid_block(q, k_new, v_new, k_pool, v_pool, page_table, kv_len,
     for s in (range(S) if seqs is None else seqs):
         L = int(kv_len[s])
         append_block(k_pool, page_table[s], L, k_new[s], page_size)
-        append_block(v_pool, page_table[s], L, v_new[s], page_size)
+        append_block(v_pool, page_table[s], L, v_new[s], page_size, slot_last=True)
         keys = gather_cache(k_pool, page_table[s], L + R, page_size)
-        vals = gather_cache(v_pool, page_table[s], L + R, page_size)
+        vals = gather_cache(v_pool, page_table[s], L + R, page_size, slot_last=True)
         out[s] = attend_rows(q[s], keys, vals, visible_hi(L, n_causal, n_mask), scale)
     return out
 
 
 def attn_sampled(q, k_new, v_new, k_pool, v_pool, page_table, kv_len, n_causal: int,
-                 n_mask: int, scale: float, samples, page_size: int = 16):
+                 n_mask: int, scale: float, samples, page_size: int = 16, decode=None):
     """Outputs for selected (s, r, h) triples, without touching the pools.
 
     Keys at [L_s, L_s + R) are taken from the window's own K/V (what the
-    append would have written).  Returns {(s, r, h): [D] float64}.
+    append would have written).  q, k_new, v_new are float64; the pools may be
+    stored in another format that ``decode`` maps to float64.
+    Returns {(s, r, h): [D] float64}.
     """
     res = {}
     by_seq = {}
@@ -125,8 +139,9 @@ def attn_sampled(q, k_new, v_new, k_pool, v_pool, page_table, kv_len, n_causal: 
     G = Hq // Hkv
     for s, rh in by_seq.items():
         L = int(kv_len[s])
-        cache_k = gather_cache(k_pool, page_table[s], L, page_size)
-        cache_v = gather_cache(v_pool, page_table[s], L, page_size)
+        cache_k = gather_cache(k_pool, page_table[s], L, page_size, decode=decode)
+        cache_v = gather_cache(v_pool, page_table[s], L, page_size, slot_last=True,
+                               decode=decode)
         keys = np.concatenate([cache_k, k_new[s]], axis=0)
         vals = np.concatenate([cache_v, v_new[s]], axis=0)
         hi = visible_hi(L, n_causal, n_mask)

@@ -66,7 +66,8 @@ class OracleModel:
 
     def __init__(self, w, k_pools, v_pools, page_size: int = 16, bf16_bits: bool = False):
         """w: synth.ModelWeights-like (float32 or, with bf16_bits, uint16 arrays).
-        k_pools/v_pools: per layer [P, Hkv, page_size, D] arrays (copied)."""
+        k_pools: per layer [P, Hkv, page_size, D]; v_pools: per layer
+        [P, Hkv, D, page_size] (copied)."""
         cv = (lambda a: (a.astype(np.uint32) << 16).view(np.float32).astype(np.float64)) \
             if bf16_bits else (lambda a: np.asarray(a, dtype=np.float64))
         self.V, self.H, self.Hq, self.Hkv, self.D = w.V, w.H, w.Hq, w.Hkv, w.D

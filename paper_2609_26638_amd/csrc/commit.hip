@@ -1,0 +1,175 @@
+// kv_commit: commit the accepted run and roll back the rest of the window's
+// KV (appendix "Self-Speculative Decoding and KV-Cache Update", items Accept,
+// Cache update, Next round).
+//
+// One workgroup, one thread per sequence.  The committed run of sequence s
+// is d_1..d_A followed by the verifier's a_{A+1} = argmax[s, A].  A stop token
+// or the output budget truncates it; the KV of x0 and the kept drafts stays
+// (kv_len += k), every other window slot is dropped.
+//
+// Pages: each sequence ends holding ceil((kv_len + R) / 16) pages.  Two
+// exclusive scans over the sequences give every surplus page its slot on the
+// free stack (pushes, sequences in order, highest logical page first) and
+// every missing page its slot below the new top (pops, sequences in order,
+// logical pages ascending), so the result is independent of thread timing.
+// Feasibility is decided before anything is written: on failure the whole
+// state is left untouched and the error bit is set.
+#include "dvs_common.h"
+
+namespace dvs {
+
+constexpr int COMMIT_THREADS = 1024;
+
+__device__ __forceinline__ int block_exclusive_scan(int v, int* sh, int& total) {
+  // Hillis-Steele over the block in shared memory (S <= 1024; runs once).
+  const int tid = threadIdx.x;
+  sh[tid] = v;
+  __syncthreads();
+  for (int off = 1; off < (int)blockDim.x; off <<= 1) {
+    const int add = tid >= off ? sh[tid - off] : 0;
+    __syncthreads();
+    sh[tid] += add;
+    __syncthreads();
+  }
+  const int incl = sh[tid];
+  total = sh[blockDim.x - 1];
+  __syncthreads();
+  return incl - v;
+}
+
+struct CommitParams {
+  int S, n_causal, n_mask, R, max_pages, pool_pages, draft_width, max_new, eos_id;
+  const int32_t* accept_len;
+  const int32_t* argmax;
+  int32_t* kv_len;
+  int32_t* page_table;
+  int32_t* num_pages;
+  int32_t* free_stack;
+  int32_t* free_top;
+  int32_t* boundary;
+  int32_t* draft;
+  int32_t* out_tokens;
+  int32_t* out_count;
+  int32_t* finished;
+  int32_t* err;
+};
+
+// j-th token of the committed run: d_{j+1} for j < A, then a_{A+1}.
+__device__ __forceinline__ int run_token(const CommitParams& p, int s, int A, int j) {
+  return j < A ? p.draft[(size_t)s * p.draft_width + j] : p.argmax[(size_t)s * p.R + A];
+}
+
+__global__ void __launch_bounds__(COMMIT_THREADS) kv_commit_kernel(CommitParams p) {
+  __shared__ int sh[COMMIT_THREADS];
+  __shared__ int s_err;
+  const int s = threadIdx.x;
+  const bool live_seq = s < p.S;
+  if (s == 0) s_err = 0;
+  __syncthreads();
+
+  int L = 0, n = 0, k = 0, need = 0, cnt = 0, A = 0;
+  bool fin = false, stop = false;
+  int last_tok = 0;
+  if (live_seq) {
+    L = p.kv_len[s];
+    n = p.num_pages[s];
+    cnt = p.out_count[s];
+    fin = p.finished[s] != 0;
+    if (!fin) {
+      A = p.accept_len[s];
+      A = A < 0 ? 0 : (A > p.n_causal - 1 ? p.n_causal - 1 : A);
+      // run = d_1..d_A, a_{A+1}; keep up to the first stop token / budget
+      for (int j = 0; j <= A; ++j) {
+        if (cnt + k >= p.max_new) { stop = true; break; }
+        const int tok = run_token(p, s, A, j);
+        ++k;
+        last_tok = tok;
+        if (p.eos_id >= 0 && tok == p.eos_id) { stop = true; break; }
+      }
+      if (cnt + k >= p.max_new) stop = true;
+    }
+    need = (L + k + p.R + DVS_PAGE_SIZE - 1) / DVS_PAGE_SIZE;
+    if (need > p.max_pages || n < 0 || n > p.max_pages || L < 0)
+      atomicOr(&s_err, DVS_ERR_MAX_PAGES);
+  }
+  const int push = live_seq && n > need ? n - need : 0;
+  const int pop = live_seq && need > n ? need - n : 0;
+  int tot_push = 0, tot_pop = 0;
+  const int push_off = block_exclusive_scan(push, sh, tot_push);
+  const int pop_off = block_exclusive_scan(pop, sh, tot_pop);
+  const int top0 = *p.free_top;
+  if (s == 0) {
+    if (tot_pop > top0 + tot_push) atomicOr(&s_err, DVS_ERR_POOL_EXHAUSTED);
+    if (top0 + tot_push > p.pool_pages || top0 < 0) atomicOr(&s_err, DVS_ERR_POOL_EXHAUSTED);
+  }
+  __syncthreads();
+  if (s_err) {
+    if (s == 0) set_err(p.err, s_err);
+    return;
+  }
+
+  int32_t* row = p.page_table + (size_t)s * p.max_pages;
+  for (int i = 0; i < push; ++i) {            // logical n-1, n-2, ... need
+    p.free_stack[top0 + push_off + i] = row[n - 1 - i];
+    row[n - 1 - i] = -1;
+  }
+  __threadfence_block();
+  __syncthreads();
+  const int top1 = top0 + tot_push;
+  for (int j = 0; j < pop; ++j) {             // logical n, n+1, ... need-1
+    const int slot = top1 - 1 - (pop_off + j);
+    row[n + j] = p.free_stack[slot];
+    p.free_stack[slot] = -1;
+  }
+  if (s == 0) *p.free_top = top1 - tot_pop;
+
+  if (live_seq) {
+    p.num_pages[s] = need;
+    if (!fin) {
+      int32_t* ot = p.out_tokens + (size_t)s * p.max_new;
+      for (int j = 0; j < k; ++j) ot[cnt + j] = run_token(p, s, A, j);
+      p.out_count[s] = cnt + k;
+      p.kv_len[s] = L + k;
+      if (k > 0) p.boundary[s] = last_tok;
+      if (p.n_mask > 0)
+        for (int j = 0; j < p.draft_width; ++j)
+          p.draft[(size_t)s * p.draft_width + j] = p.argmax[(size_t)s * p.R + p.n_causal + j];
+      p.finished[s] = stop ? 1 : 0;
+    }
+  }
+}
+
+}  // namespace dvs
+
+using namespace dvs;
+
+extern "C" int kv_commit(int32_t S, int32_t n_causal, int32_t n_mask, const int32_t* accept_len,
+                         const int32_t* argmax, int32_t* kv_len, int32_t* page_table,
+                         int32_t* num_pages, int32_t max_pages, int32_t* free_stack,
+                         int32_t* free_top, int32_t num_pool_pages, int32_t* boundary,
+                         int32_t* draft, int32_t draft_width, int32_t* out_tokens,
+                         int32_t* out_count, int32_t max_new, int32_t eos_id, int32_t* finished,
+                         int32_t* err_word, void* stream) {
+  clear_error();
+  DVS_CHECK_ARG(accept_len && argmax && kv_len && page_table && num_pages && free_stack &&
+                    free_top && boundary && out_tokens && out_count && finished,
+                "kv_commit: NULL array argument");
+  DVS_CHECK_ARG(S >= 1 && S <= COMMIT_THREADS, "kv_commit: need 1 <= S <= %d", COMMIT_THREADS);
+  DVS_CHECK_ARG(n_causal >= 1 && n_mask >= 0, "kv_commit: need n_causal >= 1, n_mask >= 0");
+  DVS_CHECK_ARG(draft_width >= 0 && (draft || draft_width == 0), "kv_commit: bad draft");
+  DVS_CHECK_ARG(draft_width >= n_causal - 1, "kv_commit: draft_width < n_causal - 1");
+  DVS_CHECK_ARG(n_mask == 0 || n_mask >= draft_width,
+                "kv_commit: mask rows (%d) must cover the draft width (%d)", n_mask, draft_width);
+  DVS_CHECK_ARG(max_pages >= 1 && num_pool_pages >= 1 && max_new >= 1,
+                "kv_commit: need max_pages, num_pool_pages, max_new >= 1");
+  CommitParams p{};
+  p.S = S; p.n_causal = n_causal; p.n_mask = n_mask; p.R = n_causal + n_mask;
+  p.max_pages = max_pages; p.pool_pages = num_pool_pages; p.draft_width = draft_width;
+  p.max_new = max_new; p.eos_id = eos_id;
+  p.accept_len = accept_len; p.argmax = argmax; p.kv_len = kv_len; p.page_table = page_table;
+  p.num_pages = num_pages; p.free_stack = free_stack; p.free_top = free_top;
+  p.boundary = boundary; p.draft = draft; p.out_tokens = out_tokens; p.out_count = out_count;
+  p.finished = finished; p.err = err_word;
+  hipLaunchKernelGGL(kv_commit_kernel, dim3(1), dim3(COMMIT_THREADS), 0, (hipStream_t)stream, p);
+  return launch_status("kv_commit");
+}

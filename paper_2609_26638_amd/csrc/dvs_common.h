@@ -1,0 +1,51 @@
+// Internal helpers shared by the HIP translation units of libdvs.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "dvs.h"
+
+namespace dvs {
+
+// Per-thread error message for dvs_last_error().
+void set_error(const char* fmt, ...);
+void clear_error();
+
+#define DVS_CHECK_ARG(cond, ...)                  \
+  do {                                            \
+    if (!(cond)) {                                \
+      ::dvs::set_error(__VA_ARGS__);              \
+      return DVS_EINVAL;                          \
+    }                                             \
+  } while (0)
+
+#define DVS_CHECK_SUPPORTED(cond, ...)            \
+  do {                                            \
+    if (!(cond)) {                                \
+      ::dvs::set_error(__VA_ARGS__);              \
+      return DVS_EUNSUPPORTED;                    \
+    }                                             \
+  } while (0)
+
+// Launch status after hipLaunchKernelGGL.
+int launch_status(const char* what);
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ float bf16_bits_to_f32(uint32_t b16) {
+  return __uint_as_float(b16 << 16);
+}
+
+__device__ __forceinline__ void set_err(int32_t* err, int32_t bit) {
+  if (err) atomicOr(err, bit);
+}
+
+}  // namespace dvs

@@ -1,0 +1,253 @@
+"""Python binding of libdvs.so (ctypes; argument marshalling only).
+
+Every entry point has the name of its C function and forwards device
+pointers of torch tensors plus sizes.  All computation happens in the HIP
+kernels; there is no fallback of any kind: if the library is missing or a
+call fails, an exception is raised.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libdvs.so")
+
+DVS_F32 = 0
+DVS_BF16 = 1
+ERR_POOL_EXHAUSTED = 1
+ERR_MAX_PAGES = 2
+ERR_NONFINITE = 4
+ERR_BAD_PAGE = 8
+
+_lib = None
+
+_c_int, _c_ptr, _c_f32, _c_size = ctypes.c_int32, ctypes.c_void_p, ctypes.c_float, ctypes.c_size_t
+
+_SIGS = {
+    "dvs_version": ([], _c_int),
+    "dvs_last_error": ([], ctypes.c_char_p),
+    "dvs_attn_workspace_bytes": ([_c_int] * 9, _c_size),
+    "attn_hybrid_block": ([_c_ptr] * 7 + [_c_int] * 8 + [_c_f32, _c_int, _c_int, _c_ptr, _c_ptr,
+                                                          _c_ptr, _c_size, _c_ptr], _c_int),
+    "argmax_accept": ([_c_ptr, _c_int, _c_int, _c_int, _c_int, _c_int, _c_ptr, _c_int, _c_ptr,
+                       _c_ptr, _c_ptr, _c_ptr], _c_int),
+    "kv_commit": ([_c_int, _c_int, _c_int, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_int, _c_ptr,
+                   _c_ptr, _c_int, _c_ptr, _c_ptr, _c_int, _c_ptr, _c_ptr, _c_int, _c_int, _c_ptr,
+                   _c_ptr, _c_ptr], _c_int),
+}
+
+EXPORTED = tuple(_SIGS)
+
+
+class DvsError(RuntimeError):
+    pass
+
+
+def lib():
+    """Load libdvs.so (once).  Raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise DvsError(f"{LIB_PATH} not found: build it with "
+                           "`python -m paper_2609_26638_amd.build` (no fallback exists)")
+        l = ctypes.CDLL(LIB_PATH)
+        for name, (args, res) in _SIGS.items():
+            f = getattr(l, name)
+            f.argtypes = args
+            f.restype = res
+        _lib = l
+    return _lib
+
+
+def _check(rc: int, what: str):
+    if rc != 0:
+        msg = lib().dvs_last_error().decode(errors="replace")
+        raise DvsError(f"{what} failed ({rc}): {msg}")
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream=None):
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _dev(t, dtype, name, ndim=None):
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise DvsError(f"{name} must be a CUDA (HIP) tensor")
+    if t.dtype != dtype:
+        raise DvsError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise DvsError(f"{name} must be contiguous")
+    if ndim is not None and t.dim() != ndim:
+        raise DvsError(f"{name} must have {ndim} dims, got {tuple(t.shape)}")
+    return t
+
+
+def _dtype_code(t):
+    if t.dtype == torch.float32:
+        return DVS_F32
+    if t.dtype == torch.bfloat16:
+        return DVS_BF16
+    raise DvsError(f"unsupported dtype {t.dtype}")
+
+
+# ---------------------------------------------------------------------------
+# attention
+# ---------------------------------------------------------------------------
+
+def attn_workspace_bytes(S, n_causal, n_mask, Hq, Hkv, D, max_pages, chunk_keys=0,
+                         dtype=DVS_BF16) -> int:
+    return int(lib().dvs_attn_workspace_bytes(S, n_causal, n_mask, Hq, Hkv, D, max_pages,
+                                              chunk_keys, dtype))
+
+
+class Workspace:
+    """Zero-initialised device scratch for attn_hybrid_block (counters must
+    start at zero; every call leaves them zero)."""
+
+    def __init__(self, nbytes: int, device="cuda"):
+        self.buf = torch.zeros(max(int(nbytes), 256), dtype=torch.uint8, device=device)
+
+    @property
+    def nbytes(self):
+        return self.buf.numel()
+
+    def ensure(self, nbytes: int):
+        if nbytes > self.nbytes:
+            self.buf = torch.zeros(int(nbytes), dtype=torch.uint8, device=self.buf.device)
+        return self
+
+
+def attn_hybrid_block(q, k_new, v_new, k_pool, v_pool, page_table, kv_len, n_causal: int,
+                      n_mask: int, softmax_scale: float, out=None, err=None, workspace=None,
+                      chunk_keys: int = 0, stream=None):
+    """q [S,R,Hq,D], k_new/v_new [S,R,Hkv,D], k_pool [P,Hkv,16,D],
+    v_pool [P,Hkv,D,16] (updated), page_table [S,max_pages] int32, kv_len [S] int32."""
+    dt = q.dtype
+    _dev(q, dt, "q", 4)
+    S, R, Hq, D = q.shape
+    _dev(k_new, dt, "k_new", 4)
+    _dev(v_new, dt, "v_new", 4)
+    Hkv = k_new.shape[2]
+    if tuple(k_new.shape) != (S, R, Hkv, D) or tuple(v_new.shape) != (S, R, Hkv, D):
+        raise DvsError("k_new / v_new must be [S, R, Hkv, D]")
+    _dev(k_pool, dt, "k_pool", 4)
+    _dev(v_pool, dt, "v_pool", 4)
+    P = k_pool.shape[0]
+    if tuple(k_pool.shape) != (P, Hkv, 16, D) or tuple(v_pool.shape) != (P, Hkv, D, 16):
+        raise DvsError("pools must be k [P,Hkv,16,D] and v [P,Hkv,D,16]")
+    _dev(page_table, torch.int32, "page_table", 2)
+    _dev(kv_len, torch.int32, "kv_len", 1)
+    if page_table.shape[0] != S or kv_len.shape[0] != S:
+        raise DvsError("page_table / kv_len must have S rows")
+    if R != n_causal + n_mask:
+        raise DvsError("R must equal n_causal + n_mask")
+    max_pages = page_table.shape[1]
+    if out is None:
+        out = torch.empty_like(q)
+    _dev(out, dt, "out", 4)
+    if err is not None:
+        _dev(err, torch.int32, "err", 1)
+    code = _dtype_code(q)
+    need = attn_workspace_bytes(S, n_causal, n_mask, Hq, Hkv, D, max_pages, chunk_keys, code)
+    if workspace is None:
+        workspace = Workspace(need, device=q.device)
+    workspace.ensure(need)
+    rc = lib().attn_hybrid_block(_ptr(q), _ptr(k_new), _ptr(v_new), _ptr(k_pool), _ptr(v_pool),
+                                 _ptr(page_table), _ptr(kv_len), S, n_causal, n_mask, Hq, Hkv, D,
+                                 max_pages, P, float(softmax_scale), code, int(chunk_keys),
+                                 _ptr(out), _ptr(err), _ptr(workspace.buf), workspace.nbytes,
+                                 _stream(stream))
+    _check(rc, "attn_hybrid_block")
+    return out
+
+
+# ---------------------------------------------------------------------------
+# argmax + acceptance
+# ---------------------------------------------------------------------------
+
+def argmax_accept(logits, n_causal: int, draft, argmax_out=None, accept_len=None, err=None,
+                  stream=None):
+    """logits [S,R,V] (f32/bf16), draft [S,W] int32 -> (argmax [S,R], accept_len [S])."""
+    _dev(logits, logits.dtype, "logits", 3)
+    S, R, V = logits.shape
+    _dev(draft, torch.int32, "draft", 2)
+    if argmax_out is None:
+        argmax_out = torch.empty((S, R), dtype=torch.int32, device=logits.device)
+    if accept_len is None:
+        accept_len = torch.empty((S,), dtype=torch.int32, device=logits.device)
+    _dev(argmax_out, torch.int32, "argmax_out", 2)
+    _dev(accept_len, torch.int32, "accept_len", 1)
+    if err is not None:
+        _dev(err, torch.int32, "err", 1)
+    rc = lib().argmax_accept(_ptr(logits), _dtype_code(logits), S, R, V, n_causal, _ptr(draft),
+                             draft.shape[1], _ptr(argmax_out), _ptr(accept_len), _ptr(err),
+                             _stream(stream))
+    _check(rc, "argmax_accept")
+    return argmax_out, accept_len
+
+
+# ---------------------------------------------------------------------------
+# commit / rollback over a device-resident decode state
+# ---------------------------------------------------------------------------
+
+class DeviceState:
+    """Device copy of the integer decode state (see synth.PagedState).
+
+    All fields are views into one flat int32 buffer, so a whole state can be
+    saved or restored with a single device-to-device copy."""
+
+    FIELDS = ("kv_len", "page_table", "num_pages", "free_stack", "boundary", "draft",
+              "out_tokens", "out_count", "finished")
+
+    def __init__(self, host, device="cuda"):
+        parts = [np.ascontiguousarray(getattr(host, f), dtype=np.int32).reshape(-1)
+                 for f in self.FIELDS]
+        parts += [np.array([host.free_top], np.int32), np.zeros(1, np.int32)]
+        flat = np.concatenate(parts)
+        self.flat = torch.from_numpy(flat).to(device)
+        off = 0
+        for f, a in zip(self.FIELDS + ("free_top", "err"), parts):
+            shape = getattr(host, f).shape if f in self.FIELDS else (1,)
+            setattr(self, f, self.flat[off:off + a.size].view(shape))
+            off += a.size
+        self.pool_pages = int(host.pool_pages)
+        self.max_pages = int(host.max_pages)
+
+    def copy_from(self, other: "DeviceState"):
+        self.flat.copy_(other.flat, non_blocking=True)
+        return self
+
+    def to_host(self, host_like):
+        h = host_like.copy()
+        for f in self.FIELDS:
+            setattr(h, f, getattr(self, f).cpu().numpy().copy())
+        h.free_top = int(self.free_top.item())
+        return h
+
+
+def kv_commit(st: DeviceState, accept_len, argmax, n_causal: int, n_mask: int,
+              eos_id: int = -1, max_new: int | None = None, stream=None):
+    S = st.kv_len.shape[0]
+    _dev(accept_len, torch.int32, "accept_len", 1)
+    _dev(argmax, torch.int32, "argmax", 2)
+    if argmax.shape != (S, n_causal + n_mask):
+        raise DvsError("argmax must be [S, n_causal + n_mask]")
+    cap = st.out_tokens.shape[1]
+    max_new = cap if max_new is None else min(int(max_new), cap)
+    if max_new != cap:
+        raise DvsError("max_new must equal the out_tokens row length")
+    rc = lib().kv_commit(S, n_causal, n_mask, _ptr(accept_len), _ptr(argmax), _ptr(st.kv_len),
+                         _ptr(st.page_table), _ptr(st.num_pages), st.max_pages,
+                         _ptr(st.free_stack), _ptr(st.free_top), st.pool_pages,
+                         _ptr(st.boundary), _ptr(st.draft), st.draft.shape[1],
+                         _ptr(st.out_tokens), _ptr(st.out_count), max_new, int(eos_id),
+                         _ptr(st.finished), _ptr(st.err), _stream(stream))
+    _check(rc, "kv_commit")

@@ -23,6 +23,7 @@ from __future__ import annotations
 
 import dataclasses
 import math
+import os
 
 import numpy as np
 
@@ -56,14 +57,35 @@ def bf16_to_f64(bits: np.ndarray) -> np.ndarray:
     return bf16_to_f32(bits).astype(np.float64)
 
 
-def _normal(rng: np.random.Generator, shape, std: float, mean: float = 0.0) -> np.ndarray:
-    out = np.empty(shape, dtype=np.float32)
-    rng.standard_normal(out=out.reshape(-1), dtype=np.float32) if out.size else None
-    if std != 1.0:
-        out *= np.float32(std)
-    if mean != 0.0:
-        out += np.float32(mean)
-    return out
+_CHUNK = 1 << 22
+
+
+def _normal(rng: np.random.Generator, shape, std: float, mean: float = 0.0,
+            bf16: bool = False) -> np.ndarray:
+    """N(mean, std) float32 (or RNE-rounded bf16 bits), drawn in fixed 4M-element
+    chunks, each from its own child stream of ``rng``, in parallel threads."""
+    n = int(np.prod(shape)) if len(shape) else 1
+    out = np.empty(n, dtype=np.uint16 if bf16 else np.float32)
+    nchunk = (n + _CHUNK - 1) // _CHUNK
+    seeds = rng.bit_generator.seed_seq.spawn(nchunk) if nchunk else []
+
+    def work(i):
+        lo, hi = i * _CHUNK, min(n, (i + 1) * _CHUNK)
+        g = np.random.Generator(np.random.PCG64(seeds[i]))
+        x = g.standard_normal(hi - lo, dtype=np.float32)
+        if std != 1.0:
+            x *= np.float32(std)
+        if mean != 0.0:
+            x += np.float32(mean)
+        out[lo:hi] = f32_to_bf16_bits(x) if bf16 else x
+
+    if nchunk > 1:
+        import concurrent.futures as cf
+        with cf.ThreadPoolExecutor(max_workers=min(16, os.cpu_count() or 1)) as ex:
+            list(ex.map(work, range(nchunk)))
+    elif nchunk == 1:
+        work(0)
+    return out.reshape(shape)
 
 
 # ----------------------------------------------------------------------------
@@ -159,8 +181,8 @@ class AttnInputs:
     q: np.ndarray          # [S, R, Hq, D]   float32 or uint16 bf16 bits
     k_new: np.ndarray      # [S, R, Hkv, D]
     v_new: np.ndarray      # [S, R, Hkv, D]
-    k_pool: np.ndarray     # [pool, Hkv, 16, D]
-    v_pool: np.ndarray     # [pool, Hkv, 16, D]
+    k_pool: np.ndarray     # [pool, Hkv, 16, D]   (slot-major pages)
+    v_pool: np.ndarray     # [pool, Hkv, D, 16]   (head-dim-major pages)
     state: PagedState
     scale: float
 
@@ -198,9 +220,8 @@ def make_attn_inputs(seed: int, S: int, kv_lens, n_causal: int, n_mask: int, Hq:
     P = st.pool_pages
     arrs = []
     for rng, shape in ((r_q, (S, R, Hq, D)), (r_k, (S, R, Hkv, D)), (r_v, (S, R, Hkv, D)),
-                       (r_kp, (P, Hkv, PAGE_SIZE, D)), (r_vp, (P, Hkv, PAGE_SIZE, D))):
-        x = _normal(rng, shape, std)
-        arrs.append(f32_to_bf16_bits(x) if dtype == "bf16" else x)
+                       (r_kp, (P, Hkv, PAGE_SIZE, D)), (r_vp, (P, Hkv, D, PAGE_SIZE))):
+        arrs.append(_normal(rng, shape, std, bf16=(dtype == "bf16")))
     return AttnInputs(dtype, S, n_causal, n_mask, Hq, Hkv, D, *arrs, state=st,
                       scale=1.0 / math.sqrt(D))
 

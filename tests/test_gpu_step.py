@@ -1,0 +1,52 @@
+"""GPU: the whole hot path (attention -> argmax/accept -> commit) on the
+32-sequence KV 1k-8k workload, checked against the oracle: attention on
+sampled rows (tolerance), accepted lengths, committed tokens and page tables
+bit for bit."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import attention as oa
+from oracle import decode as od
+from paper_2609_26638_amd import dvs, synth
+from tests.gpu_util import dev_attn, max_rel_err, to_dev, to_f64
+
+pytestmark = pytest.mark.gpu
+
+
+def test_batched_serving_step_matches_oracle():
+    print("[step] generating the 32-sequence KV 1k-8k workload", flush=True)
+    ai, li = synth.batched_serving_inputs()
+    B = ai.n_causal
+    d = dev_attn(ai)
+    st = dvs.DeviceState(ai.state)
+    logits = to_dev(li.logits, "bf16")
+    out = dvs.attn_hybrid_block(d["q"], d["k_new"], d["v_new"], d["k_pool"], d["v_pool"],
+                                st.page_table, st.kv_len, B, B, ai.scale, err=st.err)
+    am, A = dvs.argmax_accept(logits, B, st.draft, err=st.err)
+    dvs.kv_commit(st, A, am, B, B)
+    torch.cuda.synchronize()
+    assert int(st.err.item()) == 0
+    # integers: bit-exact
+    ref_am = od.top1_rows(synth.bf16_to_f64(li.logits))
+    np.testing.assert_array_equal(am.cpu().numpy(), ref_am)
+    ref_A = od.accept(ref_am, ai.state.draft, B)
+    np.testing.assert_array_equal(A.cpu().numpy(), ref_A)
+    ref_st = ai.state.copy()
+    assert od.kv_commit(ref_st, ref_A, ref_am, B, B) == 0
+    got = st.to_host(ref_st)
+    for f in ("kv_len", "page_table", "num_pages", "boundary", "draft", "out_tokens", "out_count"):
+        np.testing.assert_array_equal(getattr(got, f), getattr(ref_st, f), err_msg=f)
+    assert got.free_top == ref_st.free_top
+    # acceptance statistics follow the draft match probability 0.9
+    assert 5.0 < ref_A.mean() < 9.5
+    # attention: sampled rows
+    o = to_f64(out)
+    rng = np.random.default_rng(1)
+    samples = sorted({(int(rng.integers(ai.S)), int(rng.integers(ai.R)), int(rng.integers(16)))
+                      for _ in range(24)})
+    ref = oa.attn_sampled(ai.as_f64("q"), ai.as_f64("k_new"), ai.as_f64("v_new"), ai.k_pool,
+                          ai.v_pool, ai.state.page_table, ai.state.kv_len, B, B, ai.scale,
+                          samples, decode=synth.bf16_to_f64)
+    for (s, r, h), v in ref.items():
+        assert max_rel_err(o[s, r, h][None], v[None]) <= 2e-2, (s, r, h)

@@ -22,7 +22,7 @@ def _dense(ai, s):
     L = int(ai.state.kv_len[s])
     kp, vp = ai.as_f64("k_pool"), ai.as_f64("v_pool")
     ck = oa.gather_cache(kp, ai.state.page_table[s], L, 16)
-    cv = oa.gather_cache(vp, ai.state.page_table[s], L, 16)
+    cv = oa.gather_cache(vp, ai.state.page_table[s], L, 16, slot_last=True)
     return ck, cv
 
 
@@ -78,7 +78,7 @@ def test_append_writes_window_kv():
         L = int(ai.state.kv_len[s])
         got = oa.gather_cache(kp, ai.state.page_table[s], L + 8, 16)[L:]
         np.testing.assert_array_equal(got, kn[s])
-        got = oa.gather_cache(vp, ai.state.page_table[s], L + 8, 16)[L:]
+        got = oa.gather_cache(vp, ai.state.page_table[s], L + 8, 16, slot_last=True)[L:]
         np.testing.assert_array_equal(got, vn[s])
 
 
@@ -107,6 +107,16 @@ def test_sampled_rows_equal_full():
                                5, 3, ai.scale)
     for (s, r, h) in samples:
         np.testing.assert_allclose(sm[(s, r, h)], out[s, r, h], rtol=1e-13, atol=1e-14)
+    # pools kept in bf16 bits and decoded page by page give the same rows
+    bi = synth.make_attn_inputs(7, 3, [31, 64, 2], 5, 3, 4, 2, 16, "bf16")
+    full = oa.attn_sampled(bi.as_f64("q"), bi.as_f64("k_new"), bi.as_f64("v_new"),
+                           bi.as_f64("k_pool"), bi.as_f64("v_pool"), bi.state.page_table,
+                           bi.state.kv_len, 5, 3, bi.scale, samples)
+    lazy = oa.attn_sampled(bi.as_f64("q"), bi.as_f64("k_new"), bi.as_f64("v_new"),
+                           bi.k_pool, bi.v_pool, bi.state.page_table, bi.state.kv_len, 5, 3,
+                           bi.scale, samples, decode=synth.bf16_to_f64)
+    for key in samples:
+        np.testing.assert_array_equal(full[key], lazy[key])
 
 
 def test_constant_values_give_constant_output():
@@ -116,7 +126,7 @@ def test_constant_values_give_constant_output():
     q, kn = ai.as_f64("q"), ai.as_f64("k_new")
     c = np.linspace(-1, 1, 8)
     kp = ai.as_f64("k_pool")
-    vp = np.broadcast_to(c, ai.v_pool.shape).copy()
+    vp = np.broadcast_to(c[:, None], ai.v_pool.shape).copy()   # [P, Hkv, D, 16]
     vn = np.broadcast_to(c, ai.v_new.shape).copy()
     out = oa.attn_hybrid_block(q, kn, vn, kp, vp, ai.state.page_table, ai.state.kv_len,
                                3, 3, ai.scale)

@@ -53,7 +53,7 @@ def _tiny_model(seed, V=11, H=32, Hq=4, Hkv=2, D=8, n_layers=2, ffn=48, std=0.5,
     w = synth.make_model_weights(seed, V, H, Hq, Hkv, D, n_layers, ffn, std=std)
     rng = np.random.default_rng(seed)
     kp = [np.zeros((pool, Hkv, 16, D), np.float32) for _ in range(n_layers)]
-    vp = [np.zeros((pool, Hkv, 16, D), np.float32) for _ in range(n_layers)]
+    vp = [np.zeros((pool, Hkv, D, 16), np.float32) for _ in range(n_layers)]
     return w, kp, vp, rng
 
 
