@@ -101,6 +101,10 @@ def main():
     ap.add_argument("--chunk-keys", type=int, default=0, help="attention key chunk (0 = auto)")
     ap.add_argument("--cpu-seqs", type=int, default=16, help="oracle sample size (sequences)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--profile-attn", type=int, default=0, metavar="N",
+                    help="counter-collection mode: N attention launches on the workload, "
+                         "then one 1 GiB device-to-device copy (calibrates FETCH_SIZE / "
+                         "WRITE_SIZE against known bytes); prints no bench line")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -142,6 +146,23 @@ def main():
     ws = dvs.Workspace(dvs.attn_workspace_bytes(S, B, B, Hq, Hkv, D, host_state.max_pages,
                                                 args.chunk_keys))
     torch.cuda.synchronize()
+
+    if args.profile_attn:
+        for _ in range(args.profile_attn):
+            st.copy_from(pristine)
+            dvs.attn_hybrid_block(q, kn, vn, kp, vp, st.page_table, st.kv_len, B, B, ai.scale,
+                                  out=out, err=st.err, workspace=ws, chunk_keys=args.chunk_keys)
+        torch.cuda.synchronize()
+        src = torch.ones(1 << 30, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"profile_attn": args.profile_attn, "attn_algorithmic_bytes":
+                          attn_algorithmic_bytes(ai.state.kv_len, S, R, Hq, Hkv, D),
+                          "copy_bytes": 1 << 30, "src_hash": attn_source_hash(),
+                          "err": int(st.err.item())}), flush=True)
+        return
 
     stages = ("restore", "attn", "argmax", "commit")
 

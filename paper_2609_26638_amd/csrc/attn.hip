@@ -5,29 +5,38 @@
 // AR-Diffusion Training"; appendix items Draft forward / Verify forward):
 // window row r of a sequence with committed length L sits at position L + r;
 // a causal row (r < n_causal) sees keys <= L + r, a mask row sees every key
-// up to L + R - 1.  Keys below L are visible to every row, so only the tile
-// that reaches the window needs a mask.
+// up to L + R - 1.  Keys below L are visible to every row, so only the tiles
+// that reach the window need a mask.
 //
 // bf16 path (MFMA, gfx950)
-//   One workgroup per (key chunk, row tile, sequence, KV head).  All G query
-//   heads of the KV head and all R window rows (R*G "query rows", up to 256
-//   per workgroup) share each K/V tile staged in LDS, so the cache is read
-//   from HBM once per KV head.  Per 64-key tile:
+//   Work items are (sequence, KV head, row tile); an item's keys are cut into
+//   64-key tiles.  All G query heads of the KV head and all R window rows (up
+//   to 256 "query rows", 32 per wave) share every K/V tile staged in LDS, so
+//   the cache is read from HBM once per KV head.  Per tile and wave:
 //     S^T[key, row] = K Q^T   v_mfma_f32_32x32x16_bf16, A = K from LDS,
-//                             B = Q held in registers for the whole chunk;
-//     the C layout puts one query row per lane (16 keys per 32-key group), so
-//     the row max / sum of the online softmax are in-lane plus one exchange
-//     with lane^32, and the rescale of O touches only the lane's own row;
-//     O^T[d, row] += V^T P^T  A = V^T read from a transposed, XOR-swizzled
-//                             LDS copy of V, B = P (bf16) straight from the
-//                             score registers (same key permutation).
-//   Chunks begin at absolute multiples of chunk_keys.  A sequence spanning
-//   several chunks writes fp32 partials (m, l, O); the last workgroup of the
-//   (sequence, KV head, row tile) to finish merges them in chunk order, so
-//   results are deterministic and a row's arithmetic does not depend on the
-//   other rows of the window.
-//   The window's own K/V (positions [L, L+R)) are read from k_new / v_new and
-//   written to the pool by the workgroup whose chunk covers them.
+//                             B = Q held in registers for the whole segment;
+//     the C layout puts one query row per lane, so the online-softmax row max
+//     and sum are in-lane plus one exchange with lane^32, and the O rescale
+//     touches only the lane's own row;
+//     O^T[d, row] += V^T P^T  A = V^T slice of the head-dim-major V tile,
+//                             B = P packed to bf16 straight from the scores.
+//   Cache tiles are copied HBM -> LDS with direct 16-byte loads through a
+//   3-stage ring; the tiles that reach the window go through registers (keys
+//   < L from the pool, [L, T) from k_new / v_new, appended to the pool by row
+//   tile 0, >= T zero).
+//
+//   Two ways to cut the work (both deterministic):
+//   * aligned (chunk_keys > 0): workgroup = one chunk of one item, chunks at
+//     absolute multiples of chunk_keys, so a row's arithmetic never depends
+//     on the other rows or on the batch (a causal row equals a plain AR call
+//     at its position, bit for bit);
+//   * balanced (chunk_keys == 0): the items' tiles are concatenated and every
+//     workgroup takes an equal contiguous share, so the grid finishes together
+//     whatever the length mix; only shares that split an item publish
+//     partials.
+//   A split item's partials (m, l, O in fp32) are merged in segment order by
+//   the last workgroup to finish it (write-through stores, counter, coherent
+//   loads).
 //
 // fp32 path: a plain per-(sequence, row, head) workgroup, fp32 throughout.
 #include <math.h>
@@ -36,7 +45,13 @@
 
 namespace dvs {
 
-constexpr int KT = 64;  // keys per tile
+constexpr int KT = 64;                 // keys per tile
+constexpr int NSTAGE = 4;              // LDS ring depth for cache tiles
+constexpr int SUB_TILES = 256;         // tiles whose page ids are staged at once
+constexpr int MAX_CHUNK_KEYS = 16384;
+constexpr int BAL_MAX_SEGS = 9;        // balanced mode: segments per item (bound)
+constexpr int BAL_MAX_SEQS = 1024;     // balanced mode: sequences per call
+constexpr float RESCALE_LOG2 = 8.f;
 
 struct AttnParams {
   const void* q;
@@ -52,7 +67,12 @@ struct AttnParams {
   int32_t* counters;
   int32_t* err;
   int S, n_causal, n_mask, R, Hq, Hkv, G, max_pages, pool_pages;
-  int chunk_keys, n_chunks_max, rows_total, n_row_tiles;
+  int rows_total, n_row_tiles, n_items;
+  int balanced;      // 0: aligned chunks, 1: balanced shares
+  int chunk_tiles;   // aligned: tiles per chunk
+  int n_chunks_max;  // aligned: grid rows
+  int share_min;     // balanced: minimum tiles per workgroup
+  int max_segs;      // partial slots per item
   float scale_log2;
   float scale;
 };
@@ -60,421 +80,526 @@ struct AttnParams {
 // ---------------------------------------------------------------------------
 // LDS layouts of one 64-key tile (bf16)
 //
-// K: 64 rows of D*2 bytes (row = key), 16-byte chunks XOR-swizzled by kswz(row)
-//    so the A-operand reads (8 rows per LDS phase) hit distinct banks.
-// V: KT/16 pages x D rows x 32 bytes (row = head-dim element, 16 keys): the
-//    same layout as a head-dim-major V page of the pool, so cache tiles are a
-//    straight copy; the two 16-byte halves are swapped on every other group of
-//    4 rows, again for conflict-free operand reads.
+// K: 64 rows of D*2 bytes (row = key); the 16-byte chunks of row r are
+//    XOR-swizzled by kswz(r) so the A-operand reads (8 rows per LDS phase)
+//    hit distinct banks.
+// V: 4 pages x D rows x 32 bytes (row = head-dim element, 16 keys) - the
+//    layout of a head-dim-major V page of the pool, so cache tiles are plain
+//    copies; the two 16-byte halves swap on every other group of 4 rows.
+// Both tiles are built from 1 KB wave segments, and a page of one KV head is
+// a whole number of segments (4 KB / 3 KB / 2 KB for D = 128 / 96 / 64), so
+// every direct-load instruction reads a single, wave-uniform page.
 //
-// Key permutation: the QK^T A-operand lane m (m = 0..31 within a 32-key group)
-// is fed key kperm(m) (bits 2 and 3 of m swapped).  With the 32x32 MFMA C
-// layout, lane (row, hh) then holds in registers 0..7 the scores of keys
-// 8*hh + 0..7 and in registers 8..15 those of keys 16 + 8*hh + 0..7, which is
-// exactly the B-operand layout of a 16-key k-step of the PV product, and the
-// matching A-operand (V^T) slice is one 16-byte chunk of a V page row.
+// Key permutation: QK^T A-operand lane m (0..31 within a 32-key group) is fed
+// key kperm(m) (bits 2 and 3 of m swapped).  With the 32x32 MFMA C layout,
+// lane (row, hh) then holds in score registers 0..7 the keys 8*hh + 0..7 and
+// in registers 8..15 the keys 16 + 8*hh + 0..7: exactly the B-operand layout
+// of two 16-key PV k-steps, whose A operand is one 16-byte half of a V page
+// row.
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ int kperm(int m) {
   return (m & 0x13) | ((m & 4) << 1) | ((m & 8) >> 1);
 }
 
+// Chunk swizzles.  K (16 chunks per row): a bijection of the row's low 4 bits
+// (bits 2 and 3 swapped) so that the 8 rows kperm(0..7) and the 16 rows
+// kperm(0..15) read by consecutive lanes land on distinct 16-byte bank groups
+// whether the LDS serves 8 or 16 lanes per cycle.  V: halves swap with bit 2
+// xor bit 3 of the row, distinct over 8 and over 16 consecutive rows.
 template <int CPR>
 __device__ __forceinline__ int kswz(int row) {
-  return (CPR % 8 == 0) ? ((row & 3) | ((row >> 1) & 4)) : (row & 3);
+  if constexpr (CPR % 16 == 0) return (row & 3) | ((row >> 1) & 4) | ((row & 4) << 1);
+  else if constexpr (CPR % 8 == 0) return (row & 3) | ((row >> 1) & 4);
+  else return row & 3;
 }
 
-__device__ __forceinline__ int vswz(int d) { return (d >> 2) & 1; }
+__device__ __forceinline__ int vswz(int d) { return ((d >> 2) ^ (d >> 3)) & 1; }
 
-// s_waitcnt vmcnt(n) with the other counters left alone (gfx9 encoding).
+// s_waitcnt vmcnt(n), other counters untouched (gfx9 encoding; n <= 63).
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
   static_assert(N >= 0 && N < 64, "vmcnt range");
   __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
 }
 
-constexpr int MAX_CHUNK_KEYS = 16384;
-constexpr float RESCALE_LOG2 = 8.f;
-constexpr int NSTAGE = 3;
+// Wait until at most `tiles_after` cache tiles (NPL loads per lane each) are
+// still in flight (tiles_after in [0, NSTAGE - 2]).  A bound above 63 is
+// clamped, which only waits longer.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt_clamped() {
+  wait_vmcnt<(N < 63 ? N : 63)>();
+}
 
-template <int D, int NW, int RG>
+template <int NPL>
+__device__ __forceinline__ void wait_tiles(int tiles_after) {
+  static_assert(NSTAGE >= 2 && NSTAGE <= 4, "wait_tiles covers up to 2 tiles in flight");
+  if (NSTAGE >= 4 && tiles_after >= 2) wait_vmcnt_clamped<2 * NPL>();
+  else if (NSTAGE >= 3 && tiles_after >= 1) wait_vmcnt_clamped<NPL>();
+  else wait_vmcnt<0>();
+}
+
+template <int D, int NW>
 __global__ void __launch_bounds__(NW * 64, 1) attn_bf16_kernel(AttnParams p) {
   constexpr int NT = NW * 64;
-  constexpr int CPR = D / 8;              // 16-byte chunks per K row
+  constexpr int CPR = D / 8;
   constexpr int KROWB = D * 2;
   constexpr int KTILE_B = KT * KROWB;
   constexpr int VTILE_B = KT * D * 2;
   constexpr int STAGE_B = KTILE_B + VTILE_B;
-  constexpr int K_INS = KTILE_B / (NT * 16);   // DMA instructions per lane per tile
+  constexpr int K_INS = KTILE_B / (NT * 16);
   constexpr int V_INS = VTILE_B / (NT * 16);
   constexpr int NPL = K_INS + V_INS;
   constexpr int KS = D / 16;
   constexpr int DG = D / 32;
   constexpr int KG = KT / 32;
-  constexpr int RPW = NW * RG * 32;
+  constexpr int RPW = NW * 32;
+  constexpr int PAGE_K = 16 * KROWB;
+  constexpr int PAGE_V = D * 32;
+  constexpr int SEGPP_K = PAGE_K / 1024;
+  constexpr int SEGPP_V = PAGE_V / 1024;
+  constexpr bool KXOR = (KROWB & (KROWB - 1)) == 0;   // row stride a power of two
   static_assert(KTILE_B % (NT * 16) == 0 && VTILE_B % (NT * 16) == 0, "tile / wave mismatch");
+  static_assert(PAGE_K % 1024 == 0 && PAGE_V % 1024 == 0, "page / segment mismatch");
+  constexpr int NREG = DG * 16;
 
   __shared__ __attribute__((aligned(1024))) char smem[NSTAGE * STAGE_B];
-  __shared__ int s_pages[MAX_CHUNK_KEYS / 16 + 1];
-  __shared__ int s_flag;
+  __shared__ int s_pages[SUB_TILES * 4 + 4];
+  __shared__ int s_seq[BAL_MAX_SEQS + 1];   // balanced: tile prefix over sequences
+  __shared__ int s_flag[2];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int w = tid >> 6;
   const int hh = lane >> 5;
   const int l32 = lane & 31;
-
-  int idx = blockIdx.x;
-  const int kvh = idx % p.Hkv;
-  idx /= p.Hkv;
-  const int s = idx % p.S;
-  idx /= p.S;
-  const int rt = idx % p.n_row_tiles;
-  const int c = idx / p.n_row_tiles;
-
-  const int L = p.kv_len[s];
   const int R = p.R;
-  const int T = L + R;
-  if (L < 0 || T > p.max_pages * 16) {
-    if (c == 0 && rt == 0 && kvh == 0 && tid == 0) set_err(p.err, DVS_ERR_MAX_PAGES);
-    return;
-  }
-  const int C = p.chunk_keys;
-  const int n_chunks = (T + C - 1) / C;
-  if (c >= n_chunks) return;
-  const int k0 = c * C;
-  const int k1 = min(k0 + C, T);
-  const int pg0 = k0 >> 4;
+  const int HN = p.Hkv * p.n_row_tiles;   // items per sequence
 
   const __bf16* __restrict__ q = (const __bf16*)p.q;
   const char* __restrict__ knb = (const char*)p.k_new;
   const char* __restrict__ vnb = (const char*)p.v_new;
   char* __restrict__ kpb = (char*)p.k_pool;
   char* __restrict__ vpb = (char*)p.v_pool;
-  const int32_t* __restrict__ pt = p.page_table + (size_t)s * p.max_pages;
+  __bf16* __restrict__ out = (__bf16*)p.out;
 
-  // ---- page ids of this chunk (invalid ids are replaced by page 0 and reported)
-  if (tid == 0) s_flag = 0;
-  __syncthreads();
-  for (int i = tid; i < ((k1 + 15) >> 4) - pg0; i += NT) {
-    int pg = pt[pg0 + i];
-    if (pg < 0 || pg >= p.pool_pages) {
-      pg = 0;
-      s_flag = 1;
-    }
-    s_pages[i] = pg;
-  }
-  __syncthreads();
-  if (tid == 0 && s_flag) set_err(p.err, DVS_ERR_BAD_PAGE);
-
-  // ---- query rows of this lane: Q fragments (B operand) and visibility limit
-  bf16x8 qf[RG][KS];
-  int hi[RG], rowr[RG], rowh[RG];
-  bool rvalid[RG];
+  // ---- per-lane constant offsets of the direct loads (within a page)
+  uint32_t koff[K_INS], voff[V_INS];
 #pragma unroll
-  for (int rg = 0; rg < RG; ++rg) {
-    const int n = rt * RPW + w * RG * 32 + rg * 32 + l32;
-    rvalid[rg] = n < p.rows_total;
+  for (int j = 0; j < K_INS; ++j) {
+    const int off = (w * K_INS + j) * 1024 + lane * 16;
+    const int row = off / KROWB;
+    const int cc = ((off % KROWB) >> 4) ^ kswz<CPR>(row);
+    koff[j] = (uint32_t)((row & 15) * KROWB + cc * 16);
+  }
+#pragma unroll
+  for (int j = 0; j < V_INS; ++j) {
+    const int off = (w * V_INS + j) * 1024 + lane * 16;
+    const int rem = off % PAGE_V;
+    const int d = rem >> 5;
+    const int hc = ((rem >> 4) & 1) ^ vswz(d);
+    voff[j] = (uint32_t)(d * 32 + hc * 16);
+  }
+  // per-lane fragment offsets within a stage buffer
+  int kfrag[KG];
+#pragma unroll
+  for (int kg = 0; kg < KG; ++kg) {
+    const int row = kg * 32 + kperm(l32);
+    kfrag[kg] = row * KROWB + (KXOR ? ((hh ^ kswz<CPR>(row)) << 4) : 0);
+  }
+  const int ksw = kswz<CPR>(kperm(l32));   // same for kg = 0, 1 (row differs by 32)
+  const int vfrag = KTILE_B + l32 * 32 + ((hh ^ vswz(l32)) << 4);
+
+  // ---- work decomposition
+  // segments: (item, tile range [j0, j1), segment index k, segments nseg)
+  int u = 0, u_end = 0;          // balanced: global tile range of this workgroup
+  int share = 0;
+  int it_a = 0, c_a = 0;         // aligned: item and chunk
+  if (p.balanced) {
+    // tile prefix over sequences (invalid sequences contribute no tiles)
+    if (tid == 0) s_flag[0] = 0;
+    for (int s0 = 0; s0 < p.S; s0 += NT) {
+      __syncthreads();
+      int t = 0;
+      const int s = s0 + tid;
+      if (s < p.S) {
+        const int L = p.kv_len[s];
+        const int T = L + R;
+        if (L < 0 || T > p.max_pages * 16) {
+          s_flag[0] = 1;
+        } else {
+          t = (T + KT - 1) / KT;
+        }
+      }
+      // inclusive scan of t over this block of sequences (Hillis-Steele)
+      s_seq[1 + tid + s0] = t;   // s0 + NT <= BAL_MAX_SEQS guaranteed by the host
+      __syncthreads();
+      for (int off = 1; off < NT; off <<= 1) {
+        const int v = (tid >= off && s0 + tid < p.S) ? s_seq[1 + s0 + tid - off] : 0;
+        __syncthreads();
+        if (s0 + tid < p.S) s_seq[1 + s0 + tid] += v;
+        __syncthreads();
+      }
+      if (s0 > 0 && s0 + tid < p.S) s_seq[1 + s0 + tid] += s_seq[s0];
+      // (the carry read above sees the previous block's final value)
+    }
+    if (tid == 0) s_seq[0] = 0;
+    __syncthreads();
+    if (blockIdx.x == 0 && tid == 0 && s_flag[0]) set_err(p.err, DVS_ERR_MAX_PAGES);
+    const int U = s_seq[p.S] * HN;
+    share = max((U + (int)gridDim.x - 1) / (int)gridDim.x, p.share_min);
+    u = (int)blockIdx.x * share;
+    u_end = min(u + share, U);
+    if (u >= u_end) return;
+  } else {
+    int idx = blockIdx.x;
+    it_a = idx % p.n_items;
+    c_a = idx / p.n_items;
+  }
+
+  bool first_segment = true;
+  int s_cur = 0;                 // balanced: sequence cursor
+  while (true) {
+    int s, kvh, rt, it, j0, j1, k, nseg, L;
+    if (p.balanced) {
+      if (u >= u_end) break;
+      while (s_seq[s_cur + 1] * HN <= u) ++s_cur;
+      s = s_cur;
+      L = p.kv_len[s];
+      const int tiles = s_seq[s + 1] - s_seq[s];
+      const int local = u - s_seq[s] * HN;
+      const int qi = local / tiles;
+      j0 = local - qi * tiles;
+      j1 = min(tiles, j0 + (u_end - u));
+      it = s * HN + qi;
+      kvh = qi / p.n_row_tiles;
+      rt = qi - kvh * p.n_row_tiles;
+      const int P0 = s_seq[s] * HN + qi * tiles;     // first unit of the item
+      k = (int)blockIdx.x - P0 / share;
+      nseg = (P0 + tiles - 1) / share - P0 / share + 1;
+      u += j1 - j0;
+    } else {
+      if (!first_segment) break;
+      it = it_a;
+      s = it / HN;
+      const int qi = it - s * HN;
+      kvh = qi / p.n_row_tiles;
+      rt = qi - kvh * p.n_row_tiles;
+      L = p.kv_len[s];
+      const int T = L + R;
+      if (L < 0 || T > p.max_pages * 16) {
+        if (c_a == 0 && qi == 0 && tid == 0) set_err(p.err, DVS_ERR_MAX_PAGES);
+        return;
+      }
+      const int tiles = (T + KT - 1) / KT;
+      nseg = (tiles + p.chunk_tiles - 1) / p.chunk_tiles;
+      if (c_a >= nseg) return;
+      k = c_a;
+      j0 = c_a * p.chunk_tiles;
+      j1 = min(tiles, j0 + p.chunk_tiles);
+    }
+    if (!first_segment) __syncthreads();   // previous segment fully done with LDS
+    first_segment = false;
+    const int T = L + R;
+    const int32_t* __restrict__ pt = p.page_table + (size_t)s * p.max_pages;
+
+    // ---- rows of this lane: Q fragments (B operand), visibility limit
+    const int n = rt * RPW + w * 32 + l32;
+    const bool rvalid = n < p.rows_total;
     const int r = n / p.G;
     const int h = kvh * p.G + (n - r * p.G);
-    rowr[rg] = r;
-    rowh[rg] = h;
-    hi[rg] = !rvalid[rg] ? -1 : (r < p.n_causal ? L + r : T - 1);
+    const int hi = !rvalid ? -1 : (r < p.n_causal ? L + r : T - 1);
+    bf16x8 qf[KS];
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks)
-      qf[rg][ks] = rvalid[rg]
-          ? *(const bf16x8*)(q + (((size_t)s * R + r) * p.Hq + h) * D + ks * 16 + hh * 8)
-          : bf16x8{};
-  }
+      qf[ks] = rvalid ? *(const bf16x8*)(q + (((size_t)s * R + r) * p.Hq + h) * D + ks * 16 + hh * 8)
+                      : bf16x8{};
+    // Complete the Q loads here, then re-define the fragments through an empty
+    // asm: the waitcnt pass otherwise cannot prove inside the tile loop that
+    // they are complete and waits for every in-flight cache-tile load.
+    wait_vmcnt<0>();
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) asm volatile("" : "+v"(qf[ks]));
 
-  f32x16 o[RG][DG];
-  float m[RG], lsum[RG];
+    f32x16 o[DG];
 #pragma unroll
-  for (int rg = 0; rg < RG; ++rg) {
-    m[rg] = -INFINITY;
-    lsum[rg] = 0.f;
-#pragma unroll
-    for (int dg = 0; dg < DG; ++dg) o[rg][dg] = f32x16{};
-  }
+    for (int dg = 0; dg < DG; ++dg) o[dg] = f32x16{};
+    float m = -INFINITY, lsum = 0.f;
 
-  // ---- cache tiles (all 64 keys below L): direct global -> LDS copies
-  auto issue_tile = [&](int t0, char* buf) {
+    // ---- one tile of compute from LDS
+    auto compute_tile = [&](const char* stage, int key0, bool masked) {
+      f32x16 sacc[KG];
 #pragma unroll
-    for (int j = 0; j < K_INS; ++j) {
-      const int seg = w * K_INS + j;
-      const int off = seg * 1024 + lane * 16;
-      const int row = off / KROWB;
-      const int cc = ((off % KROWB) >> 4) ^ kswz<CPR>(row);
-      const int key = t0 + row;
-      const int pg = s_pages[(key >> 4) - pg0];
-      const char* src = kpb + ((((size_t)pg * p.Hkv + kvh) * 16 + (key & 15)) * D) * 2 + cc * 16;
-      __builtin_amdgcn_global_load_lds((const void*)src,
-                                       (__attribute__((address_space(3))) void*)(buf + seg * 1024),
-                                       16, 0, 0);
-    }
+      for (int kg = 0; kg < KG; ++kg) sacc[kg] = f32x16{};
+      // K fragments are read one k-step ahead of the MFMAs that use them
+      auto kload = [&](int ks, int kg) {
+        const int off = KXOR ? (kfrag[kg] ^ (ks << 5))
+                             : (kfrag[kg] + ((((ks << 1) | hh) ^ ksw) << 4));
+        return *(const bf16x8*)(stage + off);
+      };
+      bf16x8 ka[2][KG];
 #pragma unroll
-    for (int j = 0; j < V_INS; ++j) {
-      const int seg = w * V_INS + j;
-      const int off = seg * 1024 + lane * 16;
-      const int tp = off / (D * 32);
-      const int d = (off % (D * 32)) >> 5;
-      const int hc = ((off >> 4) & 1) ^ vswz(d);
-      const int pg = s_pages[(t0 >> 4) + tp - pg0];
-      const char* src = vpb + ((((size_t)pg * p.Hkv + kvh) * D + d) * 16) * 2 + hc * 16;
-      __builtin_amdgcn_global_load_lds((const void*)src,
-                                       (__attribute__((address_space(3))) void*)(buf + KTILE_B + seg * 1024),
-                                       16, 0, 0);
-    }
-  };
-
-  // ---- one tile of compute from LDS
-  auto compute_tile = [&](const char* kb, int t0, bool masked) {
-    const char* vb = kb + KTILE_B;
-    f32x16 sacc[KG][RG];
+      for (int kg = 0; kg < KG; ++kg) ka[0][kg] = kload(0, kg);
 #pragma unroll
-    for (int kg = 0; kg < KG; ++kg)
+      for (int ks = 0; ks < KS; ++ks) {
+        if (ks + 1 < KS) {
 #pragma unroll
-      for (int rg = 0; rg < RG; ++rg) sacc[kg][rg] = f32x16{};
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-#pragma unroll
-      for (int kg = 0; kg < KG; ++kg) {
-        const int row = kg * 32 + kperm(l32);
-        const bf16x8 a = *(const bf16x8*)(kb + row * KROWB + (((2 * ks + hh) ^ kswz<CPR>(row)) << 4));
-#pragma unroll
-        for (int rg = 0; rg < RG; ++rg)
-          sacc[kg][rg] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[rg][ks], sacc[kg][rg], 0, 0, 0);
-      }
-    }
-    if (masked) {
-#pragma unroll
-      for (int kg = 0; kg < KG; ++kg)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const int key = t0 + kg * 32 + 16 * (i >> 3) + 8 * hh + (i & 7);
-#pragma unroll
-          for (int rg = 0; rg < RG; ++rg)
-            if (key > hi[rg]) sacc[kg][rg][i] = -INFINITY;
+          for (int kg = 0; kg < KG; ++kg) ka[(ks + 1) & 1][kg] = kload(ks + 1, kg);
         }
-    }
-    bf16x8 pf[RG][KT / 16];
 #pragma unroll
-    for (int rg = 0; rg < RG; ++rg) {
-      float tmax = -INFINITY;
+        for (int kg = 0; kg < KG; ++kg)
+          sacc[kg] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[ks & 1][kg], qf[ks], sacc[kg], 0, 0, 0);
+      }
+      if (masked) {
 #pragma unroll
-      for (int kg = 0; kg < KG; ++kg)
+        for (int kg = 0; kg < KG; ++kg)
 #pragma unroll
-        for (int i = 0; i < 16; ++i) tmax = fmaxf(tmax, sacc[kg][rg][i]);
+          for (int i = 0; i < 16; ++i) {
+            const int key = key0 + kg * 32 + 16 * (i >> 3) + 8 * hh + (i & 7);
+            if (key > hi) sacc[kg][i] = -INFINITY;
+          }
+      }
+      // tile max: a tree over the lane's 16*KG scores, then lane^32
+      float mx[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) mx[j] = fmaxf(sacc[0][2 * j], sacc[0][2 * j + 1]);
+#pragma unroll
+      for (int kg = 1; kg < KG; ++kg)
+#pragma unroll
+        for (int j = 0; j < 8; ++j) mx[j] = fmaxf(mx[j], fmaxf(sacc[kg][2 * j], sacc[kg][2 * j + 1]));
+      float tmax = fmaxf(fmaxf(fmaxf(mx[0], mx[1]), fmaxf(mx[2], mx[3])),
+                         fmaxf(fmaxf(mx[4], mx[5]), fmaxf(mx[6], mx[7])));
       tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
       // The row's reference maximum m only moves when the tile maximum exceeds
-      // it by more than 2^RESCALE_LOG2 (weights stay <= 2^RESCALE_LOG2, exact
-      // after the final division by l); the wave skips the O rescale when no
-      // row moved.  The decision is per row, so rows stay independent.
+      // it by more than 2^RESCALE_LOG2 (weights stay <= 2^RESCALE_LOG2 and the
+      // final division by l is exact about it); the wave skips the O rescale
+      // when no row moved.  The decision is per row.
       const float cand = tmax * p.scale_log2;
-      const bool move = cand > m[rg] + RESCALE_LOG2;
+      const bool move = cand > m + RESCALE_LOG2;
       if (__ballot(move)) {
-        const float alpha = move ? __builtin_amdgcn_exp2f(m[rg] - cand) : 1.f;
-        lsum[rg] *= alpha;
+        const float alpha = move ? __builtin_amdgcn_exp2f(m - cand) : 1.f;
+        lsum *= alpha;
 #pragma unroll
-        for (int dg = 0; dg < DG; ++dg) o[rg][dg] *= alpha;
+        for (int dg = 0; dg < DG; ++dg) o[dg] *= alpha;
       }
-      if (move) m[rg] = cand;
-      const float msafe = (m[rg] == -INFINITY) ? 0.f : m[rg];
-      float ps = 0.f;
+      if (move) m = cand;
+      const float msafe = (m == -INFINITY) ? 0.f : m;
+      bf16x8 pf[KT / 16];
+      float psum[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int t = 0; t < KT / 16; ++t) {
         uint32_t pk[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const int i0 = 8 * (t & 1) + 2 * e;
-          const float a0 = __builtin_amdgcn_exp2f(fmaf(sacc[t >> 1][rg][i0], p.scale_log2, -msafe));
-          const float a1 = __builtin_amdgcn_exp2f(fmaf(sacc[t >> 1][rg][i0 + 1], p.scale_log2, -msafe));
-          ps += a0 + a1;
+          const float a0 = __builtin_amdgcn_exp2f(fmaf(sacc[t >> 1][i0], p.scale_log2, -msafe));
+          const float a1 = __builtin_amdgcn_exp2f(fmaf(sacc[t >> 1][i0 + 1], p.scale_log2, -msafe));
+          psum[e] += a0 + a1;
           pk[e] = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{a0, a1}, bf16x2));
         }
-        pf[rg][t] = __builtin_bit_cast(bf16x8, u32x4{pk[0], pk[1], pk[2], pk[3]});
+        pf[t] = __builtin_bit_cast(bf16x8, u32x4{pk[0], pk[1], pk[2], pk[3]});
       }
-      lsum[rg] += ps;
-    }
+      lsum += (psum[0] + psum[1]) + (psum[2] + psum[3]);
+      // V fragments are read one k-step ahead of the MFMAs that use them
+      bf16x8 va[2][DG];
 #pragma unroll
-    for (int t = 0; t < KT / 16; ++t) {
+      for (int dg = 0; dg < DG; ++dg) va[0][dg] = *(const bf16x8*)(stage + vfrag + dg * 32 * 32);
 #pragma unroll
-      for (int dg = 0; dg < DG; ++dg) {
-        const int d = dg * 32 + l32;
-        const bf16x8 a = *(const bf16x8*)(vb + (t * D + d) * 32 + ((hh ^ vswz(d)) << 4));
+      for (int t = 0; t < KT / 16; ++t) {
+        if (t + 1 < KT / 16) {
 #pragma unroll
-        for (int rg = 0; rg < RG; ++rg)
-          o[rg][dg] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pf[rg][t], o[rg][dg], 0, 0, 0);
-      }
-    }
-  };
-
-  // main (pure cache) tiles: [k0, kmain)
-  const int lfloor = (L / KT) * KT;
-  const int kmain = min(k1, max(k0, lfloor));
-  const int n_main = (kmain - k0) / KT;
-
-  // prologue: the Q loads were issued first; start NSTAGE-1 tiles, then wait
-  // only for Q (loads complete in issue order).
-#pragma unroll
-  for (int i = 0; i < NSTAGE - 1; ++i)
-    if (i < n_main) issue_tile(k0 + i * KT, smem + i * STAGE_B);
-  // (waiting for "at most 63 outstanding" is still enough: the Q loads are older)
-  if (n_main >= 2) wait_vmcnt<(2 * NPL < 63 ? 2 * NPL : 63)>();
-  else if (n_main == 1) wait_vmcnt<NPL>();
-  else wait_vmcnt<0>();
-
-  for (int i = 0; i < n_main; ++i) {
-    if (i + 1 < n_main) wait_vmcnt<NPL>();   // tile i landed (this wave's part)
-    else wait_vmcnt<0>();
-    __builtin_amdgcn_s_barrier();             // ... every wave's part; tile i-1 consumed
-    if (i + NSTAGE - 1 < n_main)
-      issue_tile(k0 + (i + NSTAGE - 1) * KT, smem + ((i + NSTAGE - 1) % NSTAGE) * STAGE_B);
-    compute_tile(smem + (i % NSTAGE) * STAGE_B, k0 + i * KT, false);
-  }
-
-  // ---- tiles that reach the window or run past T: staged through registers.
-  // Keys < L come from the pool, keys in [L, T) from k_new / v_new (and are
-  // appended to the pool by row tile 0), keys >= T are zero.
-  bool bad_new = false;
-  for (int t0 = kmain; t0 < k1; t0 += KT) {
-    __syncthreads();
-    char* kb = smem;
-    char* vb = smem + KTILE_B;
-    for (int ci = tid; ci < KT * CPR; ci += NT) {
-      const int kk = ci / CPR;
-      const int cc = ci - kk * CPR;
-      const int key = t0 + kk;
-      u32x4 val = u32x4{0, 0, 0, 0};
-      if (key < L) {
-        const int pg = s_pages[(key >> 4) - pg0];
-        val = *(const u32x4*)(kpb + ((((size_t)pg * p.Hkv + kvh) * 16 + (key & 15)) * D) * 2 + cc * 16);
-      } else if (key < T) {
-        val = *(const u32x4*)(knb + ((((size_t)s * R + (key - L)) * p.Hkv + kvh) * D) * 2 + cc * 16);
-        if (rt == 0) {
-          const int pg = s_pages[(key >> 4) - pg0];
-          *(u32x4*)(kpb + ((((size_t)pg * p.Hkv + kvh) * 16 + (key & 15)) * D) * 2 + cc * 16) = val;
+          for (int dg = 0; dg < DG; ++dg)
+            va[(t + 1) & 1][dg] = *(const bf16x8*)(stage + vfrag + ((t + 1) * D + dg * 32) * 32);
         }
-      }
-      *(u32x4*)(kb + kk * KROWB + ((cc ^ kswz<CPR>(kk)) << 4)) = val;
-    }
-    for (int ci = tid; ci < KT / 16 * D * 2; ci += NT) {
-      const int tp = ci / (D * 2);
-      const int d = (ci >> 1) % D;
-      const int hc = ci & 1;
-      const int kbase = t0 + tp * 16 + hc * 8;
-      u32x4 val = u32x4{0, 0, 0, 0};
-      if (kbase + 8 <= L) {
-        const int pg = s_pages[(kbase >> 4) - pg0];
-        val = *(const u32x4*)(vpb + ((((size_t)pg * p.Hkv + kvh) * D + d) * 16) * 2 + hc * 16);
-      } else {
-        uint16_t e16[8];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const int key = kbase + e;
-          uint16_t x = 0;
+        for (int dg = 0; dg < DG; ++dg)
+          o[dg] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[t & 1][dg], pf[t], o[dg], 0, 0, 0);
+      }
+    };
+
+    // ---- the segment's tiles, in sub-ranges whose page ids fit in LDS
+    for (int ja = j0; ja < j1; ja += SUB_TILES) {
+      const int jb = min(j1, ja + SUB_TILES);
+      const int pg_lo = ja * 4;
+      const int pg_hi = min(jb * 4, (T + 15) >> 4);
+      if (ja != j0) __syncthreads();
+      if (tid == 0) s_flag[1] = 0;
+      __syncthreads();
+      for (int i = tid; i < pg_hi - pg_lo; i += NT) {
+        int pg = pt[pg_lo + i];
+        if (pg < 0 || pg >= p.pool_pages) {
+          pg = 0;
+          s_flag[1] = 1;
+        }
+        s_pages[i] = pg;
+      }
+      __syncthreads();   // also completes the Q loads
+      if (tid == 0 && s_flag[1]) set_err(p.err, DVS_ERR_BAD_PAGE);
+
+      // cache tiles (all 64 keys below L) through the direct-load ring
+      const int jm = min(jb, max(ja, L / KT));
+      const int n_main = jm - ja;
+      auto issue = [&](int i) {
+        char* stage = smem + (i % NSTAGE) * STAGE_B;
+        const int pbase = i * 4;          // first page of tile ja+i, relative to pg_lo
+#pragma unroll
+        for (int j = 0; j < K_INS; ++j) {
+          const int seg = w * K_INS + j;
+          const int pg = __builtin_amdgcn_readfirstlane(s_pages[pbase + seg / SEGPP_K]);
+          const char* base = kpb + ((size_t)pg * p.Hkv + kvh) * PAGE_K;
+          __builtin_amdgcn_global_load_lds((const void*)(base + koff[j]),
+              (__attribute__((address_space(3))) void*)(stage + seg * 1024), 16, 0, 0);
+        }
+#pragma unroll
+        for (int j = 0; j < V_INS; ++j) {
+          const int seg = w * V_INS + j;
+          const int pg = __builtin_amdgcn_readfirstlane(s_pages[pbase + seg / SEGPP_V]);
+          const char* base = vpb + ((size_t)pg * p.Hkv + kvh) * PAGE_V;
+          __builtin_amdgcn_global_load_lds((const void*)(base + voff[j]),
+              (__attribute__((address_space(3))) void*)(stage + KTILE_B + seg * 1024), 16, 0, 0);
+        }
+      };
+#pragma unroll
+      for (int i = 0; i < NSTAGE - 1; ++i)
+        if (i < n_main) issue(i);
+      for (int i = 0; i < n_main; ++i) {
+        wait_tiles<NPL>(min(NSTAGE - 2, n_main - 1 - i));
+        __builtin_amdgcn_s_barrier();     // tile i complete for every wave; tile i-1 consumed
+        if (i + NSTAGE - 1 < n_main) issue(i + NSTAGE - 1);
+        compute_tile(smem + (i % NSTAGE) * STAGE_B, (ja + i) * KT, false);
+      }
+
+      // tiles that reach the window or run past T: staged through registers
+      for (int jt = jm; jt < jb; ++jt) {
+        const int t0 = jt * KT;
+        __syncthreads();
+        char* kb = smem;
+        char* vb = smem + KTILE_B;
+        for (int ci = tid; ci < KT * CPR; ci += NT) {
+          const int kk = ci / CPR;
+          const int cc = ci - kk * CPR;
+          const int key = t0 + kk;
+          u32x4 val = u32x4{0, 0, 0, 0};
           if (key < L) {
-            const int pg = s_pages[(key >> 4) - pg0];
-            x = ((const uint16_t*)vpb)[(((size_t)pg * p.Hkv + kvh) * D + d) * 16 + (key & 15)];
+            const int pg = s_pages[(key >> 4) - pg_lo];
+            val = *(const u32x4*)(kpb + ((size_t)pg * p.Hkv + kvh) * PAGE_K + (key & 15) * KROWB + cc * 16);
           } else if (key < T) {
-            x = ((const uint16_t*)vnb)[(((size_t)s * R + (key - L)) * p.Hkv + kvh) * D + d];
+            val = *(const u32x4*)(knb + (((size_t)s * R + (key - L)) * p.Hkv + kvh) * KROWB + cc * 16);
             if (rt == 0) {
-              const int pg = s_pages[(key >> 4) - pg0];
-              ((uint16_t*)vpb)[(((size_t)pg * p.Hkv + kvh) * D + d) * 16 + (key & 15)] = x;
+              const int pg = s_pages[(key >> 4) - pg_lo];
+              *(u32x4*)(kpb + ((size_t)pg * p.Hkv + kvh) * PAGE_K + (key & 15) * KROWB + cc * 16) = val;
             }
           }
-          e16[e] = x;
+          *(u32x4*)(kb + kk * KROWB + ((cc ^ kswz<CPR>(kk)) << 4)) = val;
         }
-        val = u32x4{e16[0] | ((uint32_t)e16[1] << 16), e16[2] | ((uint32_t)e16[3] << 16),
-                    e16[4] | ((uint32_t)e16[5] << 16), e16[6] | ((uint32_t)e16[7] << 16)};
+        for (int ci = tid; ci < KT / 16 * D * 2; ci += NT) {
+          const int tp = ci / (D * 2);
+          const int d = (ci >> 1) % D;
+          const int hc = ci & 1;
+          const int kbase = t0 + tp * 16 + hc * 8;
+          u32x4 val = u32x4{0, 0, 0, 0};
+          if (kbase + 8 <= L) {
+            const int pg = s_pages[(kbase >> 4) - pg_lo];
+            val = *(const u32x4*)(vpb + ((size_t)pg * p.Hkv + kvh) * PAGE_V + d * 32 + hc * 16);
+          } else {
+            uint16_t e16[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+              const int key = kbase + e;
+              uint16_t x = 0;
+              if (key < L) {
+                const int pg = s_pages[(key >> 4) - pg_lo];
+                x = *(const uint16_t*)(vpb + ((size_t)pg * p.Hkv + kvh) * PAGE_V + d * 32 + (key & 15) * 2);
+              } else if (key < T) {
+                x = *(const uint16_t*)(vnb + (((size_t)s * R + (key - L)) * p.Hkv + kvh) * KROWB + d * 2);
+                if (rt == 0) {
+                  const int pg = s_pages[(key >> 4) - pg_lo];
+                  *(uint16_t*)(vpb + ((size_t)pg * p.Hkv + kvh) * PAGE_V + d * 32 + (key & 15) * 2) = x;
+                }
+              }
+              e16[e] = x;
+            }
+            val = u32x4{e16[0] | ((uint32_t)e16[1] << 16), e16[2] | ((uint32_t)e16[3] << 16),
+                        e16[4] | ((uint32_t)e16[5] << 16), e16[6] | ((uint32_t)e16[7] << 16)};
+          }
+          *(u32x4*)(vb + (tp * D + d) * 32 + ((hc ^ vswz(d)) << 4)) = val;
+        }
+        __syncthreads();
+        compute_tile(smem, t0, true);
       }
-      *(u32x4*)(vb + (tp * D + d) * 32 + ((hc ^ vswz(d)) << 4)) = val;
     }
-    __syncthreads();
-    compute_tile(kb, t0, true);
-  }
-  (void)bad_new;
 
-#pragma unroll
-  for (int rg = 0; rg < RG; ++rg) lsum[rg] += __shfl_xor(lsum[rg], 32);
-
-  __bf16* __restrict__ out = (__bf16*)p.out;
-  auto write_out = [&](int rg, const f32x16* ov, float inv) {
-    if (!rvalid[rg]) return;
-    __bf16* orow = out + (((size_t)s * R + rowr[rg]) * p.Hq + rowh[rg]) * D;
-#pragma unroll
-    for (int dg = 0; dg < DG; ++dg)
-#pragma unroll
-      for (int g4 = 0; g4 < 4; ++g4) {
-        const int d = dg * 32 + 8 * g4 + 4 * hh;
-        const f32x2 v01 = f32x2{ov[dg][4 * g4 + 0] * inv, ov[dg][4 * g4 + 1] * inv};
-        const f32x2 v23 = f32x2{ov[dg][4 * g4 + 2] * inv, ov[dg][4 * g4 + 3] * inv};
-        const uint32_t w0 = __builtin_bit_cast(uint32_t, __builtin_convertvector(v01, bf16x2));
-        const uint32_t w1 = __builtin_bit_cast(uint32_t, __builtin_convertvector(v23, bf16x2));
-        *(u32x2*)(orow + d) = u32x2{w0, w1};
-      }
-  };
-
-  if (n_chunks == 1) {
-#pragma unroll
-    for (int rg = 0; rg < RG; ++rg) write_out(rg, o[rg], lsum[rg] > 0.f ? 1.f / lsum[rg] : 0.f);
-    return;
-  }
-
-  // ---- split key range: publish partials, the last workgroup merges in order
-  constexpr int NREG = RG * DG * 16;
-  const size_t item = ((size_t)s * p.Hkv + kvh) * p.n_row_tiles + rt;
-  {
-    f32x4* po = (f32x4*)(p.part_o + (item * p.n_chunks_max + c) * (size_t)(NT * NREG));
-    f32x2* pml = (f32x2*)(p.part_ml + (item * p.n_chunks_max + c) * (size_t)(NT * RG * 2));
-#pragma unroll
-    for (int rg = 0; rg < RG; ++rg) {
-      pml[rg * NT + tid] = f32x2{m[rg], lsum[rg]};
+    // ---- finish the segment
+    lsum += __shfl_xor(lsum, 32);
+    auto write_out = [&](const f32x16* ov, float inv) {
+      if (!rvalid) return;
+      __bf16* orow = out + (((size_t)s * R + r) * p.Hq + h) * D;
 #pragma unroll
       for (int dg = 0; dg < DG; ++dg)
 #pragma unroll
-        for (int q4 = 0; q4 < 4; ++q4) {
-          const f32x16& v = o[rg][dg];
-          po[((rg * DG + dg) * 4 + q4) * NT + tid] = f32x4{v[4 * q4], v[4 * q4 + 1], v[4 * q4 + 2], v[4 * q4 + 3]};
+        for (int g4 = 0; g4 < 4; ++g4) {
+          const int d = dg * 32 + 8 * g4 + 4 * hh;
+          const f32x2 v01 = f32x2{ov[dg][4 * g4 + 0] * inv, ov[dg][4 * g4 + 1] * inv};
+          const f32x2 v23 = f32x2{ov[dg][4 * g4 + 2] * inv, ov[dg][4 * g4 + 3] * inv};
+          const uint32_t w0 = __builtin_bit_cast(uint32_t, __builtin_convertvector(v01, bf16x2));
+          const uint32_t w1 = __builtin_bit_cast(uint32_t, __builtin_convertvector(v23, bf16x2));
+          *(u32x2*)(orow + d) = u32x2{w0, w1};
         }
+    };
+    if (nseg == 1) {
+      write_out(o, lsum > 0.f ? 1.f / lsum : 0.f);
+      continue;
     }
-  }
-  __threadfence();
-  __syncthreads();
-  if (tid == 0) s_flag = (atomicAdd(&p.counters[item], 1) == n_chunks - 1);
-  __syncthreads();
-  if (!s_flag) return;
-  __threadfence();
-
-  const f32x4* pob = (const f32x4*)(p.part_o + item * p.n_chunks_max * (size_t)(NT * NREG));
-  const f32x2* pmlb = (const f32x2*)(p.part_ml + item * p.n_chunks_max * (size_t)(NT * RG * 2));
+    // Publish the partial with write-through (agent-coherent) stores, wait for
+    // them, then count in; the workgroup that completes the item merges with
+    // coherent loads.  No L2-wide write-back or invalidate is needed.
+    const size_t slot = (size_t)it * p.max_segs + k;
+    {
+      float* po = p.part_o + slot * (size_t)(NT * NREG);
+      float* pml = p.part_ml + slot * (size_t)(NT * 2);
+      __hip_atomic_store(pml + tid, m, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(pml + NT + tid, lsum, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 #pragma unroll
-  for (int rg = 0; rg < RG; ++rg) {
+      for (int dg = 0; dg < DG; ++dg)
+#pragma unroll
+        for (int i = 0; i < 16; ++i)
+          __hip_atomic_store(po + (dg * 16 + i) * NT + tid, o[dg][i], __ATOMIC_RELAXED,
+                             __HIP_MEMORY_SCOPE_AGENT);
+    }
+    wait_vmcnt<0>();
+    __syncthreads();
+    if (tid == 0)
+      s_flag[0] = (__hip_atomic_fetch_add(&p.counters[it], 1, __ATOMIC_RELAXED,
+                                          __HIP_MEMORY_SCOPE_AGENT) == nseg - 1);
+    __syncthreads();
+    if (!s_flag[0]) continue;
+    const float* pob = p.part_o + (size_t)it * p.max_segs * (NT * NREG);
+    const float* pmlb = p.part_ml + (size_t)it * p.max_segs * (NT * 2);
     float M = -INFINITY;
-    for (int cc = 0; cc < n_chunks; ++cc) M = fmaxf(M, pmlb[(size_t)cc * NT * RG + rg * NT + tid].x);
+    for (int c = 0; c < nseg; ++c)
+      M = fmaxf(M, __hip_atomic_load(pmlb + (size_t)c * NT * 2 + tid, __ATOMIC_RELAXED,
+                                     __HIP_MEMORY_SCOPE_AGENT));
     const float Ms = (M == -INFINITY) ? 0.f : M;
     f32x16 acc[DG];
 #pragma unroll
     for (int dg = 0; dg < DG; ++dg) acc[dg] = f32x16{};
     float lt = 0.f;
-    for (int cc = 0; cc < n_chunks; ++cc) {
-      const f32x2 ml = pmlb[(size_t)cc * NT * RG + rg * NT + tid];
-      const float wgt = __builtin_amdgcn_exp2f(ml.x - Ms);
-      lt += wgt * ml.y;
-      const f32x4* src = pob + (size_t)cc * NT * NREG / 4;
+    for (int c = 0; c < nseg; ++c) {
+      const float* src_ml = pmlb + (size_t)c * NT * 2;
+      const float mc = __hip_atomic_load(src_ml + tid, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      const float lc = __hip_atomic_load(src_ml + NT + tid, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      const float wgt = __builtin_amdgcn_exp2f(mc - Ms);
+      lt += wgt * lc;
+      const float* src = pob + (size_t)c * NT * NREG;
 #pragma unroll
       for (int dg = 0; dg < DG; ++dg)
 #pragma unroll
-        for (int q4 = 0; q4 < 4; ++q4) {
-          const f32x4 v = src[((rg * DG + dg) * 4 + q4) * NT + tid];
-          acc[dg][4 * q4 + 0] += wgt * v.x;
-          acc[dg][4 * q4 + 1] += wgt * v.y;
-          acc[dg][4 * q4 + 2] += wgt * v.z;
-          acc[dg][4 * q4 + 3] += wgt * v.w;
-        }
+        for (int i = 0; i < 16; ++i)
+          acc[dg][i] += wgt * __hip_atomic_load(src + (dg * 16 + i) * NT + tid, __ATOMIC_RELAXED,
+                                                __HIP_MEMORY_SCOPE_AGENT);
     }
-    write_out(rg, acc, lt > 0.f ? 1.f / lt : 0.f);
+    write_out(acc, lt > 0.f ? 1.f / lt : 0.f);
+    if (tid == 0) __hip_atomic_store(&p.counters[it], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
-  if (tid == 0) p.counters[item] = 0;
 }
 
 // ---------------------------------------------------------------------------
@@ -590,11 +715,25 @@ __global__ void __launch_bounds__(256) attn_f32_kernel(AttnParams p) {
 // host side
 // ---------------------------------------------------------------------------
 struct AttnPlan {
-  int nw, rg, rows_total, rows_per_wg, n_row_tiles, chunk, n_chunks_max;
+  int nw, rows_total, rows_per_wg, n_row_tiles, n_items, balanced;
+  int chunk_tiles, n_chunks_max, share_min, max_segs, grid;
   size_t off_counters, off_ml, off_o, bytes;
 };
 
 static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+static int device_cus() {
+  static int cus = 0;
+  if (cus == 0) {
+    int dev = 0, v = 0;
+    if (hipGetDevice(&dev) == hipSuccess &&
+        hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && v > 0)
+      cus = v;
+    else
+      cus = 256;
+  }
+  return cus;
+}
 
 static AttnPlan plan_attn(int S, int R, int Hq, int Hkv, int D, int max_pages, int chunk_keys,
                           int dtype) {
@@ -602,41 +741,36 @@ static AttnPlan plan_attn(int S, int R, int Hq, int Hkv, int D, int max_pages, i
   const int G = Hq / Hkv;
   pl.rows_total = R * G;
   if (dtype == DVS_BF16) {
-    const int groups = (pl.rows_total + 31) / 32;  // 32-row MFMA groups
-    if (groups >= 8) {
-      pl.nw = 4; pl.rg = 2;
-    } else if (groups >= 4) {
-      pl.nw = 2; pl.rg = 2;
-    } else if (groups >= 2) {
-      pl.nw = 1; pl.rg = 2;
-    } else {
-      pl.nw = 1; pl.rg = 1;
-    }
+    const int groups = (pl.rows_total + 31) / 32;   // 32-row MFMA groups
+    pl.nw = groups >= 8 ? 8 : (groups >= 4 ? 4 : (groups >= 2 ? 2 : 1));
+    if (D == 96 && pl.nw > 4) pl.nw = 4;   // a 96-wide tile splits over at most 4 waves
   } else {
-    pl.nw = 4; pl.rg = 1;
+    pl.nw = 4;
   }
-  pl.rows_per_wg = pl.nw * pl.rg * 32;
+  pl.rows_per_wg = pl.nw * 32;
   pl.n_row_tiles = (pl.rows_total + pl.rows_per_wg - 1) / pl.rows_per_wg;
-  const long long max_keys = (long long)max_pages * DVS_PAGE_SIZE;
-  int C = chunk_keys;
-  if (C <= 0) {
-    const long long items = (long long)S * Hkv * pl.n_row_tiles;
-    long long want = (max_keys * items + 1535) / 1536;
-    want = (want + KT - 1) / KT * KT;
-    if (want < 256) want = 256;
-    if (want > MAX_CHUNK_KEYS) want = MAX_CHUNK_KEYS;
-    C = (int)want;
+  pl.n_items = S * Hkv * pl.n_row_tiles;
+  const int max_tiles = (max_pages * DVS_PAGE_SIZE + KT - 1) / KT;
+  pl.balanced = (chunk_keys == 0 && S <= BAL_MAX_SEQS) ? 1 : 0;
+  if (pl.balanced) {
+    pl.share_min = (max_tiles + BAL_MAX_SEGS - 2) / (BAL_MAX_SEGS - 1);
+    if (pl.share_min < 1) pl.share_min = 1;
+    pl.max_segs = BAL_MAX_SEGS;
+    pl.grid = device_cus();
+  } else {
+    int C = chunk_keys > 0 ? chunk_keys : 4096;
+    pl.chunk_tiles = C / KT;
+    pl.n_chunks_max = (max_tiles + pl.chunk_tiles - 1) / pl.chunk_tiles;
+    pl.max_segs = pl.n_chunks_max;
+    pl.grid = pl.n_chunks_max * pl.n_items;
   }
-  pl.chunk = C;
-  pl.n_chunks_max = (int)((max_keys + C - 1) / C);
   const int NT = pl.nw * 64;
-  const size_t items = (size_t)S * Hkv * pl.n_row_tiles;
+  const size_t slots = (size_t)pl.n_items * pl.max_segs;
   if (dtype == DVS_BF16) {
-    const size_t nreg = (size_t)pl.rg * (D / 32) * 16;
     pl.off_counters = 0;
-    pl.off_ml = align256(items * sizeof(int32_t));
-    pl.off_o = pl.off_ml + align256(items * pl.n_chunks_max * (size_t)NT * pl.rg * 2 * sizeof(float));
-    pl.bytes = pl.off_o + align256(items * pl.n_chunks_max * (size_t)NT * nreg * sizeof(float));
+    pl.off_ml = align256((size_t)pl.n_items * sizeof(int32_t));
+    pl.off_o = pl.off_ml + align256(slots * NT * 2 * sizeof(float));
+    pl.bytes = pl.off_o + align256(slots * NT * (size_t)(D / 32) * 16 * sizeof(float));
   } else {
     pl.bytes = 256;
   }
@@ -644,15 +778,16 @@ static AttnPlan plan_attn(int S, int R, int Hq, int Hkv, int D, int max_pages, i
 }
 
 template <int D>
-static void launch_bf16(const AttnPlan& pl, const AttnParams& prm, int grid, hipStream_t st) {
-  if (pl.nw == 4)
-    hipLaunchKernelGGL((attn_bf16_kernel<D, 4, 2>), dim3(grid), dim3(256), 0, st, prm);
-  else if (pl.nw == 2)
-    hipLaunchKernelGGL((attn_bf16_kernel<D, 2, 2>), dim3(grid), dim3(128), 0, st, prm);
-  else if (pl.rg == 2)
-    hipLaunchKernelGGL((attn_bf16_kernel<D, 1, 2>), dim3(grid), dim3(64), 0, st, prm);
-  else
-    hipLaunchKernelGGL((attn_bf16_kernel<D, 1, 1>), dim3(grid), dim3(64), 0, st, prm);
+static void launch_bf16(const AttnPlan& pl, const AttnParams& prm, hipStream_t st) {
+  switch (pl.nw) {
+    case 8:
+      if constexpr (D != 96)
+        hipLaunchKernelGGL((attn_bf16_kernel<D, 8>), dim3(pl.grid), dim3(512), 0, st, prm);
+      break;
+    case 4: hipLaunchKernelGGL((attn_bf16_kernel<D, 4>), dim3(pl.grid), dim3(256), 0, st, prm); break;
+    case 2: hipLaunchKernelGGL((attn_bf16_kernel<D, 2>), dim3(pl.grid), dim3(128), 0, st, prm); break;
+    default: hipLaunchKernelGGL((attn_bf16_kernel<D, 1>), dim3(pl.grid), dim3(64), 0, st, prm); break;
+  }
 }
 
 }  // namespace dvs
@@ -663,7 +798,7 @@ extern "C" size_t dvs_attn_workspace_bytes(int32_t S, int32_t n_causal, int32_t 
                                            int32_t Hq, int32_t Hkv, int32_t D, int32_t max_pages,
                                            int32_t chunk_keys, int32_t dtype) {
   if (S < 1 || n_causal < 0 || n_mask < 0 || n_causal + n_mask < 1 || Hkv < 1 || Hq < Hkv ||
-      Hq % Hkv != 0 || max_pages < 1)
+      Hq % Hkv != 0 || max_pages < 1 || chunk_keys < 0)
     return 0;
   return plan_attn(S, n_causal + n_mask, Hq, Hkv, D, max_pages, chunk_keys, dtype).bytes;
 }
@@ -700,8 +835,9 @@ extern "C" int attn_hybrid_block(const void* q, const void* k_new, const void* v
   prm.page_table = page_table; prm.kv_len = kv_len; prm.out = out; prm.err = err_word;
   prm.S = S; prm.n_causal = n_causal; prm.n_mask = n_mask; prm.R = R; prm.Hq = Hq;
   prm.Hkv = Hkv; prm.G = Hq / Hkv; prm.max_pages = max_pages; prm.pool_pages = num_pool_pages;
-  prm.chunk_keys = pl.chunk; prm.n_chunks_max = pl.n_chunks_max; prm.rows_total = pl.rows_total;
-  prm.n_row_tiles = pl.n_row_tiles;
+  prm.rows_total = pl.rows_total; prm.n_row_tiles = pl.n_row_tiles; prm.n_items = pl.n_items;
+  prm.balanced = pl.balanced; prm.chunk_tiles = pl.chunk_tiles;
+  prm.n_chunks_max = pl.n_chunks_max; prm.share_min = pl.share_min; prm.max_segs = pl.max_segs;
   prm.scale = softmax_scale;
   prm.scale_log2 = softmax_scale * 1.4426950408889634f;
   hipStream_t st = (hipStream_t)stream;
@@ -710,11 +846,10 @@ extern "C" int attn_hybrid_block(const void* q, const void* k_new, const void* v
     prm.counters = (int32_t*)(ws + pl.off_counters);
     prm.part_ml = (float*)(ws + pl.off_ml);
     prm.part_o = (float*)(ws + pl.off_o);
-    const long long grid = (long long)pl.n_chunks_max * pl.n_row_tiles * S * Hkv;
-    DVS_CHECK_SUPPORTED(grid < (1LL << 31), "attn_hybrid_block: grid too large");
-    if (D == 128) launch_bf16<128>(pl, prm, (int)grid, st);
-    else if (D == 96) launch_bf16<96>(pl, prm, (int)grid, st);
-    else launch_bf16<64>(pl, prm, (int)grid, st);
+    DVS_CHECK_SUPPORTED((long long)pl.grid < (1LL << 31), "attn_hybrid_block: grid too large");
+    if (D == 128) launch_bf16<128>(pl, prm, st);
+    else if (D == 96) launch_bf16<96>(pl, prm, st);
+    else launch_bf16<64>(pl, prm, st);
   } else {
     const long long grid = (long long)S * R * Hq;
     DVS_CHECK_SUPPORTED(grid < (1LL << 31), "attn_hybrid_block: grid too large");
