@@ -171,6 +171,79 @@ int kv_commit(int32_t S, int32_t n_causal, int32_t n_mask, const int32_t* accept
               int32_t* out_count, int32_t max_new, int32_t eos_id, int32_t* finished,
               int32_t* err_word, void* stream);
 
+/* ------------------------------------------------------------------------
+ * draft_verify_step
+ *
+ * One fused self-speculative step of a decoder (method "Self-Speculative
+ * Decoding"; appendix "Self-Speculative Decoding and KV-Cache Update"): the
+ * window rows are embedded -- causal rows [x0, d_1..d_{n_causal-1}] from
+ * state->boundary / state->draft, mask rows as the mask-token embedding, row
+ * `vocab` of the table (Method "AR-to-Diffusion Conversion") -- and run
+ * through every layer:
+ *     h = RMSNorm(x) * g_attn;  q, k, v = h Wq^T, h Wk^T, h Wv^T;
+ *     rotate-half rotary embedding at position kv_len + r (theta rope_theta);
+ *     o = attn_hybrid_block(q, k, v, layer pools);  x += o Wo^T;
+ *     if ffn > 0: h = RMSNorm(x) * g_mlp;  x += (silu(h Wg^T) * (h Wu^T)) Wd^T
+ * then logits = (RMSNorm(x) * g_final) Wlm^T, argmax_accept and kv_commit on
+ * the state.  With (n_causal, n_mask) = (B, B) this is the fused step;
+ * (1, 0) is one greedy AR step.
+ *
+ * Weights are row-major [out_features, in_features]; all live in device
+ * memory, in the model dtype (DVS_F32 or DVS_BF16; fp32 accumulation, fp32
+ * residual stream, fp32 logits).  A row's arithmetic does not depend on how
+ * many rows the call carries, so AR and fused calls agree bit for bit on the
+ * causal rows (for the attention this needs chunk_keys > 0).
+ *
+ * logits_out [S*R, vocab] float, argmax_out [S*R], accept_out [S] int32 are
+ * optional (NULL = kept in the workspace).  workspace: at least
+ * dvs_step_workspace_bytes() bytes, zero-filled before its first use.
+ * ---------------------------------------------------------------------- */
+typedef struct dvs_layer {
+  const void* wq;      /* [n_heads*head_dim, hidden]        */
+  const void* wk;      /* [n_kv_heads*head_dim, hidden]     */
+  const void* wv;      /* [n_kv_heads*head_dim, hidden]     */
+  const void* wo;      /* [hidden, n_heads*head_dim]        */
+  const void* g_attn;  /* [hidden] RMSNorm gain             */
+  const void* g_mlp;   /* [hidden]       (ffn > 0 only)     */
+  const void* w_gate;  /* [ffn, hidden]  (ffn > 0 only)     */
+  const void* w_up;    /* [ffn, hidden]  (ffn > 0 only)     */
+  const void* w_down;  /* [hidden, ffn]  (ffn > 0 only)     */
+  void* k_pool;        /* [num_pool_pages, n_kv_heads, 16, head_dim] */
+  void* v_pool;        /* [num_pool_pages, n_kv_heads, head_dim, 16] */
+} dvs_layer;
+
+typedef struct dvs_model {
+  int32_t dtype;       /* DVS_F32 or DVS_BF16 */
+  int32_t n_layers, vocab, hidden, n_heads, n_kv_heads, head_dim, ffn;
+  float rope_theta, rms_eps;
+  const void* embed;   /* [vocab + 1, hidden]; row vocab = mask token [M] */
+  const void* g_final; /* [hidden] */
+  const void* lm_head; /* [vocab, hidden] */
+  const dvs_layer* layers; /* HOST array of n_layers descriptors */
+} dvs_model;
+
+typedef struct dvs_state {
+  int32_t S, max_pages, num_pool_pages, draft_width, max_new, eos_id;
+  int32_t* kv_len;     /* [S]                 */
+  int32_t* page_table; /* [S, max_pages]      */
+  int32_t* num_pages;  /* [S]                 */
+  int32_t* free_stack; /* [num_pool_pages]    */
+  int32_t* free_top;   /* [1]                 */
+  int32_t* boundary;   /* [S] x0              */
+  int32_t* draft;      /* [S, draft_width]    */
+  int32_t* out_tokens; /* [S, max_new]        */
+  int32_t* out_count;  /* [S]                 */
+  int32_t* finished;   /* [S]                 */
+  int32_t* err_word;   /* [1] (may be NULL)   */
+} dvs_state;
+
+size_t dvs_step_workspace_bytes(const dvs_model* m, int32_t S, int32_t n_causal, int32_t n_mask,
+                                int32_t max_pages, int32_t chunk_keys);
+
+int draft_verify_step(const dvs_model* m, const dvs_state* st, int32_t n_causal, int32_t n_mask,
+                      int32_t chunk_keys, float* logits_out, int32_t* argmax_out,
+                      int32_t* accept_out, void* workspace, size_t ws_bytes, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

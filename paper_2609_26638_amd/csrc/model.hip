@@ -1,0 +1,372 @@
+// draft_verify_step: one fused self-speculative step of a decoder.
+//
+// Row inputs (Method "AR-to-Diffusion Conversion": the only architectural
+// addition is the embedding of the mask token [M]):
+//   causal rows r = 0..n_causal-1 : [x0, d_1, .., d_{n_causal-1}]
+//   mask rows                     : [M] (embedding row `vocab`)
+// then per layer: RMSNorm -> Q/K/V projections -> rotary positions at
+// kv_len + r -> attn_hybrid_block (appends the window's K/V) -> O projection
+// + residual -> [RMSNorm -> SwiGLU MLP + residual], final RMSNorm, LM head,
+// and the hot-path tail argmax_accept -> kv_commit.
+//
+// Every matrix product is C[m, n] = sum_k A[m, k] * W[n, k] with weights laid
+// out [out, in] so both MFMA operands are contiguous along k.  One wave owns
+// 32 output columns for ALL rows: it streams its weight rows exactly once, in
+// ascending k, and accumulates every 32-row group of A against them.  A row's
+// result therefore never depends on how many rows the call carries, so an AR
+// call (1 row) and a fused call (2B rows) produce bit-identical rows.
+#include <math.h>
+
+#include "dvs_common.h"
+
+namespace dvs {
+
+// ---------------------------------------------------------------------------
+// small element-wise kernels
+// ---------------------------------------------------------------------------
+template <typename T> __device__ __forceinline__ float to_f(T v);
+template <> __device__ __forceinline__ float to_f<float>(float v) { return v; }
+template <> __device__ __forceinline__ float to_f<__bf16>(__bf16 v) { return (float)v; }
+template <typename T> __device__ __forceinline__ T from_f(float v);
+template <> __device__ __forceinline__ float from_f<float>(float v) { return v; }
+template <> __device__ __forceinline__ __bf16 from_f<__bf16>(float v) { return (__bf16)v; }
+
+// x[m, :] = embed[token(m), :] (fp32 residual stream)
+template <typename T>
+__global__ void embed_rows_kernel(const T* __restrict__ embed, int H, int vocab, int R, int n_causal,
+                                  const int32_t* __restrict__ boundary,
+                                  const int32_t* __restrict__ draft, int draft_width,
+                                  float* __restrict__ x) {
+  const int mrow = blockIdx.x;
+  const int s = mrow / R, r = mrow - s * R;
+  int tok = vocab;  // [M]
+  if (r < n_causal) tok = (r == 0) ? boundary[s] : draft[(size_t)s * draft_width + (r - 1)];
+  if (tok < 0 || tok > vocab) tok = vocab;
+  const T* e = embed + (size_t)tok * H;
+  for (int i = threadIdx.x; i < H; i += blockDim.x) x[(size_t)mrow * H + i] = to_f(e[i]);
+}
+
+// out[m, :] = x[m, :] / sqrt(mean(x^2) + eps) * g   (one workgroup per row)
+template <typename T>
+__global__ void __launch_bounds__(256) rmsnorm_kernel(const float* __restrict__ x, const T* __restrict__ g,
+                                                      int H, float eps, T* __restrict__ out) {
+  __shared__ float red[4];
+  const int mrow = blockIdx.x;
+  const float* xr = x + (size_t)mrow * H;
+  float ss = 0.f;
+  for (int i = threadIdx.x; i < H; i += 256) ss = fmaf(xr[i], xr[i], ss);
+  for (int off = 32; off > 0; off >>= 1) ss += __shfl_xor(ss, off);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
+  __syncthreads();
+  const float tot = (red[0] + red[1]) + (red[2] + red[3]);
+  const float inv = 1.0f / sqrtf(tot / (float)H + eps);
+  for (int i = threadIdx.x; i < H; i += 256)
+    out[(size_t)mrow * H + i] = from_f<T>(xr[i] * inv * to_f(g[i]));
+}
+
+// rotate-half rotary embedding, in place, position kv_len[s] + r; angles in
+// double precision (positions reach thousands of radians).
+template <typename T>
+__global__ void rope_kernel(T* __restrict__ x, int M, int R, int nh, int D, double log2_theta,
+                            const int32_t* __restrict__ kv_len) {
+  const int half = D / 2;
+  const long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (long long)M * nh * half) return;
+  const int i = (int)(idx % half);
+  const long long mh = idx / half;
+  const int mrow = (int)(mh / nh);
+  const int s = mrow / R, r = mrow - s * R;
+  const double pos = (double)(kv_len[s] + r);
+  const double inv = exp2(-2.0 * i / D * log2_theta);
+  double sn, cs;
+  sincos(pos * inv, &sn, &cs);
+  T* v = x + mh * D;
+  const float x1 = to_f(v[i]), x2 = to_f(v[i + half]);
+  v[i] = from_f<T>((float)(x1 * cs - x2 * sn));
+  v[i + half] = from_f<T>((float)(x1 * sn + x2 * cs));
+}
+
+template <typename T>
+__global__ void silu_mul_kernel(const T* __restrict__ gate, const T* __restrict__ up, long long n,
+                                T* __restrict__ out) {
+  const long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  const float g = to_f(gate[i]);
+  out[i] = from_f<T>(g / (1.0f + expf(-g)) * to_f(up[i]));
+}
+
+// ---------------------------------------------------------------------------
+// GEMM: C[m, n] (=, or += into an fp32 residual) sum_k A[m, k] W[n, k]
+// One wave per 32 output columns; it walks k in ascending order, loading each
+// weight fragment once and applying it to every 32-row group of A (up to
+// MG_MAX groups, the rest in further passes).
+// ---------------------------------------------------------------------------
+constexpr int MG_MAX = 8;   // 32-row groups per pass (256 rows)
+
+// bf16: v_mfma_f32_32x32x16_bf16, A lane = row, W lane = column, 8 k each
+__global__ void __launch_bounds__(256) gemm_bf16_kernel(const __bf16* __restrict__ A,
+                                                        const __bf16* __restrict__ W, int M, int N,
+                                                        int K, void* __restrict__ C, int c_f32,
+                                                        int accumulate) {
+  float* __restrict__ Cf = c_f32 ? (float*)C : nullptr;
+  __bf16* __restrict__ Cb = c_f32 ? nullptr : (__bf16*)C;
+  const int lane = threadIdx.x & 63;
+  const int wave = blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6);
+  const int n0 = wave * 32;
+  if (n0 >= N) return;
+  const int l32 = lane & 31, hh = lane >> 5;
+  const int ncol = n0 + l32;
+  const bool nvalid = ncol < N;
+  const __bf16* wrow = W + (size_t)(nvalid ? ncol : n0) * K;
+  for (int m0 = 0; m0 < M; m0 += MG_MAX * 32) {
+    const int ng = min(MG_MAX, (M - m0 + 31) / 32);
+    f32x16 acc[MG_MAX];
+#pragma unroll
+    for (int g = 0; g < MG_MAX; ++g) acc[g] = f32x16{};
+    for (int k0 = 0; k0 < K; k0 += 16) {
+      const bf16x8 b = nvalid ? *(const bf16x8*)(wrow + k0 + hh * 8) : bf16x8{};
+#pragma unroll
+      for (int g = 0; g < MG_MAX; ++g) {
+        if (g < ng) {
+          const int mrow = m0 + g * 32 + l32;
+          const bf16x8 a = mrow < M ? *(const bf16x8*)(A + (size_t)mrow * K + k0 + hh * 8) : bf16x8{};
+          acc[g] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc[g], 0, 0, 0);
+        }
+      }
+    }
+    if (!nvalid) continue;
+#pragma unroll
+    for (int g = 0; g < MG_MAX; ++g) {
+      if (g >= ng) break;
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int mrow = m0 + g * 32 + 8 * (i >> 2) + 4 * hh + (i & 3);
+        if (mrow >= M) continue;
+        const size_t o = (size_t)mrow * N + ncol;
+        if (Cf) {
+          if (accumulate) Cf[o] += acc[g][i];
+          else Cf[o] = acc[g][i];
+        } else {
+          Cb[o] = (__bf16)acc[g][i];
+        }
+      }
+    }
+  }
+}
+
+// fp32: v_mfma_f32_32x32x2_f32; lane (row|col, hh) takes k = k0 + 4*hh + j in
+// MFMA j, so one 16-byte load per operand feeds 4 MFMAs.
+__global__ void __launch_bounds__(256) gemm_f32_kernel(const float* __restrict__ A,
+                                                       const float* __restrict__ W, int M, int N,
+                                                       int K, float* __restrict__ Cf, int accumulate) {
+  const int lane = threadIdx.x & 63;
+  const int wave = blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6);
+  const int n0 = wave * 32;
+  if (n0 >= N) return;
+  const int l32 = lane & 31, hh = lane >> 5;
+  const int ncol = n0 + l32;
+  const bool nvalid = ncol < N;
+  const float* wrow = W + (size_t)(nvalid ? ncol : n0) * K;
+  for (int m0 = 0; m0 < M; m0 += MG_MAX * 32) {
+    const int ng = min(MG_MAX, (M - m0 + 31) / 32);
+    f32x16 acc[MG_MAX];
+#pragma unroll
+    for (int g = 0; g < MG_MAX; ++g) acc[g] = f32x16{};
+    for (int k0 = 0; k0 < K; k0 += 8) {
+      const f32x4 b = nvalid ? *(const f32x4*)(wrow + k0 + hh * 4) : f32x4{};
+#pragma unroll
+      for (int g = 0; g < MG_MAX; ++g) {
+        if (g < ng) {
+          const int mrow = m0 + g * 32 + l32;
+          const f32x4 a = mrow < M ? *(const f32x4*)(A + (size_t)mrow * K + k0 + hh * 4) : f32x4{};
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            acc[g] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[j], b[j], acc[g], 0, 0, 0);
+        }
+      }
+    }
+    if (!nvalid) continue;
+#pragma unroll
+    for (int g = 0; g < MG_MAX; ++g) {
+      if (g >= ng) break;
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int mrow = m0 + g * 32 + 8 * (i >> 2) + 4 * hh + (i & 3);
+        if (mrow >= M) continue;
+        const size_t o = (size_t)mrow * N + ncol;
+        if (accumulate) Cf[o] += acc[g][i];
+        else Cf[o] = acc[g][i];
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// host orchestration
+// ---------------------------------------------------------------------------
+struct StepLayout {
+  size_t x, h, q, k, v, att, gate, up, act, logits, am, acc, attn_ws, total, attn_bytes;
+};
+
+static size_t al(size_t v) { return (v + 255) & ~(size_t)255; }
+
+static bool model_ok(const dvs_model* m) {
+  return m && (m->dtype == DVS_F32 || m->dtype == DVS_BF16) && m->n_layers >= 1 && m->vocab >= 1 &&
+         m->hidden >= 1 && m->n_kv_heads >= 1 && m->n_heads >= m->n_kv_heads &&
+         m->n_heads % m->n_kv_heads == 0 && m->embed && m->g_final && m->lm_head && m->layers &&
+         m->hidden % 16 == 0 && (m->ffn == 0 || m->ffn % 16 == 0);
+}
+
+static StepLayout step_layout(const dvs_model* m, int S, int n_causal, int n_mask, int max_pages,
+                              int chunk_keys) {
+  StepLayout L{};
+  const size_t M = (size_t)S * (n_causal + n_mask);
+  const size_t es = m->dtype == DVS_BF16 ? 2 : 4;
+  const size_t qd = (size_t)m->n_heads * m->head_dim, kd = (size_t)m->n_kv_heads * m->head_dim;
+  size_t off = 0;
+  L.x = off; off += al(M * m->hidden * 4);
+  L.h = off; off += al(M * m->hidden * es);
+  L.q = off; off += al(M * qd * es);
+  L.k = off; off += al(M * kd * es);
+  L.v = off; off += al(M * kd * es);
+  L.att = off; off += al(M * qd * es);
+  L.gate = off; off += al(M * (size_t)m->ffn * es);
+  L.up = off; off += al(M * (size_t)m->ffn * es);
+  L.act = off; off += al(M * (size_t)m->ffn * es);
+  L.logits = off; off += al(M * (size_t)m->vocab * 4);
+  L.am = off; off += al(M * 4);
+  L.acc = off; off += al((size_t)S * 4);
+  L.attn_bytes = dvs_attn_workspace_bytes(S, n_causal, n_mask, m->n_heads, m->n_kv_heads,
+                                          m->head_dim, max_pages, chunk_keys, m->dtype);
+  L.attn_ws = off; off += al(L.attn_bytes);
+  L.total = off;
+  return L;
+}
+
+// C = A W^T (or C += for the fp32 residual).  `c_f32` selects an fp32 output
+// for bf16 models (residual stream, logits); fp32 models always write fp32.
+static int gemm(int dtype, const void* A, const void* W, int M, int N, int K, void* C, int c_f32,
+                int accumulate, hipStream_t st) {
+  const int waves = (N + 31) / 32;
+  const int blocks = (waves + 3) / 4;
+  if (dtype == DVS_BF16)
+    hipLaunchKernelGGL(gemm_bf16_kernel, dim3(blocks), dim3(256), 0, st, (const __bf16*)A,
+                       (const __bf16*)W, M, N, K, C, c_f32, accumulate);
+  else
+    hipLaunchKernelGGL(gemm_f32_kernel, dim3(blocks), dim3(256), 0, st, (const float*)A,
+                       (const float*)W, M, N, K, (float*)C, accumulate);
+  return launch_status("draft_verify_step(gemm)");
+}
+
+template <typename T>
+static int run_step(const dvs_model* m, const dvs_state* st, int n_causal, int n_mask,
+                    int chunk_keys, const StepLayout& L, char* ws, float* logits_out,
+                    int32_t* argmax_out, int32_t* accept_out, hipStream_t stream) {
+  const int S = st->S, R = n_causal + n_mask, M = S * R;
+  const int H = m->hidden, D = m->head_dim, Hq = m->n_heads, Hkv = m->n_kv_heads;
+  const int dt = m->dtype;
+  float* x = (float*)(ws + L.x);
+  T* h = (T*)(ws + L.h);
+  T* q = (T*)(ws + L.q);
+  T* k = (T*)(ws + L.k);
+  T* v = (T*)(ws + L.v);
+  T* att = (T*)(ws + L.att);
+  T* gate = (T*)(ws + L.gate);
+  T* up = (T*)(ws + L.up);
+  T* act = (T*)(ws + L.act);
+  float* logits = logits_out ? logits_out : (float*)(ws + L.logits);
+  int32_t* am = argmax_out ? argmax_out : (int32_t*)(ws + L.am);
+  int32_t* acc = accept_out ? accept_out : (int32_t*)(ws + L.acc);
+  int rc;
+  const double log2_theta = log2((double)m->rope_theta);
+
+  hipLaunchKernelGGL(embed_rows_kernel<T>, dim3(M), dim3(256), 0, stream, (const T*)m->embed, H,
+                     m->vocab, R, n_causal, st->boundary, st->draft, st->draft_width, x);
+  if ((rc = launch_status("draft_verify_step(embed)"))) return rc;
+  for (int l = 0; l < m->n_layers; ++l) {
+    const dvs_layer& ly = m->layers[l];
+    hipLaunchKernelGGL(rmsnorm_kernel<T>, dim3(M), dim3(256), 0, stream, x, (const T*)ly.g_attn, H,
+                       m->rms_eps, h);
+    if ((rc = gemm(dt, h, ly.wq, M, Hq * D, H, q, 0, 0, stream))) return rc;
+    if ((rc = gemm(dt, h, ly.wk, M, Hkv * D, H, k, 0, 0, stream))) return rc;
+    if ((rc = gemm(dt, h, ly.wv, M, Hkv * D, H, v, 0, 0, stream))) return rc;
+    const long long nq = (long long)M * Hq * (D / 2), nk = (long long)M * Hkv * (D / 2);
+    hipLaunchKernelGGL(rope_kernel<T>, dim3((unsigned)((nq + 255) / 256)), dim3(256), 0, stream, q, M,
+                       R, Hq, D, log2_theta, st->kv_len);
+    hipLaunchKernelGGL(rope_kernel<T>, dim3((unsigned)((nk + 255) / 256)), dim3(256), 0, stream, k, M,
+                       R, Hkv, D, log2_theta, st->kv_len);
+    if ((rc = launch_status("draft_verify_step(rope)"))) return rc;
+    rc = attn_hybrid_block(q, k, v, ly.k_pool, ly.v_pool, st->page_table, st->kv_len, S, n_causal,
+                           n_mask, Hq, Hkv, D, st->max_pages, st->num_pool_pages,
+                           (float)(1.0 / sqrt((double)D)), dt, chunk_keys, att, st->err_word,
+                           ws + L.attn_ws, L.attn_bytes, stream);
+    if (rc) return rc;
+    if ((rc = gemm(dt, att, ly.wo, M, H, Hq * D, x, 1, 1, stream))) return rc;
+    if (m->ffn > 0) {
+      hipLaunchKernelGGL(rmsnorm_kernel<T>, dim3(M), dim3(256), 0, stream, x, (const T*)ly.g_mlp,
+                         H, m->rms_eps, h);
+      if ((rc = gemm(dt, h, ly.w_gate, M, m->ffn, H, gate, 0, 0, stream))) return rc;
+      if ((rc = gemm(dt, h, ly.w_up, M, m->ffn, H, up, 0, 0, stream))) return rc;
+      const long long n = (long long)M * m->ffn;
+      hipLaunchKernelGGL(silu_mul_kernel<T>, dim3((unsigned)((n + 255) / 256)), dim3(256), 0,
+                         stream, gate, up, n, act);
+      if ((rc = launch_status("draft_verify_step(silu)"))) return rc;
+      if ((rc = gemm(dt, act, ly.w_down, M, H, m->ffn, x, 1, 1, stream))) return rc;
+    }
+  }
+  hipLaunchKernelGGL(rmsnorm_kernel<T>, dim3(M), dim3(256), 0, stream, x, (const T*)m->g_final, H,
+                     m->rms_eps, h);
+  if ((rc = gemm(dt, h, m->lm_head, M, m->vocab, H, logits, 1, 0, stream))) return rc;
+  rc = argmax_accept(logits, DVS_F32, S, R, m->vocab, n_causal, st->draft, st->draft_width, am, acc,
+                     st->err_word, stream);
+  if (rc) return rc;
+  return kv_commit(S, n_causal, n_mask, acc, am, st->kv_len, st->page_table, st->num_pages,
+                   st->max_pages, st->free_stack, st->free_top, st->num_pool_pages, st->boundary,
+                   st->draft, st->draft_width, st->out_tokens, st->out_count, st->max_new, st->eos_id,
+                   st->finished, st->err_word, stream);
+}
+
+}  // namespace dvs
+
+using namespace dvs;
+
+extern "C" size_t dvs_step_workspace_bytes(const dvs_model* m, int32_t S, int32_t n_causal,
+                                           int32_t n_mask, int32_t max_pages, int32_t chunk_keys) {
+  if (!model_ok(m) || S < 1 || n_causal < 1 || n_mask < 0 || max_pages < 1) return 0;
+  return step_layout(m, S, n_causal, n_mask, max_pages, chunk_keys).total;
+}
+
+extern "C" int draft_verify_step(const dvs_model* m, const dvs_state* st, int32_t n_causal,
+                                 int32_t n_mask, int32_t chunk_keys, float* logits_out,
+                                 int32_t* argmax_out, int32_t* accept_out, void* workspace,
+                                 size_t ws_bytes, void* stream) {
+  clear_error();
+  DVS_CHECK_ARG(model_ok(m), "draft_verify_step: invalid model description");
+  DVS_CHECK_ARG(st && st->S >= 1 && st->kv_len && st->page_table && st->num_pages &&
+                    st->free_stack && st->free_top && st->boundary && st->out_tokens &&
+                    st->out_count && st->finished,
+                "draft_verify_step: invalid state description");
+  DVS_CHECK_ARG(n_causal >= 1 && n_mask >= 0, "draft_verify_step: need n_causal >= 1");
+  DVS_CHECK_ARG(st->draft_width >= n_causal - 1 && (st->draft || st->draft_width == 0),
+                "draft_verify_step: draft narrower than n_causal - 1");
+  for (int l = 0; l < m->n_layers; ++l) {
+    const dvs_layer& ly = m->layers[l];
+    DVS_CHECK_ARG(ly.wq && ly.wk && ly.wv && ly.wo && ly.g_attn && ly.k_pool && ly.v_pool,
+                  "draft_verify_step: layer %d incomplete", l);
+    DVS_CHECK_ARG(m->ffn == 0 || (ly.g_mlp && ly.w_gate && ly.w_up && ly.w_down),
+                  "draft_verify_step: layer %d MLP incomplete", l);
+  }
+  DVS_CHECK_SUPPORTED(m->head_dim == 64 || m->head_dim == 96 || m->head_dim == 128,
+                      "draft_verify_step: head_dim %d", m->head_dim);
+  const StepLayout L = step_layout(m, st->S, n_causal, n_mask, st->max_pages, chunk_keys);
+  if (!workspace || ws_bytes < L.total) {
+    set_error("draft_verify_step: workspace needs %zu bytes, got %zu", L.total, ws_bytes);
+    return DVS_EWORKSPACE;
+  }
+  hipStream_t s = (hipStream_t)stream;
+  if (m->dtype == DVS_BF16)
+    return run_step<__bf16>(m, st, n_causal, n_mask, chunk_keys, L, (char*)workspace, logits_out,
+                            argmax_out, accept_out, s);
+  return run_step<float>(m, st, n_causal, n_mask, chunk_keys, L, (char*)workspace, logits_out,
+                         argmax_out, accept_out, s);
+}

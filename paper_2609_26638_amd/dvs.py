@@ -40,6 +40,34 @@ _SIGS = {
                    _c_ptr, _c_ptr], _c_int),
 }
 
+class DvsLayer(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in ("wq", "wk", "wv", "wo", "g_attn", "g_mlp", "w_gate",
+                                                "w_up", "w_down", "k_pool", "v_pool")]
+
+
+class DvsModel(ctypes.Structure):
+    _fields_ = [("dtype", ctypes.c_int32), ("n_layers", ctypes.c_int32), ("vocab", ctypes.c_int32),
+                ("hidden", ctypes.c_int32), ("n_heads", ctypes.c_int32),
+                ("n_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("ffn", ctypes.c_int32), ("rope_theta", ctypes.c_float),
+                ("rms_eps", ctypes.c_float), ("embed", ctypes.c_void_p),
+                ("g_final", ctypes.c_void_p), ("lm_head", ctypes.c_void_p),
+                ("layers", ctypes.POINTER(DvsLayer))]
+
+
+class DvsState(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in ("S", "max_pages", "num_pool_pages", "draft_width",
+                                              "max_new", "eos_id")] + \
+               [(n, ctypes.c_void_p) for n in ("kv_len", "page_table", "num_pages", "free_stack",
+                                               "free_top", "boundary", "draft", "out_tokens",
+                                               "out_count", "finished", "err_word")]
+
+
+_SIGS["dvs_step_workspace_bytes"] = ([ctypes.POINTER(DvsModel), _c_int, _c_int, _c_int, _c_int,
+                                      _c_int], _c_size)
+_SIGS["draft_verify_step"] = ([ctypes.POINTER(DvsModel), ctypes.POINTER(DvsState), _c_int, _c_int,
+                               _c_int, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_size, _c_ptr], _c_int)
+
 EXPORTED = tuple(_SIGS)
 
 
@@ -251,3 +279,89 @@ def kv_commit(st: DeviceState, accept_len, argmax, n_causal: int, n_mask: int,
                          _ptr(st.out_tokens), _ptr(st.out_count), max_new, int(eos_id),
                          _ptr(st.finished), _ptr(st.err), _stream(stream))
     _check(rc, "kv_commit")
+
+
+# ---------------------------------------------------------------------------
+# whole-step decoder
+# ---------------------------------------------------------------------------
+
+def _to_dev_weight(a: np.ndarray, dtype: str, transpose: bool, device="cuda"):
+    """float32 host array -> device tensor in the model dtype (bf16 by RNE)."""
+    a = np.ascontiguousarray(a.T if transpose else a, dtype=np.float32)
+    if dtype == "bf16":
+        from . import synth
+        bits = synth.f32_to_bf16_bits(a)
+        return torch.from_numpy(bits.view(np.int16)).view(torch.bfloat16).to(device)
+    return torch.from_numpy(a).to(device)
+
+
+class DeviceModel:
+    """Decoder weights (uploaded as [out, in]) and per-layer KV pools on the
+    device, described to the library by a dvs_model struct."""
+
+    def __init__(self, w, k_pools, v_pools, dtype: str = "f32", device="cuda"):
+        self.dtype = dtype
+        tw = lambda a: _to_dev_weight(a, dtype, True, device)      # [in,out] -> [out,in]
+        tv = lambda a: _to_dev_weight(a, dtype, False, device)
+        self.embed = tv(w.embed)
+        self.g_final = tv(w.g_final)
+        self.lm_head = tw(w.lm_head)
+        self.keep = []
+        self.k_pools, self.v_pools = [], []
+        layers = (DvsLayer * w.n_layers)()
+        for l in range(w.n_layers):
+            kp = k_pools[l] if isinstance(k_pools[l], torch.Tensor) else tv(k_pools[l])
+            vp = v_pools[l] if isinstance(v_pools[l], torch.Tensor) else tv(v_pools[l])
+            self.k_pools.append(kp)
+            self.v_pools.append(vp)
+            t = dict(wq=tw(w.wq[l]), wk=tw(w.wk[l]), wv=tw(w.wv[l]), wo=tw(w.wo[l]),
+                     g_attn=tv(w.g_attn[l]))
+            if w.ffn:
+                t.update(g_mlp=tv(w.g_mlp[l]), w_gate=tw(w.w_gate[l]), w_up=tw(w.w_up[l]),
+                         w_down=tw(w.w_down[l]))
+            self.keep.append(t)
+            for n, v in t.items():
+                setattr(layers[l], n, v.data_ptr())
+            layers[l].k_pool = kp.data_ptr()
+            layers[l].v_pool = vp.data_ptr()
+        self.layers = layers
+        self.desc = DvsModel(DVS_BF16 if dtype == "bf16" else DVS_F32, w.n_layers, w.V, w.H, w.Hq,
+                             w.Hkv, w.D, w.ffn, float(w.rope_theta), float(w.eps),
+                             self.embed.data_ptr(), self.g_final.data_ptr(),
+                             self.lm_head.data_ptr(), layers)
+        self.V, self.H = w.V, w.H
+        self.ws = None
+
+    def workspace_bytes(self, S, n_causal, n_mask, max_pages, chunk_keys=0) -> int:
+        return int(lib().dvs_step_workspace_bytes(ctypes.byref(self.desc), S, n_causal, n_mask,
+                                                  max_pages, chunk_keys))
+
+
+def _state_desc(st: DeviceState, eos_id: int) -> DvsState:
+    S = st.kv_len.shape[0]
+    return DvsState(S, st.max_pages, st.pool_pages, st.draft.shape[1], st.out_tokens.shape[1],
+                    int(eos_id), st.kv_len.data_ptr(), st.page_table.data_ptr(),
+                    st.num_pages.data_ptr(), st.free_stack.data_ptr(), st.free_top.data_ptr(),
+                    st.boundary.data_ptr(), st.draft.data_ptr(), st.out_tokens.data_ptr(),
+                    st.out_count.data_ptr(), st.finished.data_ptr(), st.err.data_ptr())
+
+
+def draft_verify_step(model: DeviceModel, st: DeviceState, n_causal: int, n_mask: int,
+                      chunk_keys: int = 0, eos_id: int = -1, logits_out=None, argmax_out=None,
+                      accept_out=None, stream=None):
+    """One fused step (or an AR step with n_causal=1, n_mask=0) on the device."""
+    S = st.kv_len.shape[0]
+    need = model.workspace_bytes(S, n_causal, n_mask, st.max_pages, chunk_keys)
+    if need == 0:
+        raise DvsError("draft_verify_step: invalid configuration")
+    if model.ws is None or model.ws.nbytes < need:
+        model.ws = Workspace(need, device=st.kv_len.device)
+    for t, name in ((logits_out, "logits_out"), (argmax_out, "argmax_out"), (accept_out, "accept_out")):
+        if t is not None:
+            _dev(t, torch.float32 if name == "logits_out" else torch.int32, name)
+    sd = _state_desc(st, eos_id)
+    rc = lib().draft_verify_step(ctypes.byref(model.desc), ctypes.byref(sd), n_causal, n_mask,
+                                 int(chunk_keys), _ptr(logits_out), _ptr(argmax_out),
+                                 _ptr(accept_out), _ptr(model.ws.buf), model.ws.nbytes,
+                                 _stream(stream))
+    _check(rc, "draft_verify_step")
