@@ -31,8 +31,9 @@
  *     exhaustion, non-finite logits, ...) OR a DVS_ERR_* bit into the
  *     caller's int32 `err_word` (device memory, never cleared by the
  *     library); the affected sequences are left unmodified.
- *   - Page size is fixed at 16 tokens.  KV pools are laid out
- *     [num_pool_pages, Hkv, 16, D]; logical position p of sequence s lives in
+ *   - Page size is fixed at 16 tokens.  K pools are laid out
+ *     [num_pool_pages, Hkv, 16, D] and V pools head-dim-major
+ *     [num_pool_pages, Hkv, D, 16]; logical position p of sequence s lives in
  *     page page_table[s * max_pages + p / 16], slot p % 16.
  *   - dtype: DVS_F32 (float) or DVS_BF16 (bfloat16 storage, fp32 accumulate).
  */
@@ -84,7 +85,8 @@ const char* dvs_last_error(void);
  *   q       [S, R, Hq, D]     window queries (after any position encoding)
  *   k_new   [S, R, Hkv, D]    window keys, written to positions [L, L+R)
  *   v_new   [S, R, Hkv, D]    window values, written likewise
- *   k_pool, v_pool [num_pool_pages, Hkv, 16, D]  paged cache (updated)
+ *   k_pool  [num_pool_pages, Hkv, 16, D]  paged K cache (updated)
+ *   v_pool  [num_pool_pages, Hkv, D, 16]  paged V cache, head-dim-major (updated)
  *   page_table [S, max_pages] int32, kv_len [S] int32 (read only)
  *   out     [S, R, Hq, D]     attention output, same dtype as q
  *   chunk_keys   key-range split per workgroup (multiple of 64; 0 = auto).
@@ -93,10 +95,11 @@ const char* dvs_last_error(void);
  *   err_word     int32 device word (may be NULL): DVS_ERR_MAX_PAGES if
  *                L + R > max_pages * 16, DVS_ERR_BAD_PAGE for a page id
  *                outside the pool; such sequences are skipped.
- *   workspace    >= dvs_attn_workspace_bytes(...) bytes of device memory.
- *                Its first 4 * S * Hkv * ceil(R*Hq/Hkv / 256) bytes are
- *                counters that must be zero before the first call (e.g.
- *                cleared once at allocation); every call leaves them zero.
+ *   workspace    >= dvs_attn_workspace_bytes(...) bytes of device memory,
+ *                zero-filled before its first call with a given shape (S, R,
+ *                heads, D, max_pages, chunk_keys); its leading bytes are
+ *                split-merge counters that every call leaves zero again, so
+ *                later calls of the same shape need no clearing.
  *                Calls that share a workspace must not overlap in time.
  * Requirements: Hq % Hkv == 0, D in {64, 96, 128}, R >= 1, S >= 1, all
  * pointers non-NULL (except err_word), softmax_scale > 0.
@@ -196,7 +199,8 @@ int kv_commit(int32_t S, int32_t n_causal, int32_t n_mask, const int32_t* accept
  *
  * logits_out [S*R, vocab] float, argmax_out [S*R], accept_out [S] int32 are
  * optional (NULL = kept in the workspace).  workspace: at least
- * dvs_step_workspace_bytes() bytes, zero-filled before its first use.
+ * dvs_step_workspace_bytes() bytes; no initialisation needed (the call clears
+ * what must start at zero), and it may be shared with dvs_prefill.
  * ---------------------------------------------------------------------- */
 typedef struct dvs_layer {
   const void* wq;      /* [n_heads*head_dim, hidden]        */
@@ -243,6 +247,29 @@ size_t dvs_step_workspace_bytes(const dvs_model* m, int32_t S, int32_t n_causal,
 int draft_verify_step(const dvs_model* m, const dvs_state* st, int32_t n_causal, int32_t n_mask,
                       int32_t chunk_keys, float* logits_out, int32_t* argmax_out,
                       int32_t* accept_out, void* workspace, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * dvs_prefill
+ *
+ * Prefill of a fresh sequence (appendix item State: the first boundary token
+ * is produced by prefill).  The window is the P prefix rows (causal) followed
+ * by n_mask mask rows (bidirectional block), at positions 0 .. P+n_mask-1, so
+ * the prefix KV is cached and the mask rows give the first draft:
+ *   row r < P takes embed[prefix_tokens[s, r]] when that id is in
+ *   [0, vocab) and x_prefix[s, r, :] otherwise (e.g. vision-encoder outputs;
+ *   fp32, [S, P, hidden]); either array may be NULL when unused.
+ * Afterwards kv_len = P, boundary = top-1 of row P-1 (also appended to the
+ * output as the first committed token), draft[j] = top-1 of mask row j.
+ * kv_len must be 0 on entry and every sequence must already hold pages for
+ * positions [0, P + max(n_mask, R of the next step)).  logits_out (optional)
+ * receives [S, n_mask + 1, vocab] fp32 for rows P-1 .. P+n_mask-1.
+ * ---------------------------------------------------------------------- */
+size_t dvs_prefill_workspace_bytes(const dvs_model* m, int32_t S, int32_t P, int32_t n_mask,
+                                   int32_t max_pages, int32_t chunk_keys);
+
+int dvs_prefill(const dvs_model* m, const dvs_state* st, int32_t P, int32_t n_mask,
+                const int32_t* prefix_tokens, const float* x_prefix, int32_t chunk_keys,
+                float* logits_out, void* workspace, size_t ws_bytes, void* stream);
 
 #ifdef __cplusplus
 }

@@ -790,6 +790,13 @@ static void launch_bf16(const AttnPlan& pl, const AttnParams& prm, hipStream_t s
   }
 }
 
+size_t attn_counter_bytes(int S, int R, int Hq, int Hkv, int D, int max_pages, int chunk_keys,
+                          int dtype) {
+  if (dtype != DVS_BF16) return 0;
+  const AttnPlan pl = plan_attn(S, R, Hq, Hkv, D, max_pages, chunk_keys, dtype);
+  return pl.off_ml - pl.off_counters;
+}
+
 }  // namespace dvs
 
 using namespace dvs;

@@ -31,6 +31,11 @@ void clear_error();
 // Launch status after hipLaunchKernelGGL.
 int launch_status(const char* what);
 
+// Bytes at the start of an attention workspace that hold the split-merge
+// counters (zero between calls) for the given call shape.
+size_t attn_counter_bytes(int S, int R, int Hq, int Hkv, int D, int max_pages, int chunk_keys,
+                          int dtype);
+
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));

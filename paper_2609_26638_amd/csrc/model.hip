@@ -86,6 +86,61 @@ __global__ void rope_kernel(T* __restrict__ x, int M, int R, int nh, int D, doub
   v[i + half] = from_f<T>((float)(x1 * sn + x2 * cs));
 }
 
+// Prefill rows: row r < P of sequence s takes embed[tokens[s, r]] when that
+// id is >= 0 and otherwise the given vector x_prefix[s, r, :] (e.g. a vision
+// encoder output); rows r >= P are mask tokens.
+template <typename T>
+__global__ void embed_prefill_kernel(const T* __restrict__ embed, int H, int vocab, int R, int P,
+                                     const int32_t* __restrict__ tokens,
+                                     const float* __restrict__ x_prefix, float* __restrict__ x) {
+  const int mrow = blockIdx.x;
+  const int s = mrow / R, r = mrow - s * R;
+  int tok = vocab;
+  const float* src = nullptr;
+  if (r < P) {
+    tok = tokens ? tokens[(size_t)s * P + r] : -1;
+    if (tok < 0 || tok >= vocab) {
+      tok = -1;
+      if (x_prefix) src = x_prefix + ((size_t)s * P + r) * H;
+      else tok = vocab;
+    }
+  }
+  for (int i = threadIdx.x; i < H; i += blockDim.x)
+    x[(size_t)mrow * H + i] = src ? src[i] : to_f(embed[(size_t)tok * H + i]);
+}
+
+// dst[s*n + j, :] = src[s*R + r0 + j, :]  (rows whose logits are needed)
+template <typename T>
+__global__ void gather_rows_kernel(const T* __restrict__ src, int H, int R, int r0, int n,
+                                   T* __restrict__ dst) {
+  const int row = blockIdx.x;
+  const int s = row / n, j = row - s * n;
+  const T* a = src + ((size_t)s * R + r0 + j) * H;
+  for (int i = threadIdx.x; i < H; i += blockDim.x) dst[(size_t)row * H + i] = a[i];
+}
+
+// After a prefill of P rows: kv_len = P, the top-1 of row P-1 is the first
+// committed token and boundary, the mask rows' top-1 tokens the first draft.
+// am holds per sequence the top-1 of rows P-1 .. P+n_mask-1.
+__global__ void prefill_commit_kernel(int S, int P, int n_mask, const int32_t* __restrict__ am,
+                                      int32_t* kv_len, int32_t* boundary, int32_t* draft,
+                                      int draft_width, int32_t* out_tokens, int32_t* out_count,
+                                      int max_new, int eos_id, int32_t* finished) {
+  const int s = blockIdx.x * blockDim.x + threadIdx.x;
+  if (s >= S) return;
+  const int n = n_mask + 1;
+  const int first = am[(size_t)s * n];
+  kv_len[s] = P;
+  boundary[s] = first;
+  for (int j = 0; j < draft_width && j < n_mask; ++j) draft[(size_t)s * draft_width + j] = am[(size_t)s * n + 1 + j];
+  const int c = out_count[s];
+  if (c < max_new) {
+    out_tokens[(size_t)s * max_new + c] = first;
+    out_count[s] = c + 1;
+  }
+  finished[s] = ((eos_id >= 0 && first == eos_id) || c + 1 >= max_new) ? 1 : 0;
+}
+
 template <typename T>
 __global__ void silu_mul_kernel(const T* __restrict__ gate, const T* __restrict__ up, long long n,
                                 T* __restrict__ out) {
@@ -205,8 +260,14 @@ __global__ void __launch_bounds__(256) gemm_f32_kernel(const float* __restrict__
 // host orchestration
 // ---------------------------------------------------------------------------
 struct StepLayout {
-  size_t x, h, q, k, v, att, gate, up, act, logits, am, acc, attn_ws, total, attn_bytes;
+  size_t x, h, hsel, q, k, v, att, gate, up, act, logits, am, acc, attn_ws, total, attn_bytes,
+      attn_counters;
 };
+
+__global__ void zero_words_kernel(int32_t* __restrict__ p, int n) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = 0;
+}
 
 static size_t al(size_t v) { return (v + 255) & ~(size_t)255; }
 
@@ -217,8 +278,10 @@ static bool model_ok(const dvs_model* m) {
          m->hidden % 16 == 0 && (m->ffn == 0 || m->ffn % 16 == 0);
 }
 
+// logit_rows: rows that get LM-head logits (every window row for a step;
+// the last prefix row and the mask rows for a prefill)
 static StepLayout step_layout(const dvs_model* m, int S, int n_causal, int n_mask, int max_pages,
-                              int chunk_keys) {
+                              int chunk_keys, size_t logit_rows) {
   StepLayout L{};
   const size_t M = (size_t)S * (n_causal + n_mask);
   const size_t es = m->dtype == DVS_BF16 ? 2 : 4;
@@ -226,6 +289,7 @@ static StepLayout step_layout(const dvs_model* m, int S, int n_causal, int n_mas
   size_t off = 0;
   L.x = off; off += al(M * m->hidden * 4);
   L.h = off; off += al(M * m->hidden * es);
+  L.hsel = off; off += al(logit_rows * m->hidden * es);
   L.q = off; off += al(M * qd * es);
   L.k = off; off += al(M * kd * es);
   L.v = off; off += al(M * kd * es);
@@ -233,11 +297,13 @@ static StepLayout step_layout(const dvs_model* m, int S, int n_causal, int n_mas
   L.gate = off; off += al(M * (size_t)m->ffn * es);
   L.up = off; off += al(M * (size_t)m->ffn * es);
   L.act = off; off += al(M * (size_t)m->ffn * es);
-  L.logits = off; off += al(M * (size_t)m->vocab * 4);
-  L.am = off; off += al(M * 4);
+  L.logits = off; off += al(logit_rows * (size_t)m->vocab * 4);
+  L.am = off; off += al(logit_rows * 4);
   L.acc = off; off += al((size_t)S * 4);
   L.attn_bytes = dvs_attn_workspace_bytes(S, n_causal, n_mask, m->n_heads, m->n_kv_heads,
                                           m->head_dim, max_pages, chunk_keys, m->dtype);
+  L.attn_counters = attn_counter_bytes(S, n_causal + n_mask, m->n_heads, m->n_kv_heads,
+                                       m->head_dim, max_pages, chunk_keys, m->dtype);
   L.attn_ws = off; off += al(L.attn_bytes);
   L.total = off;
   return L;
@@ -258,10 +324,11 @@ static int gemm(int dtype, const void* A, const void* W, int M, int N, int K, vo
   return launch_status("draft_verify_step(gemm)");
 }
 
+// The decoder stack on the rows in x (fp32, [M, hidden]); leaves the final
+// RMSNorm output in h.  The window is (n_causal, n_mask) rows per sequence.
 template <typename T>
-static int run_step(const dvs_model* m, const dvs_state* st, int n_causal, int n_mask,
-                    int chunk_keys, const StepLayout& L, char* ws, float* logits_out,
-                    int32_t* argmax_out, int32_t* accept_out, hipStream_t stream) {
+static int forward_layers(const dvs_model* m, const dvs_state* st, int n_causal, int n_mask,
+                          int chunk_keys, const StepLayout& L, char* ws, hipStream_t stream) {
   const int S = st->S, R = n_causal + n_mask, M = S * R;
   const int H = m->hidden, D = m->head_dim, Hq = m->n_heads, Hkv = m->n_kv_heads;
   const int dt = m->dtype;
@@ -274,15 +341,16 @@ static int run_step(const dvs_model* m, const dvs_state* st, int n_causal, int n
   T* gate = (T*)(ws + L.gate);
   T* up = (T*)(ws + L.up);
   T* act = (T*)(ws + L.act);
-  float* logits = logits_out ? logits_out : (float*)(ws + L.logits);
-  int32_t* am = argmax_out ? argmax_out : (int32_t*)(ws + L.am);
-  int32_t* acc = accept_out ? accept_out : (int32_t*)(ws + L.acc);
   int rc;
+  // The workspace may carry another call shape's data where this shape keeps
+  // the attention's split counters: clear them once; every attention call
+  // leaves them zero for the next layer.
+  if (L.attn_counters) {
+    const int nw = (int)(L.attn_counters / 4);
+    hipLaunchKernelGGL(zero_words_kernel, dim3((nw + 255) / 256), dim3(256), 0, stream,
+                       (int32_t*)(ws + L.attn_ws), nw);
+  }
   const double log2_theta = log2((double)m->rope_theta);
-
-  hipLaunchKernelGGL(embed_rows_kernel<T>, dim3(M), dim3(256), 0, stream, (const T*)m->embed, H,
-                     m->vocab, R, n_causal, st->boundary, st->draft, st->draft_width, x);
-  if ((rc = launch_status("draft_verify_step(embed)"))) return rc;
   for (int l = 0; l < m->n_layers; ++l) {
     const dvs_layer& ly = m->layers[l];
     hipLaunchKernelGGL(rmsnorm_kernel<T>, dim3(M), dim3(256), 0, stream, x, (const T*)ly.g_attn, H,
@@ -316,7 +384,25 @@ static int run_step(const dvs_model* m, const dvs_state* st, int n_causal, int n
   }
   hipLaunchKernelGGL(rmsnorm_kernel<T>, dim3(M), dim3(256), 0, stream, x, (const T*)m->g_final, H,
                      m->rms_eps, h);
-  if ((rc = gemm(dt, h, m->lm_head, M, m->vocab, H, logits, 1, 0, stream))) return rc;
+  return launch_status("draft_verify_step(final norm)");
+}
+
+template <typename T>
+static int run_step(const dvs_model* m, const dvs_state* st, int n_causal, int n_mask,
+                    int chunk_keys, const StepLayout& L, char* ws, float* logits_out,
+                    int32_t* argmax_out, int32_t* accept_out, hipStream_t stream) {
+  const int S = st->S, R = n_causal + n_mask, M = S * R;
+  float* logits = logits_out ? logits_out : (float*)(ws + L.logits);
+  int32_t* am = argmax_out ? argmax_out : (int32_t*)(ws + L.am);
+  int32_t* acc = accept_out ? accept_out : (int32_t*)(ws + L.acc);
+  hipLaunchKernelGGL(embed_rows_kernel<T>, dim3(M), dim3(256), 0, stream, (const T*)m->embed,
+                     m->hidden, m->vocab, R, n_causal, st->boundary, st->draft, st->draft_width,
+                     (float*)(ws + L.x));
+  int rc;
+  if ((rc = launch_status("draft_verify_step(embed)"))) return rc;
+  if ((rc = forward_layers<T>(m, st, n_causal, n_mask, chunk_keys, L, ws, stream))) return rc;
+  if ((rc = gemm(m->dtype, ws + L.h, m->lm_head, M, m->vocab, m->hidden, logits, 1, 0, stream)))
+    return rc;
   rc = argmax_accept(logits, DVS_F32, S, R, m->vocab, n_causal, st->draft, st->draft_width, am, acc,
                      st->err_word, stream);
   if (rc) return rc;
@@ -326,6 +412,33 @@ static int run_step(const dvs_model* m, const dvs_state* st, int n_causal, int n
                    st->finished, st->err_word, stream);
 }
 
+template <typename T>
+static int run_prefill(const dvs_model* m, const dvs_state* st, int P, int n_mask,
+                       const int32_t* tokens, const float* x_prefix, int chunk_keys,
+                       const StepLayout& L, char* ws, float* logits_out, hipStream_t stream) {
+  const int S = st->S, R = P + n_mask, M = S * R, nsel = n_mask + 1;
+  hipLaunchKernelGGL(embed_prefill_kernel<T>, dim3(M), dim3(256), 0, stream, (const T*)m->embed,
+                     m->hidden, m->vocab, R, P, tokens, x_prefix, (float*)(ws + L.x));
+  int rc;
+  if ((rc = launch_status("dvs_prefill(embed)"))) return rc;
+  if ((rc = forward_layers<T>(m, st, P, n_mask, chunk_keys, L, ws, stream))) return rc;
+  // LM head only for rows P-1 .. P+n_mask-1 (the first token and the draft)
+  T* hsel = (T*)(ws + L.hsel);
+  hipLaunchKernelGGL(gather_rows_kernel<T>, dim3(S * nsel), dim3(256), 0, stream,
+                     (const T*)(ws + L.h), m->hidden, R, P - 1, nsel, hsel);
+  float* logits = logits_out ? logits_out : (float*)(ws + L.logits);
+  if ((rc = gemm(m->dtype, hsel, m->lm_head, S * nsel, m->vocab, m->hidden, logits, 1, 0, stream)))
+    return rc;
+  int32_t* am = (int32_t*)(ws + L.am);
+  int32_t* acc = (int32_t*)(ws + L.acc);
+  rc = argmax_accept(logits, DVS_F32, S, nsel, m->vocab, 1, nullptr, 0, am, acc, st->err_word, stream);
+  if (rc) return rc;
+  hipLaunchKernelGGL(prefill_commit_kernel, dim3((S + 255) / 256), dim3(256), 0, stream, S, P,
+                     n_mask, am, st->kv_len, st->boundary, st->draft, st->draft_width,
+                     st->out_tokens, st->out_count, st->max_new, st->eos_id, st->finished);
+  return launch_status("dvs_prefill(commit)");
+}
+
 }  // namespace dvs
 
 using namespace dvs;
@@ -333,7 +446,8 @@ using namespace dvs;
 extern "C" size_t dvs_step_workspace_bytes(const dvs_model* m, int32_t S, int32_t n_causal,
                                            int32_t n_mask, int32_t max_pages, int32_t chunk_keys) {
   if (!model_ok(m) || S < 1 || n_causal < 1 || n_mask < 0 || max_pages < 1) return 0;
-  return step_layout(m, S, n_causal, n_mask, max_pages, chunk_keys).total;
+  return step_layout(m, S, n_causal, n_mask, max_pages, chunk_keys,
+                     (size_t)S * (n_causal + n_mask)).total;
 }
 
 extern "C" int draft_verify_step(const dvs_model* m, const dvs_state* st, int32_t n_causal,
@@ -358,7 +472,8 @@ extern "C" int draft_verify_step(const dvs_model* m, const dvs_state* st, int32_
   }
   DVS_CHECK_SUPPORTED(m->head_dim == 64 || m->head_dim == 96 || m->head_dim == 128,
                       "draft_verify_step: head_dim %d", m->head_dim);
-  const StepLayout L = step_layout(m, st->S, n_causal, n_mask, st->max_pages, chunk_keys);
+  const StepLayout L = step_layout(m, st->S, n_causal, n_mask, st->max_pages, chunk_keys,
+                                   (size_t)st->S * (n_causal + n_mask));
   if (!workspace || ws_bytes < L.total) {
     set_error("draft_verify_step: workspace needs %zu bytes, got %zu", L.total, ws_bytes);
     return DVS_EWORKSPACE;
@@ -369,4 +484,40 @@ extern "C" int draft_verify_step(const dvs_model* m, const dvs_state* st, int32_
                             argmax_out, accept_out, s);
   return run_step<float>(m, st, n_causal, n_mask, chunk_keys, L, (char*)workspace, logits_out,
                          argmax_out, accept_out, s);
+}
+
+extern "C" size_t dvs_prefill_workspace_bytes(const dvs_model* m, int32_t S, int32_t P,
+                                              int32_t n_mask, int32_t max_pages,
+                                              int32_t chunk_keys) {
+  if (!model_ok(m) || S < 1 || P < 1 || n_mask < 0 || max_pages < 1) return 0;
+  return step_layout(m, S, P, n_mask, max_pages, chunk_keys, (size_t)S * (n_mask + 1)).total;
+}
+
+extern "C" int dvs_prefill(const dvs_model* m, const dvs_state* st, int32_t P, int32_t n_mask,
+                           const int32_t* prefix_tokens, const float* x_prefix, int32_t chunk_keys,
+                           float* logits_out, void* workspace, size_t ws_bytes, void* stream) {
+  clear_error();
+  DVS_CHECK_ARG(model_ok(m), "dvs_prefill: invalid model description");
+  DVS_CHECK_ARG(st && st->S >= 1 && st->kv_len && st->page_table && st->boundary &&
+                    st->out_tokens && st->out_count && st->finished,
+                "dvs_prefill: invalid state description");
+  DVS_CHECK_ARG(P >= 1 && n_mask >= 0, "dvs_prefill: need P >= 1, n_mask >= 0");
+  DVS_CHECK_ARG(prefix_tokens || x_prefix, "dvs_prefill: no prefix inputs");
+  DVS_CHECK_ARG(n_mask >= st->draft_width && (st->draft || st->draft_width == 0),
+                "dvs_prefill: mask rows (%d) must cover the draft width (%d)", n_mask,
+                st->draft_width);
+  DVS_CHECK_SUPPORTED(m->head_dim == 64 || m->head_dim == 96 || m->head_dim == 128,
+                      "dvs_prefill: head_dim %d", m->head_dim);
+  const StepLayout L = step_layout(m, st->S, P, n_mask, st->max_pages, chunk_keys,
+                                   (size_t)st->S * (n_mask + 1));
+  if (!workspace || ws_bytes < L.total) {
+    set_error("dvs_prefill: workspace needs %zu bytes, got %zu", L.total, ws_bytes);
+    return DVS_EWORKSPACE;
+  }
+  hipStream_t s = (hipStream_t)stream;
+  if (m->dtype == DVS_BF16)
+    return run_prefill<__bf16>(m, st, P, n_mask, prefix_tokens, x_prefix, chunk_keys, L,
+                               (char*)workspace, logits_out, s);
+  return run_prefill<float>(m, st, P, n_mask, prefix_tokens, x_prefix, chunk_keys, L,
+                            (char*)workspace, logits_out, s);
 }

@@ -68,6 +68,11 @@ _SIGS["dvs_step_workspace_bytes"] = ([ctypes.POINTER(DvsModel), _c_int, _c_int, 
 _SIGS["draft_verify_step"] = ([ctypes.POINTER(DvsModel), ctypes.POINTER(DvsState), _c_int, _c_int,
                                _c_int, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_size, _c_ptr], _c_int)
 
+_SIGS["dvs_prefill_workspace_bytes"] = ([ctypes.POINTER(DvsModel), _c_int, _c_int, _c_int, _c_int,
+                                         _c_int], _c_size)
+_SIGS["dvs_prefill"] = ([ctypes.POINTER(DvsModel), ctypes.POINTER(DvsState), _c_int, _c_int, _c_ptr,
+                         _c_ptr, _c_int, _c_ptr, _c_ptr, _c_size, _c_ptr], _c_int)
+
 EXPORTED = tuple(_SIGS)
 
 
@@ -137,11 +142,21 @@ def attn_workspace_bytes(S, n_causal, n_mask, Hq, Hkv, D, max_pages, chunk_keys=
 
 
 class Workspace:
-    """Zero-initialised device scratch for attn_hybrid_block (counters must
-    start at zero; every call leaves them zero)."""
+    """Zero-initialised device scratch.  attn_hybrid_block keeps split-merge
+    counters at its start, which must be zero when a call shape first uses
+    it and which every call leaves zero; `shape` remembers the last shape so
+    a change of shape clears the buffer again."""
 
     def __init__(self, nbytes: int, device="cuda"):
         self.buf = torch.zeros(max(int(nbytes), 256), dtype=torch.uint8, device=device)
+        self.shape = None
+
+    def prepare(self, nbytes: int, shape):
+        self.ensure(nbytes)
+        if shape != self.shape:
+            self.buf.zero_()
+            self.shape = shape
+        return self
 
     @property
     def nbytes(self):
@@ -150,6 +165,7 @@ class Workspace:
     def ensure(self, nbytes: int):
         if nbytes > self.nbytes:
             self.buf = torch.zeros(int(nbytes), dtype=torch.uint8, device=self.buf.device)
+            self.shape = None
         return self
 
 
@@ -187,7 +203,7 @@ def attn_hybrid_block(q, k_new, v_new, k_pool, v_pool, page_table, kv_len, n_cau
     need = attn_workspace_bytes(S, n_causal, n_mask, Hq, Hkv, D, max_pages, chunk_keys, code)
     if workspace is None:
         workspace = Workspace(need, device=q.device)
-    workspace.ensure(need)
+    workspace.prepare(need, ("attn", S, R, Hq, Hkv, D, max_pages, int(chunk_keys), code))
     rc = lib().attn_hybrid_block(_ptr(q), _ptr(k_new), _ptr(v_new), _ptr(k_pool), _ptr(v_pool),
                                  _ptr(page_table), _ptr(kv_len), S, n_causal, n_mask, Hq, Hkv, D,
                                  max_pages, P, float(softmax_scale), code, int(chunk_keys),
@@ -365,3 +381,25 @@ def draft_verify_step(model: DeviceModel, st: DeviceState, n_causal: int, n_mask
                                  _ptr(accept_out), _ptr(model.ws.buf), model.ws.nbytes,
                                  _stream(stream))
     _check(rc, "draft_verify_step")
+
+
+def prefill(model: DeviceModel, st: DeviceState, P: int, n_mask: int, prefix_tokens=None,
+            x_prefix=None, chunk_keys: int = 0, eos_id: int = -1, logits_out=None, stream=None):
+    """Prefill P prefix rows (token ids and/or given fp32 embeddings) plus
+    n_mask mask rows; sets kv_len, boundary, first draft and first token."""
+    S = st.kv_len.shape[0]
+    if prefix_tokens is not None:
+        _dev(prefix_tokens, torch.int32, "prefix_tokens", 2)
+    if x_prefix is not None:
+        _dev(x_prefix, torch.float32, "x_prefix", 3)
+    need = int(lib().dvs_prefill_workspace_bytes(ctypes.byref(model.desc), S, P, n_mask,
+                                                 st.max_pages, chunk_keys))
+    if need == 0:
+        raise DvsError("dvs_prefill: invalid configuration")
+    if model.ws is None or model.ws.nbytes < need:
+        model.ws = Workspace(need, device=st.kv_len.device)
+    sd = _state_desc(st, eos_id)
+    rc = lib().dvs_prefill(ctypes.byref(model.desc), ctypes.byref(sd), P, n_mask,
+                           _ptr(prefix_tokens), _ptr(x_prefix), int(chunk_keys), _ptr(logits_out),
+                           _ptr(model.ws.buf), model.ws.nbytes, _stream(stream))
+    _check(rc, "dvs_prefill")

@@ -392,3 +392,52 @@ def long_document_inputs(seed: int = 4, S: int = 64, kv=(4096, 16384), B: int = 
     li = make_logit_inputs(seed, S, B, B, V, 4.0, match_p)
     ai.state.draft[:] = li.draft
     return ai, li
+
+
+@dataclasses.dataclass
+class StackInputs:
+    weights: ModelWeights
+    vision: np.ndarray        # [S, n_vision, H] float32 ~N(0, 1)
+    prompt: np.ndarray        # [S, n_prompt] int32 uniform over the vocabulary
+    state: PagedState         # kv_len = 0, pages for the prefill window and growth
+    B: int
+    max_new: int
+
+    @property
+    def P(self) -> int:
+        return self.vision.shape[1] + self.prompt.shape[1]
+
+    def prefix_tokens(self) -> np.ndarray:
+        """[S, P] ids: -1 for the vision rows (take the given vectors), then the prompt."""
+        S = self.vision.shape[0]
+        ids = np.full((S, self.P), -1, dtype=np.int32)
+        ids[:, self.vision.shape[1]:] = self.prompt
+        return ids
+
+    def x_prefix(self) -> np.ndarray:
+        """[S, P, H] float32: the vision vectors, zeros for the prompt rows."""
+        S, nv, H = self.vision.shape
+        x = np.zeros((S, self.P, H), dtype=np.float32)
+        x[:, :nv] = self.vision
+        return x
+
+
+def decoder_stack_inputs(seed: int = 3, S: int = 8, n_layers: int = 16, H: int = 1536,
+                         Hq: int = 16, Hkv: int = 4, D: int = 96, ffn: int = 4096, V: int = 65536,
+                         n_vision: int = 1024, n_prompt: int = 64, B: int = 16,
+                         max_new: int = 1024) -> StackInputs:
+    """Random-init decoder stack (weights N(0, 0.02)), a prefix of synthetic
+    vision embeddings N(0, 1) plus uniform prompt tokens, block size B."""
+    w = make_model_weights(seed, V, H, Hq, Hkv, D, n_layers, ffn, std=0.02)
+    ss = np.random.SeedSequence([seed, 0x5AC4])
+    r_vis, r_prompt, r_pages = [np.random.Generator(np.random.PCG64(c)) for c in ss.spawn(3)]
+    vision = _normal(r_vis, (S, n_vision, H), 1.0)
+    prompt = r_prompt.integers(0, V, size=(S, n_prompt)).astype(np.int32)
+    P = n_vision + n_prompt
+    R = 2 * B
+    max_pages = (P + max_new + R + PAGE_SIZE - 1) // PAGE_SIZE + 2
+    growth = S * ((max_new + R + PAGE_SIZE - 1) // PAGE_SIZE + 2)
+    st = make_paged_state(r_pages, np.full(S, P, dtype=np.int64), R, max_pages, scatter=True,
+                          slack=0.0, extra_pages=growth, n_causal=B, max_new=max_new)
+    st.kv_len[:] = 0
+    return StackInputs(weights=w, vision=vision, prompt=prompt, state=st, B=B, max_new=max_new)

@@ -47,6 +47,13 @@ CASES = [
     ("b32_long", 27, 2, [4100, 3000], 32, 32, 16, 4, 128, "bf16", 1024),
     ("fp32_gqa_ragged", 28, 3, [0, 40, 333], 4, 4, 8, 2, 128, "f32", 0),
     ("fp32_d96", 29, 2, [17, 100], 3, 5, 6, 3, 96, "f32", 0),
+    # head_dim 96 at every wave count: AR rows (1 wave), a B=16 window (4
+    # waves), and a prefill-shaped window (no cache, hundreds of causal rows)
+    ("ar_row_d96", 30, 3, [1, 63, 1100], 1, 0, 16, 4, 96, "bf16", 64),
+    ("ar_row_d96_balanced", 33, 3, [1, 63, 1100], 1, 0, 16, 4, 96, "bf16", 0),
+    ("window_d96_4waves", 32, 2, [1088, 500], 16, 16, 16, 4, 96, "bf16", 0),
+    ("prefill_d96", 31, 2, [0, 0], 300, 16, 16, 4, 96, "bf16", 64),
+    ("prefill_d128_balanced", 34, 2, [0, 0], 200, 8, 8, 2, 128, "bf16", 0),
 ]
 
 

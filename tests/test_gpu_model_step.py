@@ -166,3 +166,115 @@ def test_bf16_model_step_matches_oracle_replay():
     A_gpu = od.accept(am_gpu, st_host.draft, B)
     assert od.kv_commit(replay, A_gpu, am_gpu, B, B) == 0
     _states_equal(st, replay)
+
+
+def _embed_prefix_f64(w_bits, vision, prompt):
+    """Oracle-side prefix rows: vision vectors, then embedding rows of the prompt."""
+    emb = synth.bf16_to_f64(w_bits.embed)
+    return np.concatenate([vision.astype(np.float64), emb[prompt]], axis=1)
+
+
+def _bf16_weights(w):
+    wb = synth.ModelWeights(**{**w.__dict__})
+    for name in ("embed", "g_final", "lm_head"):
+        setattr(wb, name, synth.f32_to_bf16_bits(getattr(w, name)))
+    for name in ("wq", "wk", "wv", "wo", "g_attn", "g_mlp", "w_gate", "w_up", "w_down"):
+        setattr(wb, name, [synth.f32_to_bf16_bits(a) for a in getattr(w, name)])
+    return wb
+
+
+def test_prefill_matches_oracle_small():
+    B = 8
+    si = synth.decoder_stack_inputs(seed=9, S=3, n_layers=2, H=256, Hq=4, Hkv=2, D=64, ffn=512,
+                                    V=512, n_vision=24, n_prompt=16, B=B, max_new=64)
+    P, S, H = si.P, 3, 256
+    w = si.weights
+    pool = si.state.pool_pages
+    kps = [np.zeros((pool, 2, 16, 64), np.uint16) for _ in range(2)]
+    vps = [np.zeros((pool, 2, 64, 16), np.uint16) for _ in range(2)]
+    wb = _bf16_weights(w)
+    om = OracleModel(wb, kps, vps, bf16_bits=True)
+    ref = si.state.copy()
+    logits_ref = om.prefill(ref, _embed_prefix_f64(wb, si.vision, si.prompt), B)
+    dm = dvs.DeviceModel(w, _dev_pools(kps, "bf16"), _dev_pools(vps, "bf16"), "bf16")
+    st = dvs.DeviceState(si.state)
+    lg = torch.empty((S * (B + 1), w.V), dtype=torch.float32, device="cuda")
+    dvs.prefill(dm, st, P, B, prefix_tokens=torch.from_numpy(si.prefix_tokens()).cuda(),
+                x_prefix=torch.from_numpy(si.x_prefix()).cuda(), logits_out=lg)
+    torch.cuda.synchronize()
+    assert int(st.err.item()) == 0
+    got = lg.cpu().numpy().reshape(S, B + 1, w.V).astype(np.float64)
+    assert max_rel_err(got, logits_ref[:, P - 1:P + B]) <= 5e-2
+    am = od.top1_rows(got)
+    host = st.to_host(si.state)
+    np.testing.assert_array_equal(host.kv_len, [P] * S)
+    np.testing.assert_array_equal(host.boundary, am[:, 0])
+    np.testing.assert_array_equal(host.draft, am[:, 1:B])
+    np.testing.assert_array_equal(host.out_tokens[:, 0], am[:, 0])
+    np.testing.assert_array_equal(host.out_count, [1] * S)
+    # the prefix KV written by the GPU equals the oracle's within bf16 rounding
+    kp0 = synth.bf16_to_f64(dm.k_pools[0].cpu().view(torch.int16).numpy().view(np.uint16))
+    for s in range(S):
+        pages = si.state.page_table[s, :(P + 15) // 16]
+        a = kp0[pages].transpose(0, 2, 1, 3).reshape(-1, 2, 64)[:P]
+        b = om.k_pools[0][pages].transpose(0, 2, 1, 3).reshape(-1, 2, 64)[:P]
+        assert max_rel_err(a, b) <= 3e-2
+    # a step after the prefill, on the workspace the prefill laid out
+    # differently, equals the same step on a fresh workspace, bit for bit
+    st2 = dvs.DeviceState(st.to_host(si.state))
+    pools2 = ([k.clone() for k in dm.k_pools], [v.clone() for v in dm.v_pools])
+    lg_a = torch.empty((S * 2 * B, w.V), dtype=torch.float32, device="cuda")
+    dvs.draft_verify_step(dm, st, B, B, logits_out=lg_a)
+    dm2 = dvs.DeviceModel(w, pools2[0], pools2[1], "bf16")
+    lg_b = torch.empty_like(lg_a)
+    dvs.draft_verify_step(dm2, st2, B, B, logits_out=lg_b)
+    torch.cuda.synchronize()
+    assert int(st.err.item()) == 0 and int(st2.err.item()) == 0
+    assert torch.equal(lg_a, lg_b)
+
+
+def _run_stack(si, dtype, mode, chunk):
+    """prefill then AR (mode 'ar') or fused steps until max_new tokens; returns
+    the host state, the number of steps and the device seconds of the loop."""
+    w = si.weights
+    pool = si.state.pool_pages
+    L = w.n_layers
+    kps = [torch.zeros((pool, w.Hkv, 16, w.D), dtype=torch.bfloat16, device="cuda") for _ in range(L)]
+    vps = [torch.zeros((pool, w.Hkv, w.D, 16), dtype=torch.bfloat16, device="cuda") for _ in range(L)]
+    dm = dvs.DeviceModel(w, kps, vps, dtype)
+    st = dvs.DeviceState(si.state)
+    dvs.prefill(dm, st, si.P, si.B, prefix_tokens=torch.from_numpy(si.prefix_tokens()).cuda(),
+                x_prefix=torch.from_numpy(si.x_prefix()).cuda(), chunk_keys=chunk)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    steps = 0
+    while True:
+        for _ in range(16):
+            if mode == "ar":
+                dvs.draft_verify_step(dm, st, 1, 0, chunk_keys=chunk)
+            else:
+                dvs.draft_verify_step(dm, st, si.B, si.B, chunk_keys=chunk)
+            steps += 1
+        if int(st.finished.min().item()) == 1 or steps > 4 * si.max_new:
+            break
+    e1.record()
+    torch.cuda.synchronize()
+    assert int(st.err.item()) == 0
+    return st.to_host(si.state), steps, e0.elapsed_time(e1) / 1e3
+
+
+def test_decoder_stack_selfspec_equals_ar():
+    """The 16-layer bf16 stack (hidden 1536, 16/4 heads, head_dim 96, SwiGLU
+    4096, vocab 65536), 8 sequences with 1024 vision embeddings + 64 prompt
+    tokens, B=16, decoded to 1024 tokens: the self-speculative stream equals
+    greedy AR token for token."""
+    print("[stack] generating the 16-layer stack", flush=True)
+    si = synth.decoder_stack_inputs()
+    ar, ar_steps, ar_s = _run_stack(si, "bf16", "ar", 64)
+    print(f"[stack] AR {ar_steps} steps {ar_s:.2f} s", flush=True)
+    ss, ss_steps, ss_s = _run_stack(si, "bf16", "fused", 64)
+    print(f"[stack] self-spec {ss_steps} steps {ss_s:.2f} s", flush=True)
+    np.testing.assert_array_equal(ar.out_count, [si.max_new] * 8)
+    np.testing.assert_array_equal(ss.out_count, [si.max_new] * 8)
+    np.testing.assert_array_equal(ss.out_tokens, ar.out_tokens)
