@@ -54,6 +54,9 @@ CASES = [
     ("window_d96_4waves", 32, 2, [1088, 500], 16, 16, 16, 4, 96, "bf16", 0),
     ("prefill_d96", 31, 2, [0, 0], 300, 16, 16, 4, 96, "bf16", 64),
     ("prefill_d128_balanced", 34, 2, [0, 0], 200, 8, 8, 2, 128, "bf16", 0),
+    ("d64_wide", 35, 2, [300, 77], 32, 32, 8, 2, 64, "bf16", 0),
+    ("d64_wide_aligned", 36, 3, [5, 300, 1200], 16, 16, 8, 2, 64, "bf16", 128),
+    ("d128_aligned_narrow", 37, 2, [700, 33], 4, 4, 8, 2, 128, "bf16", 256),
 ]
 
 
