@@ -574,10 +574,19 @@ __global__ void __launch_bounds__(NW * 64, 1) attn_bf16_kernel(AttnParams p) {
     if (!s_flag[0]) continue;
     const float* pob = p.part_o + (size_t)it * p.max_segs * (NT * NREG);
     const float* pmlb = p.part_ml + (size_t)it * p.max_segs * (NT * 2);
+    // Partials are read with coherent loads; every batch is issued in full
+    // before any of it is used, so the loads overlap instead of each one
+    // waiting for the previous.
     float M = -INFINITY;
-    for (int c = 0; c < nseg; ++c)
-      M = fmaxf(M, __hip_atomic_load(pmlb + (size_t)c * NT * 2 + tid, __ATOMIC_RELAXED,
-                                     __HIP_MEMORY_SCOPE_AGENT));
+    for (int c0 = 0; c0 < nseg; c0 += 8) {
+      float mv[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+        mv[j] = __hip_atomic_load(pmlb + (size_t)min(c0 + j, nseg - 1) * NT * 2 + tid, __ATOMIC_RELAXED,
+                                  __HIP_MEMORY_SCOPE_AGENT);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) M = fmaxf(M, mv[j]);   // repeats of the last segment are harmless
+    }
     const float Ms = (M == -INFINITY) ? 0.f : M;
     f32x16 acc[DG];
 #pragma unroll
@@ -585,17 +594,19 @@ __global__ void __launch_bounds__(NW * 64, 1) attn_bf16_kernel(AttnParams p) {
     float lt = 0.f;
     for (int c = 0; c < nseg; ++c) {
       const float* src_ml = pmlb + (size_t)c * NT * 2;
+      const float* src = pob + (size_t)c * NT * NREG;
+      float pv[NREG];
+#pragma unroll
+      for (int i = 0; i < NREG; ++i)
+        pv[i] = __hip_atomic_load(src + i * NT + tid, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       const float mc = __hip_atomic_load(src_ml + tid, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       const float lc = __hip_atomic_load(src_ml + NT + tid, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       const float wgt = __builtin_amdgcn_exp2f(mc - Ms);
       lt += wgt * lc;
-      const float* src = pob + (size_t)c * NT * NREG;
 #pragma unroll
       for (int dg = 0; dg < DG; ++dg)
 #pragma unroll
-        for (int i = 0; i < 16; ++i)
-          acc[dg][i] += wgt * __hip_atomic_load(src + (dg * 16 + i) * NT + tid, __ATOMIC_RELAXED,
-                                                __HIP_MEMORY_SCOPE_AGENT);
+        for (int i = 0; i < 16; ++i) acc[dg][i] += wgt * pv[dg * 16 + i];
     }
     write_out(acc, lt > 0.f ? 1.f / lt : 0.f);
     if (tid == 0) __hip_atomic_store(&p.counters[it], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);

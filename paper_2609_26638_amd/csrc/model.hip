@@ -15,6 +15,7 @@
 // ascending k, and accumulates every 32-row group of A against them.  A row's
 // result therefore never depends on how many rows the call carries, so an AR
 // call (1 row) and a fused call (2B rows) produce bit-identical rows.
+#include <algorithm>
 #include <math.h>
 
 #include "dvs_common.h"
@@ -209,6 +210,163 @@ __global__ void __launch_bounds__(256) gemm_bf16_kernel(const __bf16* __restrict
   }
 }
 
+// ---------------------------------------------------------------------------
+// bf16 GEMM for the decoder stack: C[m, n] (=, or += into the fp32 residual)
+// sum_k A[m, k] W[n, k].  The weights are streamed once; the row count is
+// small (8..256 window rows) or a long prefill.
+//
+// A workgroup owns 32 output columns and a K range; its 4 waves split that
+// range in four, each accumulating all rows of a 256-row pass with
+// v_mfma_f32_32x32x16_bf16 (A lane = row, W lane = column, 8 k each).  The
+// four partial tiles are summed through LDS in wave order.  When the column
+// count alone cannot fill the chip, the K range is further split over
+// `ksplit` workgroups: each publishes its fp32 tile with write-through stores
+// and the last one to finish (counter) sums the tiles in split order.
+// Every output element is therefore reduced in an order fixed by (N, K)
+// alone: a row's result does not depend on how many rows the call carries,
+// which keeps a fused step's causal rows bit-identical to AR steps.
+// ---------------------------------------------------------------------------
+constexpr int GK_ROWS = 256;   // rows per pass
+constexpr int GK_MAXSPLIT = 32;
+
+// MG: 32-row groups per pass (1, 2, 4 or 8); KU: k-steps whose operands are
+// loaded before their MFMAs are issued.
+template <int MG>
+__global__ void __launch_bounds__(256, 1) gemm_bf16_sk_kernel(
+    const __bf16* __restrict__ A, const __bf16* __restrict__ W, int M, int N, int K, void* C,
+    int c_f32, int accumulate, int ksplit, float* __restrict__ part, int32_t* __restrict__ counters) {
+  constexpr int KU = MG >= 4 ? 2 : 4;
+  constexpr int PR = MG * 32;   // rows per pass
+  __shared__ float red[4][PR][33];
+  __shared__ int s_last;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int l32 = lane & 31, hh = lane >> 5;
+  const int NB = (N + 31) / 32;
+  const int nb = blockIdx.x % NB;
+  const int ks = blockIdx.x / NB;
+  const int n0 = nb * 32;
+  const int kc = K / ksplit, kw = kc / 4;
+  const int kbeg = ks * kc + w * kw;
+  const int ncol = n0 + l32;
+  const bool nvalid = ncol < N;
+  const __bf16* wrow = W + (size_t)(nvalid ? ncol : 0) * K;
+  float* Cf = c_f32 ? (float*)C : nullptr;
+  __bf16* Cb = c_f32 ? nullptr : (__bf16*)C;
+  for (int m0 = 0; m0 < M; m0 += PR) {
+    f32x16 acc[MG];
+#pragma unroll
+    for (int g = 0; g < MG; ++g) acc[g] = f32x16{};
+    const __bf16* arow[MG];
+    bool avalid[MG];
+#pragma unroll
+    for (int g = 0; g < MG; ++g) {
+      const int mrow = m0 + g * 32 + l32;
+      avalid[g] = mrow < M;
+      arow[g] = A + (size_t)(avalid[g] ? mrow : 0) * K;
+    }
+    int k0 = kbeg;
+    for (; k0 + 16 * KU <= kbeg + kw; k0 += 16 * KU) {
+      bf16x8 bf[KU], af[KU][MG];
+#pragma unroll
+      for (int u = 0; u < KU; ++u) {
+        bf[u] = nvalid ? *(const bf16x8*)(wrow + k0 + 16 * u + hh * 8) : bf16x8{};
+#pragma unroll
+        for (int g = 0; g < MG; ++g)
+          af[u][g] = avalid[g] ? *(const bf16x8*)(arow[g] + k0 + 16 * u + hh * 8) : bf16x8{};
+      }
+#pragma unroll
+      for (int u = 0; u < KU; ++u)
+#pragma unroll
+        for (int g = 0; g < MG; ++g) acc[g] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[u][g], bf[u], acc[g], 0, 0, 0);
+    }
+    for (; k0 < kbeg + kw; k0 += 16) {
+      const bf16x8 b = nvalid ? *(const bf16x8*)(wrow + k0 + hh * 8) : bf16x8{};
+#pragma unroll
+      for (int g = 0; g < MG; ++g) {
+        const bf16x8 a = avalid[g] ? *(const bf16x8*)(arow[g] + k0 + hh * 8) : bf16x8{};
+        acc[g] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc[g], 0, 0, 0);
+      }
+    }
+    // C layout: lane (col l32, hh), register i holds row 8*(i>>2) + 4*hh + (i&3)
+#pragma unroll
+    for (int g = 0; g < MG; ++g)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) red[w][g * 32 + 8 * (i >> 2) + 4 * hh + (i & 3)][l32] = acc[g][i];
+    __syncthreads();
+    // thread t sums column t&31 of rows (t>>5) + 8j over the four waves, in
+    // order; a residual being accumulated into is read in one batch first
+    const int col = tid & 31, n = n0 + col;
+    float cur[PR / 8];
+    if (ksplit == 1 && Cf && accumulate) {
+#pragma unroll
+      for (int j = 0; j < PR / 8; ++j) {
+        const int mrow = m0 + (tid >> 5) + 8 * j;
+        cur[j] = (mrow < M && n < N) ? Cf[(size_t)mrow * N + n] : 0.f;
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < PR / 8; ++j) {
+      const int r = (tid >> 5) + 8 * j;
+      const float v = ((red[0][r][col] + red[1][r][col]) + red[2][r][col]) + red[3][r][col];
+      const int mrow = m0 + r;
+      if (mrow >= M || n >= N) continue;
+      if (ksplit > 1) {
+        __hip_atomic_store(part + ((size_t)ks * M + mrow) * N + n, v, __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+      } else {
+        const size_t o = (size_t)mrow * N + n;
+        if (Cf) Cf[o] = accumulate ? cur[j] + v : v;
+        else Cb[o] = (__bf16)v;
+      }
+    }
+    __syncthreads();   // red is reused by the next pass
+  }
+  if (ksplit == 1) return;
+  // split K (M <= PR here): the last workgroup of the column block sums the
+  // splits in order; the loads of one split are issued together
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  if (tid == 0)
+    s_last = __hip_atomic_fetch_add(&counters[nb], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
+             ksplit - 1;
+  __syncthreads();
+  if (!s_last) return;
+  const int col = tid & 31, n = n0 + col;
+  float sum[PR / 8];
+#pragma unroll
+  for (int j = 0; j < PR / 8; ++j) sum[j] = 0.f;
+  for (int sp = 0; sp < ksplit; ++sp) {
+    float v[PR / 8];
+#pragma unroll
+    for (int j = 0; j < PR / 8; ++j) {
+      const int mrow = (tid >> 5) + 8 * j;
+      v[j] = (mrow < M && n < N)
+                 ? __hip_atomic_load(part + ((size_t)sp * M + mrow) * N + n, __ATOMIC_RELAXED,
+                                     __HIP_MEMORY_SCOPE_AGENT)
+                 : 0.f;
+    }
+#pragma unroll
+    for (int j = 0; j < PR / 8; ++j) sum[j] += v[j];
+  }
+  float cur[PR / 8];
+  if (Cf && accumulate) {
+#pragma unroll
+    for (int j = 0; j < PR / 8; ++j) {
+      const int mrow = (tid >> 5) + 8 * j;
+      cur[j] = (mrow < M && n < N) ? Cf[(size_t)mrow * N + n] : 0.f;
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < PR / 8; ++j) {
+    const int mrow = (tid >> 5) + 8 * j;
+    if (mrow >= M || n >= N) continue;
+    const size_t o = (size_t)mrow * N + n;
+    if (Cf) Cf[o] = accumulate ? cur[j] + sum[j] : sum[j];
+    else Cb[o] = (__bf16)sum[j];
+  }
+  if (tid == 0) __hip_atomic_store(&counters[nb], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 // fp32: v_mfma_f32_32x32x2_f32; lane (row|col, hh) takes k = k0 + 4*hh + j in
 // MFMA j, so one 16-byte load per operand feeds 4 MFMAs.
 __global__ void __launch_bounds__(256) gemm_f32_kernel(const float* __restrict__ A,
@@ -261,8 +419,26 @@ __global__ void __launch_bounds__(256) gemm_f32_kernel(const float* __restrict__
 // ---------------------------------------------------------------------------
 struct StepLayout {
   size_t x, h, hsel, q, k, v, att, gate, up, act, logits, am, acc, attn_ws, total, attn_bytes,
-      attn_counters;
+      attn_counters, gemm_part, gemm_part_bytes, gemm_counters, n_gemm_counters;
 };
+
+// K splits of a bf16 GEMM over workgroups: enough column blocks x splits to
+// fill the chip, a split being a multiple of 64 of K.  A function of (N, K)
+// for every call of up to 256 rows (so row results do not depend on the row
+// count); longer calls (prefill) have rows enough and do not split.
+static int gemm_ksplit(int M, int N, int K) {
+  if (M > GK_ROWS || K % 64 != 0) return 1;
+  static_assert(GK_MAXSPLIT >= 1, "split bound");
+  const int nb = (N + 31) / 32;
+  const int target = (256 + nb - 1) / nb;
+  if (target <= 1) return 1;
+  const int units = K / 64;
+  for (int d = target; d <= units && d <= GK_MAXSPLIT; ++d)
+    if (units % d == 0) return d;
+  for (int d = std::min(units, GK_MAXSPLIT); d > 1; --d)
+    if (units % d == 0) return d;
+  return 1;
+}
 
 __global__ void zero_words_kernel(int32_t* __restrict__ p, int n) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
@@ -305,17 +481,54 @@ static StepLayout step_layout(const dvs_model* m, int S, int n_causal, int n_mas
   L.attn_counters = attn_counter_bytes(S, n_causal + n_mask, m->n_heads, m->n_kv_heads,
                                        m->head_dim, max_pages, chunk_keys, m->dtype);
   L.attn_ws = off; off += al(L.attn_bytes);
+  // split-K partials and counters of the largest bf16 GEMM of the call
+  if (m->dtype == DVS_BF16) {
+    const int H = m->hidden;
+    const int shapes[6][3] = {{(int)M, (int)qd, H}, {(int)M, (int)kd, H}, {(int)M, H, (int)qd},
+                              {(int)M, m->ffn, H}, {(int)M, H, m->ffn}, {(int)logit_rows, m->vocab, H}};
+    size_t part = 0, cnt = 0;
+    for (const auto& sh : shapes) {
+      if (sh[1] <= 0) continue;
+      const int ksp = gemm_ksplit(sh[0], sh[1], sh[2]);
+      if (ksp > 1) {
+        part = std::max(part, (size_t)ksp * sh[0] * sh[1] * 4);
+        cnt = std::max(cnt, (size_t)(sh[1] + 31) / 32);
+      }
+    }
+    L.gemm_part = off; off += al(part); L.gemm_part_bytes = part;
+    L.gemm_counters = off; off += al(cnt * 4); L.n_gemm_counters = cnt;
+  }
   L.total = off;
   return L;
 }
 
 // C = A W^T (or C += for the fp32 residual).  `c_f32` selects an fp32 output
 // for bf16 models (residual stream, logits); fp32 models always write fp32.
-static int gemm(int dtype, const void* A, const void* W, int M, int N, int K, void* C, int c_f32,
-                int accumulate, hipStream_t st) {
+static int gemm(const StepLayout& L, char* ws, int dtype, const void* A, const void* W, int M,
+                int N, int K, void* C, int c_f32, int accumulate, hipStream_t st) {
   const int waves = (N + 31) / 32;
   const int blocks = (waves + 3) / 4;
-  if (dtype == DVS_BF16)
+  if (dtype == DVS_BF16 && K % 64 == 0) {
+    const int ksp = gemm_ksplit(M, N, K);
+    const int nb = (N + 31) / 32;
+    if (ksp > 1 && ((size_t)ksp * M * N * 4 > L.gemm_part_bytes || (size_t)nb > L.n_gemm_counters)) {
+      set_error("draft_verify_step: GEMM split workspace too small");
+      return DVS_EWORKSPACE;
+    }
+    float* part = (float*)(ws + L.gemm_part);
+    int32_t* cnt = (int32_t*)(ws + L.gemm_counters);
+    const dim3 grid(nb * ksp), blk(256);
+    // rows per pass: the smallest power-of-two number of 32-row groups
+    // covering M (up to 256 rows); the reduction order does not depend on it
+    if (M <= 32)
+      hipLaunchKernelGGL(gemm_bf16_sk_kernel<1>, grid, blk, 0, st, (const __bf16*)A, (const __bf16*)W, M, N, K, C, c_f32, accumulate, ksp, part, cnt);
+    else if (M <= 64)
+      hipLaunchKernelGGL(gemm_bf16_sk_kernel<2>, grid, blk, 0, st, (const __bf16*)A, (const __bf16*)W, M, N, K, C, c_f32, accumulate, ksp, part, cnt);
+    else if (M <= 128)
+      hipLaunchKernelGGL(gemm_bf16_sk_kernel<4>, grid, blk, 0, st, (const __bf16*)A, (const __bf16*)W, M, N, K, C, c_f32, accumulate, ksp, part, cnt);
+    else
+      hipLaunchKernelGGL(gemm_bf16_sk_kernel<8>, grid, blk, 0, st, (const __bf16*)A, (const __bf16*)W, M, N, K, C, c_f32, accumulate, ksp, part, cnt);
+  } else if (dtype == DVS_BF16)
     hipLaunchKernelGGL(gemm_bf16_kernel, dim3(blocks), dim3(256), 0, st, (const __bf16*)A,
                        (const __bf16*)W, M, N, K, C, c_f32, accumulate);
   else
@@ -350,14 +563,19 @@ static int forward_layers(const dvs_model* m, const dvs_state* st, int n_causal,
     hipLaunchKernelGGL(zero_words_kernel, dim3((nw + 255) / 256), dim3(256), 0, stream,
                        (int32_t*)(ws + L.attn_ws), nw);
   }
+  if (L.n_gemm_counters) {
+    const int nw = (int)L.n_gemm_counters;
+    hipLaunchKernelGGL(zero_words_kernel, dim3((nw + 255) / 256), dim3(256), 0, stream,
+                       (int32_t*)(ws + L.gemm_counters), nw);
+  }
   const double log2_theta = log2((double)m->rope_theta);
   for (int l = 0; l < m->n_layers; ++l) {
     const dvs_layer& ly = m->layers[l];
     hipLaunchKernelGGL(rmsnorm_kernel<T>, dim3(M), dim3(256), 0, stream, x, (const T*)ly.g_attn, H,
                        m->rms_eps, h);
-    if ((rc = gemm(dt, h, ly.wq, M, Hq * D, H, q, 0, 0, stream))) return rc;
-    if ((rc = gemm(dt, h, ly.wk, M, Hkv * D, H, k, 0, 0, stream))) return rc;
-    if ((rc = gemm(dt, h, ly.wv, M, Hkv * D, H, v, 0, 0, stream))) return rc;
+    if ((rc = gemm(L, ws, dt, h, ly.wq, M, Hq * D, H, q, 0, 0, stream))) return rc;
+    if ((rc = gemm(L, ws, dt, h, ly.wk, M, Hkv * D, H, k, 0, 0, stream))) return rc;
+    if ((rc = gemm(L, ws, dt, h, ly.wv, M, Hkv * D, H, v, 0, 0, stream))) return rc;
     const long long nq = (long long)M * Hq * (D / 2), nk = (long long)M * Hkv * (D / 2);
     hipLaunchKernelGGL(rope_kernel<T>, dim3((unsigned)((nq + 255) / 256)), dim3(256), 0, stream, q, M,
                        R, Hq, D, log2_theta, st->kv_len);
@@ -369,17 +587,17 @@ static int forward_layers(const dvs_model* m, const dvs_state* st, int n_causal,
                            (float)(1.0 / sqrt((double)D)), dt, chunk_keys, att, st->err_word,
                            ws + L.attn_ws, L.attn_bytes, stream);
     if (rc) return rc;
-    if ((rc = gemm(dt, att, ly.wo, M, H, Hq * D, x, 1, 1, stream))) return rc;
+    if ((rc = gemm(L, ws, dt, att, ly.wo, M, H, Hq * D, x, 1, 1, stream))) return rc;
     if (m->ffn > 0) {
       hipLaunchKernelGGL(rmsnorm_kernel<T>, dim3(M), dim3(256), 0, stream, x, (const T*)ly.g_mlp,
                          H, m->rms_eps, h);
-      if ((rc = gemm(dt, h, ly.w_gate, M, m->ffn, H, gate, 0, 0, stream))) return rc;
-      if ((rc = gemm(dt, h, ly.w_up, M, m->ffn, H, up, 0, 0, stream))) return rc;
+      if ((rc = gemm(L, ws, dt, h, ly.w_gate, M, m->ffn, H, gate, 0, 0, stream))) return rc;
+      if ((rc = gemm(L, ws, dt, h, ly.w_up, M, m->ffn, H, up, 0, 0, stream))) return rc;
       const long long n = (long long)M * m->ffn;
       hipLaunchKernelGGL(silu_mul_kernel<T>, dim3((unsigned)((n + 255) / 256)), dim3(256), 0,
                          stream, gate, up, n, act);
       if ((rc = launch_status("draft_verify_step(silu)"))) return rc;
-      if ((rc = gemm(dt, act, ly.w_down, M, H, m->ffn, x, 1, 1, stream))) return rc;
+      if ((rc = gemm(L, ws, dt, act, ly.w_down, M, H, m->ffn, x, 1, 1, stream))) return rc;
     }
   }
   hipLaunchKernelGGL(rmsnorm_kernel<T>, dim3(M), dim3(256), 0, stream, x, (const T*)m->g_final, H,
@@ -401,7 +619,7 @@ static int run_step(const dvs_model* m, const dvs_state* st, int n_causal, int n
   int rc;
   if ((rc = launch_status("draft_verify_step(embed)"))) return rc;
   if ((rc = forward_layers<T>(m, st, n_causal, n_mask, chunk_keys, L, ws, stream))) return rc;
-  if ((rc = gemm(m->dtype, ws + L.h, m->lm_head, M, m->vocab, m->hidden, logits, 1, 0, stream)))
+  if ((rc = gemm(L, ws, m->dtype, ws + L.h, m->lm_head, M, m->vocab, m->hidden, logits, 1, 0, stream)))
     return rc;
   rc = argmax_accept(logits, DVS_F32, S, R, m->vocab, n_causal, st->draft, st->draft_width, am, acc,
                      st->err_word, stream);
@@ -427,7 +645,7 @@ static int run_prefill(const dvs_model* m, const dvs_state* st, int P, int n_mas
   hipLaunchKernelGGL(gather_rows_kernel<T>, dim3(S * nsel), dim3(256), 0, stream,
                      (const T*)(ws + L.h), m->hidden, R, P - 1, nsel, hsel);
   float* logits = logits_out ? logits_out : (float*)(ws + L.logits);
-  if ((rc = gemm(m->dtype, hsel, m->lm_head, S * nsel, m->vocab, m->hidden, logits, 1, 0, stream)))
+  if ((rc = gemm(L, ws, m->dtype, hsel, m->lm_head, S * nsel, m->vocab, m->hidden, logits, 1, 0, stream)))
     return rc;
   int32_t* am = (int32_t*)(ws + L.am);
   int32_t* acc = (int32_t*)(ws + L.acc);

@@ -271,9 +271,9 @@ def test_decoder_stack_selfspec_equals_ar():
     greedy AR token for token."""
     print("[stack] generating the 16-layer stack", flush=True)
     si = synth.decoder_stack_inputs()
-    ar, ar_steps, ar_s = _run_stack(si, "bf16", "ar", 64)
+    ar, ar_steps, ar_s = _run_stack(si, "bf16", "ar", 256)
     print(f"[stack] AR {ar_steps} steps {ar_s:.2f} s", flush=True)
-    ss, ss_steps, ss_s = _run_stack(si, "bf16", "fused", 64)
+    ss, ss_steps, ss_s = _run_stack(si, "bf16", "fused", 256)
     print(f"[stack] self-spec {ss_steps} steps {ss_s:.2f} s", flush=True)
     np.testing.assert_array_equal(ar.out_count, [si.max_new] * 8)
     np.testing.assert_array_equal(ss.out_count, [si.max_new] * 8)
