@@ -138,6 +138,70 @@ __device__ __forceinline__ void wait_tiles(int tiles_after) {
   else wait_vmcnt<0>();
 }
 
+template <int N>
+struct IC {
+  static constexpr int value = N;
+};
+
+template <int I, int N, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (I < N) {
+    f(IC<I>{});
+    static_for<I + 1, N>(f);
+  }
+}
+
+__device__ __forceinline__ uint32_t lds_addr(const void* ptr) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)ptr;
+}
+
+// MFMA operand fragments of the producer/consumer kernel are read from LDS
+// with explicit waits: the compiler's wait insertion cannot tell the ring
+// slot being read from the slots in-flight direct loads are filling, and
+// would drain all of them before every read.  LDS reads complete in order,
+// so "at most N LDS operations outstanding" completes every read but the N
+// youngest; operations the compiler adds only make the wait longer.  The
+// wait names the fragment as an in/out operand, so no use of it can be
+// scheduled above the wait.
+template <int OFF>
+__device__ __forceinline__ bf16x8 lds_read16(uint32_t addr) {
+  static_assert(OFF >= 0 && OFF < 65536, "ds offset field");
+  bf16x8 r;
+  asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(r) : "v"(addr), "n"(OFF) : "memory");
+  return r;
+}
+
+template <int N>
+__device__ __forceinline__ void lds_wait(bf16x8& frag) {
+  static_assert(N >= 0 && N < 16, "lgkmcnt range");
+  asm volatile("s_waitcnt lgkmcnt(%1)" : "+v"(frag) : "n"(N) : "memory");
+}
+
+// Issue the N reads rd(n) in order with DEPTH in flight; hand read n to
+// use(n, fragment) once it has arrived.  A ring slot is refilled one use
+// after it was consumed.
+template <int N, int DEPTH, typename RD, typename USE>
+__device__ __forceinline__ void lds_pipeline(RD&& rd, USE&& use) {
+  constexpr int RING = DEPTH + 1;
+  constexpr int PRE = DEPTH < N ? DEPTH : N;
+  bf16x8 ring[RING];
+  static_for<0, PRE>([&](auto c) { ring[decltype(c)::value % RING] = rd(c); });
+  static_for<0, N>([&](auto c) {
+    constexpr int n = decltype(c)::value;
+    constexpr int issued = (n + DEPTH < N) ? n + DEPTH : N;
+    lds_wait<issued - (n + 1)>(ring[n % RING]);
+    use(c, ring[n % RING]);
+    if constexpr (n + DEPTH < N) ring[(n + DEPTH) % RING] = rd(IC<n + DEPTH>{});
+  });
+}
+
+// Barrier for the producer/consumer kernel: completes this wave's LDS
+// operations (P hand-off writes, fragment reads) and meets the other waves.
+// Inline, so no compiler-inserted wait for in-flight direct loads rides on it.
+__device__ __forceinline__ void pc_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
 template <int D, int NW>
 __global__ void __launch_bounds__(NW * 64, 1) attn_bf16_kernel(AttnParams p) {
   constexpr int NT = NW * 64;
@@ -614,6 +678,630 @@ __global__ void __launch_bounds__(NW * 64, 1) attn_bf16_kernel(AttnParams p) {
 }
 
 // ---------------------------------------------------------------------------
+// bf16, balanced work split, wide windows (>= 128 query rows per KV head):
+// producer/consumer wave pairs.
+//
+// Pair k owns 64 query rows as two 32-row groups.  Its producer wave computes
+// S^T = K Q^T for both groups (every K fragment read from LDS feeds two
+// MFMAs) and the online softmax, and hands P (bf16, already in the PV MFMA's
+// B-operand order) and the rescale factors to its consumer wave through LDS.
+// The consumer wave accumulates O^T += V^T P^T for both groups (every V
+// fragment feeds two MFMAs) and issues all direct cache loads.  Tile i of a
+// segment takes one period of two halves:
+//     producer:  QK(i)               | softmax(i), P(i) -> LDS
+//     consumer:  P(i-1) -> registers, | O rescale, PV(i-1)
+//                loads of group i    |
+// so the consumer's MFMAs run under the producer's vector-ALU softmax (the
+// two waves of a pair share a SIMD).  K and V tiles live in separate 3-slot
+// rings: group g(i) = {K(i+2), V(i+1)} is issued in period i into the slots
+// of K(i-1) and V(i-2), whose last readers finished in period i-1; period i
+// waits for g(i-2) = {K(i), V(i-1)}.  A group's K part past the last tile
+// re-reads the last tile into a dead slot, so every group has the same load
+// count.  Producer and consumer keep their state in separate branches (the
+// two roles' registers are not live at the same time), and both walk the
+// same sequence of barriers.
+// ---------------------------------------------------------------------------
+constexpr int PC_NSTAGE = 3;
+constexpr int PC_LDS_DEPTH = 6;
+
+template <int D, int NP>
+__global__ void __launch_bounds__(NP * 128, 1) attn_bf16_pc_kernel(AttnParams p) {
+  constexpr int NC = NP * 64;            // threads per role
+  constexpr int CPR = D / 8;
+  constexpr int KROWB = D * 2;
+  constexpr int KTILE_B = KT * KROWB;
+  constexpr int VTILE_B = KT * D * 2;
+  constexpr int K_INS = KTILE_B / (NC * 16);
+  constexpr int V_INS = VTILE_B / (NC * 16);
+  constexpr int NPL = K_INS + V_INS;
+  constexpr int KS = D / 16;
+  constexpr int DG = D / 32;
+  constexpr int RPWG = NP * 64;
+  constexpr int PAGE_K = 16 * KROWB;
+  constexpr int PAGE_V = D * 32;
+  constexpr int SEGPP_K = PAGE_K / 1024;
+  constexpr int SEGPP_V = PAGE_V / 1024;
+  constexpr bool KXOR = (KROWB & (KROWB - 1)) == 0;
+  constexpr int NS = PC_NSTAGE;
+  constexpr int OREG = 2 * DG * 16;      // partial O floats per consumer thread
+  static_assert(KTILE_B % (NC * 16) == 0 && VTILE_B % (NC * 16) == 0, "tile / wave mismatch");
+  static_assert(PAGE_K % 1024 == 0 && PAGE_V % 1024 == 0, "page / segment mismatch");
+  static_assert(NPL < 64, "vmcnt range");
+  static_assert(NP == 4 && K_INS == SEGPP_K && V_INS == SEGPP_V, "consumer wave k copies page k of a tile");
+
+  __shared__ __attribute__((aligned(1024))) char kring[NS * KTILE_B];
+  __shared__ __attribute__((aligned(1024))) char vring[NS * VTILE_B];
+  __shared__ u32x4 s_P[NP][2][4][64];    // P of a pair: [group][16-key step][lane]
+  __shared__ float s_alpha[NP][2][32];
+  __shared__ int s_resc[NP];
+  __shared__ int s_pages[SUB_TILES * 4 + 4];
+  __shared__ int s_seq[BAL_MAX_SEQS + 1];
+  __shared__ int s_flag[2];
+
+  const int tid = threadIdx.x;
+  // wave-uniform role (an SGPR), so the role branch is a real branch: its
+  // two sides run different barrier sequences and keep separate registers
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const bool prod = w < NP;
+  const int kp = prod ? w : w - NP;      // pair
+  const int R = p.R;
+  const int HN = p.Hkv * p.n_row_tiles;
+
+  const __bf16* __restrict__ q = (const __bf16*)p.q;
+  const char* __restrict__ knb = (const char*)p.k_new;
+  const char* __restrict__ vnb = (const char*)p.v_new;
+  char* __restrict__ kpb = (char*)p.k_pool;
+  char* __restrict__ vpb = (char*)p.v_pool;
+  __bf16* __restrict__ out = (__bf16*)p.out;
+
+  // ---- balanced split: tile prefix over sequences, equal shares
+  if (tid == 0) s_flag[0] = 0;
+  for (int s0 = 0; s0 < p.S; s0 += NP * 128) {
+    __syncthreads();
+    int t = 0;
+    const int s = s0 + tid;
+    if (s < p.S) {
+      const int L = p.kv_len[s];
+      const int T = L + R;
+      if (L < 0 || T > p.max_pages * 16) s_flag[0] = 1;
+      else t = (T + KT - 1) / KT;
+    }
+    s_seq[1 + tid + s0] = t;
+    __syncthreads();
+    for (int off = 1; off < NP * 128; off <<= 1) {
+      const int v = (tid >= off && s0 + tid < p.S) ? s_seq[1 + s0 + tid - off] : 0;
+      __syncthreads();
+      if (s0 + tid < p.S) s_seq[1 + s0 + tid] += v;
+      __syncthreads();
+    }
+    if (s0 > 0 && s0 + tid < p.S) s_seq[1 + s0 + tid] += s_seq[s0];
+  }
+  if (tid == 0) s_seq[0] = 0;
+  __syncthreads();
+  if (blockIdx.x == 0 && tid == 0 && s_flag[0]) set_err(p.err, DVS_ERR_MAX_PAGES);
+  const int U = s_seq[p.S] * HN;
+  const int share = max((U + (int)gridDim.x - 1) / (int)gridDim.x, p.share_min);
+  const int u0 = (int)blockIdx.x * share;
+  const int u_end = min(u0 + share, U);
+  if (u0 >= u_end) return;
+
+  // The two roles run separate copies of the segment loop (the same
+  // segments and the same barrier sequence), so the register allocation of
+  // one role never sees the other's live values.
+  auto segments = [&](auto role) {
+    constexpr bool PROD = decltype(role)::value != 0;
+    bool first_segment = true;
+    int s_cur = 0;
+    int u = u0;
+    while (u < u_end) {
+      // Per-lane values are derived every segment from an opaque copy of the
+      // thread index: hoisted out of the loop they would stay live across the
+      // code of both roles.
+      int tidv = tid;
+      asm volatile("" : "+v"(tidv));
+      const int lane = tidv & 63;
+      const int hh = lane >> 5;
+      const int l32 = lane & 31;
+      const int ct = tidv - NC;            // consumer thread index (consumers only)
+      while (s_seq[s_cur + 1] * HN <= u) ++s_cur;
+      const int s = s_cur;
+      const int L = p.kv_len[s];
+      const int tiles = s_seq[s + 1] - s_seq[s];
+      const int local = u - s_seq[s] * HN;
+      const int qi = local / tiles;
+      const int j0 = local - qi * tiles;
+      const int j1 = min(tiles, j0 + (u_end - u));
+      const int it = s * HN + qi;
+      const int kvh = qi / p.n_row_tiles;
+      const int rt = qi - kvh * p.n_row_tiles;
+      const int P0 = s_seq[s] * HN + qi * tiles;
+      const int kseg = (int)blockIdx.x - P0 / share;
+      const int nseg = (P0 + tiles - 1) / share - P0 / share + 1;
+      u += j1 - j0;
+      if (!first_segment) __syncthreads();
+      first_segment = false;
+      const int T = L + R;
+      const int32_t* __restrict__ pt = p.page_table + (size_t)s * p.max_pages;
+
+      // the lane's two rows (one per group) and their visibility limits
+      bool rvalid[2];
+      int rr[2], hq[2], hi[2];
+#pragma unroll
+      for (int g = 0; g < 2; ++g) {
+        const int n = rt * RPWG + kp * 64 + g * 32 + l32;
+        rvalid[g] = n < p.rows_total;
+        rr[g] = n / p.G;
+        hq[g] = kvh * p.G + (n - rr[g] * p.G);
+        hi[g] = !rvalid[g] ? -1 : (rr[g] < p.n_causal ? L + rr[g] : T - 1);
+      }
+
+      auto stage_pages = [&](int ja, int jb) {
+        const int pg_lo = ja * 4;
+        const int pg_hi = min(jb * 4, (T + 15) >> 4);
+        if (ja != j0) __syncthreads();
+        if (tid == 0) s_flag[1] = 0;
+        __syncthreads();
+        for (int i = tidv; i < pg_hi - pg_lo; i += NP * 128) {
+          int pg = pt[pg_lo + i];
+          if (pg < 0 || pg >= p.pool_pages) {
+            pg = 0;
+            s_flag[1] = 1;
+          }
+          s_pages[i] = pg;
+        }
+        __syncthreads();
+        if (tid == 0 && s_flag[1]) set_err(p.err, DVS_ERR_BAD_PAGE);
+      };
+      // window tiles (reach [L, T) or past it): every thread stages them,
+      // keys < L from the pool, [L, T) from k_new / v_new (appended to the pool
+      // by row tile 0), >= T zero; K into K slot 0, V into V slot 0
+      auto fill_window_tile = [&](int t0, int pg_lo) {
+        int tidw = tidv;   // opaque: nothing of the fill is hoisted out of it
+        asm volatile("" : "+v"(tidw));
+        char* kb = kring;
+        char* vb = vring;
+        for (int ci = tidw; ci < KT * CPR; ci += NP * 128) {
+          const int kk = ci / CPR;
+          const int cc = ci - kk * CPR;
+          const int key = t0 + kk;
+          u32x4 val = u32x4{0, 0, 0, 0};
+          if (key < L) {
+            const int pg = s_pages[(key >> 4) - pg_lo];
+            val = *(const u32x4*)(kpb + ((size_t)pg * p.Hkv + kvh) * PAGE_K + (key & 15) * KROWB + cc * 16);
+          } else if (key < T) {
+            val = *(const u32x4*)(knb + (((size_t)s * R + (key - L)) * p.Hkv + kvh) * KROWB + cc * 16);
+            if (rt == 0) {
+              const int pg = s_pages[(key >> 4) - pg_lo];
+              *(u32x4*)(kpb + ((size_t)pg * p.Hkv + kvh) * PAGE_K + (key & 15) * KROWB + cc * 16) = val;
+            }
+          }
+          *(u32x4*)(kb + kk * KROWB + ((cc ^ kswz<CPR>(kk)) << 4)) = val;
+        }
+        for (int ci = tidw; ci < KT / 16 * D * 2; ci += NP * 128) {
+          const int tp = ci / (D * 2);
+          const int d = (ci >> 1) % D;
+          const int hc = ci & 1;
+          const int kbase = t0 + tp * 16 + hc * 8;
+          u32x4 val = u32x4{0, 0, 0, 0};
+          if (kbase + 8 <= L) {
+            const int pg = s_pages[(kbase >> 4) - pg_lo];
+            val = *(const u32x4*)(vpb + ((size_t)pg * p.Hkv + kvh) * PAGE_V + d * 32 + hc * 16);
+          } else {
+            uint16_t e16[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+              const int key = kbase + e;
+              uint16_t x = 0;
+              if (key < L) {
+                const int pg = s_pages[(key >> 4) - pg_lo];
+                x = *(const uint16_t*)(vpb + ((size_t)pg * p.Hkv + kvh) * PAGE_V + d * 32 + (key & 15) * 2);
+              } else if (key < T) {
+                x = *(const uint16_t*)(vnb + (((size_t)s * R + (key - L)) * p.Hkv + kvh) * KROWB + d * 2);
+                if (rt == 0) {
+                  const int pg = s_pages[(key >> 4) - pg_lo];
+                  *(uint16_t*)(vpb + ((size_t)pg * p.Hkv + kvh) * PAGE_V + d * 32 + (key & 15) * 2) = x;
+                }
+              }
+              e16[e] = x;
+            }
+            val = u32x4{e16[0] | ((uint32_t)e16[1] << 16), e16[2] | ((uint32_t)e16[3] << 16),
+                        e16[4] | ((uint32_t)e16[5] << 16), e16[6] | ((uint32_t)e16[7] << 16)};
+          }
+          *(u32x4*)(vb + (tp * D + d) * 32 + ((hc ^ vswz(d)) << 4)) = val;
+        }
+      };
+      const size_t slot = (size_t)it * p.max_segs + kseg;
+
+      if constexpr (PROD) {
+        // =================== producer: QK and softmax ===================
+        bf16x8 qf[2][KS];
+#pragma unroll
+        for (int g = 0; g < 2; ++g)
+#pragma unroll
+          for (int ks = 0; ks < KS; ++ks)
+            qf[g][ks] = rvalid[g]
+                            ? *(const bf16x8*)(q + (((size_t)s * R + rr[g]) * p.Hq + hq[g]) * D + ks * 16 + hh * 8)
+                            : bf16x8{};
+        wait_vmcnt<0>();
+#pragma unroll
+        for (int g = 0; g < 2; ++g)
+#pragma unroll
+          for (int ks = 0; ks < KS; ++ks) asm volatile("" : "+v"(qf[g][ks]));
+        const int krow = kperm(l32);
+        const int kfrag = krow * KROWB + (KXOR ? ((hh ^ kswz<CPR>(krow)) << 4) : 0);
+        const int ksw = kswz<CPR>(krow);
+        float m[2] = {-INFINITY, -INFINITY}, lsum[2] = {0.f, 0.f};
+        f32x16 sacc[2][2];
+
+        auto qk = [&](const char* kst) {
+          const uint32_t kb = lds_addr(kst);
+#pragma unroll
+          for (int g = 0; g < 2; ++g)
+#pragma unroll
+            for (int kg = 0; kg < 2; ++kg) sacc[g][kg] = f32x16{};
+          // read n = ks * 2 + kg: K rows of key group kg, head-dim step ks
+          lds_pipeline<KS * 2, PC_LDS_DEPTH>(
+              [&](auto c) {
+                constexpr int n = decltype(c)::value;
+                constexpr int ks = n / 2, kg = n % 2;
+                const int row_off = kg * 32 * KROWB;
+                const uint32_t a = KXOR ? (kb + (uint32_t)(row_off + (kfrag ^ (ks << 5))))
+                                        : (kb + (uint32_t)(row_off + kfrag + ((((ks << 1) | hh) ^ ksw) << 4)));
+                return lds_read16<0>(a);
+              },
+              [&](auto c, const bf16x8& kf) {
+                constexpr int n = decltype(c)::value;
+                constexpr int ks = n / 2, kg = n % 2;
+                sacc[0][kg] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[0][ks], sacc[0][kg], 0, 0, 0);
+                sacc[1][kg] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[1][ks], sacc[1][kg], 0, 0, 0);
+              });
+        };
+        // softmax of both groups; P (bf16, B-operand order), the rescale
+        // factors and the "some row moved" flag go to the pair's LDS slots
+        auto softmax_out = [&](bool masked, int key0) {
+          bool any_move = false;
+#pragma unroll
+          for (int g = 0; g < 2; ++g) {
+            if (masked) {
+#pragma unroll
+              for (int kg = 0; kg < 2; ++kg)
+#pragma unroll
+                for (int i = 0; i < 16; ++i) {
+                  const int key = key0 + kg * 32 + 16 * (i >> 3) + 8 * hh + (i & 7);
+                  if (key > hi[g]) sacc[g][kg][i] = -INFINITY;
+                }
+            }
+            // tile max: two running max3 chains (one per 32-key group); a
+            // chain keeps the compiler's NaN canonicalization to its head
+            float ma = sacc[g][0][0], mb = sacc[g][1][0];
+#pragma unroll
+            for (int i = 1; i < 16; ++i) {
+              ma = fmaxf(ma, sacc[g][0][i]);
+              mb = fmaxf(mb, sacc[g][1][i]);
+            }
+            float tmax = fmaxf(ma, mb);
+            tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
+            // lazy rescale: the reference maximum moves only by more than
+            // 2^RESCALE_LOG2; the consumer rescales O and l before its next PV
+            const float cand = tmax * p.scale_log2;
+            const bool move = cand > m[g] + RESCALE_LOG2;
+            const float alpha = move ? __builtin_amdgcn_exp2f(m[g] - cand) : 1.f;
+            if (move) m[g] = cand;
+            any_move |= move;
+            if (hh == 0) s_alpha[kp][g][l32] = alpha;
+            const float msafe = (m[g] == -INFINITY) ? 0.f : m[g];
+#pragma unroll
+            for (int t = 0; t < KT / 16; ++t) {
+              uint32_t pk[4];
+#pragma unroll
+              for (int e = 0; e < 4; ++e) {
+                const int i0 = 8 * (t & 1) + 2 * e;
+                const float a0 = __builtin_amdgcn_exp2f(fmaf(sacc[g][t >> 1][i0], p.scale_log2, -msafe));
+                const float a1 = __builtin_amdgcn_exp2f(fmaf(sacc[g][t >> 1][i0 + 1], p.scale_log2, -msafe));
+                pk[e] = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{a0, a1}, bf16x2));
+              }
+              s_P[kp][g][t][lane] = u32x4{pk[0], pk[1], pk[2], pk[3]};
+            }
+          }
+          const bool anyw = __ballot(any_move) != 0;
+          if (lane == 0) s_resc[kp] = anyw ? 1 : 0;
+        };
+
+        for (int ja = j0; ja < j1; ja += SUB_TILES) {
+          const int jb = min(j1, ja + SUB_TILES);
+          stage_pages(ja, jb);
+          const int jm = min(jb, max(ja, L / KT));
+          const int n_main = jm - ja;
+          for (int i = 0; n_main > 0 && i <= n_main; ++i) {
+            pc_barrier();   // A: K(i) landed, P(i-1) taken
+            if (i < n_main) qk(kring + (i % NS) * KTILE_B);
+            pc_barrier();   // B: consumers hold P(i-1)
+            if (i < n_main) softmax_out(false, 0);
+          }
+          for (int jt = jm; jt < jb; ++jt) {
+            __syncthreads();
+            fill_window_tile(jt * KT, ja * 4);
+            __syncthreads();
+            qk(kring);
+            softmax_out(true, jt * KT);
+            __syncthreads();                                 // P of the window tile ready
+            __syncthreads();                                 // consumer done with it
+          }
+        }
+        // segment-final m (l is the consumer's)
+        __syncthreads();                                     // F1
+        if (nseg == 1) continue;
+        float* pml = p.part_ml + slot * (size_t)(2 * RPWG);
+        if (hh == 0) {
+#pragma unroll
+          for (int g = 0; g < 2; ++g)
+            __hip_atomic_store(pml + kp * 64 + g * 32 + l32, m[g], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+        wait_vmcnt<0>();
+        __syncthreads();                                     // F2
+        if (tid == 0)
+          s_flag[0] = (__hip_atomic_fetch_add(&p.counters[it], 1, __ATOMIC_RELAXED,
+                                              __HIP_MEMORY_SCOPE_AGENT) == nseg - 1);
+        __syncthreads();                                     // F3
+        if (s_flag[0] && tid == 0)
+          __hip_atomic_store(&p.counters[it], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        continue;
+      } else {
+        // =================== consumer: loads, O rescale, PV ===================
+        const int vfrag = l32 * 32 + ((hh ^ vswz(l32)) << 4);
+        f32x16 o[2][DG];
+#pragma unroll
+        for (int g = 0; g < 2; ++g)
+#pragma unroll
+          for (int dg = 0; dg < DG; ++dg) o[g][dg] = f32x16{};
+        // l of the lane's two rows over the lane's half of every tile's keys:
+        // the sum of the bf16 weights the PV products use
+        float lrow[2] = {0.f, 0.f};
+        // P of one tile as handed over by the producer (declared per period so
+        // that it is not carried around the tile loop)
+        struct Hand {
+          u32x4 pf[2][4];
+          float alpha[2];
+          int resc;
+        };
+        auto take_p = [&](Hand& hd) {   // P, rescale factors and flag of the producer's last tile
+#pragma unroll
+          for (int g = 0; g < 2; ++g) {
+#pragma unroll
+            for (int t = 0; t < 4; ++t) hd.pf[g][t] = s_P[kp][g][t][lane];
+            hd.alpha[g] = s_alpha[kp][g][l32];
+          }
+          hd.resc = s_resc[kp];
+          __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0): the P reads are done before the barrier
+        };
+        // l: rescale, then add the tile's weights (a bf16 word widens to fp32
+        // exactly: it is the high half).  Vector-ALU work, placed where the
+        // pair's SIMD is busy with the producer's matrix products.
+        auto add_l = [&](const Hand& hd) {
+#pragma unroll
+          for (int g = 0; g < 2; ++g) {
+            float acc = 0.f;
+#pragma unroll
+            for (int t = 0; t < 4; ++t)
+#pragma unroll
+              for (int e = 0; e < 4; ++e)
+                acc += __uint_as_float(hd.pf[g][t][e] << 16) + __uint_as_float(hd.pf[g][t][e] & 0xffff0000u);
+            lrow[g] = fmaf(lrow[g], hd.alpha[g], acc);
+          }
+        };
+        auto pv = [&](const Hand& hd, const char* vst) {
+          if (hd.resc) {
+#pragma unroll
+            for (int g = 0; g < 2; ++g)
+#pragma unroll
+              for (int dg = 0; dg < DG; ++dg) o[g][dg] *= hd.alpha[g];
+          }
+          const uint32_t vb = lds_addr(vst) + (uint32_t)vfrag;
+          // read n = t * DG + dg: V^T rows dg*32.. of key step t
+          lds_pipeline<(KT / 16) * DG, PC_LDS_DEPTH>(
+              [&](auto c) {
+                constexpr int n = decltype(c)::value;
+                constexpr int t = n / DG, dg = n % DG;
+                return lds_read16<(t * D + dg * 32) * 32>(vb);
+              },
+              [&](auto c, const bf16x8& vf) {
+                constexpr int n = decltype(c)::value;
+                constexpr int t = n / DG, dg = n % DG;
+                o[0][dg] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, __builtin_bit_cast(bf16x8, hd.pf[0][t]), o[0][dg], 0, 0, 0);
+                o[1][dg] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, __builtin_bit_cast(bf16x8, hd.pf[1][t]), o[1][dg], 0, 0, 0);
+              });
+        };
+
+        for (int ja = j0; ja < j1; ja += SUB_TILES) {
+          const int jb = min(j1, ja + SUB_TILES);
+          stage_pages(ja, jb);
+          const int jm = min(jb, max(ja, L / KT));
+          const int n_main = jm - ja;
+          // With 4 pairs, consumer wave k copies page k of every 4-page tile
+          // (its K_INS / V_INS 1 KB segments are exactly that page).
+          int kpg = 0, vpg = 0;
+          auto fetch_pages = [&](int gi) {   // group gi = {K(gi+2), V(gi+1)}, clamped
+            const int ik = max(0, min(gi + 2, n_main - 1));
+            const int iv = max(0, min(gi + 1, n_main - 1));
+            kpg = __builtin_amdgcn_readfirstlane(s_pages[ik * 4 + kp]);
+            vpg = __builtin_amdgcn_readfirstlane(s_pages[iv * 4 + kp]);
+          };
+          auto issue_group = [&](int gi) {
+            // page bases are wave-uniform; the per-lane offsets are made opaque
+            // here so that base + offset stays a scalar base plus a 32-bit
+            // vector offset instead of hoisted 64-bit per-lane pointers
+            // (the lane's source offsets within the page are recomputed per group
+            // from an opaque lane index: cheaper than 2 * 4 registers held
+            // across the tile loop)
+            int ln = lane;
+            asm volatile("" : "+v"(ln));
+            {
+              const char* base = kpb + ((size_t)kpg * p.Hkv + kvh) * PAGE_K;
+              char* dst = kring + ((gi + 2 + NS) % NS) * KTILE_B + kp * (K_INS * 1024);
+#pragma unroll
+              for (int j = 0; j < K_INS; ++j) {
+                const int off = j * 1024 + ln * 16;      // byte within the page
+                const int row = off / KROWB;
+                const int cc = ((off % KROWB) >> 4) ^ kswz<CPR>(row);
+                const uint32_t src = (uint32_t)(row * KROWB + cc * 16);
+                __builtin_amdgcn_global_load_lds((const void*)(base + src),
+                    (__attribute__((address_space(3))) void*)(dst + j * 1024), 16, 0, 0);
+              }
+            }
+            {
+              const char* base = vpb + ((size_t)vpg * p.Hkv + kvh) * PAGE_V;
+              char* dst = vring + ((gi + 1 + NS) % NS) * VTILE_B + kp * (V_INS * 1024);
+#pragma unroll
+              for (int j = 0; j < V_INS; ++j) {
+                const int off = j * 1024 + ln * 16;
+                const int d = off >> 5;
+                const int hc = ((off >> 4) & 1) ^ vswz(d);
+                const uint32_t src = (uint32_t)(d * 32 + hc * 16);
+                __builtin_amdgcn_global_load_lds((const void*)(base + src),
+                    (__attribute__((address_space(3))) void*)(dst + j * 1024), 16, 0, 0);
+              }
+            }
+          };
+          if (n_main > 0) {
+            // g(-2) = {K(0), V(-1) re-reading tile 0 into the dead slot}, g(-1);
+            // older stores (a previous segment's output) are drained first so
+            // the counted waits below only count this ring's loads
+            wait_vmcnt<0>();
+            fetch_pages(-2);
+            issue_group(-2);
+            fetch_pages(-1);
+            issue_group(-1);
+            if (n_main >= 2) fetch_pages(0);
+          }
+          for (int i = 0; n_main > 0 && i <= n_main; ++i) {
+            // g(i-1) is in flight (issued) iff i <= n_main - 1
+            if (i <= n_main - 1) wait_vmcnt<NPL>();
+            else wait_vmcnt<0>();
+            pc_barrier();   // A
+            Hand hd;
+            if (i >= 1) take_p(hd);
+            if (i <= n_main - 2) {
+              issue_group(i);
+              if (i + 1 <= n_main - 2) fetch_pages(i + 1);
+            }
+            if (i >= 1) add_l(hd);
+            pc_barrier();   // B
+            if (i >= 1) pv(hd, vring + ((i - 1) % NS) * VTILE_B);
+          }
+          for (int jt = jm; jt < jb; ++jt) {
+            __syncthreads();
+            fill_window_tile(jt * KT, ja * 4);
+            __syncthreads();
+            __syncthreads();                                   // producer's P of the window tile
+            Hand hd;
+            take_p(hd);
+            add_l(hd);
+            pv(hd, vring);
+            __syncthreads();
+          }
+        }
+        __syncthreads();                                       // F1
+#pragma unroll
+        for (int g = 0; g < 2; ++g) lrow[g] += __shfl_xor(lrow[g], 32);
+        auto write_cols = [&](int g, int dg, const f32x16& ov, float inv) {   // columns dg*32..+31
+          if (!rvalid[g]) return;
+          __bf16* orow = out + (((size_t)s * R + rr[g]) * p.Hq + hq[g]) * D;
+#pragma unroll
+          for (int g4 = 0; g4 < 4; ++g4) {
+            const int d = dg * 32 + 8 * g4 + 4 * hh;
+            const f32x2 v01 = f32x2{ov[4 * g4 + 0] * inv, ov[4 * g4 + 1] * inv};
+            const f32x2 v23 = f32x2{ov[4 * g4 + 2] * inv, ov[4 * g4 + 3] * inv};
+            const uint32_t w0 = __builtin_bit_cast(uint32_t, __builtin_convertvector(v01, bf16x2));
+            const uint32_t w1 = __builtin_bit_cast(uint32_t, __builtin_convertvector(v23, bf16x2));
+            *(u32x2*)(orow + d) = u32x2{w0, w1};
+          }
+        };
+        if (nseg == 1) {
+#pragma unroll
+          for (int g = 0; g < 2; ++g)
+#pragma unroll
+            for (int dg = 0; dg < DG; ++dg) write_cols(g, dg, o[g][dg], lrow[g] > 0.f ? 1.f / lrow[g] : 0.f);
+          continue;
+        }
+        {
+          float* po = p.part_o + slot * (size_t)(NC * OREG);
+          if (hh == 0) {
+            float* pml = p.part_ml + slot * (size_t)(2 * RPWG);
+#pragma unroll
+            for (int g = 0; g < 2; ++g)
+              __hip_atomic_store(pml + RPWG + kp * 64 + g * 32 + l32, lrow[g], __ATOMIC_RELAXED,
+                                 __HIP_MEMORY_SCOPE_AGENT);
+          }
+#pragma unroll
+          for (int g = 0; g < 2; ++g)
+#pragma unroll
+            for (int dg = 0; dg < DG; ++dg)
+#pragma unroll
+              for (int i = 0; i < 16; ++i)
+                __hip_atomic_store(po + ((g * DG + dg) * 16 + i) * NC + ct, o[g][dg][i], __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_AGENT);
+        }
+        wait_vmcnt<0>();
+        __syncthreads();                                       // F2
+        __syncthreads();                                       // F3 (counter decided)
+        if (!s_flag[0]) continue;
+        // the last workgroup of the item merges, in segment order, with batched
+        // coherent loads; 16 output columns at a time keeps the merge's
+        // registers small
+        const float* pob = p.part_o + (size_t)it * p.max_segs * (NC * OREG);
+        const float* pmlb = p.part_ml + (size_t)it * p.max_segs * (2 * RPWG);
+#pragma unroll
+        for (int g = 0; g < 2; ++g) {
+          const int rloc = kp * 64 + g * 32 + l32;
+          float M = -INFINITY;
+          for (int c0 = 0; c0 < nseg; c0 += 8) {
+            float mv[8];
+#pragma unroll
+            for (int j = 0; j < 8; ++j)
+              mv[j] = __hip_atomic_load(pmlb + (size_t)min(c0 + j, nseg - 1) * (2 * RPWG) + rloc, __ATOMIC_RELAXED,
+                                        __HIP_MEMORY_SCOPE_AGENT);
+#pragma unroll
+            for (int j = 0; j < 8; ++j) M = fmaxf(M, mv[j]);   // repeats of the last segment are harmless
+          }
+          const float Ms = (M == -INFINITY) ? 0.f : M;
+          float lt = 0.f;
+          for (int c = 0; c < nseg; ++c) {
+            const float mc = __hip_atomic_load(pmlb + (size_t)c * (2 * RPWG) + rloc, __ATOMIC_RELAXED,
+                                               __HIP_MEMORY_SCOPE_AGENT);
+            const float lc = __hip_atomic_load(pmlb + (size_t)c * (2 * RPWG) + RPWG + rloc, __ATOMIC_RELAXED,
+                                               __HIP_MEMORY_SCOPE_AGENT);
+            lt += __builtin_amdgcn_exp2f(mc - Ms) * lc;
+          }
+          const float inv = lt > 0.f ? 1.f / lt : 0.f;
+#pragma unroll
+          for (int dg = 0; dg < DG; ++dg) {
+            f32x16 acc = f32x16{};
+            for (int c = 0; c < nseg; ++c) {
+              // opaque offset: the loads' addresses are formed here rather than
+              // hoisted out of the loop as 16 live address pairs
+              int off = c * (NC * OREG) + (g * DG + dg) * 16 * NC + ct;
+              asm volatile("" : "+v"(off));
+              float v[16];
+#pragma unroll
+              for (int i = 0; i < 16; ++i)
+                v[i] = __hip_atomic_load(pob + off + i * NC, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+              const float mc = __hip_atomic_load(pmlb + (size_t)c * (2 * RPWG) + rloc, __ATOMIC_RELAXED,
+                                                 __HIP_MEMORY_SCOPE_AGENT);
+              const float wgt = __builtin_amdgcn_exp2f(mc - Ms);
+#pragma unroll
+              for (int i = 0; i < 16; ++i) acc[i] += wgt * v[i];
+            }
+            write_cols(g, dg, acc, inv);
+          }
+        }
+      }
+    }
+  };
+  if (prod) segments(IC<1>{});
+  else segments(IC<0>{});
+}
+
+// ---------------------------------------------------------------------------
 // fp32: one workgroup per (sequence, window row, query head); 256 threads.
 // Scores for a 256-key tile in LDS, online softmax over tiles, thread d
 // accumulates output element d.
@@ -726,7 +1414,7 @@ __global__ void __launch_bounds__(256) attn_f32_kernel(AttnParams p) {
 // host side
 // ---------------------------------------------------------------------------
 struct AttnPlan {
-  int nw, rows_total, rows_per_wg, n_row_tiles, n_items, balanced;
+  int nw, rows_total, rows_per_wg, n_row_tiles, n_items, balanced, pc;
   int chunk_tiles, n_chunks_max, share_min, max_segs, grid;
   size_t off_counters, off_ml, off_o, bytes;
 };
@@ -751,10 +1439,15 @@ static AttnPlan plan_attn(int S, int R, int Hq, int Hkv, int D, int max_pages, i
   AttnPlan pl{};
   const int G = Hq / Hkv;
   pl.rows_total = R * G;
+  pl.balanced = (chunk_keys == 0 && S <= BAL_MAX_SEQS) ? 1 : 0;
   if (dtype == DVS_BF16) {
     const int groups = (pl.rows_total + 31) / 32;   // 32-row MFMA groups
     pl.nw = groups >= 8 ? 8 : (groups >= 4 ? 4 : (groups >= 2 ? 2 : 1));
     if (D == 96 && pl.nw > 4) pl.nw = 4;   // a 96-wide tile splits over at most 4 waves
+    // wide windows in the balanced split: producer/consumer pairs, 4 pairs
+    // (8 waves, one producer and one consumer per SIMD) over 256 rows
+    pl.pc = (pl.balanced && pl.rows_total > 128) ? 1 : 0;
+    if (pl.pc) pl.nw = 8;
   } else {
     pl.nw = 4;
   }
@@ -762,7 +1455,6 @@ static AttnPlan plan_attn(int S, int R, int Hq, int Hkv, int D, int max_pages, i
   pl.n_row_tiles = (pl.rows_total + pl.rows_per_wg - 1) / pl.rows_per_wg;
   pl.n_items = S * Hkv * pl.n_row_tiles;
   const int max_tiles = (max_pages * DVS_PAGE_SIZE + KT - 1) / KT;
-  pl.balanced = (chunk_keys == 0 && S <= BAL_MAX_SEQS) ? 1 : 0;
   if (pl.balanced) {
     pl.share_min = (max_tiles + BAL_MAX_SEGS - 2) / (BAL_MAX_SEGS - 1);
     if (pl.share_min < 1) pl.share_min = 1;
@@ -790,6 +1482,10 @@ static AttnPlan plan_attn(int S, int R, int Hq, int Hkv, int D, int max_pages, i
 
 template <int D>
 static void launch_bf16(const AttnPlan& pl, const AttnParams& prm, hipStream_t st) {
+  if (pl.pc) {
+    hipLaunchKernelGGL((attn_bf16_pc_kernel<D, 4>), dim3(pl.grid), dim3(512), 0, st, prm);
+    return;
+  }
   switch (pl.nw) {
     case 8:
       if constexpr (D != 96)

@@ -57,6 +57,12 @@ CASES = [
     ("d64_wide", 35, 2, [300, 77], 32, 32, 8, 2, 64, "bf16", 0),
     ("d64_wide_aligned", 36, 3, [5, 300, 1200], 16, 16, 8, 2, 64, "bf16", 128),
     ("d128_aligned_narrow", 37, 2, [700, 33], 4, 4, 8, 2, 128, "bf16", 256),
+    # wide windows in the balanced split (the producer/consumer kernel):
+    # ragged lengths incl. an empty cache, head_dim 96, two row tiles with a
+    # partly filled second one
+    ("pc_d128_ragged", 38, 3, [0, 77, 5000], 32, 32, 16, 4, 128, "bf16", 0),
+    ("pc_d96_wide", 39, 2, [1500, 3000], 48, 16, 16, 4, 96, "bf16", 0),
+    ("pc_d128_two_row_tiles", 40, 2, [900, 2100], 40, 40, 16, 4, 128, "bf16", 0),
 ]
 
 
@@ -127,6 +133,14 @@ def test_mask_rows_do_not_change_causal_rows():
 def test_bad_page_reported_without_fault():
     ai = synth.make_attn_inputs(44, 2, [200, 64], 4, 4, 8, 2, 64, "bf16", scatter=True)
     ai.state.page_table[1, 1] = 10 ** 6
+    err = torch.zeros(1, dtype=torch.int32, device="cuda")
+    _run(ai, 0, err=err)
+    assert int(err.item()) & dvs.ERR_BAD_PAGE
+
+
+def test_bad_page_reported_without_fault_wide_window():
+    ai = synth.make_attn_inputs(46, 2, [900, 64], 32, 32, 8, 2, 128, "bf16", scatter=True)
+    ai.state.page_table[0, 3] = -5
     err = torch.zeros(1, dtype=torch.int32, device="cuda")
     _run(ai, 0, err=err)
     assert int(err.item()) & dvs.ERR_BAD_PAGE
