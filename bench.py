@@ -241,7 +241,7 @@ def main():
         "roofline": {
             "bound": "hbm", "achieved": round(attn_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": round(attn_gbs / HBM_PEAK_GBS, 4), "traffic": traffic,
-            "kernel": "attn_bf16_kernel<128,8> (head_dim, waves)", "algorithmic_bytes": attn_bytes,
+            "kernel": "attn_bf16_pc_kernel<128,4> (head_dim, producer/consumer pairs)", "algorithmic_bytes": attn_bytes,
             "avg_ms": round(stage_ms["attn"], 4),
         },
         "breakdown_ms": {k: round(v, 4) for k, v in stage_ms.items()},

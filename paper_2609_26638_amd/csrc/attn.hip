@@ -138,6 +138,106 @@ __device__ __forceinline__ void wait_tiles(int tiles_after) {
   else wait_vmcnt<0>();
 }
 
+// ---------------------------------------------------------------------------
+// A tile that reaches the window [L, T) or runs past T, staged through
+// registers into the K / V LDS tiles (kb, vb): keys < L from the pool,
+// [L, T) from k_new / v_new (and, when `append`, written to their pool
+// slots), >= T zero.  Every load of a thread is issued before any of its
+// stores (a pool append could alias a pool read as far as the compiler can
+// tell, which would otherwise serialize one memory round trip per element);
+// invalid elements read a harmless in-bounds address and are zeroed after.
+// ---------------------------------------------------------------------------
+template <int D, int NT>
+__device__ __forceinline__ void fill_window_tile(int tid, int t0, int pg_lo, int L, int T, int s, int R,
+                                                 int Hkv, int kvh, bool append, const int* s_pages,
+                                                 char* __restrict__ kpb, char* __restrict__ vpb,
+                                                 const char* __restrict__ knb, const char* __restrict__ vnb,
+                                                 char* kb, char* vb) {
+  constexpr int CPR = D / 8;
+  constexpr int KROWB = D * 2;
+  constexpr int PAGE_K = 16 * KROWB;
+  constexpr int PAGE_V = D * 32;
+  constexpr int NKC = KT * CPR;              // 16-byte K chunks per tile
+  constexpr int NKI = (NKC + NT - 1) / NT;
+  constexpr int NVC = KT / 16 * D * 2;       // 16-byte V chunks (8 keys of one head-dim row)
+  constexpr int NVI = (NVC + NT - 1) / NT;
+  // ---- K, in batches of up to KB chunks per thread
+  constexpr int KB = NKI < 4 ? NKI : 4;
+#pragma unroll 1
+  for (int k0 = 0; k0 < NKI; k0 += KB) {
+    u32x4 kv[KB];
+#pragma unroll
+    for (int k = 0; k < KB; ++k) {
+      const int ci = tid + (k0 + k) * NT;
+      const int kk = ci / CPR, cc = ci - (ci / CPR) * CPR;
+      const int key = t0 + kk;
+      const char* src = knb;
+      bool valid = false;
+      if (ci < NKC && key < L) {
+        src = kpb + ((size_t)s_pages[(key >> 4) - pg_lo] * Hkv + kvh) * PAGE_K + (key & 15) * KROWB + cc * 16;
+        valid = true;
+      } else if (ci < NKC && key < T) {
+        src = knb + (((size_t)s * R + (key - L)) * Hkv + kvh) * KROWB + cc * 16;
+        valid = true;
+      }
+      const u32x4 x = *(const u32x4*)src;
+      kv[k] = valid ? x : u32x4{0, 0, 0, 0};
+    }
+#pragma unroll
+    for (int k = 0; k < KB; ++k) {
+      const int ci = tid + (k0 + k) * NT;
+      if (ci >= NKC) break;
+      const int kk = ci / CPR, cc = ci - (ci / CPR) * CPR;
+      const int key = t0 + kk;
+      *(u32x4*)(kb + kk * KROWB + ((cc ^ kswz<CPR>(kk)) << 4)) = kv[k];
+      if (append && key >= L && key < T)
+        *(u32x4*)(kpb + ((size_t)s_pages[(key >> 4) - pg_lo] * Hkv + kvh) * PAGE_K + (key & 15) * KROWB + cc * 16) = kv[k];
+    }
+  }
+  // ---- V (head-dim-major rows of 16 keys)
+#pragma unroll 1
+  for (int k = 0; k < NVI; ++k) {
+    const int ci = tid + k * NT;
+    if (ci >= NVC) break;
+    const int tp = ci / (D * 2);
+    const int d = (ci >> 1) % D;
+    const int hc = ci & 1;
+    const int kbase = t0 + tp * 16 + hc * 8;
+    u32x4 val;
+    if (kbase + 8 <= L) {
+      val = *(const u32x4*)(vpb + ((size_t)s_pages[(kbase >> 4) - pg_lo] * Hkv + kvh) * PAGE_V + d * 32 + hc * 16);
+    } else {
+      uint16_t e16[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int key = kbase + e;
+        const char* src = vnb;
+        bool valid = false;
+        if (key < L) {
+          src = vpb + ((size_t)s_pages[(key >> 4) - pg_lo] * Hkv + kvh) * PAGE_V + d * 32 + (key & 15) * 2;
+          valid = true;
+        } else if (key < T) {
+          src = vnb + (((size_t)s * R + (key - L)) * Hkv + kvh) * KROWB + d * 2;
+          valid = true;
+        }
+        const uint16_t x = *(const uint16_t*)src;
+        e16[e] = valid ? x : (uint16_t)0;
+      }
+      if (append) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const int key = kbase + e;
+          if (key >= L && key < T)
+            *(uint16_t*)(vpb + ((size_t)s_pages[(key >> 4) - pg_lo] * Hkv + kvh) * PAGE_V + d * 32 + (key & 15) * 2) = e16[e];
+        }
+      }
+      val = u32x4{e16[0] | ((uint32_t)e16[1] << 16), e16[2] | ((uint32_t)e16[3] << 16),
+                  e16[4] | ((uint32_t)e16[5] << 16), e16[6] | ((uint32_t)e16[7] << 16)};
+    }
+    *(u32x4*)(vb + (tp * D + d) * 32 + ((hc ^ vswz(d)) << 4)) = val;
+  }
+}
+
 template <int N>
 struct IC {
   static constexpr int value = N;
@@ -536,57 +636,8 @@ __global__ void __launch_bounds__(NW * 64, 1) attn_bf16_kernel(AttnParams p) {
       for (int jt = jm; jt < jb; ++jt) {
         const int t0 = jt * KT;
         __syncthreads();
-        char* kb = smem;
-        char* vb = smem + KTILE_B;
-        for (int ci = tid; ci < KT * CPR; ci += NT) {
-          const int kk = ci / CPR;
-          const int cc = ci - kk * CPR;
-          const int key = t0 + kk;
-          u32x4 val = u32x4{0, 0, 0, 0};
-          if (key < L) {
-            const int pg = s_pages[(key >> 4) - pg_lo];
-            val = *(const u32x4*)(kpb + ((size_t)pg * p.Hkv + kvh) * PAGE_K + (key & 15) * KROWB + cc * 16);
-          } else if (key < T) {
-            val = *(const u32x4*)(knb + (((size_t)s * R + (key - L)) * p.Hkv + kvh) * KROWB + cc * 16);
-            if (rt == 0) {
-              const int pg = s_pages[(key >> 4) - pg_lo];
-              *(u32x4*)(kpb + ((size_t)pg * p.Hkv + kvh) * PAGE_K + (key & 15) * KROWB + cc * 16) = val;
-            }
-          }
-          *(u32x4*)(kb + kk * KROWB + ((cc ^ kswz<CPR>(kk)) << 4)) = val;
-        }
-        for (int ci = tid; ci < KT / 16 * D * 2; ci += NT) {
-          const int tp = ci / (D * 2);
-          const int d = (ci >> 1) % D;
-          const int hc = ci & 1;
-          const int kbase = t0 + tp * 16 + hc * 8;
-          u32x4 val = u32x4{0, 0, 0, 0};
-          if (kbase + 8 <= L) {
-            const int pg = s_pages[(kbase >> 4) - pg_lo];
-            val = *(const u32x4*)(vpb + ((size_t)pg * p.Hkv + kvh) * PAGE_V + d * 32 + hc * 16);
-          } else {
-            uint16_t e16[8];
-#pragma unroll
-            for (int e = 0; e < 8; ++e) {
-              const int key = kbase + e;
-              uint16_t x = 0;
-              if (key < L) {
-                const int pg = s_pages[(key >> 4) - pg_lo];
-                x = *(const uint16_t*)(vpb + ((size_t)pg * p.Hkv + kvh) * PAGE_V + d * 32 + (key & 15) * 2);
-              } else if (key < T) {
-                x = *(const uint16_t*)(vnb + (((size_t)s * R + (key - L)) * p.Hkv + kvh) * KROWB + d * 2);
-                if (rt == 0) {
-                  const int pg = s_pages[(key >> 4) - pg_lo];
-                  *(uint16_t*)(vpb + ((size_t)pg * p.Hkv + kvh) * PAGE_V + d * 32 + (key & 15) * 2) = x;
-                }
-              }
-              e16[e] = x;
-            }
-            val = u32x4{e16[0] | ((uint32_t)e16[1] << 16), e16[2] | ((uint32_t)e16[3] << 16),
-                        e16[4] | ((uint32_t)e16[5] << 16), e16[6] | ((uint32_t)e16[7] << 16)};
-          }
-          *(u32x4*)(vb + (tp * D + d) * 32 + ((hc ^ vswz(d)) << 4)) = val;
-        }
+        fill_window_tile<D, NT>(tid, t0, pg_lo, L, T, s, R, p.Hkv, kvh, rt == 0, s_pages, kpb, vpb, knb, vnb,
+                                smem, smem + KTILE_B);
         __syncthreads();
         compute_tile(smem, t0, true);
       }
@@ -855,60 +906,11 @@ __global__ void __launch_bounds__(NP * 128, 1) attn_bf16_pc_kernel(AttnParams p)
       // window tiles (reach [L, T) or past it): every thread stages them,
       // keys < L from the pool, [L, T) from k_new / v_new (appended to the pool
       // by row tile 0), >= T zero; K into K slot 0, V into V slot 0
-      auto fill_window_tile = [&](int t0, int pg_lo) {
+      auto fill_window = [&](int t0, int pg_lo) {
         int tidw = tidv;   // opaque: nothing of the fill is hoisted out of it
         asm volatile("" : "+v"(tidw));
-        char* kb = kring;
-        char* vb = vring;
-        for (int ci = tidw; ci < KT * CPR; ci += NP * 128) {
-          const int kk = ci / CPR;
-          const int cc = ci - kk * CPR;
-          const int key = t0 + kk;
-          u32x4 val = u32x4{0, 0, 0, 0};
-          if (key < L) {
-            const int pg = s_pages[(key >> 4) - pg_lo];
-            val = *(const u32x4*)(kpb + ((size_t)pg * p.Hkv + kvh) * PAGE_K + (key & 15) * KROWB + cc * 16);
-          } else if (key < T) {
-            val = *(const u32x4*)(knb + (((size_t)s * R + (key - L)) * p.Hkv + kvh) * KROWB + cc * 16);
-            if (rt == 0) {
-              const int pg = s_pages[(key >> 4) - pg_lo];
-              *(u32x4*)(kpb + ((size_t)pg * p.Hkv + kvh) * PAGE_K + (key & 15) * KROWB + cc * 16) = val;
-            }
-          }
-          *(u32x4*)(kb + kk * KROWB + ((cc ^ kswz<CPR>(kk)) << 4)) = val;
-        }
-        for (int ci = tidw; ci < KT / 16 * D * 2; ci += NP * 128) {
-          const int tp = ci / (D * 2);
-          const int d = (ci >> 1) % D;
-          const int hc = ci & 1;
-          const int kbase = t0 + tp * 16 + hc * 8;
-          u32x4 val = u32x4{0, 0, 0, 0};
-          if (kbase + 8 <= L) {
-            const int pg = s_pages[(kbase >> 4) - pg_lo];
-            val = *(const u32x4*)(vpb + ((size_t)pg * p.Hkv + kvh) * PAGE_V + d * 32 + hc * 16);
-          } else {
-            uint16_t e16[8];
-#pragma unroll
-            for (int e = 0; e < 8; ++e) {
-              const int key = kbase + e;
-              uint16_t x = 0;
-              if (key < L) {
-                const int pg = s_pages[(key >> 4) - pg_lo];
-                x = *(const uint16_t*)(vpb + ((size_t)pg * p.Hkv + kvh) * PAGE_V + d * 32 + (key & 15) * 2);
-              } else if (key < T) {
-                x = *(const uint16_t*)(vnb + (((size_t)s * R + (key - L)) * p.Hkv + kvh) * KROWB + d * 2);
-                if (rt == 0) {
-                  const int pg = s_pages[(key >> 4) - pg_lo];
-                  *(uint16_t*)(vpb + ((size_t)pg * p.Hkv + kvh) * PAGE_V + d * 32 + (key & 15) * 2) = x;
-                }
-              }
-              e16[e] = x;
-            }
-            val = u32x4{e16[0] | ((uint32_t)e16[1] << 16), e16[2] | ((uint32_t)e16[3] << 16),
-                        e16[4] | ((uint32_t)e16[5] << 16), e16[6] | ((uint32_t)e16[7] << 16)};
-          }
-          *(u32x4*)(vb + (tp * D + d) * 32 + ((hc ^ vswz(d)) << 4)) = val;
-        }
+        fill_window_tile<D, NP * 128>(tidw, t0, pg_lo, L, T, s, R, p.Hkv, kvh, rt == 0, s_pages, kpb, vpb, knb,
+                                      vnb, kring, vring);
       };
       const size_t slot = (size_t)it * p.max_segs + kseg;
 
@@ -1020,7 +1022,7 @@ __global__ void __launch_bounds__(NP * 128, 1) attn_bf16_pc_kernel(AttnParams p)
           }
           for (int jt = jm; jt < jb; ++jt) {
             __syncthreads();
-            fill_window_tile(jt * KT, ja * 4);
+            fill_window(jt * KT, ja * 4);
             __syncthreads();
             qk(kring);
             softmax_out(true, jt * KT);
@@ -1190,7 +1192,7 @@ __global__ void __launch_bounds__(NP * 128, 1) attn_bf16_pc_kernel(AttnParams p)
           }
           for (int jt = jm; jt < jb; ++jt) {
             __syncthreads();
-            fill_window_tile(jt * KT, ja * 4);
+            fill_window(jt * KT, ja * 4);
             __syncthreads();
             __syncthreads();                                   // producer's P of the window tile
             Hand hd;

@@ -83,7 +83,7 @@ def main():
     t.add_argument("--fetch", required=True, help="output directory of the FETCH_SIZE run")
     t.add_argument("--write", required=True, help="output directory of the WRITE_SIZE run")
     t.add_argument("--meta", required=True, help="the JSON line bench.py --profile-attn printed")
-    t.add_argument("--kernel", default="attn_bf16_kernel")
+    t.add_argument("--kernel", default="attn_bf16")
     t.add_argument("--command", required=True)
     t.add_argument("--out", required=True)
     a = ap.parse_args()
