@@ -2,26 +2,21 @@
 //
 // Top-1 (the verifier's greedy prediction; appendix "AR-Equivalence and
 // Equality Testing" uses top-1 decoding): the largest logit wins, the lowest
-// index among equal maxima, -0.0 == +0.0.  Each value is mapped to an
-// order-preserving unsigned key (sign-magnitude -> two's-complement order)
-// after folding -0.0 onto +0.0; (key, index) pairs are reduced with
-// "larger key, then smaller index" packed into one 64-bit max.
+// index among equal maxima, -0.0 == +0.0.  Each thread keeps its first
+// maximum (values compared as floats); the per-thread winners are mapped to
+// order-preserving unsigned keys (sign-magnitude -> two's-complement order,
+// -0.0 folded onto +0.0) and reduced with "larger key, then smaller index"
+// packed into one 64-bit max.
 //
 // Acceptance (method "Self-Speculative Decoding"; appendix item Accept):
 // a_j = top1(row j-1); A = longest prefix of the draft with d_j == a_j.
 //
 // The argmax is a pure HBM stream: one workgroup per row, 16-byte loads with
-// several in flight per thread, wavefront shuffles, then LDS across waves.
+// several in flight per thread, about two vector instructions per element
+// (max3 chain, NaN/infinity probe), wavefront shuffles, then LDS across waves.
 #include "dvs_common.h"
 
 namespace dvs {
-
-__device__ __forceinline__ uint32_t key_bf16(uint32_t b, bool& nonfinite) {
-  b &= 0xffffu;
-  if ((b & 0x7fffu) == 0) b = 0;                        // -0.0 -> +0.0
-  if ((b & 0x7f80u) == 0x7f80u) nonfinite = true;
-  return (b & 0x8000u) ? (~b & 0xffffu) : (b | 0x8000u);
-}
 
 __device__ __forceinline__ uint32_t key_f32(uint32_t u, bool& nonfinite) {
   if ((u & 0x7fffffffu) == 0) u = 0;
@@ -41,6 +36,16 @@ __device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int m) {
 }
 
 template <bool BF16>
+__device__ __forceinline__ float elem_f(const u32x4& x, int e) {
+  if constexpr (BF16) {
+    const uint32_t w = x[e >> 1];
+    return __uint_as_float((e & 1) ? (w & 0xffff0000u) : (w << 16));   // bf16 -> fp32 is exact
+  } else {
+    return __uint_as_float(x[e]);
+  }
+}
+
+template <bool BF16>
 __global__ void __launch_bounds__(256) argmax_kernel(const void* __restrict__ logits, int V,
                                                      int32_t* __restrict__ argmax_out,
                                                      int32_t* err) {
@@ -50,11 +55,17 @@ __global__ void __launch_bounds__(256) argmax_kernel(const void* __restrict__ lo
   const size_t row = blockIdx.x;
   const int tid = threadIdx.x;
   const char* base = (const char*)logits + row * (size_t)V * (BF16 ? 2 : 4);
-  bool nonfinite = false;
-  uint32_t bk = 0;
+  // Every thread visits its elements in increasing index order, so its first
+  // maximum is kept by a strict comparison.  Values are compared as floats
+  // (-0.0 == +0.0); a NaN never wins a comparison, and x * 0 turns any NaN or
+  // infinity into a NaN in `nf`, which flags the row.
+  float best = -INFINITY;
   int bi = 0x7fffffff;
+  float nf = 0.f;
 
-  // vectorised body when the row start is 16-byte aligned
+  // vectorised body when the row start is 16-byte aligned: per batch of UNR
+  // vectors, a running max3 chain; only a batch that beats the thread's best
+  // is scanned again for the position of its first maximum
   const bool aligned = ((((uintptr_t)base) & 15) == 0);
   const int nvec = aligned ? V / EPV : 0;
   int v0 = 0;
@@ -62,43 +73,51 @@ __global__ void __launch_bounds__(256) argmax_kernel(const void* __restrict__ lo
     u32x4 buf[UNR];
 #pragma unroll
     for (int u = 0; u < UNR; ++u) buf[u] = ((const u32x4*)base)[v0 + u * 256 + tid];
+    float bm = -INFINITY;
 #pragma unroll
-    for (int u = 0; u < UNR; ++u) {
-      const int e0 = (v0 + u * 256 + tid) * EPV;
+    for (int u = 0; u < UNR; ++u)
 #pragma unroll
       for (int e = 0; e < EPV; ++e) {
-        const uint32_t w = buf[u][BF16 ? (e >> 1) : e];
-        const uint32_t bits = BF16 ? ((e & 1) ? (w >> 16) : (w & 0xffffu)) : w;
-        const uint32_t k = BF16 ? key_bf16(bits, nonfinite) : key_f32(bits, nonfinite);
-        if (k > bk) { bk = k; bi = e0 + e; }
+        const float x = elem_f<BF16>(buf[u], e);
+        bm = fmaxf(bm, x);
+        nf = fmaf(x, 0.f, nf);
       }
+    if (bm > best) {
+      int at = 0x7fffffff;
+#pragma unroll
+      for (int u = UNR - 1; u >= 0; --u)
+#pragma unroll
+        for (int e = EPV - 1; e >= 0; --e)
+          if (elem_f<BF16>(buf[u], e) == bm) at = (v0 + u * 256 + tid) * EPV + e;
+      best = bm;
+      bi = at;
     }
   }
   for (int vi = v0 + tid; vi < nvec; vi += 256) {
     const u32x4 x = ((const u32x4*)base)[vi];
 #pragma unroll
     for (int e = 0; e < EPV; ++e) {
-      const uint32_t w = x[BF16 ? (e >> 1) : e];
-      const uint32_t bits = BF16 ? ((e & 1) ? (w >> 16) : (w & 0xffffu)) : w;
-      const uint32_t k = BF16 ? key_bf16(bits, nonfinite) : key_f32(bits, nonfinite);
-      if (k > bk) { bk = k; bi = vi * EPV + e; }
+      const float f = elem_f<BF16>(x, e);
+      nf = fmaf(f, 0.f, nf);
+      if (f > best) { best = f; bi = vi * EPV + e; }
     }
   }
   // scalar tail (and the whole row when unaligned)
   for (int i = nvec * EPV + tid; i < V; i += 256) {
-    uint32_t k;
-    if (BF16) k = key_bf16(((const uint16_t*)base)[i], nonfinite);
-    else k = key_f32(((const uint32_t*)base)[i], nonfinite);
-    if (k > bk || (k == bk && i < bi)) { bk = k; bi = i; }
+    const float f = BF16 ? __uint_as_float((uint32_t)((const uint16_t*)base)[i] << 16)
+                         : ((const float*)base)[i];
+    nf = fmaf(f, 0.f, nf);
+    if (f > best) { best = f; bi = i; }
   }
 
-  uint64_t best = (bi == 0x7fffffff) ? 0 : pack_ki(bk, bi);
+  bool nonfinite = nf != nf;
+  uint64_t bp = (bi == 0x7fffffff) ? 0 : pack_ki(key_f32(__float_as_uint(best), nonfinite), bi);
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) {
-    const uint64_t o = shfl_xor_u64(best, off);
-    best = o > best ? o : best;
+    const uint64_t o = shfl_xor_u64(bp, off);
+    bp = o > bp ? o : bp;
   }
-  if ((tid & 63) == 0) sred[tid >> 6] = best;
+  if ((tid & 63) == 0) sred[tid >> 6] = bp;
   if (nonfinite) set_err(err, DVS_ERR_NONFINITE);
   __syncthreads();
   if (tid == 0) {

@@ -33,9 +33,11 @@ def test_argmax_accept_planted_bf16(S, B, V, p):
     assert err == 0
 
 
-@pytest.mark.parametrize("dtype,V", [("f32", 37), ("f32", 4096), ("bf16", 37), ("bf16", 4099)])
-def test_argmax_ties_and_signed_zero(dtype, V):
-    x = synth.tied_logits(11, 4, 6, V)
+@pytest.mark.parametrize("dtype,V,levels", [("f32", 37, 4), ("f32", 4096, 4), ("bf16", 37, 4), ("bf16", 4099, 4),
+                                            ("bf16", 65536, 4), ("f32", 16384, 4), ("bf16", 65536, 2),
+                                            ("f32", 16384, 2)])
+def test_argmax_ties_and_signed_zero(dtype, V, levels):
+    x = synth.tied_logits(11, 4, 6, V, levels=levels)
     if dtype == "bf16":
         x = synth.f32_to_bf16_bits(x)
         ref = od.top1_rows(synth.bf16_to_f64(x))
@@ -62,6 +64,34 @@ def test_argmax_nonfinite_flagged():
     x[0, 1, 9] = np.nan
     _, _, err = _argmax(x, "f32", 1, np.zeros((1, 0), np.int32))
     assert err & dvs.ERR_NONFINITE
+
+
+@pytest.mark.parametrize("bits", [0x7FC0, 0xFFC0, 0x7F80, 0xFF80], ids=["nan", "neg_nan", "inf", "neg_inf"])
+def test_argmax_nonfinite_flagged_long_bf16_row(bits):
+    """A NaN or an infinity deep inside a vocabulary-sized bf16 row (the
+    batched vector path) raises the flag."""
+    x = synth.f32_to_bf16_bits(np.random.default_rng(3).standard_normal((1, 2, 65536)).astype(np.float32))
+    x[0, 1, 40001] = bits
+    _, _, err = _argmax(x, "bf16", 1, np.zeros((1, 0), np.int32))
+    assert err & dvs.ERR_NONFINITE
+
+
+def test_argmax_ties_in_vectorized_path_bf16():
+    """Equal maxima planted at two positions of 65536-wide rows: in one 16-byte
+    vector, in one thread's batch, across threads, across batches, at the row
+    ends.  The lowest index must win."""
+    pairs = [(100, 103), (8 * 5, 8 * (5 + 256)), (8 * 7 + 2, 8 * 8 + 1), (8 * 9, 8 * (9 + 2048)),
+             (3, 65535), (0, 65535), (8 * 2047 + 7, 8 * 4095 + 7)]
+    rng = np.random.default_rng(4)
+    x = np.clip(rng.standard_normal((1, len(pairs), 65536)), -6, 6).astype(np.float32)
+    for r, (a, b) in enumerate(pairs):
+        x[0, r, a] = 7.5
+        x[0, r, b] = 7.5
+    xb = synth.f32_to_bf16_bits(x)
+    am, _, err = _argmax(xb, "bf16", 1, np.zeros((1, 0), np.int32))
+    ref = od.top1_rows(synth.bf16_to_f64(xb))
+    np.testing.assert_array_equal(am, ref)
+    assert [int(v) for v in am[0]] == [min(a, b) for a, b in pairs] and err == 0
 
 
 def _dev_state(st):
