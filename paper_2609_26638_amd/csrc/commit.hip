@@ -19,6 +19,7 @@
 namespace dvs {
 
 constexpr int COMMIT_THREADS = 1024;
+constexpr int RUN_CHUNK = 8;
 
 __device__ __forceinline__ int block_exclusive_scan(int v, int* sh, int& total) {
   // Hillis-Steele over the block in shared memory (S <= 1024; runs once).
@@ -78,13 +79,25 @@ __global__ void __launch_bounds__(COMMIT_THREADS) kv_commit_kernel(CommitParams 
     if (!fin) {
       A = p.accept_len[s];
       A = A < 0 ? 0 : (A > p.n_causal - 1 ? p.n_causal - 1 : A);
-      // run = d_1..d_A, a_{A+1}; keep up to the first stop token / budget
-      for (int j = 0; j <= A; ++j) {
-        if (cnt + k >= p.max_new) { stop = true; break; }
-        const int tok = run_token(p, s, A, j);
-        ++k;
-        last_tok = tok;
-        if (p.eos_id >= 0 && tok == p.eos_id) { stop = true; break; }
+      // run = d_1..d_A, a_{A+1}; keep up to the first stop token / budget.
+      // Tokens are fetched RUN_CHUNK at a time (independent loads, one memory
+      // round trip per chunk), then scanned in order.
+      bool done = false;
+      for (int j0 = 0; j0 <= A && !done; j0 += RUN_CHUNK) {
+        int tk[RUN_CHUNK];
+#pragma unroll
+        for (int u = 0; u < RUN_CHUNK; ++u) tk[u] = run_token(p, s, A, min(j0 + u, A));
+#pragma unroll
+        for (int u = 0; u < RUN_CHUNK; ++u) {
+          if (done || j0 + u > A) continue;
+          if (cnt + k >= p.max_new) {
+            stop = done = true;
+          } else {
+            ++k;
+            last_tok = tk[u];
+            if (p.eos_id >= 0 && tk[u] == p.eos_id) stop = done = true;
+          }
+        }
       }
       if (cnt + k >= p.max_new) stop = true;
     }
@@ -127,13 +140,28 @@ __global__ void __launch_bounds__(COMMIT_THREADS) kv_commit_kernel(CommitParams 
     p.num_pages[s] = need;
     if (!fin) {
       int32_t* ot = p.out_tokens + (size_t)s * p.max_new;
-      for (int j = 0; j < k; ++j) ot[cnt + j] = run_token(p, s, A, j);
+      for (int j0 = 0; j0 < k; j0 += RUN_CHUNK) {   // loads of a chunk first, then its stores
+        int tk[RUN_CHUNK];
+#pragma unroll
+        for (int u = 0; u < RUN_CHUNK; ++u) tk[u] = run_token(p, s, A, min(j0 + u, k - 1));
+#pragma unroll
+        for (int u = 0; u < RUN_CHUNK; ++u)
+          if (j0 + u < k) ot[cnt + j0 + u] = tk[u];
+      }
       p.out_count[s] = cnt + k;
       p.kv_len[s] = L + k;
       if (k > 0) p.boundary[s] = last_tok;
-      if (p.n_mask > 0)
-        for (int j = 0; j < p.draft_width; ++j)
-          p.draft[(size_t)s * p.draft_width + j] = p.argmax[(size_t)s * p.R + p.n_causal + j];
+      if (p.n_mask > 0) {
+        for (int j0 = 0; j0 < p.draft_width; j0 += RUN_CHUNK) {
+          int tk[RUN_CHUNK];
+#pragma unroll
+          for (int u = 0; u < RUN_CHUNK; ++u)
+            tk[u] = p.argmax[(size_t)s * p.R + p.n_causal + min(j0 + u, p.draft_width - 1)];
+#pragma unroll
+          for (int u = 0; u < RUN_CHUNK; ++u)
+            if (j0 + u < p.draft_width) p.draft[(size_t)s * p.draft_width + j0 + u] = tk[u];
+        }
+      }
       p.finished[s] = stop ? 1 : 0;
     }
   }
