@@ -913,6 +913,90 @@ __global__ void __launch_bounds__(NP * 128, 1) attn_bf16_pc_kernel(AttnParams p)
                                       vnb, kring, vring);
       };
       const size_t slot = (size_t)it * p.max_segs + kseg;
+      // Merge of a split item by its last workgroup, all 512 threads: rows'
+      // segment weights exp2(m_c - M) / sum_c exp2(m_c - M) l_c go to LDS
+      // (the K ring is idle by then), then every thread combines whole runs
+      // of 4 output columns of one row, in segment order, with batched
+      // coherent loads, and stores them as 8 bf16 bytes.
+      auto merge_all = [&]() {
+        const float* pob = p.part_o + (size_t)it * p.max_segs * (NC * OREG);
+        const float* pmlb = p.part_ml + (size_t)it * p.max_segs * (2 * RPWG);
+        float* s_w = (float*)kring;   // [BAL_MAX_SEGS][RPWG]
+        if (tid < RPWG) {
+          float mv[BAL_MAX_SEGS], lv[BAL_MAX_SEGS];
+#pragma unroll
+          for (int c = 0; c < BAL_MAX_SEGS; ++c) {
+            const int cc = min(c, nseg - 1);
+            mv[c] = __hip_atomic_load(pmlb + (size_t)cc * (2 * RPWG) + tid, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            lv[c] = __hip_atomic_load(pmlb + (size_t)cc * (2 * RPWG) + RPWG + tid, __ATOMIC_RELAXED,
+                                      __HIP_MEMORY_SCOPE_AGENT);
+          }
+          float M = -INFINITY;
+#pragma unroll
+          for (int c = 0; c < BAL_MAX_SEGS; ++c) M = fmaxf(M, mv[c]);   // repeats of the last segment are harmless
+          const float Ms = (M == -INFINITY) ? 0.f : M;
+          float lt = 0.f;
+#pragma unroll
+          for (int c = 0; c < BAL_MAX_SEGS; ++c)
+            if (c < nseg) lt += __builtin_amdgcn_exp2f(mv[c] - Ms) * lv[c];
+          const float inv = lt > 0.f ? 1.f / lt : 0.f;
+#pragma unroll
+          for (int c = 0; c < BAL_MAX_SEGS; ++c)
+            if (c < nseg) s_w[c * RPWG + tid] = __builtin_amdgcn_exp2f(mv[c] - Ms) * inv;
+        }
+        __syncthreads();
+        // thread -> (row lane ct of the partial layout, half of its 4-column runs)
+        const int ct = tid & (NC - 1);
+        const int half = tid / NC;
+        const int mkp = ct >> 6, mlane = ct & 63, ml32 = mlane & 31, mhh = mlane >> 5;
+        constexpr int NQ = 2 * DG * 4;           // 4-column runs per row lane
+        constexpr int QB = 4;                    // runs per batch
+        static_assert((NQ / 2) % QB == 0, "merge batches");
+#pragma unroll 1
+        for (int q0 = 0; q0 < NQ / 2; q0 += QB) {
+          float acc[QB][4];
+#pragma unroll
+          for (int b = 0; b < QB; ++b)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) acc[b][j] = 0.f;
+#pragma unroll 1
+          for (int c = 0; c < nseg; ++c) {
+            // opaque offset: the addresses are formed here, not hoisted
+            int off = c * (NC * OREG) + ct;
+            asm volatile("" : "+v"(off));
+            float v[QB][4];
+#pragma unroll
+            for (int b = 0; b < QB; ++b) {
+              const int q = half + 2 * (q0 + b);     // run index: g, dg, i4
+              const int base_i = (q >> 2) * 16 + (q & 3) * 4;   // (g * DG + dg) * 16 + 4 * i4
+#pragma unroll
+              for (int j = 0; j < 4; ++j)
+                v[b][j] = __hip_atomic_load(pob + off + (base_i + j) * NC, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
+#pragma unroll
+            for (int b = 0; b < QB; ++b) {
+              const int q = half + 2 * (q0 + b);
+              const int g = q / (DG * 4);
+              const float wc = s_w[c * RPWG + mkp * 64 + g * 32 + ml32];
+#pragma unroll
+              for (int j = 0; j < 4; ++j) acc[b][j] += wc * v[b][j];
+            }
+          }
+#pragma unroll
+          for (int b = 0; b < QB; ++b) {
+            const int q = half + 2 * (q0 + b);
+            const int g = q / (DG * 4), dg = (q / 4) % DG, i4 = q & 3;
+            const int n = rt * RPWG + mkp * 64 + g * 32 + ml32;
+            if (n >= p.rows_total) continue;
+            const int r = n / p.G;
+            const int h = kvh * p.G + (n - r * p.G);
+            const int d = dg * 32 + 8 * i4 + 4 * mhh;
+            const uint32_t w0 = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{acc[b][0], acc[b][1]}, bf16x2));
+            const uint32_t w1 = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{acc[b][2], acc[b][3]}, bf16x2));
+            *(u32x2*)(out + (((size_t)s * R + r) * p.Hq + h) * D + d) = u32x2{w0, w1};
+          }
+        }
+      };
 
       if constexpr (PROD) {
         // =================== producer: QK and softmax ===================
@@ -1045,8 +1129,10 @@ __global__ void __launch_bounds__(NP * 128, 1) attn_bf16_pc_kernel(AttnParams p)
           s_flag[0] = (__hip_atomic_fetch_add(&p.counters[it], 1, __ATOMIC_RELAXED,
                                               __HIP_MEMORY_SCOPE_AGENT) == nseg - 1);
         __syncthreads();                                     // F3
-        if (s_flag[0] && tid == 0)
-          __hip_atomic_store(&p.counters[it], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (s_flag[0]) {
+          if (tid == 0) __hip_atomic_store(&p.counters[it], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          merge_all();
+        }
         continue;
       } else {
         // =================== consumer: loads, O rescale, PV ===================
@@ -1246,56 +1332,7 @@ __global__ void __launch_bounds__(NP * 128, 1) attn_bf16_pc_kernel(AttnParams p)
         wait_vmcnt<0>();
         __syncthreads();                                       // F2
         __syncthreads();                                       // F3 (counter decided)
-        if (!s_flag[0]) continue;
-        // the last workgroup of the item merges, in segment order, with batched
-        // coherent loads; 16 output columns at a time keeps the merge's
-        // registers small
-        const float* pob = p.part_o + (size_t)it * p.max_segs * (NC * OREG);
-        const float* pmlb = p.part_ml + (size_t)it * p.max_segs * (2 * RPWG);
-#pragma unroll
-        for (int g = 0; g < 2; ++g) {
-          const int rloc = kp * 64 + g * 32 + l32;
-          float M = -INFINITY;
-          for (int c0 = 0; c0 < nseg; c0 += 8) {
-            float mv[8];
-#pragma unroll
-            for (int j = 0; j < 8; ++j)
-              mv[j] = __hip_atomic_load(pmlb + (size_t)min(c0 + j, nseg - 1) * (2 * RPWG) + rloc, __ATOMIC_RELAXED,
-                                        __HIP_MEMORY_SCOPE_AGENT);
-#pragma unroll
-            for (int j = 0; j < 8; ++j) M = fmaxf(M, mv[j]);   // repeats of the last segment are harmless
-          }
-          const float Ms = (M == -INFINITY) ? 0.f : M;
-          float lt = 0.f;
-          for (int c = 0; c < nseg; ++c) {
-            const float mc = __hip_atomic_load(pmlb + (size_t)c * (2 * RPWG) + rloc, __ATOMIC_RELAXED,
-                                               __HIP_MEMORY_SCOPE_AGENT);
-            const float lc = __hip_atomic_load(pmlb + (size_t)c * (2 * RPWG) + RPWG + rloc, __ATOMIC_RELAXED,
-                                               __HIP_MEMORY_SCOPE_AGENT);
-            lt += __builtin_amdgcn_exp2f(mc - Ms) * lc;
-          }
-          const float inv = lt > 0.f ? 1.f / lt : 0.f;
-#pragma unroll
-          for (int dg = 0; dg < DG; ++dg) {
-            f32x16 acc = f32x16{};
-            for (int c = 0; c < nseg; ++c) {
-              // opaque offset: the loads' addresses are formed here rather than
-              // hoisted out of the loop as 16 live address pairs
-              int off = c * (NC * OREG) + (g * DG + dg) * 16 * NC + ct;
-              asm volatile("" : "+v"(off));
-              float v[16];
-#pragma unroll
-              for (int i = 0; i < 16; ++i)
-                v[i] = __hip_atomic_load(pob + off + i * NC, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-              const float mc = __hip_atomic_load(pmlb + (size_t)c * (2 * RPWG) + rloc, __ATOMIC_RELAXED,
-                                                 __HIP_MEMORY_SCOPE_AGENT);
-              const float wgt = __builtin_amdgcn_exp2f(mc - Ms);
-#pragma unroll
-              for (int i = 0; i < 16; ++i) acc[i] += wgt * v[i];
-            }
-            write_cols(g, dg, acc, inv);
-          }
-        }
+        if (s_flag[0]) merge_all();
       }
     }
   };
