@@ -238,18 +238,6 @@ __device__ __forceinline__ void fill_window_tile(int tid, int t0, int pg_lo, int
   }
 }
 
-template <int N>
-struct IC {
-  static constexpr int value = N;
-};
-
-template <int I, int N, typename F>
-__device__ __forceinline__ void static_for(F&& f) {
-  if constexpr (I < N) {
-    f(IC<I>{});
-    static_for<I + 1, N>(f);
-  }
-}
 
 __device__ __forceinline__ uint32_t lds_addr(const void* ptr) {
   return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)ptr;

@@ -53,4 +53,19 @@ __device__ __forceinline__ void set_err(int32_t* err, int32_t bit) {
   if (err) atomicOr(err, bit);
 }
 
+// Compile-time loop: f(IC<I>{}) for I = B .. E-1, so that an index can select
+// registers (ring slots, fragment arrays) without dynamic indexing.
+template <int N>
+struct IC {
+  static constexpr int value = N;
+};
+
+template <int I, int N, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (I < N) {
+    f(IC<I>{});
+    static_for<I + 1, N>(f);
+  }
+}
+
 }  // namespace dvs

@@ -214,157 +214,272 @@ __global__ void __launch_bounds__(256) gemm_bf16_kernel(const __bf16* __restrict
 // bf16 GEMM for the decoder stack: C[m, n] (=, or += into the fp32 residual)
 // sum_k A[m, k] W[n, k].  The weights are streamed once; the row count is
 // small (8..256 window rows) or a long prefill.
-//
-// A workgroup owns 32 output columns and a K range; its 4 waves split that
-// range in four, each accumulating all rows of a 256-row pass with
-// v_mfma_f32_32x32x16_bf16 (A lane = row, W lane = column, 8 k each).  The
-// four partial tiles are summed through LDS in wave order.  When the column
-// count alone cannot fill the chip, the K range is further split over
-// `ksplit` workgroups: each publishes its fp32 tile with write-through stores
-// and the last one to finish (counter) sums the tiles in split order.
-// Every output element is therefore reduced in an order fixed by (N, K)
-// alone: a row's result does not depend on how many rows the call carries,
-// which keeps a fused step's causal rows bit-identical to AR steps.
 // ---------------------------------------------------------------------------
-constexpr int GK_ROWS = 256;   // rows per pass
 constexpr int GK_MAXSPLIT = 32;
 
-// MG: 32-row groups per pass (1, 2, 4 or 8); KU: k-steps whose operands are
-// loaded before their MFMAs are issued.
-template <int MG>
-__global__ void __launch_bounds__(256, 1) gemm_bf16_sk_kernel(
+// ---------------------------------------------------------------------------
+// gemm_rt_kernel<MT>: C[M, N] = A[M, K] W[N, K]^T (bf16 operands, fp32
+// accumulation), tiles of MT rows x 128 columns staged through LDS.
+//
+// Row invariance.  K is cut into KS logical splits of kc = K / KS (a multiple
+// of 64), KS a function of (N, K) only.  Every output element is
+//     p_0 + p_1 + ... + p_{KS-1}      (fp32, in this order)
+// where p_s is the MFMA accumulation of split s over its 16-wide k-steps in
+// order.  Two mappings compute exactly that, whatever the row count:
+//   * split per workgroup (calls of at most 32 rows): p_s is published with
+//     write-through stores and the last workgroup of the column block adds
+//     the splits in order;
+//   * all splits in one workgroup (longer calls): the running ordered sum
+//     stays in registers.
+// A fused step's causal rows are therefore bit-identical to AR steps.
+//
+// Waves: MT = 32 -> 1 x 4 (each wave 32 rows x 32 columns); MT >= 64 ->
+// 2 x 2 (each wave MT/2 rows x 64 columns).  Per 64-wide K chunk all 256
+// threads copy the A tile (MT x 64) and the W tile (128 x 64) into a
+// double-buffered LDS pair (16-byte chunks XOR-swizzled by row so the MFMA
+// operand reads are conflict-free); the global loads of the next P - 1
+// chunks are in flight while the current chunk is multiplied.
+// ---------------------------------------------------------------------------
+constexpr int RT_NT = 128;   // columns per tile
+constexpr int RT_KC = 64;    // K per LDS chunk
+
+// SPLITS = false: one logical split only (KS == 1), no running sum kept.
+template <int MT, bool SPLITS>
+__global__ void __launch_bounds__(256, 1) gemm_rt_kernel(
     const __bf16* __restrict__ A, const __bf16* __restrict__ W, int M, int N, int K, void* C,
-    int c_f32, int accumulate, int ksplit, float* __restrict__ part, int32_t* __restrict__ counters) {
-  constexpr int KU = MG >= 4 ? 2 : 4;
-  constexpr int PR = MG * 32;   // rows per pass
-  __shared__ float red[4][PR][33];
+    int c_f32, int accumulate, int KS, int split_per_wg, float* __restrict__ part,
+    int32_t* __restrict__ counters) {
+  constexpr bool WIDE = MT >= 64;
+  constexpr int RG = WIDE ? MT / 64 : 1;   // 32-row groups per wave
+  constexpr int CG = WIDE ? 2 : 1;         // 32-column groups per wave
+  constexpr int A_LD = MT * RT_KC / 8 / 256;      // 16-byte A chunks per thread per K chunk
+  constexpr int W_LD = RT_NT * RT_KC / 8 / 256;   // 16-byte W chunks per thread per K chunk
+  static_assert(A_LD >= 1 && W_LD >= 1, "tile / threads");
+  __shared__ __attribute__((aligned(16))) char s_a[2][MT * RT_KC * 2];
+  __shared__ __attribute__((aligned(16))) char s_w[2][RT_NT * RT_KC * 2];
   __shared__ int s_last;
+
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int l32 = lane & 31, hh = lane >> 5;
-  const int NB = (N + 31) / 32;
-  const int nb = blockIdx.x % NB;
-  const int ks = blockIdx.x / NB;
-  const int n0 = nb * 32;
-  const int kc = K / ksplit, kw = kc / 4;
-  const int kbeg = ks * kc + w * kw;
-  const int ncol = n0 + l32;
-  const bool nvalid = ncol < N;
-  const __bf16* wrow = W + (size_t)(nvalid ? ncol : 0) * K;
+  const int NBK = (N + RT_NT - 1) / RT_NT;
+  const int nb = blockIdx.x % NBK;
+  const int rest = blockIdx.x / NBK;
+  const int n0 = nb * RT_NT;
+  // split-per-workgroup: blockIdx selects (column block, split), one row tile;
+  // otherwise (column block, row tile) and every split
+  const int s_first = split_per_wg ? rest : 0;
+  const int s_end = split_per_wg ? rest + 1 : KS;
+  const int m0 = split_per_wg ? 0 : rest * MT;
+  const int kc = K / KS;
+  const int wr = WIDE ? (w >> 1) : 0, wc = WIDE ? (w & 1) : w;
+  const int row_w = wr * (MT / (WIDE ? 2 : 1));   // first tile row of the wave
+  const int col_w = wc * (CG * 32);               // first tile column of the wave
+
+  // global -> register staging of K chunks, P - 1 chunks ahead of the one
+  // being multiplied (ring slot = chunk index mod P)
+  constexpr int P = MT <= 64 ? 4 : 2;
+  u32x4 ra[P][A_LD], rw[P][W_LD];
+  auto load_chunk = [&](int k0, u32x4 (&xa)[A_LD], u32x4 (&xw)[W_LD]) {
+#pragma unroll
+    for (int j = 0; j < A_LD; ++j) {
+      const int idx = tid + j * 256;
+      const int r = idx >> 3, c = idx & 7;
+      // unconditional loads (rows past the end re-read the last row and are
+      // zeroed after), so that the wait counts stay exact across the ring
+      const int mrow = m0 + r;
+      const u32x4 x = *(const u32x4*)(A + (size_t)min(mrow, M - 1) * K + k0 + c * 8);
+      xa[j] = mrow < M ? x : u32x4{0, 0, 0, 0};
+    }
+#pragma unroll
+    for (int j = 0; j < W_LD; ++j) {
+      const int idx = tid + j * 256;
+      const int r = idx >> 3, c = idx & 7;
+      const int n = n0 + r;
+      const u32x4 x = *(const u32x4*)(W + (size_t)min(n, N - 1) * K + k0 + c * 8);
+      xw[j] = n < N ? x : u32x4{0, 0, 0, 0};
+    }
+  };
+  auto store_chunk = [&](int buf, const u32x4 (&xa)[A_LD], const u32x4 (&xw)[W_LD]) {
+#pragma unroll
+    for (int j = 0; j < A_LD; ++j) {
+      const int idx = tid + j * 256;
+      const int r = idx >> 3, c = idx & 7;
+      *(u32x4*)(s_a[buf] + r * 128 + ((c ^ (r & 7)) << 4)) = xa[j];
+    }
+#pragma unroll
+    for (int j = 0; j < W_LD; ++j) {
+      const int idx = tid + j * 256;
+      const int r = idx >> 3, c = idx & 7;
+      *(u32x4*)(s_w[buf] + r * 128 + ((c ^ (r & 7)) << 4)) = xw[j];
+    }
+  };
+
+  f32x16 acc[RG][CG], sum[SPLITS ? RG : 1][SPLITS ? CG : 1];
+  if constexpr (SPLITS) {
+#pragma unroll
+    for (int a = 0; a < RG; ++a)
+#pragma unroll
+      for (int b = 0; b < CG; ++b) sum[a][b] = f32x16{};
+  }
+
+  const int nch = kc / RT_KC;
+  const int total = (s_end - s_first) * nch;
+  auto chunk_k0 = [&](int t) { return (s_first + t / nch) * kc + (t % nch) * RT_KC; };
+  static_for<0, P - 1>([&](auto c) {
+    constexpr int i = decltype(c)::value;
+    load_chunk(chunk_k0(min(i, total - 1)), ra[i], rw[i]);
+  });
+  store_chunk(0, ra[0], rw[0]);
+  __syncthreads();
+  // one chunk: acc reset at a split start, the next-but-(P-2) chunk's loads
+  // (clamped to the last chunk: a harmless re-read), the products, the
+  // ordered split sum, the next chunk into the other LDS buffer
+  auto step = [&](int t, auto cs) {
+    constexpr int sl = decltype(cs)::value;   // ring slot of chunk t
+    const int ch = t % nch;
+    if (ch == 0) {
+#pragma unroll
+      for (int a = 0; a < RG; ++a)
+#pragma unroll
+        for (int b = 0; b < CG; ++b) acc[a][b] = f32x16{};
+    }
+    load_chunk(chunk_k0(min(t + P - 1, total - 1)), ra[(sl + P - 1) % P], rw[(sl + P - 1) % P]);
+    const char* sa = s_a[t & 1];
+    const char* sw = s_w[t & 1];
+#pragma unroll
+    for (int ks = 0; ks < RT_KC / 16; ++ks) {
+      const int ch16 = ks * 2 + hh;   // 16-byte chunk of the row holding this lane's 8 k values
+      bf16x8 af[RG], bf[CG];
+#pragma unroll
+      for (int a = 0; a < RG; ++a) {
+        const int r = row_w + a * 32 + l32;
+        af[a] = *(const bf16x8*)(sa + r * 128 + ((ch16 ^ (r & 7)) << 4));
+      }
+#pragma unroll
+      for (int b = 0; b < CG; ++b) {
+        const int r = col_w + b * 32 + l32;
+        bf[b] = *(const bf16x8*)(sw + r * 128 + ((ch16 ^ (r & 7)) << 4));
+      }
+#pragma unroll
+      for (int a = 0; a < RG; ++a)
+#pragma unroll
+        for (int b = 0; b < CG; ++b)
+          acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[a], bf[b], acc[a][b], 0, 0, 0);
+    }
+    if (SPLITS && ch == nch - 1) {   // split complete: ordered running sum
+#pragma unroll
+      for (int a = 0; a < RG; ++a)
+#pragma unroll
+        for (int b = 0; b < CG; ++b) sum[a][b] += acc[a][b];
+    }
+    store_chunk((t + 1) & 1, ra[(sl + 1) % P], rw[(sl + 1) % P]);
+    __syncthreads();
+  };
+  // whole groups of P chunks keep the ring slots compile-time; the tail runs
+  // the same steps one by one
+  int t0 = 0;
+  for (; t0 + P <= total; t0 += P) static_for<0, P>([&](auto c) { step(t0 + decltype(c)::value, c); });
+  static_for<0, P - 1>([&](auto c) {
+    if (t0 + decltype(c)::value < total) step(t0 + decltype(c)::value, c);
+  });
+
+  // element (a, b, i) of this lane: row m0 + row_w + 32a + 8(i>>2) + 4hh + (i&3),
+  // column n0 + col_w + 32b + l32
   float* Cf = c_f32 ? (float*)C : nullptr;
   __bf16* Cb = c_f32 ? nullptr : (__bf16*)C;
-  for (int m0 = 0; m0 < M; m0 += PR) {
-    f32x16 acc[MG];
+  auto write_out = [&](f32x16 (&v)[RG][CG]) {
 #pragma unroll
-    for (int g = 0; g < MG; ++g) acc[g] = f32x16{};
-    const __bf16* arow[MG];
-    bool avalid[MG];
+    for (int a = 0; a < RG; ++a)
 #pragma unroll
-    for (int g = 0; g < MG; ++g) {
-      const int mrow = m0 + g * 32 + l32;
-      avalid[g] = mrow < M;
-      arow[g] = A + (size_t)(avalid[g] ? mrow : 0) * K;
-    }
-    int k0 = kbeg;
-    for (; k0 + 16 * KU <= kbeg + kw; k0 += 16 * KU) {
-      bf16x8 bf[KU], af[KU][MG];
+      for (int b = 0; b < CG; ++b) {
+        const int n = n0 + col_w + b * 32 + l32;
+        float cur[16];
+        if (Cf && accumulate) {
 #pragma unroll
-      for (int u = 0; u < KU; ++u) {
-        bf[u] = nvalid ? *(const bf16x8*)(wrow + k0 + 16 * u + hh * 8) : bf16x8{};
+          for (int i = 0; i < 16; ++i) {
+            const int mrow = m0 + row_w + a * 32 + 8 * (i >> 2) + 4 * hh + (i & 3);
+            cur[i] = (mrow < M && n < N) ? Cf[(size_t)mrow * N + n] : 0.f;
+          }
+        }
 #pragma unroll
-        for (int g = 0; g < MG; ++g)
-          af[u][g] = avalid[g] ? *(const bf16x8*)(arow[g] + k0 + 16 * u + hh * 8) : bf16x8{};
+        for (int i = 0; i < 16; ++i) {
+          const int mrow = m0 + row_w + a * 32 + 8 * (i >> 2) + 4 * hh + (i & 3);
+          if (mrow >= M || n >= N) continue;
+          const size_t o = (size_t)mrow * N + n;
+          if (Cf) Cf[o] = accumulate ? cur[i] + v[a][b][i] : v[a][b][i];
+          else Cb[o] = (__bf16)v[a][b][i];
+        }
       }
+  };
+  if constexpr (!SPLITS) {
+    // 0 + p_0, as in the split paths (keeps the sign of a zero sum alike)
 #pragma unroll
-      for (int u = 0; u < KU; ++u)
+    for (int a = 0; a < RG; ++a)
 #pragma unroll
-        for (int g = 0; g < MG; ++g) acc[g] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[u][g], bf[u], acc[g], 0, 0, 0);
-    }
-    for (; k0 < kbeg + kw; k0 += 16) {
-      const bf16x8 b = nvalid ? *(const bf16x8*)(wrow + k0 + hh * 8) : bf16x8{};
+      for (int b = 0; b < CG; ++b) acc[a][b] = f32x16{} + acc[a][b];
+    write_out(acc);
+    return;
+  } else {
+  if (!split_per_wg || KS == 1) {
+    write_out(sum);
+    return;
+  }
+  if constexpr (MT == 32) {   // the host uses one split per workgroup only with 32-row tiles
+    // split per workgroup (MT == 32, m0 == 0): publish p_s, count in; the last
+    // workgroup of the column block adds the splits in order
 #pragma unroll
-      for (int g = 0; g < MG; ++g) {
-        const bf16x8 a = avalid[g] ? *(const bf16x8*)(arow[g] + k0 + hh * 8) : bf16x8{};
-        acc[g] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc[g], 0, 0, 0);
+    for (int a = 0; a < RG; ++a)
+#pragma unroll
+      for (int b = 0; b < CG; ++b) {
+        const int n = n0 + col_w + b * 32 + l32;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const int mrow = row_w + a * 32 + 8 * (i >> 2) + 4 * hh + (i & 3);
+          if (mrow < M && n < N)
+            __hip_atomic_store(part + ((size_t)s_first * M + mrow) * N + n, sum[a][b][i], __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
+        }
       }
-    }
-    // C layout: lane (col l32, hh), register i holds row 8*(i>>2) + 4*hh + (i&3)
-#pragma unroll
-    for (int g = 0; g < MG; ++g)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) red[w][g * 32 + 8 * (i >> 2) + 4 * hh + (i & 3)][l32] = acc[g][i];
+    __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
-    // thread t sums column t&31 of rows (t>>5) + 8j over the four waves, in
-    // order; a residual being accumulated into is read in one batch first
-    const int col = tid & 31, n = n0 + col;
-    float cur[PR / 8];
-    if (ksplit == 1 && Cf && accumulate) {
+    if (tid == 0)
+      s_last = __hip_atomic_fetch_add(&counters[nb], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == KS - 1;
+    __syncthreads();
+    if (!s_last) return;
+    if (tid == 0) __hip_atomic_store(&counters[nb], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    f32x16 tot[RG][CG];
 #pragma unroll
-      for (int j = 0; j < PR / 8; ++j) {
-        const int mrow = m0 + (tid >> 5) + 8 * j;
-        cur[j] = (mrow < M && n < N) ? Cf[(size_t)mrow * N + n] : 0.f;
+    for (int a = 0; a < RG; ++a)
+#pragma unroll
+      for (int b = 0; b < CG; ++b) tot[a][b] = f32x16{};
+    // (MT == 32 here: one 32 x 32 tile per wave) splits are loaded SPB at a
+    // time, every load of a batch issued before any is added, then added in
+    // split order
+    constexpr int SPB = 8;
+    const int n = n0 + col_w + l32;
+    for (int sp0 = 0; sp0 < KS; sp0 += SPB) {
+      float v[SPB][16];
+#pragma unroll
+      for (int q = 0; q < SPB; ++q) {
+        const int sp = min(sp0 + q, KS - 1);
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const int mrow = row_w + 8 * (i >> 2) + 4 * hh + (i & 3);
+          const int mr = min(mrow, M - 1), nn = min(n, N - 1);
+          v[q][i] = __hip_atomic_load(part + ((size_t)sp * M + mr) * N + nn, __ATOMIC_RELAXED,
+                                      __HIP_MEMORY_SCOPE_AGENT);
+        }
       }
+#pragma unroll
+      for (int q = 0; q < SPB; ++q)
+        if (sp0 + q < KS) {
+#pragma unroll
+          for (int i = 0; i < 16; ++i) tot[0][0][i] += v[q][i];
+        }
     }
-#pragma unroll
-    for (int j = 0; j < PR / 8; ++j) {
-      const int r = (tid >> 5) + 8 * j;
-      const float v = ((red[0][r][col] + red[1][r][col]) + red[2][r][col]) + red[3][r][col];
-      const int mrow = m0 + r;
-      if (mrow >= M || n >= N) continue;
-      if (ksplit > 1) {
-        __hip_atomic_store(part + ((size_t)ks * M + mrow) * N + n, v, __ATOMIC_RELAXED,
-                           __HIP_MEMORY_SCOPE_AGENT);
-      } else {
-        const size_t o = (size_t)mrow * N + n;
-        if (Cf) Cf[o] = accumulate ? cur[j] + v : v;
-        else Cb[o] = (__bf16)v;
-      }
-    }
-    __syncthreads();   // red is reused by the next pass
+    write_out(tot);
   }
-  if (ksplit == 1) return;
-  // split K (M <= PR here): the last workgroup of the column block sums the
-  // splits in order; the loads of one split are issued together
-  __builtin_amdgcn_s_waitcnt(0);
-  __syncthreads();
-  if (tid == 0)
-    s_last = __hip_atomic_fetch_add(&counters[nb], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
-             ksplit - 1;
-  __syncthreads();
-  if (!s_last) return;
-  const int col = tid & 31, n = n0 + col;
-  float sum[PR / 8];
-#pragma unroll
-  for (int j = 0; j < PR / 8; ++j) sum[j] = 0.f;
-  for (int sp = 0; sp < ksplit; ++sp) {
-    float v[PR / 8];
-#pragma unroll
-    for (int j = 0; j < PR / 8; ++j) {
-      const int mrow = (tid >> 5) + 8 * j;
-      v[j] = (mrow < M && n < N)
-                 ? __hip_atomic_load(part + ((size_t)sp * M + mrow) * N + n, __ATOMIC_RELAXED,
-                                     __HIP_MEMORY_SCOPE_AGENT)
-                 : 0.f;
-    }
-#pragma unroll
-    for (int j = 0; j < PR / 8; ++j) sum[j] += v[j];
   }
-  float cur[PR / 8];
-  if (Cf && accumulate) {
-#pragma unroll
-    for (int j = 0; j < PR / 8; ++j) {
-      const int mrow = (tid >> 5) + 8 * j;
-      cur[j] = (mrow < M && n < N) ? Cf[(size_t)mrow * N + n] : 0.f;
-    }
-  }
-#pragma unroll
-  for (int j = 0; j < PR / 8; ++j) {
-    const int mrow = (tid >> 5) + 8 * j;
-    if (mrow >= M || n >= N) continue;
-    const size_t o = (size_t)mrow * N + n;
-    if (Cf) Cf[o] = accumulate ? cur[j] + sum[j] : sum[j];
-    else Cb[o] = (__bf16)sum[j];
-  }
-  if (tid == 0) __hip_atomic_store(&counters[nb], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // fp32: v_mfma_f32_32x32x2_f32; lane (row|col, hh) takes k = k0 + 4*hh + j in
@@ -422,14 +537,14 @@ struct StepLayout {
       attn_counters, gemm_part, gemm_part_bytes, gemm_counters, n_gemm_counters;
 };
 
-// K splits of a bf16 GEMM over workgroups: enough column blocks x splits to
-// fill the chip, a split being a multiple of 64 of K.  A function of (N, K)
-// for every call of up to 256 rows (so row results do not depend on the row
-// count); longer calls (prefill) have rows enough and do not split.
-static int gemm_ksplit(int M, int N, int K) {
-  if (M > GK_ROWS || K % 64 != 0) return 1;
+// Logical K splits of a bf16 GEMM: enough 128-column blocks x splits to
+// fill the chip when each split is a workgroup, a split being a multiple of
+// 64 of K.  A function of (N, K) only, so that row results do not depend on
+// the row count.
+static int gemm_ksplit(int N, int K) {
+  if (K % 64 != 0) return 1;
   static_assert(GK_MAXSPLIT >= 1, "split bound");
-  const int nb = (N + 31) / 32;
+  const int nb = (N + RT_NT - 1) / RT_NT;
   const int target = (256 + nb - 1) / nb;
   if (target <= 1) return 1;
   const int units = K / 64;
@@ -438,6 +553,15 @@ static int gemm_ksplit(int M, int N, int K) {
   for (int d = std::min(units, GK_MAXSPLIT); d > 1; --d)
     if (units % d == 0) return d;
   return 1;
+}
+
+// Rows per tile when all splits run in one workgroup (more than 32 rows):
+// the largest tile that still gives 256 workgroups, else 32.
+static int gemm_rows_per_tile(int M, int N) {
+  const long long nb = (N + RT_NT - 1) / RT_NT;
+  for (int mt = 256; mt >= 64; mt >>= 1)
+    if (mt / 2 < M && nb * ((M + mt - 1) / mt) >= 256) return mt;
+  return 32;
 }
 
 __global__ void zero_words_kernel(int32_t* __restrict__ p, int n) {
@@ -488,11 +612,11 @@ static StepLayout step_layout(const dvs_model* m, int S, int n_causal, int n_mas
                               {(int)M, m->ffn, H}, {(int)M, H, m->ffn}, {(int)logit_rows, m->vocab, H}};
     size_t part = 0, cnt = 0;
     for (const auto& sh : shapes) {
-      if (sh[1] <= 0) continue;
-      const int ksp = gemm_ksplit(sh[0], sh[1], sh[2]);
+      if (sh[1] <= 0 || sh[0] > 32) continue;   // only calls of <= 32 rows publish split partials
+      const int ksp = gemm_ksplit(sh[1], sh[2]);
       if (ksp > 1) {
         part = std::max(part, (size_t)ksp * sh[0] * sh[1] * 4);
-        cnt = std::max(cnt, (size_t)(sh[1] + 31) / 32);
+        cnt = std::max(cnt, (size_t)(sh[1] + RT_NT - 1) / RT_NT);
       }
     }
     L.gemm_part = off; off += al(part); L.gemm_part_bytes = part;
@@ -509,25 +633,29 @@ static int gemm(const StepLayout& L, char* ws, int dtype, const void* A, const v
   const int waves = (N + 31) / 32;
   const int blocks = (waves + 3) / 4;
   if (dtype == DVS_BF16 && K % 64 == 0) {
-    const int ksp = gemm_ksplit(M, N, K);
-    const int nb = (N + 31) / 32;
-    if (ksp > 1 && ((size_t)ksp * M * N * 4 > L.gemm_part_bytes || (size_t)nb > L.n_gemm_counters)) {
+    const int ksp = gemm_ksplit(N, K);
+    const int nb = (N + RT_NT - 1) / RT_NT;
+    const bool split_wg = M <= 32 && ksp > 1;
+    if (split_wg && ((size_t)ksp * M * N * 4 > L.gemm_part_bytes || (size_t)nb > L.n_gemm_counters)) {
       set_error("draft_verify_step: GEMM split workspace too small");
       return DVS_EWORKSPACE;
     }
     float* part = (float*)(ws + L.gemm_part);
     int32_t* cnt = (int32_t*)(ws + L.gemm_counters);
-    const dim3 grid(nb * ksp), blk(256);
-    // rows per pass: the smallest power-of-two number of 32-row groups
-    // covering M (up to 256 rows); the reduction order does not depend on it
-    if (M <= 32)
-      hipLaunchKernelGGL(gemm_bf16_sk_kernel<1>, grid, blk, 0, st, (const __bf16*)A, (const __bf16*)W, M, N, K, C, c_f32, accumulate, ksp, part, cnt);
-    else if (M <= 64)
-      hipLaunchKernelGGL(gemm_bf16_sk_kernel<2>, grid, blk, 0, st, (const __bf16*)A, (const __bf16*)W, M, N, K, C, c_f32, accumulate, ksp, part, cnt);
-    else if (M <= 128)
-      hipLaunchKernelGGL(gemm_bf16_sk_kernel<4>, grid, blk, 0, st, (const __bf16*)A, (const __bf16*)W, M, N, K, C, c_f32, accumulate, ksp, part, cnt);
-    else
-      hipLaunchKernelGGL(gemm_bf16_sk_kernel<8>, grid, blk, 0, st, (const __bf16*)A, (const __bf16*)W, M, N, K, C, c_f32, accumulate, ksp, part, cnt);
+    int mt = M <= 32 ? 32 : gemm_rows_per_tile(M, N);
+    if (mt == 256 && ksp > 1) mt = 128;   // the 256-row tile keeps no running split sum
+    const long long grid = split_wg ? (long long)nb * ksp : (long long)nb * ((M + mt - 1) / mt);
+    DVS_CHECK_SUPPORTED(grid < (1LL << 31), "draft_verify_step: GEMM grid too large");
+    const dim3 g((unsigned)grid), blk(256);
+    const __bf16* a = (const __bf16*)A;
+    const __bf16* wt = (const __bf16*)W;
+    const int sw = split_wg ? 1 : 0;
+    switch (mt) {
+      case 256: hipLaunchKernelGGL((gemm_rt_kernel<256, false>), g, blk, 0, st, a, wt, M, N, K, C, c_f32, accumulate, ksp, sw, part, cnt); break;
+      case 128: hipLaunchKernelGGL((gemm_rt_kernel<128, true>), g, blk, 0, st, a, wt, M, N, K, C, c_f32, accumulate, ksp, sw, part, cnt); break;
+      case 64: hipLaunchKernelGGL((gemm_rt_kernel<64, true>), g, blk, 0, st, a, wt, M, N, K, C, c_f32, accumulate, ksp, sw, part, cnt); break;
+      default: hipLaunchKernelGGL((gemm_rt_kernel<32, true>), g, blk, 0, st, a, wt, M, N, K, C, c_f32, accumulate, ksp, sw, part, cnt); break;
+    }
   } else if (dtype == DVS_BF16)
     hipLaunchKernelGGL(gemm_bf16_kernel, dim3(blocks), dim3(256), 0, st, (const __bf16*)A,
                        (const __bf16*)W, M, N, K, C, c_f32, accumulate);
