@@ -1154,16 +1154,32 @@ __global__ void __launch_bounds__(NP * 128, 1) attn_bf16_pc_kernel(AttnParams p)
         // exactly: it is the high half).  Vector-ALU work, placed where the
         // pair's SIMD is busy with the producer's matrix products.
         auto add_l = [&](const Hand& hd) {
+          // acc += w.lo + w.hi by one dot product with (1, 1) in bf16, the two
+          // rows' chains interleaved.  Written as inline assembly (the dot2
+          // builtin, fed the elements of a 4-word vector, read element 0 for
+          // all four); the compiler then does not know these are dot
+          // instructions, so each block ends with the wait states another
+          // vector instruction needs before it reads a dot result (s_nop 4).
+          const uint32_t ones = 0x3f803f80u;
+          float acc0 = 0.f, acc1 = 0.f;
 #pragma unroll
-          for (int g = 0; g < 2; ++g) {
-            float acc = 0.f;
-#pragma unroll
-            for (int t = 0; t < 4; ++t)
-#pragma unroll
-              for (int e = 0; e < 4; ++e)
-                acc += __uint_as_float(hd.pf[g][t][e] << 16) + __uint_as_float(hd.pf[g][t][e] & 0xffff0000u);
-            lrow[g] = fmaf(lrow[g], hd.alpha[g], acc);
+          for (int t = 0; t < 4; ++t) {
+            const u32x4 w0 = hd.pf[0][t], w1 = hd.pf[1][t];
+            asm("v_dot2c_f32_bf16 %0, %2, %10\n\t"
+                "v_dot2c_f32_bf16 %1, %6, %10\n\t"
+                "v_dot2c_f32_bf16 %0, %3, %10\n\t"
+                "v_dot2c_f32_bf16 %1, %7, %10\n\t"
+                "v_dot2c_f32_bf16 %0, %4, %10\n\t"
+                "v_dot2c_f32_bf16 %1, %8, %10\n\t"
+                "v_dot2c_f32_bf16 %0, %5, %10\n\t"
+                "v_dot2c_f32_bf16 %1, %9, %10\n\t"
+                "s_nop 4"
+                : "+v"(acc0), "+v"(acc1)
+                : "v"(w0[0]), "v"(w0[1]), "v"(w0[2]), "v"(w0[3]),
+                  "v"(w1[0]), "v"(w1[1]), "v"(w1[2]), "v"(w1[3]), "v"(ones));
           }
+          lrow[0] = fmaf(lrow[0], hd.alpha[0], acc0);
+          lrow[1] = fmaf(lrow[1], hd.alpha[1], acc1);
         };
         auto pv = [&](const Hand& hd, const char* vst) {
           if (hd.resc) {
@@ -1214,12 +1230,28 @@ __global__ void __launch_bounds__(NP * 128, 1) attn_bf16_pc_kernel(AttnParams p)
             {
               const char* base = kpb + ((size_t)kpg * p.Hkv + kvh) * PAGE_K;
               char* dst = kring + ((gi + 2 + NS) % NS) * KTILE_B + kp * (K_INS * 1024);
+              // byte offset within the page of the lane's chunk of segment 0; when
+              // a 1 KB segment holds whole rows, segment j's rows are 1024/KROWB*j
+              // above segment 0's (their low bits are the lane's) and kswz is a
+              // bit selection, so segment j's offset is segment 0's XOR a constant
+              constexpr bool KLIN = (1024 % KROWB) == 0;
+              constexpr uint32_t RPK = KLIN ? 1024 / KROWB : 1;
+              const uint32_t off0 = (uint32_t)ln * 16u;
+              const uint32_t row0 = off0 / (uint32_t)KROWB;
+              const uint32_t src0 = row0 * (uint32_t)KROWB +
+                  ((((off0 % (uint32_t)KROWB) >> 4) ^ (uint32_t)kswz<CPR>((int)row0)) << 4);
 #pragma unroll
               for (int j = 0; j < K_INS; ++j) {
-                const int off = j * 1024 + ln * 16;      // byte within the page
-                const int row = off / KROWB;
-                const int cc = ((off % KROWB) >> 4) ^ kswz<CPR>(row);
-                const uint32_t src = (uint32_t)(row * KROWB + cc * 16);
+                uint32_t src;
+                if constexpr (KLIN) {
+                  src = (uint32_t)j * 1024u + (src0 ^ ((uint32_t)kswz<CPR>((int)(RPK * j)) << 4));
+                } else {
+                  // unsigned: the row division by a constant stays a mul_hi
+                  const uint32_t off = (uint32_t)j * 1024u + off0;
+                  const uint32_t row = off / (uint32_t)KROWB;
+                  const uint32_t cc = ((off % (uint32_t)KROWB) >> 4) ^ (uint32_t)kswz<CPR>((int)row);
+                  src = row * (uint32_t)KROWB + cc * 16u;
+                }
                 __builtin_amdgcn_global_load_lds((const void*)(base + src),
                     (__attribute__((address_space(3))) void*)(dst + j * 1024), 16, 0, 0);
               }
@@ -1229,10 +1261,10 @@ __global__ void __launch_bounds__(NP * 128, 1) attn_bf16_pc_kernel(AttnParams p)
               char* dst = vring + ((gi + 1 + NS) % NS) * VTILE_B + kp * (V_INS * 1024);
 #pragma unroll
               for (int j = 0; j < V_INS; ++j) {
-                const int off = j * 1024 + ln * 16;
-                const int d = off >> 5;
-                const int hc = ((off >> 4) & 1) ^ vswz(d);
-                const uint32_t src = (uint32_t)(d * 32 + hc * 16);
+                const uint32_t off = (uint32_t)j * 1024u + (uint32_t)ln * 16u;
+                const uint32_t d = off >> 5;
+                const uint32_t hc = ((off >> 4) & 1u) ^ (uint32_t)vswz((int)d);
+                const uint32_t src = d * 32u + hc * 16u;
                 __builtin_amdgcn_global_load_lds((const void*)(base + src),
                     (__attribute__((address_space(3))) void*)(dst + j * 1024), 16, 0, 0);
               }
@@ -1260,7 +1292,12 @@ __global__ void __launch_bounds__(NP * 128, 1) attn_bf16_pc_kernel(AttnParams p)
               issue_group(i);
               if (i + 1 <= n_main - 2) fetch_pages(i + 1);
             }
-            if (i >= 1) add_l(hd);
+            if (i >= 1) {
+              add_l(hd);
+              // keep the sums on this side of the barrier (they would
+              // otherwise sink into the matrix-product phase)
+              asm volatile("" ::"v"(lrow[0]), "v"(lrow[1]));
+            }
             pc_barrier();   // B
             if (i >= 1) pv(hd, vring + ((i - 1) % NS) * VTILE_B);
           }
