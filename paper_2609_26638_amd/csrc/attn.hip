@@ -1151,35 +1151,20 @@ __global__ void __launch_bounds__(NP * 128, 1) attn_bf16_pc_kernel(AttnParams p)
           __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0): the P reads are done before the barrier
         };
         // l: rescale, then add the tile's weights (a bf16 word widens to fp32
-        // exactly: it is the high half).  Vector-ALU work, placed where the
-        // pair's SIMD is busy with the producer's matrix products.
+        // exactly: it is the high half).  Plain vector-ALU work, placed where
+        // the pair's SIMD is busy with the producer's matrix products (a dot2
+        // against (1, 1) was slower here: it competed with those products).
         auto add_l = [&](const Hand& hd) {
-          // acc += w.lo + w.hi by one dot product with (1, 1) in bf16, the two
-          // rows' chains interleaved.  Written as inline assembly (the dot2
-          // builtin, fed the elements of a 4-word vector, read element 0 for
-          // all four); the compiler then does not know these are dot
-          // instructions, so each block ends with the wait states another
-          // vector instruction needs before it reads a dot result (s_nop 4).
-          const uint32_t ones = 0x3f803f80u;
-          float acc0 = 0.f, acc1 = 0.f;
 #pragma unroll
-          for (int t = 0; t < 4; ++t) {
-            const u32x4 w0 = hd.pf[0][t], w1 = hd.pf[1][t];
-            asm("v_dot2c_f32_bf16 %0, %2, %10\n\t"
-                "v_dot2c_f32_bf16 %1, %6, %10\n\t"
-                "v_dot2c_f32_bf16 %0, %3, %10\n\t"
-                "v_dot2c_f32_bf16 %1, %7, %10\n\t"
-                "v_dot2c_f32_bf16 %0, %4, %10\n\t"
-                "v_dot2c_f32_bf16 %1, %8, %10\n\t"
-                "v_dot2c_f32_bf16 %0, %5, %10\n\t"
-                "v_dot2c_f32_bf16 %1, %9, %10\n\t"
-                "s_nop 4"
-                : "+v"(acc0), "+v"(acc1)
-                : "v"(w0[0]), "v"(w0[1]), "v"(w0[2]), "v"(w0[3]),
-                  "v"(w1[0]), "v"(w1[1]), "v"(w1[2]), "v"(w1[3]), "v"(ones));
+          for (int g = 0; g < 2; ++g) {
+            float acc = 0.f;
+#pragma unroll
+            for (int t = 0; t < 4; ++t)
+#pragma unroll
+              for (int e = 0; e < 4; ++e)
+                acc += __uint_as_float(hd.pf[g][t][e] << 16) + __uint_as_float(hd.pf[g][t][e] & 0xffff0000u);
+            lrow[g] = fmaf(lrow[g], hd.alpha[g], acc);
           }
-          lrow[0] = fmaf(lrow[0], hd.alpha[0], acc0);
-          lrow[1] = fmaf(lrow[1], hd.alpha[1], acc1);
         };
         auto pv = [&](const Hand& hd, const char* vst) {
           if (hd.resc) {
@@ -1212,11 +1197,22 @@ __global__ void __launch_bounds__(NP * 128, 1) attn_bf16_pc_kernel(AttnParams p)
           // With 4 pairs, consumer wave k copies page k of every 4-page tile
           // (its K_INS / V_INS 1 KB segments are exactly that page).
           int kpg = 0, vpg = 0;
-          auto fetch_pages = [&](int gi) {   // group gi = {K(gi+2), V(gi+1)}, clamped
+          // page ids of group gi = {K(gi+2), V(gi+1)} (clamped), read in two
+          // halves so that the LDS reads can share a wait with other reads
+          int kraw = 0, vraw = 0;
+          auto read_pages = [&](int gi) {
             const int ik = max(0, min(gi + 2, n_main - 1));
             const int iv = max(0, min(gi + 1, n_main - 1));
-            kpg = __builtin_amdgcn_readfirstlane(s_pages[ik * 4 + kp]);
-            vpg = __builtin_amdgcn_readfirstlane(s_pages[iv * 4 + kp]);
+            kraw = s_pages[ik * 4 + kp];
+            vraw = s_pages[iv * 4 + kp];
+          };
+          auto take_pages = [&]() {
+            kpg = __builtin_amdgcn_readfirstlane(kraw);
+            vpg = __builtin_amdgcn_readfirstlane(vraw);
+          };
+          auto fetch_pages = [&](int gi) {
+            read_pages(gi);
+            take_pages();
           };
           auto issue_group = [&](int gi) {
             // page bases are wave-uniform; the per-lane offsets are made opaque
@@ -1287,11 +1283,10 @@ __global__ void __launch_bounds__(NP * 128, 1) attn_bf16_pc_kernel(AttnParams p)
             else wait_vmcnt<0>();
             pc_barrier();   // A
             Hand hd;
+            // the next group's page ids are read with the hand-off (one wait)
+            const bool nxt = i + 1 <= n_main - 2;
+            if (nxt) read_pages(i + 1);
             if (i >= 1) take_p(hd);
-            if (i <= n_main - 2) {
-              issue_group(i);
-              if (i + 1 <= n_main - 2) fetch_pages(i + 1);
-            }
             if (i >= 1) {
               add_l(hd);
               // keep the sums on this side of the barrier (they would
@@ -1300,6 +1295,13 @@ __global__ void __launch_bounds__(NP * 128, 1) attn_bf16_pc_kernel(AttnParams p)
             }
             pc_barrier();   // B
             if (i >= 1) pv(hd, vring + ((i - 1) % NS) * VTILE_B);
+            // The copies go out after the products: issuing 8 direct loads
+            // stalls the wave while the load path drains them, which here
+            // overlaps the producer's softmax instead of delaying barrier B.
+            // Slots: K(i+2) replaces K(i-1) (read by QK(i-1) before barrier
+            // A), V(i+1) replaces V(i-2) (read by PV(i-2) last period).
+            if (i <= n_main - 2) issue_group(i);
+            if (nxt) take_pages();
           }
           for (int jt = jm; jt < jb; ++jt) {
             __syncthreads();
