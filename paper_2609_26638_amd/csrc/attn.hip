@@ -520,7 +520,10 @@ __global__ void __launch_bounds__(NW * 64, 1) attn_bf16_kernel(AttnParams p) {
         for (int j = 0; j < 8; ++j) mx[j] = fmaxf(mx[j], fmaxf(sacc[kg][2 * j], sacc[kg][2 * j + 1]));
       float tmax = fmaxf(fmaxf(fmaxf(mx[0], mx[1]), fmaxf(mx[2], mx[3])),
                          fmaxf(fmaxf(mx[4], mx[5]), fmaxf(mx[6], mx[7])));
-      tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
+      {
+        const f32x2 hp = halves_pair(tmax);
+        tmax = fmaxf(hp[0], hp[1]);
+      }
       // The row's reference maximum m only moves when the tile maximum exceeds
       // it by more than 2^RESCALE_LOG2 (weights stay <= 2^RESCALE_LOG2 and the
       // final division by l is exact about it); the wave skips the O rescale
@@ -632,7 +635,10 @@ __global__ void __launch_bounds__(NW * 64, 1) attn_bf16_kernel(AttnParams p) {
     }
 
     // ---- finish the segment
-    lsum += __shfl_xor(lsum, 32);
+    {
+      const f32x2 hp = halves_pair(lsum);
+      lsum = hp[0] + hp[1];
+    }
     auto write_out = [&](const f32x16* ov, float inv) {
       if (!rvalid) return;
       __bf16* orow = out + (((size_t)s * R + r) * p.Hq + h) * D;
@@ -1054,7 +1060,10 @@ __global__ void __launch_bounds__(NP * 128, 1) attn_bf16_pc_kernel(AttnParams p)
               mb = fmaxf(mb, sacc[g][1][i]);
             }
             float tmax = fmaxf(ma, mb);
-            tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
+            {
+              const f32x2 hp = halves_pair(tmax);
+              tmax = fmaxf(hp[0], hp[1]);
+            }
             // lazy rescale: the reference maximum moves only by more than
             // 2^RESCALE_LOG2; the consumer rescales O and l before its next PV
             const float cand = tmax * p.scale_log2;
@@ -1214,7 +1223,7 @@ __global__ void __launch_bounds__(NP * 128, 1) attn_bf16_pc_kernel(AttnParams p)
             read_pages(gi);
             take_pages();
           };
-          auto issue_group = [&](int gi) {
+          auto issue_k = [&](int gi) {   // K(gi + 2)
             // page bases are wave-uniform; the per-lane offsets are made opaque
             // here so that base + offset stays a scalar base plus a 32-bit
             // vector offset instead of hoisted 64-bit per-lane pointers
@@ -1252,6 +1261,10 @@ __global__ void __launch_bounds__(NP * 128, 1) attn_bf16_pc_kernel(AttnParams p)
                     (__attribute__((address_space(3))) void*)(dst + j * 1024), 16, 0, 0);
               }
             }
+          };
+          auto issue_v = [&](int gi) {   // V(gi + 1)
+            int ln = lane;
+            asm volatile("" : "+v"(ln));
             {
               const char* base = vpb + ((size_t)vpg * p.Hkv + kvh) * PAGE_V;
               char* dst = vring + ((gi + 1 + NS) % NS) * VTILE_B + kp * (V_INS * 1024);
@@ -1265,6 +1278,10 @@ __global__ void __launch_bounds__(NP * 128, 1) attn_bf16_pc_kernel(AttnParams p)
                     (__attribute__((address_space(3))) void*)(dst + j * 1024), 16, 0, 0);
               }
             }
+          };
+          auto issue_group = [&](int gi) {
+            issue_k(gi);
+            issue_v(gi);
           };
           if (n_main > 0) {
             // g(-2) = {K(0), V(-1) re-reading tile 0 into the dead slot}, g(-1);
@@ -1317,7 +1334,10 @@ __global__ void __launch_bounds__(NP * 128, 1) attn_bf16_pc_kernel(AttnParams p)
         }
         __syncthreads();                                       // F1
 #pragma unroll
-        for (int g = 0; g < 2; ++g) lrow[g] += __shfl_xor(lrow[g], 32);
+        for (int g = 0; g < 2; ++g) {
+          const f32x2 hp = halves_pair(lrow[g]);
+          lrow[g] = hp[0] + hp[1];
+        }
         auto write_cols = [&](int g, int dg, const f32x16& ov, float inv) {   // columns dg*32..+31
           if (!rvalid[g]) return;
           __bf16* orow = out + (((size_t)s * R + rr[g]) * p.Hq + hq[g]) * D;

@@ -49,6 +49,17 @@ __device__ __forceinline__ float bf16_bits_to_f32(uint32_t b16) {
   return __uint_as_float(b16 << 16);
 }
 
+// The value of lane ^ 32 and this lane's, in lane order: (v[l & 31], v[l | 32]).
+// gfx950's v_permlane32_swap exchanges the upper half of its first operand
+// with the lower half of its second; with both equal to v, lane l ends up
+// holding v[l & 31] in the first result and v[l | 32] in the second (a VALU
+// exchange, not the LDS round trip of a general shuffle).  Both halves see the
+// pair in the same order, so a sum of the two is identical on all 64 lanes.
+__device__ __forceinline__ f32x2 halves_pair(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return f32x2{__uint_as_float(r[0]), __uint_as_float(r[1])};
+}
+
 __device__ __forceinline__ void set_err(int32_t* err, int32_t bit) {
   if (err) atomicOr(err, bit);
 }
