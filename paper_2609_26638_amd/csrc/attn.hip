@@ -747,6 +747,16 @@ __global__ void __launch_bounds__(NW * 64, 1) attn_bf16_kernel(AttnParams p) {
 // same sequence of barriers.
 // ---------------------------------------------------------------------------
 constexpr int PC_NSTAGE = 3;
+// Producer/consumer kernel, balanced split: cost units of a tile.  A tile
+// that reaches the window (staged through registers, unpipelined) costs about
+// 4.5 cache tiles (measured: 10.5 us against 2.3 us), so a workgroup's share
+// counts it that way instead of as one tile.
+constexpr int PC_WM = 4;    // units of a cache tile (keys below L)
+constexpr int PC_WW = 18;   // units of a window tile
+// units added to the last tile of an item: the end of a segment there (the
+// partial's publication, the next item's page staging and, for the last
+// workgroup to finish the item, the merge)
+constexpr int PC_WE = 24;
 constexpr int PC_LDS_DEPTH = 6;
 
 template <int D, int NP>
@@ -799,7 +809,9 @@ __global__ void __launch_bounds__(NP * 128, 1) attn_bf16_pc_kernel(AttnParams p)
   char* __restrict__ vpb = (char*)p.v_pool;
   __bf16* __restrict__ out = (__bf16*)p.out;
 
-  // ---- balanced split: tile prefix over sequences, equal shares
+  // ---- balanced split: cost-unit prefix over sequences (every item of a
+  // sequence has the same tiles), equal shares of units; a tile belongs to
+  // the workgroup whose share holds its first unit
   if (tid == 0) s_flag[0] = 0;
   for (int s0 = 0; s0 < p.S; s0 += NP * 128) {
     __syncthreads();
@@ -809,7 +821,7 @@ __global__ void __launch_bounds__(NP * 128, 1) attn_bf16_pc_kernel(AttnParams p)
       const int L = p.kv_len[s];
       const int T = L + R;
       if (L < 0 || T > p.max_pages * 16) s_flag[0] = 1;
-      else t = (T + KT - 1) / KT;
+      else t = PC_WM * (L / KT) + PC_WW * ((T + KT - 1) / KT - L / KT) + PC_WE;
     }
     s_seq[1 + tid + s0] = t;
     __syncthreads();
@@ -851,18 +863,30 @@ __global__ void __launch_bounds__(NP * 128, 1) attn_bf16_pc_kernel(AttnParams p)
       while (s_seq[s_cur + 1] * HN <= u) ++s_cur;
       const int s = s_cur;
       const int L = p.kv_len[s];
-      const int tiles = s_seq[s + 1] - s_seq[s];
-      const int local = u - s_seq[s] * HN;
-      const int qi = local / tiles;
-      const int j0 = local - qi * tiles;
-      const int j1 = min(tiles, j0 + (u_end - u));
+      const int iu = s_seq[s + 1] - s_seq[s];            // units of one item
+      const int qi = (u - s_seq[s] * HN) / iu;
+      const int P0 = s_seq[s] * HN + qi * iu;             // first unit of the item
+      const int nm = L / KT;                              // cache tiles
+      const int tiles = (L + R + KT - 1) / KT;
+      // first tile whose first unit is >= x (x in [0, iu]; iu maps to tiles)
+      auto tile_at = [&](int x) {
+        return x <= PC_WM * nm ? (x + PC_WM - 1) / PC_WM
+                               : min(tiles, nm + (x - PC_WM * nm + PC_WW - 1) / PC_WW);
+      };
+      auto owner = [&](int j) {   // workgroup holding tile j's first unit
+        return (P0 + (j <= nm ? PC_WM * j : PC_WM * nm + PC_WW * (j - nm))) / share;
+      };
+      const int j0 = tile_at(u - P0);
+      const int j1 = tile_at(min(u_end, P0 + iu) - P0);
+      u = P0 + iu;
+      // (share >= PC_WW + PC_WE, the longest span of a tile: every workgroup
+      // between an item's first and last owners holds at least one of its tiles)
+      if (j0 >= j1) continue;
       const int it = s * HN + qi;
       const int kvh = qi / p.n_row_tiles;
       const int rt = qi - kvh * p.n_row_tiles;
-      const int P0 = s_seq[s] * HN + qi * tiles;
-      const int kseg = (int)blockIdx.x - P0 / share;
-      const int nseg = (P0 + tiles - 1) / share - P0 / share + 1;
-      u += j1 - j0;
+      const int kseg = (int)blockIdx.x - owner(0);
+      const int nseg = owner(tiles - 1) - owner(0) + 1;
       if (!first_segment) __syncthreads();
       first_segment = false;
       const int T = L + R;
@@ -1542,7 +1566,15 @@ static AttnPlan plan_attn(int S, int R, int Hq, int Hkv, int D, int max_pages, i
   pl.n_items = S * Hkv * pl.n_row_tiles;
   const int max_tiles = (max_pages * DVS_PAGE_SIZE + KT - 1) / KT;
   if (pl.balanced) {
-    pl.share_min = (max_tiles + BAL_MAX_SEGS - 2) / (BAL_MAX_SEGS - 1);
+    if (pl.pc) {
+      // in cost units; an item has at most (R + KT - 1) / KT + 1 window tiles
+      const int R = pl.rows_total / G;
+      const int nwin = (R + KT - 1) / KT + 1;
+      const int max_units = PC_WM * max_tiles + (PC_WW - PC_WM) * nwin + PC_WE;
+      pl.share_min = std::max((max_units + BAL_MAX_SEGS - 2) / (BAL_MAX_SEGS - 1), PC_WW + PC_WE);
+    } else {
+      pl.share_min = (max_tiles + BAL_MAX_SEGS - 2) / (BAL_MAX_SEGS - 1);
+    }
     if (pl.share_min < 1) pl.share_min = 1;
     pl.max_segs = BAL_MAX_SEGS;
     pl.grid = device_cus();
