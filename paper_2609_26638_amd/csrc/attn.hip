@@ -157,84 +157,124 @@ __device__ __forceinline__ void fill_window_tile(int tid, int t0, int pg_lo, int
   constexpr int KROWB = D * 2;
   constexpr int PAGE_K = 16 * KROWB;
   constexpr int PAGE_V = D * 32;
-  constexpr int NKC = KT * CPR;              // 16-byte K chunks per tile
-  constexpr int NKI = (NKC + NT - 1) / NT;
-  constexpr int NVC = KT / 16 * D * 2;       // 16-byte V chunks (8 keys of one head-dim row)
-  constexpr int NVI = (NVC + NT - 1) / NT;
-  // ---- K, in batches of up to KB chunks per thread
-  constexpr int KB = NKI < 4 ? NKI : 4;
+  constexpr int NKC = KT * CPR;              // 16-byte K chunks per tile (key-major)
+  constexpr int NVC = KT / 16 * D * 2;       // 16-byte V chunks of the LDS tile (8 keys of one head-dim row)
+  constexpr int NNC = KT * CPR;              // 16-byte v_new chunks (8 head-dim values of one key)
+  constexpr int NKI = (NKC + NT - 1) / NT, NVI = (NVC + NT - 1) / NT, NNI = (NNC + NT - 1) / NT;
+  // Per thread up to QB chunks of each kind per batch (one batch at 512
+  // threads); every global load of a batch is issued before any store.
+  //   K:  key rows, from the pool (key < L), k_new (< T) or zero.
+  //   V pool part: LDS chunk (head-dim row d, 8 keys) from the pool's
+  //       head-dim-major page when its keys are < L (element by element where
+  //       the chunk straddles L; its keys >= L are left to the next part).
+  //   V new part: a v_new chunk (one key, 8 head-dim values) for keys in
+  //       [L, T), zero for keys >= T, written to the 8 head-dim rows of the
+  //       key with 2-byte LDS stores (and appended to the pool the same way).
+  // The two V parts write disjoint bytes of the tile.
+  constexpr int QB = 2;
+  constexpr int NBK = (NKI + QB - 1) / QB, NBV = (NVI + QB - 1) / QB, NBN = (NNI + QB - 1) / QB;
+  constexpr int NB = NBK > NBV ? (NBK > NBN ? NBK : NBN) : (NBV > NBN ? NBV : NBN);
 #pragma unroll 1
-  for (int k0 = 0; k0 < NKI; k0 += KB) {
-    u32x4 kv[KB];
+  for (int b = 0; b < NB; ++b) {
+    // ---- page ids (LDS), read together; index clamped into the array for
+    // chunks whose page is not used
+    int kpg[QB], vpg[QB], npg[QB];
 #pragma unroll
-    for (int k = 0; k < KB; ++k) {
-      const int ci = tid + (k0 + k) * NT;
-      const int kk = ci / CPR, cc = ci - (ci / CPR) * CPR;
-      const int key = t0 + kk;
-      const char* src = knb;
-      bool valid = false;
-      if (ci < NKC && key < L) {
-        src = kpb + ((size_t)s_pages[(key >> 4) - pg_lo] * Hkv + kvh) * PAGE_K + (key & 15) * KROWB + cc * 16;
-        valid = true;
-      } else if (ci < NKC && key < T) {
-        src = knb + (((size_t)s * R + (key - L)) * Hkv + kvh) * KROWB + cc * 16;
-        valid = true;
-      }
-      const u32x4 x = *(const u32x4*)src;
-      kv[k] = valid ? x : u32x4{0, 0, 0, 0};
+    for (int k = 0; k < QB; ++k) {
+      const int ck = tid + (b * QB + k) * NT;
+      kpg[k] = s_pages[min(max(((t0 + ck / CPR) >> 4) - pg_lo, 0), SUB_TILES * 4 - 1)];
+      const int cv = tid + (b * QB + k) * NT;
+      vpg[k] = s_pages[min(max(((t0 + (cv / (D * 2)) * 16) >> 4) - pg_lo, 0), SUB_TILES * 4 - 1)];
+      const int cn = tid + (b * QB + k) * NT;
+      npg[k] = s_pages[min(max(((t0 + cn / CPR) >> 4) - pg_lo, 0), SUB_TILES * 4 - 1)];
     }
+    // ---- loads
+    u32x4 kv[QB], pv[QB], nv[QB];
+    uint16_t pe[QB][8];
 #pragma unroll
-    for (int k = 0; k < KB; ++k) {
-      const int ci = tid + (k0 + k) * NT;
-      if (ci >= NKC) break;
-      const int kk = ci / CPR, cc = ci - (ci / CPR) * CPR;
-      const int key = t0 + kk;
-      *(u32x4*)(kb + kk * KROWB + ((cc ^ kswz<CPR>(kk)) << 4)) = kv[k];
-      if (append && key >= L && key < T)
-        *(u32x4*)(kpb + ((size_t)s_pages[(key >> 4) - pg_lo] * Hkv + kvh) * PAGE_K + (key & 15) * KROWB + cc * 16) = kv[k];
-    }
-  }
-  // ---- V (head-dim-major rows of 16 keys)
-#pragma unroll 1
-  for (int k = 0; k < NVI; ++k) {
-    const int ci = tid + k * NT;
-    if (ci >= NVC) break;
-    const int tp = ci / (D * 2);
-    const int d = (ci >> 1) % D;
-    const int hc = ci & 1;
-    const int kbase = t0 + tp * 16 + hc * 8;
-    u32x4 val;
-    if (kbase + 8 <= L) {
-      val = *(const u32x4*)(vpb + ((size_t)s_pages[(kbase >> 4) - pg_lo] * Hkv + kvh) * PAGE_V + d * 32 + hc * 16);
-    } else {
-      uint16_t e16[8];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const int key = kbase + e;
-        const char* src = vnb;
-        bool valid = false;
-        if (key < L) {
-          src = vpb + ((size_t)s_pages[(key >> 4) - pg_lo] * Hkv + kvh) * PAGE_V + d * 32 + (key & 15) * 2;
-          valid = true;
-        } else if (key < T) {
-          src = vnb + (((size_t)s * R + (key - L)) * Hkv + kvh) * KROWB + d * 2;
-          valid = true;
-        }
-        const uint16_t x = *(const uint16_t*)src;
-        e16[e] = valid ? x : (uint16_t)0;
+    for (int k = 0; k < QB; ++k) {
+      {   // K
+        const int ci = tid + (b * QB + k) * NT;
+        const int key = t0 + ci / CPR, cc = ci % CPR;
+        const bool live = b * QB + k < NKI && ci < NKC;
+        const bool inpool = live && key < L, innew = live && key >= L && key < T;
+        const char* src = inpool ? kpb + ((size_t)kpg[k] * Hkv + kvh) * PAGE_K + (key & 15) * KROWB + cc * 16
+                                 : knb + (((size_t)s * R + (innew ? key - L : 0)) * Hkv + kvh) * KROWB + cc * 16;
+        const u32x4 x = *(const u32x4*)src;
+        kv[k] = (inpool || innew) ? x : u32x4{0, 0, 0, 0};
       }
-      if (append) {
+      {   // V, pool part
+        const int ci = tid + (b * QB + k) * NT;
+        const int d = (ci >> 1) % D;
+        const int kbase = t0 + (ci / (D * 2)) * 16 + (ci & 1) * 8;
+        const bool live = b * QB + k < NVI && ci < NVC;
+        const char* vpage = vpb + ((size_t)vpg[k] * Hkv + kvh) * PAGE_V + d * 32 + (kbase & 15) * 2;
+        const bool whole = live && kbase + 8 <= L;
+        const u32x4 x = *(const u32x4*)(whole ? vpage : vnb);
+        pv[k] = x;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const int key = kbase + e;
-          if (key >= L && key < T)
-            *(uint16_t*)(vpb + ((size_t)s_pages[(key >> 4) - pg_lo] * Hkv + kvh) * PAGE_V + d * 32 + (key & 15) * 2) = e16[e];
+        for (int e = 0; e < 8; ++e) {   // straddling chunk only (rare): keys < L
+          const bool el = live && !whole && kbase + e < L;
+          const uint16_t y = *(const uint16_t*)(el ? vpage + 2 * e : vnb);
+          pe[k][e] = y;
         }
       }
-      val = u32x4{e16[0] | ((uint32_t)e16[1] << 16), e16[2] | ((uint32_t)e16[3] << 16),
-                  e16[4] | ((uint32_t)e16[5] << 16), e16[6] | ((uint32_t)e16[7] << 16)};
+      {   // V, new part
+        const int ci = tid + (b * QB + k) * NT;
+        const int key = t0 + ci / CPR, cc = ci % CPR;
+        const bool live = b * QB + k < NNI && ci < NNC && key >= L && key < T;
+        const u32x4 x = *(const u32x4*)(vnb + (((size_t)s * R + (live ? key - L : 0)) * Hkv + kvh) * KROWB + cc * 16);
+        nv[k] = live ? x : u32x4{0, 0, 0, 0};
+      }
     }
-    *(u32x4*)(vb + (tp * D + d) * 32 + ((hc ^ vswz(d)) << 4)) = val;
+    // ---- stores: LDS tiles, then the pool appends of keys in [L, T)
+#pragma unroll
+    for (int k = 0; k < QB; ++k) {
+      {   // K
+        const int ci = tid + (b * QB + k) * NT;
+        const int kk = ci / CPR, cc = ci % CPR;
+        const int key = t0 + kk;
+        if (b * QB + k < NKI && ci < NKC) {
+          *(u32x4*)(kb + kk * KROWB + ((cc ^ kswz<CPR>(kk)) << 4)) = kv[k];
+          if (append && key >= L && key < T)
+            *(u32x4*)(kpb + ((size_t)kpg[k] * Hkv + kvh) * PAGE_K + (key & 15) * KROWB + cc * 16) = kv[k];
+        }
+      }
+      {   // V, pool part
+        const int ci = tid + (b * QB + k) * NT;
+        const int tp = ci / (D * 2);
+        const int d = (ci >> 1) % D;
+        const int hc = ci & 1;
+        const int kbase = t0 + tp * 16 + hc * 8;
+        char* dst = vb + (tp * D + d) * 32 + ((hc ^ vswz(d)) << 4);
+        if (b * QB + k < NVI && ci < NVC) {
+          if (kbase + 8 <= L) {
+            *(u32x4*)dst = pv[k];
+          } else if (kbase < L) {
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+              if (kbase + e < L) *(uint16_t*)(dst + 2 * e) = pe[k][e];
+          }
+        }
+      }
+      {   // V, new part (keys >= L of the tile, zeros past T)
+        const int ci = tid + (b * QB + k) * NT;
+        const int kk = ci / CPR, cc = ci % CPR;
+        const int key = t0 + kk;
+        if (b * QB + k < NNI && ci < NNC && key >= L) {
+          const int tp = kk >> 4, kin = kk & 15;
+          const uint32_t w[4] = {nv[k][0], nv[k][1], nv[k][2], nv[k][3]};
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            const int d = cc * 8 + j;
+            const uint16_t v = (uint16_t)(w[j >> 1] >> (16 * (j & 1)));
+            *(uint16_t*)(vb + (tp * D + d) * 32 + ((((kin >> 3) ^ vswz(d)) << 4) | ((kin & 7) * 2))) = v;
+            if (append && key < T)
+              *(uint16_t*)(vpb + ((size_t)npg[k] * Hkv + kvh) * PAGE_V + d * 32 + (key & 15) * 2) = v;
+          }
+        }
+      }
+    }
   }
 }
 
@@ -1125,14 +1165,16 @@ __global__ void __launch_bounds__(NP * 128, 1) attn_bf16_pc_kernel(AttnParams p)
             pc_barrier();   // B: consumers hold P(i-1)
             if (i < n_main) softmax_out(false, 0);
           }
+          // LDS-only barriers: the fill's pool appends are read by no one in
+          // this launch, so they need not complete before the tile is used
           for (int jt = jm; jt < jb; ++jt) {
-            __syncthreads();
+            pc_barrier();
             fill_window(jt * KT, ja * 4);
-            __syncthreads();
+            pc_barrier();
             qk(kring);
             softmax_out(true, jt * KT);
-            __syncthreads();                                 // P of the window tile ready
-            __syncthreads();                                 // consumer done with it
+            pc_barrier();                                    // P of the window tile ready
+            pc_barrier();                                    // consumer done with it
           }
         }
         // segment-final m (l is the consumer's)
@@ -1345,15 +1387,15 @@ __global__ void __launch_bounds__(NP * 128, 1) attn_bf16_pc_kernel(AttnParams p)
             if (nxt) take_pages();
           }
           for (int jt = jm; jt < jb; ++jt) {
-            __syncthreads();
+            pc_barrier();
             fill_window(jt * KT, ja * 4);
-            __syncthreads();
-            __syncthreads();                                   // producer's P of the window tile
+            pc_barrier();
+            pc_barrier();                                      // producer's P of the window tile
             Hand hd;
             take_p(hd);
             add_l(hd);
             pv(hd, vring);
-            __syncthreads();
+            pc_barrier();
           }
         }
         __syncthreads();                                       // F1
