@@ -32,6 +32,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+MFMA_PEAK_TFLOPS = 2500.0   # dense bf16 matrix cores (no sparsity)
 COUNTERS = os.path.join(ROOT, "profiles", "attn_long_document_counters.json")
 ATTN_SOURCES = [os.path.join(ROOT, "paper_2609_26638_amd", "csrc", f)
                 for f in ("attn.hip", "dvs_common.h")]
@@ -52,6 +53,32 @@ def attn_algorithmic_bytes(kv_len, S, R, Hq, Hkv, D, b=2) -> int:
     qo = 2 * S * R * Hq * D * b
     pages = int(sum((int(L) + 15) // 16 for L in kv_len)) * 4
     return kv + window + qo + pages
+
+
+def attn_algorithmic_flops(kv_len, S, R, Hq, D) -> int:
+    """Matrix-product flops of one launch: QK^T and PV over every key a row
+    can see, counted for all keys of the window (the masked part of the
+    window block is negligible)."""
+    return int(sum(4 * (int(L) + R) * R * Hq * D for L in kv_len))
+
+
+def copy_ceiling_gbs(nbytes=1 << 30, reps=5):
+    """Device-to-device copy rate (bytes read + written per second), the
+    measured ceiling next to the 8 TB/s datasheet peak."""
+    import torch
+    src = torch.ones(nbytes, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        dst.copy_(src)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    del src, dst
+    return 2 * nbytes / (ms / 1e3) / 1e9
 
 
 def cpu_baseline(ai, li, n_seq: int):
@@ -240,6 +267,7 @@ def main():
         torch.cuda.synchronize()
         print(json.dumps({"profile_attn": args.profile_attn, "attn_algorithmic_bytes":
                           attn_algorithmic_bytes(ai.state.kv_len, S, R, Hq, Hkv, D),
+                          "attn_algorithmic_flops": attn_algorithmic_flops(ai.state.kv_len, S, R, Hq, D),
                           "copy_bytes": 1 << 30, "src_hash": attn_source_hash(),
                           "err": int(st.err.item())}), flush=True)
         return
@@ -292,6 +320,10 @@ def main():
     value = tokens_per_step / (ms_nosync / 1e3)
     attn_bytes = attn_algorithmic_bytes(ai.state.kv_len, S, R, Hq, Hkv, D)
     attn_gbs = attn_bytes / (stage_ms["attn"] / 1e3) / 1e9
+    attn_flops = attn_algorithmic_flops(ai.state.kv_len, S, R, Hq, D)
+    attn_tflops = attn_flops / (stage_ms["attn"] / 1e3) / 1e12
+    argmax_gbs = S * R * V * 2 / (stage_ms["argmax"] / 1e3) / 1e9
+    copy_gbs = copy_ceiling_gbs()
     traffic = None
     if os.path.exists(COUNTERS):
         c = json.load(open(COUNTERS))
@@ -323,7 +355,13 @@ def main():
             "frac": round(attn_gbs / HBM_PEAK_GBS, 4), "traffic": traffic,
             "kernel": "attn_bf16_pc_kernel<128,4> (head_dim, producer/consumer pairs)", "algorithmic_bytes": attn_bytes,
             "avg_ms": round(stage_ms["attn"], 4),
+            # secondary figures: the same launches against the measured copy
+            # rate and against the dense bf16 matrix-core peak
+            "copy_ceiling_gbs": round(copy_gbs, 1), "frac_of_copy": round(attn_gbs / copy_gbs, 4),
+            "algorithmic_flops": attn_flops, "mfma_tflops": round(attn_tflops, 1),
+            "mfma_peak_tflops": MFMA_PEAK_TFLOPS, "mfma_frac": round(attn_tflops / MFMA_PEAK_TFLOPS, 4),
         },
+        "argmax_gbs": round(argmax_gbs, 1),
         "breakdown_ms": {k: round(v, 4) for k, v in stage_ms.items()},
         "tokens_per_step": tokens_per_step,
         "accept_mean": round(accept_mean, 3),

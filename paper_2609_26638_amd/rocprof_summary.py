@@ -10,6 +10,12 @@
   dispatches.  The result is written as JSON next to the source hash the
   bench compares against, so that a changed kernel does not report stale
   traffic.
+* ``matrix``: matrix-core and vector-ALU use of one kernel from a ``--pmc``
+  run with GRBM_GUI_ACTIVE, SQ_VALU_MFMA_BUSY_CYCLES, SQ_VALU_MFMA_COEXEC_CYCLES,
+  SQ_ACTIVE_INST_VALU and SQ_INSTS_VALU_MFMA_MOPS_BF16: the clock (GPU busy
+  cycles over the dispatch's duration), the share of SIMD cycles the matrix
+  core was busy, the vector ALU's share, both at once, and the matrix flops
+  executed against the algorithmic count.
 """
 import argparse
 import collections
@@ -56,6 +62,17 @@ def per_dispatch(counter_dir, counter):
     return acc
 
 
+def _meta(path):
+    meta = None
+    for line in open(path):
+        line = line.strip()
+        if line.startswith("{") and "profile_attn" in line:
+            meta = json.loads(line)
+    if meta is None:
+        raise SystemExit("no profile_attn line in " + path)
+    return meta
+
+
 def traffic(fetch_dir, write_dir, kernel, copy_bytes):
     out = {}
     for counter, d in (("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)):
@@ -68,6 +85,49 @@ def traffic(fetch_dir, write_dir, kernel, copy_bytes):
         scale = copy_bytes / (copy_kib * 1024.0)
         out[counter] = {"kib_per_dispatch": vals, "copy_kib": copy_kib, "scale": scale,
                         "bytes_per_dispatch": sum(vals) / len(vals) * 1024.0 * scale}
+    return out
+
+
+def per_dispatch_instances(counter_dir):
+    """{dispatch id: {"name", "ns", counter: [instance values]}}"""
+    acc = collections.OrderedDict()
+    for r in _rows(counter_dir, "counter_collection.csv"):
+        d = int(r["Dispatch_Id"])
+        e = acc.setdefault(d, {"name": r["Kernel_Name"],
+                               "ns": int(r["End_Timestamp"]) - int(r["Start_Timestamp"])})
+        e.setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
+    return acc
+
+
+def _gpu_agent(counter_dir):
+    for r in _rows(counter_dir, "agent_info.csv"):
+        if r.get("Agent_Type") == "GPU":
+            return r
+    return {}
+
+
+def matrix(counter_dir, kernel, flops):
+    ag = _gpu_agent(counter_dir)
+    xcc = int(ag.get("Num_Xcc", 8)) or 8
+    simds = int(ag.get("Simd_Count", 1024)) or 1024
+    cus = int(ag.get("Cu_Count", 256)) or 256
+    out = []
+    for d, e in per_dispatch_instances(counter_dir).items():
+        if kernel not in e["name"]:
+            continue
+        # GRBM_GUI_ACTIVE comes summed over the XCDs: busy cycles of one XCD
+        gui = sum(e["GRBM_GUI_ACTIVE"]) / xcc
+        res = {"dispatch": d, "duration_us": e["ns"] / 1e3, "clock_ghz": gui / e["ns"],
+               "mfma_busy_pct": 100.0 * sum(e["SQ_VALU_MFMA_BUSY_CYCLES"]) / (gui * simds),
+               "mfma_and_valu_pct": 100.0 * sum(e["SQ_VALU_MFMA_COEXEC_CYCLES"]) / (gui * simds),
+               "valu_busy_pct": 100.0 * sum(e["SQ_ACTIVE_INST_VALU"]) / (gui * cus)}
+        if "SQ_INSTS_VALU_MFMA_MOPS_BF16" in e:
+            ex = sum(e["SQ_INSTS_VALU_MFMA_MOPS_BF16"]) * 512.0
+            res["mfma_flops"] = ex
+            res["mfma_flops_over_algorithmic"] = ex / flops if flops else None
+        out.append(res)
+    if not out:
+        raise ValueError(f"no {kernel} dispatch in {counter_dir}")
     return out
 
 
@@ -86,18 +146,35 @@ def main():
     t.add_argument("--kernel", default="attn_bf16")
     t.add_argument("--command", required=True)
     t.add_argument("--out", required=True)
+    m = sub.add_parser("matrix")
+    m.add_argument("--pmc", required=True, help="output directory of the --pmc run")
+    m.add_argument("--meta", required=True, help="the JSON line bench.py --profile-attn printed")
+    m.add_argument("--kernel", default="attn_bf16")
+    m.add_argument("--command", required=True)
+    m.add_argument("--out", required=True)
     a = ap.parse_args()
+    if a.cmd == "matrix":
+        meta = _meta(a.meta)
+        per = matrix(a.pmc, a.kernel, meta.get("attn_algorithmic_flops"))
+        keys = [k for k in per[0] if k != "dispatch"]
+        # the first launch of the process reads start-up cycles into its
+        # busy count; the mean is over the later ones
+        later = per[1:] if len(per) > 1 else per
+        res = {"kernel": a.kernel, "src_hash": meta["src_hash"], "command": a.command,
+               "algorithmic_flops": meta.get("attn_algorithmic_flops"), "launches": len(per),
+               "mean_over": "launches 2..N" if len(per) > 1 else "launch 1",
+               "mean": {k: sum(p[k] for p in later) / len(later) for k in keys},
+               "per_launch": per}
+        with open(a.out, "w") as f:
+            json.dump(res, f, indent=1)
+            f.write("\n")
+        print(json.dumps(res["mean"]))
+        return
     if a.cmd == "stats":
         with open(a.out, "w") as f:
             f.write(kernel_stats_md(a.stats, a.title, a.command))
         return
-    meta = None
-    for line in open(a.meta):
-        line = line.strip()
-        if line.startswith("{") and "profile_attn" in line:
-            meta = json.loads(line)
-    if meta is None:
-        raise SystemExit("no profile_attn line in " + a.meta)
+    meta = _meta(a.meta)
     tr = traffic(a.fetch, a.write, a.kernel, meta["copy_bytes"])
     total = tr["FETCH_SIZE"]["bytes_per_dispatch"] + tr["WRITE_SIZE"]["bytes_per_dispatch"]
     res = {"kernel": a.kernel, "src_hash": meta["src_hash"], "command": a.command,
