@@ -1345,7 +1345,7 @@ __global__ void __launch_bounds__(NP * 128, 1) attn_bf16_pc_kernel(AttnParams p)
               }
             }
           };
-          auto issue_group = [&](int gi) {
+          auto issue_group = [&](int gi) {   // prologue groups
             issue_k(gi);
             issue_v(gi);
           };
@@ -1377,13 +1377,15 @@ __global__ void __launch_bounds__(NP * 128, 1) attn_bf16_pc_kernel(AttnParams p)
               asm volatile("" ::"v"(lrow[0]), "v"(lrow[1]));
             }
             pc_barrier();   // B
-            if (i >= 1) pv(hd, vring + ((i - 1) % NS) * VTILE_B);
-            // The copies go out after the products: issuing 8 direct loads
-            // stalls the wave while the load path drains them, which here
-            // overlaps the producer's softmax instead of delaying barrier B.
+            // The copies go out in phase 2, around the products: issuing 8
+            // direct loads stalls the wave while the load path drains them,
+            // which here overlaps the producer's softmax instead of delaying
+            // barrier B; K (needed first) before the products, V after them.
             // Slots: K(i+2) replaces K(i-1) (read by QK(i-1) before barrier
             // A), V(i+1) replaces V(i-2) (read by PV(i-2) last period).
-            if (i <= n_main - 2) issue_group(i);
+            if (i <= n_main - 2) issue_k(i);
+            if (i >= 1) pv(hd, vring + ((i - 1) % NS) * VTILE_B);
+            if (i <= n_main - 2) issue_v(i);
             if (nxt) take_pages();
           }
           for (int jt = jm; jt < jb; ++jt) {
