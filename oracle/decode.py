@@ -35,6 +35,20 @@ boundary is the last committed token (item Next round).  A stop condition
 (EOS or the output budget) truncates the committed run at that token and
 freezes the sequence (item Next round, last sentence).
 
+The paper's own round (two forwards)
+------------------------------------
+The appendix round is also kept here, as written: a draft forward over
+``[x0, [M] x B]`` (1 causal row, B mask rows) gives ``a0`` from the boundary
+row and ``d_j`` from mask row j (j = 1..B); x0's causal KV from that forward
+is kept (``kv_len`` + 1); a verify forward over ``[a0, d_1..d_B]`` (B + 1
+causal rows, no mask rows) at positions ``L + 1 ..`` overwrites the draft's
+mask-row slots and gives ``a_j = top1(row j-1)``, j = 1..B+1; A in 0..B is the
+longest prefix with ``d_j == a_j``; the round commits ``a0, d_1..d_A,
+a_{A+1}`` (2..B+2 tokens).  Its commit is ``kv_commit`` with ``lead = a0``:
+the run starts with the lead token and, since the kept x0 is already in
+``kv_len``, the new length is ``kv_len + k - 1``; the pages cover the next
+round's windows, ``[L', L' + B + 2)`` (``window = B + 2``).
+
 Top-1 rule: the maximum logit wins; among equal maxima the lowest vocabulary
 index wins; -0.0 and +0.0 are equal.  Non-finite logits are an error.
 
@@ -101,19 +115,25 @@ def accept(argmax: np.ndarray, draft: np.ndarray, n_causal: int) -> np.ndarray:
     return A
 
 
-def committed_run(argmax_row: np.ndarray, draft_row: np.ndarray, A: int) -> list:
-    """The tokens a step commits before any stop rule: d_1..d_A then a_{A+1}."""
-    return [int(draft_row[j - 1]) for j in range(1, A + 1)] + [int(argmax_row[A])]
+def committed_run(argmax_row: np.ndarray, draft_row: np.ndarray, A: int, lead=None) -> list:
+    """The tokens a step commits before any stop rule: d_1..d_A then a_{A+1},
+    after the lead token a0 in the two-forward round."""
+    run = [int(draft_row[j - 1]) for j in range(1, A + 1)] + [int(argmax_row[A])]
+    return run if lead is None else [int(lead)] + run
 
 
 def kv_commit(st, accept_len: np.ndarray, argmax: np.ndarray, n_causal: int, n_mask: int,
-              eos_id: int = -1, max_new: int | None = None, page_size: int = 16) -> int:
+              eos_id: int = -1, max_new: int | None = None, page_size: int = 16,
+              lead: np.ndarray | None = None, window: int | None = None) -> int:
     """Apply one step's commit to ``st`` (a synth.PagedState-like object) in place.
 
+    ``lead`` (two-forward round): per-sequence a0, committed first; the
+    boundary's KV is then already in ``kv_len``.  ``window``: rows of the next
+    window the pages must cover (default n_causal + n_mask).
     Returns the error word (0 on success; on error ``st`` is unchanged).
     """
     S = st.kv_len.shape[0]
-    R = n_causal + n_mask
+    R = n_causal + n_mask if window is None else window
     W = st.draft.shape[1]
     if n_mask > 0 and n_mask < W:
         raise ValueError("mask rows must cover the draft width")
@@ -129,7 +149,8 @@ def kv_commit(st, accept_len: np.ndarray, argmax: np.ndarray, n_causal: int, n_m
     for s in range(S):
         if st.finished[s]:
             continue
-        run = committed_run(argmax[s], st.draft[s], int(accept_len[s]))
+        run = committed_run(argmax[s], st.draft[s], int(accept_len[s]),
+                            None if lead is None else lead[s])
         kept = []
         stop = False
         for tok in run:
@@ -143,7 +164,7 @@ def kv_commit(st, accept_len: np.ndarray, argmax: np.ndarray, n_causal: int, n_m
         if st.out_count[s] + len(kept) >= max_new:
             stop = True
         runs[s] = kept
-        new_len[s] = st.kv_len[s] + len(kept)
+        new_len[s] = st.kv_len[s] + len(kept) - (0 if lead is None else 1)
         if kept:
             new_bound[s] = kept[-1]
         if n_mask > 0:

@@ -138,6 +138,33 @@ class OracleModel:
                              page_size=self.page_size)
         return logits, am, A, err
 
+    def literal_round(self, st, B: int, eos_id: int = -1, max_new=None):
+        """The paper's two-forward round (appendix "Self-Speculative Decoding
+        and KV-Cache Update"); see oracle.decode.  Pages must cover
+        [L, L + B + 2).  Returns (draft logits, verify logits, verify top-1,
+        accept_len, err)."""
+        S = st.kv_len.shape[0]
+        live = st.finished == 0
+        # draft forward: [x0, [M] x B]; a0 from the boundary row, d_j from mask row j
+        tok = np.empty((S, B + 1), dtype=np.int64)
+        tok[:, 0] = st.boundary
+        tok[:, 1:] = self.mask_id
+        logits_d = self.forward(self.embed[tok], st, 1, B)
+        am_d = odec.top1_rows(logits_d)
+        a0 = am_d[:, 0].copy()
+        st.draft[live, :B] = am_d[live, 1:B + 1]
+        st.kv_len[live] += 1                      # x0's causal KV is kept
+        # verify forward: [a0, d_1..d_B] under causal attention from L + 1
+        tok_v = np.empty((S, B + 1), dtype=np.int64)
+        tok_v[:, 0] = a0
+        tok_v[:, 1:] = st.draft[:, :B]
+        logits_v = self.forward(self.embed[tok_v], st, B + 1, 0)
+        am_v = odec.top1_rows(logits_v)
+        A = odec.accept(am_v, st.draft, B + 1)
+        err = odec.kv_commit(st, A, am_v, B + 1, 0, eos_id=eos_id, max_new=max_new,
+                             page_size=self.page_size, lead=a0, window=B + 2)
+        return logits_d, logits_v, am_v, A, err
+
     def ar_step(self, st, eos_id: int = -1, max_new=None):
         """One greedy AR step: window [x0]; commits its top-1."""
         tok = st.boundary[:, None].astype(np.int64)

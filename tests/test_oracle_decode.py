@@ -103,6 +103,35 @@ def test_commit_golden_example():
         assert list(st.out_tokens[s, :st.out_count[s]]) == toks
 
 
+def test_literal_round_commit_hand_example():
+    # Two-forward round, B = 2: the verify window is [a0, d_1, d_2] (3 causal
+    # rows), kv_len already counts x0, the run is a0, d_1..d_A, a_{A+1} and
+    # the pages must cover the next round's [L', L' + B + 2).  Page size 4.
+    # seq0: L0 = 5 (kv_len 6), a0 = 40, d = [7, 8], verify top-1 [7, 50, 60]:
+    #   a_1 = 7 = d_1, a_2 = 50 != 8 -> A = 1; run [40, 7, 50]; L' = 6 + 3 - 1 = 8;
+    #   boundary 50; needs ceil((8 + 4) / 4) = 3 pages, holds 3.
+    # seq1: L0 = 2 (kv_len 3), a0 = 41, d = [9, 10], top-1 [9, 10, 61]: A = 2;
+    #   run [41, 9, 10, 61]; L' = 3 + 4 - 1 = 6; boundary 61; needs ceil(10 / 4)
+    #   = 3, holds 2 -> pops the stack top (page 42) into logical page 2.
+    st = _state_from({
+        "kv_len": [6, 3], "page_table": [[10, 11, 12, -1], [20, 21, -1, -1]],
+        "num_pages": [3, 2], "free_stack": [40, 41, 42, -1], "free_top": 3,
+        "boundary": [100, 200], "draft": [[7, 8], [9, 10]]})
+    am = np.array([[7, 50, 60], [9, 10, 61]], np.int32)
+    A = od.accept(am, st.draft, 3)
+    np.testing.assert_array_equal(A, [1, 2])
+    err = od.kv_commit(st, A, am, 3, 0, page_size=4, lead=np.array([40, 41]), window=4)
+    assert err == 0
+    np.testing.assert_array_equal(st.kv_len, [8, 6])
+    np.testing.assert_array_equal(st.boundary, [50, 61])
+    assert list(st.out_tokens[0, :st.out_count[0]]) == [40, 7, 50]
+    assert list(st.out_tokens[1, :st.out_count[1]]) == [41, 9, 10, 61]
+    np.testing.assert_array_equal(st.page_table, [[10, 11, 12, -1], [20, 21, 42, -1]])
+    np.testing.assert_array_equal(st.num_pages, [3, 3])
+    assert st.free_top == 2
+    np.testing.assert_array_equal(st.draft, [[7, 8], [9, 10]])   # no mask rows: unchanged
+
+
 def test_commit_max_new_truncates():
     g = json.load(open(os.path.join(GOLDEN, "commit_example.json")))
     st = _state_from(g["before"])

@@ -6,7 +6,12 @@ the paper's AR-equivalence argument (committed stream of self-speculative
 decoding == greedy AR, in exact arithmetic) on small random-init models,
 B=1 reducing to AR, a draft equal to the AR continuation being fully
 accepted, and every draft over a tiny vocabulary committing the AR tokens.
+The paper's two-forward round: its stream equals greedy AR, and its
+accounting (a round commits A + 2 tokens in two forwards, so tokens per
+forward = (A + 2) / 2) matches the acceptance / TPF pairs the paper prints.
 """
+import json
+import os
 import itertools
 
 import numpy as np
@@ -57,12 +62,14 @@ def _tiny_model(seed, V=11, H=32, Hq=4, Hkv=2, D=8, n_layers=2, ffn=48, std=0.5,
     return w, kp, vp, rng
 
 
-def _prefilled(seed, S=2, P=9, B=4, **kw):
+def _prefilled(seed, S=2, P=9, B=4, n_causal=None, **kw):
     w, kp, vp, rng = _tiny_model(seed, **kw)
     m = om.OracleModel(w, kp, vp)
-    st = synth.make_paged_state(rng, np.zeros(S, np.int64), P + 2 * B, max_pages=32,
+    rows = P + max(2 * B, B + 2)
+    st = synth.make_paged_state(rng, np.zeros(S, np.int64), rows, max_pages=32,
                                 scatter=True, slack=0.0, extra_pages=kp[0].shape[0] - S * 2
-                                - (P + 2 * B) // 16 * S, n_causal=B, max_new=256)
+                                - rows // 16 * S, n_causal=B if n_causal is None else n_causal,
+                                max_new=256)
     x = rng.standard_normal((S, P, w.H))
     m.prefill(st, x, B)
     return m, st
@@ -153,3 +160,50 @@ def test_b1_step_is_ar_step():
         assert err == 0 and list(A) == [0, 0]
     for s in range(2):
         assert list(ss.out_tokens[s, :ss.out_count[s]]) == ar[s]
+
+
+@pytest.mark.parametrize("seed,B", [(10, 4), (11, 3), (12, 1), (13, 6)])
+def test_literal_round_stream_equals_greedy_ar(seed, B):
+    m, st = _prefilled(seed, B=B, n_causal=B + 1)
+    n = 30
+    ar = _ar_tokens(m, st, n)
+    ms, ss = _clone(m), st.copy()
+    rounds = 0
+    while min(ss.out_count) < n + 1:
+        before = ss.out_count.copy()
+        _, _, _, A, err = ms.literal_round(ss, B)
+        assert err == 0
+        assert np.all((A >= 0) & (A <= B))
+        # a round commits a0, d_1..d_A and a_{A+1}
+        np.testing.assert_array_equal(ss.out_count - before, A + 2)
+        rounds += 1
+    for s in range(ss.kv_len.shape[0]):
+        got = list(ss.out_tokens[s, :ss.out_count[s]])
+        L = min(len(got), len(ar[s]))
+        assert got[:L] == ar[s][:L]
+        # KV holds every committed token but the boundary: the prompt, x0 and
+        # the committed run up to its last token
+        assert ss.kv_len[s] == st.kv_len[s] + ss.out_count[s] - 1
+    assert rounds <= (n + 1) // 2 + 1
+
+
+def test_literal_round_accounting_gives_tokens_per_forward():
+    B = 4
+    m, st = _prefilled(14, B=B, n_causal=B + 1, std=0.9)
+    ms, ss = _clone(m), st.copy()
+    As, committed = [], 0
+    for _ in range(8):
+        before = int(ss.out_count.sum())
+        _, _, _, A, err = ms.literal_round(ss, B)
+        assert err == 0
+        As.extend(int(a) for a in A)
+        committed += int(ss.out_count.sum()) - before
+    forwards = 2 * 8 * ss.kv_len.shape[0]         # two forwards per round and sequence
+    assert committed / forwards == (np.mean(As) + 2) / 2
+
+
+def test_tpf_identity_against_printed_table():
+    g = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "tpf_by_content_type.json")))
+    for row in g["rows"]:
+        # the paper prints one decimal: the identity must agree to that digit
+        assert abs((row["accepted"] + 2) / 2 - row["tpf"]) <= 0.05 + 1e-12, row
