@@ -175,6 +175,30 @@ int kv_commit(int32_t S, int32_t n_causal, int32_t n_mask, const int32_t* accept
               int32_t* err_word, void* stream);
 
 /* ------------------------------------------------------------------------
+ * kv_commit_round
+ *
+ * The commit of the paper's two-forward round (appendix "Self-Speculative
+ * Decoding and KV-Cache Update", items Accept, Cache update, Next round),
+ * after a verify forward over [a0, d_1..d_B] (n_causal = B + 1, no mask
+ * rows).  Same as kv_commit with R = B + 1 except:
+ *   run      = a0, d_1..d_A, a_{A+1}   (a0 = lead[s]; A = accept_len[s] <= B,
+ *              a_j = argmax[s, j-1]; 2..B+2 tokens before truncation);
+ *   kv_len[s] += k - 1  (kv_len already counts x0, kept from the draft
+ *                        forward; a0 and the kept drafts add their slots);
+ *   pages cover the next round's windows: ceil((kv_len + B + 2) / 16);
+ *   draft is not changed (the next round drafts afresh).
+ *   lead [S] int32 (read); argmax [S, B + 1]; other arrays as in kv_commit.
+ * Requirements: 1 <= S <= 1024, B >= 1, draft_width >= B.
+ * ---------------------------------------------------------------------- */
+int kv_commit_round(int32_t S, int32_t B, const int32_t* lead, const int32_t* accept_len,
+                    const int32_t* argmax, int32_t* kv_len, int32_t* page_table, int32_t* num_pages,
+                    int32_t max_pages, int32_t* free_stack, int32_t* free_top,
+                    int32_t num_pool_pages, int32_t* boundary, int32_t* draft,
+                    int32_t draft_width, int32_t* out_tokens, int32_t* out_count,
+                    int32_t max_new, int32_t eos_id, int32_t* finished, int32_t* err_word,
+                    void* stream);
+
+/* ------------------------------------------------------------------------
  * draft_verify_step
  *
  * One fused self-speculative step of a decoder (method "Self-Speculative
@@ -247,6 +271,32 @@ size_t dvs_step_workspace_bytes(const dvs_model* m, int32_t S, int32_t n_causal,
 int draft_verify_step(const dvs_model* m, const dvs_state* st, int32_t n_causal, int32_t n_mask,
                       int32_t chunk_keys, float* logits_out, int32_t* argmax_out,
                       int32_t* accept_out, void* workspace, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * literal_round
+ *
+ * One round of the paper's two-forward self-speculative decoding (appendix
+ * "Self-Speculative Decoding and KV-Cache Update"), with the layers of
+ * draft_verify_step:
+ *   1. draft forward over [x0, [M] x B] at positions L .. L+B (1 causal row,
+ *      B mask rows): a0 = top-1 of the boundary row, d_j = top-1 of mask row
+ *      j, written to state->draft[s, 0..B-1]; x0's causal KV is kept
+ *      (kv_len + 1);
+ *   2. verify forward over [a0, d_1..d_B] at positions L+1 .. L+B+1 (B + 1
+ *      causal rows; its K/V overwrites the draft's mask-row slots):
+ *      a_j = top-1 of row j-1, j = 1..B+1;
+ *   3. A = longest prefix with d_j == a_j; kv_commit_round commits a0,
+ *      d_1..d_A, a_{A+1} (2..B+2 tokens) and keeps pages for [L', L'+B+2).
+ * Pages must cover [L, L + B + 2) on entry (kv_commit_round leaves them so;
+ * after dvs_prefill the caller's page reservation must).  logits_out [S*(B+1), vocab]
+ * receives the verify forward's logits, argmax_out [S*(B+1)] its top-1 and
+ * accept_out [S] the accepted lengths (each optional).  workspace: at least
+ * dvs_step_workspace_bytes(m, S, B + 1, 0, max_pages, chunk_keys) bytes.
+ * With chunk_keys > 0 every committed token equals greedy AR's bit for bit.
+ * ---------------------------------------------------------------------- */
+int literal_round(const dvs_model* m, const dvs_state* st, int32_t B, int32_t chunk_keys,
+                  float* logits_out, int32_t* argmax_out, int32_t* accept_out, void* workspace,
+                  size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
  * dvs_prefill

@@ -7,7 +7,12 @@
 // or the output budget truncates it; the KV of x0 and the kept drafts stays
 // (kv_len += k), every other window slot is dropped.
 //
-// Pages: each sequence ends holding ceil((kv_len + R) / 16) pages.  Two
+// The paper's two-forward round commits through the same kernel with a lead
+// token: the run is a0, d_1..d_A, a_{A+1}, kv_len already counts the kept x0
+// (so kv_len += k - 1), and the pages cover the next round's windows.
+//
+// Pages: each sequence ends holding ceil((kv_len + W) / 16) pages, W the
+// window of the next call (R, or B + 2 in the two-forward round).  Two
 // exclusive scans over the sequences give every surplus page its slot on the
 // free stack (pushes, sequences in order, highest logical page first) and
 // every missing page its slot below the new top (pops, sequences in order,
@@ -39,7 +44,8 @@ __device__ __forceinline__ int block_exclusive_scan(int v, int* sh, int& total) 
 }
 
 struct CommitParams {
-  int S, n_causal, n_mask, R, max_pages, pool_pages, draft_width, max_new, eos_id;
+  int S, n_causal, n_mask, R, window, max_pages, pool_pages, draft_width, max_new, eos_id;
+  const int32_t* lead;   // two-forward round: a0 per sequence, committed first (else NULL)
   const int32_t* accept_len;
   const int32_t* argmax;
   int32_t* kv_len;
@@ -55,8 +61,12 @@ struct CommitParams {
   int32_t* err;
 };
 
-// j-th token of the committed run: d_{j+1} for j < A, then a_{A+1}.
+// j-th token of the committed run: [a0,] d_1..d_A, a_{A+1}.
 __device__ __forceinline__ int run_token(const CommitParams& p, int s, int A, int j) {
+  if (p.lead) {
+    if (j == 0) return p.lead[s];
+    --j;
+  }
   return j < A ? p.draft[(size_t)s * p.draft_width + j] : p.argmax[(size_t)s * p.R + A];
 }
 
@@ -79,17 +89,19 @@ __global__ void __launch_bounds__(COMMIT_THREADS) kv_commit_kernel(CommitParams 
     if (!fin) {
       A = p.accept_len[s];
       A = A < 0 ? 0 : (A > p.n_causal - 1 ? p.n_causal - 1 : A);
-      // run = d_1..d_A, a_{A+1}; keep up to the first stop token / budget.
-      // Tokens are fetched RUN_CHUNK at a time (independent loads, one memory
-      // round trip per chunk), then scanned in order.
+      // run = [a0,] d_1..d_A, a_{A+1} (last index jl); keep up to the first
+      // stop token / budget.  Tokens are fetched RUN_CHUNK at a time
+      // (independent loads, one memory round trip per chunk), then scanned in
+      // order.
+      const int jl = A + (p.lead ? 1 : 0);
       bool done = false;
-      for (int j0 = 0; j0 <= A && !done; j0 += RUN_CHUNK) {
+      for (int j0 = 0; j0 <= jl && !done; j0 += RUN_CHUNK) {
         int tk[RUN_CHUNK];
 #pragma unroll
-        for (int u = 0; u < RUN_CHUNK; ++u) tk[u] = run_token(p, s, A, min(j0 + u, A));
+        for (int u = 0; u < RUN_CHUNK; ++u) tk[u] = run_token(p, s, A, min(j0 + u, jl));
 #pragma unroll
         for (int u = 0; u < RUN_CHUNK; ++u) {
-          if (done || j0 + u > A) continue;
+          if (done || j0 + u > jl) continue;
           if (cnt + k >= p.max_new) {
             stop = done = true;
           } else {
@@ -101,7 +113,8 @@ __global__ void __launch_bounds__(COMMIT_THREADS) kv_commit_kernel(CommitParams 
       }
       if (cnt + k >= p.max_new) stop = true;
     }
-    need = (L + k + p.R + DVS_PAGE_SIZE - 1) / DVS_PAGE_SIZE;
+    // new length: + k, or + k - 1 when kv_len already counts the kept x0
+    need = (L + k - (p.lead && !fin ? 1 : 0) + p.window + DVS_PAGE_SIZE - 1) / DVS_PAGE_SIZE;
     if (need > p.max_pages || n < 0 || n > p.max_pages || L < 0)
       atomicOr(&s_err, DVS_ERR_MAX_PAGES);
   }
@@ -149,7 +162,7 @@ __global__ void __launch_bounds__(COMMIT_THREADS) kv_commit_kernel(CommitParams 
           if (j0 + u < k) ot[cnt + j0 + u] = tk[u];
       }
       p.out_count[s] = cnt + k;
-      p.kv_len[s] = L + k;
+      p.kv_len[s] = L + k - (p.lead ? 1 : 0);
       if (k > 0) p.boundary[s] = last_tok;
       if (p.n_mask > 0) {
         for (int j0 = 0; j0 < p.draft_width; j0 += RUN_CHUNK) {
@@ -171,6 +184,39 @@ __global__ void __launch_bounds__(COMMIT_THREADS) kv_commit_kernel(CommitParams 
 
 using namespace dvs;
 
+static int launch_commit(const char* who, int32_t S, int32_t n_causal, int32_t n_mask,
+                         int32_t window, const int32_t* lead, const int32_t* accept_len,
+                         const int32_t* argmax, int32_t* kv_len, int32_t* page_table,
+                         int32_t* num_pages, int32_t max_pages, int32_t* free_stack,
+                         int32_t* free_top, int32_t num_pool_pages, int32_t* boundary,
+                         int32_t* draft, int32_t draft_width, int32_t* out_tokens,
+                         int32_t* out_count, int32_t max_new, int32_t eos_id, int32_t* finished,
+                         int32_t* err_word, void* stream) {
+  DVS_CHECK_ARG(accept_len && argmax && kv_len && page_table && num_pages && free_stack &&
+                    free_top && boundary && out_tokens && out_count && finished,
+                "%s: NULL array argument", who);
+  DVS_CHECK_ARG(S >= 1 && S <= COMMIT_THREADS, "%s: need 1 <= S <= %d", who, COMMIT_THREADS);
+  DVS_CHECK_ARG(n_causal >= 1 && n_mask >= 0, "%s: need n_causal >= 1, n_mask >= 0", who);
+  DVS_CHECK_ARG(draft_width >= 0 && (draft || draft_width == 0), "%s: bad draft", who);
+  DVS_CHECK_ARG(draft_width >= n_causal - 1, "%s: draft_width < n_causal - 1", who);
+  DVS_CHECK_ARG(n_mask == 0 || n_mask >= draft_width,
+                "%s: mask rows (%d) must cover the draft width (%d)", who, n_mask, draft_width);
+  DVS_CHECK_ARG(max_pages >= 1 && num_pool_pages >= 1 && max_new >= 1,
+                "%s: need max_pages, num_pool_pages, max_new >= 1", who);
+  DVS_CHECK_ARG(window >= n_causal + n_mask, "%s: window (%d) < n_causal + n_mask", who, window);
+  CommitParams p{};
+  p.S = S; p.n_causal = n_causal; p.n_mask = n_mask; p.R = n_causal + n_mask; p.window = window;
+  p.lead = lead;
+  p.max_pages = max_pages; p.pool_pages = num_pool_pages; p.draft_width = draft_width;
+  p.max_new = max_new; p.eos_id = eos_id;
+  p.accept_len = accept_len; p.argmax = argmax; p.kv_len = kv_len; p.page_table = page_table;
+  p.num_pages = num_pages; p.free_stack = free_stack; p.free_top = free_top;
+  p.boundary = boundary; p.draft = draft; p.out_tokens = out_tokens; p.out_count = out_count;
+  p.finished = finished; p.err = err_word;
+  hipLaunchKernelGGL(kv_commit_kernel, dim3(1), dim3(COMMIT_THREADS), 0, (hipStream_t)stream, p);
+  return launch_status(who);
+}
+
 extern "C" int kv_commit(int32_t S, int32_t n_causal, int32_t n_mask, const int32_t* accept_len,
                          const int32_t* argmax, int32_t* kv_len, int32_t* page_table,
                          int32_t* num_pages, int32_t max_pages, int32_t* free_stack,
@@ -179,25 +225,24 @@ extern "C" int kv_commit(int32_t S, int32_t n_causal, int32_t n_mask, const int3
                          int32_t* out_count, int32_t max_new, int32_t eos_id, int32_t* finished,
                          int32_t* err_word, void* stream) {
   clear_error();
-  DVS_CHECK_ARG(accept_len && argmax && kv_len && page_table && num_pages && free_stack &&
-                    free_top && boundary && out_tokens && out_count && finished,
-                "kv_commit: NULL array argument");
-  DVS_CHECK_ARG(S >= 1 && S <= COMMIT_THREADS, "kv_commit: need 1 <= S <= %d", COMMIT_THREADS);
-  DVS_CHECK_ARG(n_causal >= 1 && n_mask >= 0, "kv_commit: need n_causal >= 1, n_mask >= 0");
-  DVS_CHECK_ARG(draft_width >= 0 && (draft || draft_width == 0), "kv_commit: bad draft");
-  DVS_CHECK_ARG(draft_width >= n_causal - 1, "kv_commit: draft_width < n_causal - 1");
-  DVS_CHECK_ARG(n_mask == 0 || n_mask >= draft_width,
-                "kv_commit: mask rows (%d) must cover the draft width (%d)", n_mask, draft_width);
-  DVS_CHECK_ARG(max_pages >= 1 && num_pool_pages >= 1 && max_new >= 1,
-                "kv_commit: need max_pages, num_pool_pages, max_new >= 1");
-  CommitParams p{};
-  p.S = S; p.n_causal = n_causal; p.n_mask = n_mask; p.R = n_causal + n_mask;
-  p.max_pages = max_pages; p.pool_pages = num_pool_pages; p.draft_width = draft_width;
-  p.max_new = max_new; p.eos_id = eos_id;
-  p.accept_len = accept_len; p.argmax = argmax; p.kv_len = kv_len; p.page_table = page_table;
-  p.num_pages = num_pages; p.free_stack = free_stack; p.free_top = free_top;
-  p.boundary = boundary; p.draft = draft; p.out_tokens = out_tokens; p.out_count = out_count;
-  p.finished = finished; p.err = err_word;
-  hipLaunchKernelGGL(kv_commit_kernel, dim3(1), dim3(COMMIT_THREADS), 0, (hipStream_t)stream, p);
-  return launch_status("kv_commit");
+  return launch_commit("kv_commit", S, n_causal, n_mask, n_causal + n_mask, nullptr, accept_len,
+                       argmax, kv_len, page_table, num_pages, max_pages, free_stack, free_top,
+                       num_pool_pages, boundary, draft, draft_width, out_tokens, out_count, max_new,
+                       eos_id, finished, err_word, stream);
+}
+
+extern "C" int kv_commit_round(int32_t S, int32_t B, const int32_t* lead, const int32_t* accept_len,
+                               const int32_t* argmax, int32_t* kv_len, int32_t* page_table,
+                               int32_t* num_pages, int32_t max_pages, int32_t* free_stack,
+                               int32_t* free_top, int32_t num_pool_pages, int32_t* boundary,
+                               int32_t* draft, int32_t draft_width, int32_t* out_tokens,
+                               int32_t* out_count, int32_t max_new, int32_t eos_id,
+                               int32_t* finished, int32_t* err_word, void* stream) {
+  clear_error();
+  DVS_CHECK_ARG(lead != nullptr, "kv_commit_round: NULL lead");
+  DVS_CHECK_ARG(B >= 1, "kv_commit_round: need B >= 1");
+  return launch_commit("kv_commit_round", S, B + 1, 0, B + 2, lead, accept_len, argmax, kv_len,
+                       page_table, num_pages, max_pages, free_stack, free_top, num_pool_pages,
+                       boundary, draft, draft_width, out_tokens, out_count, max_new, eos_id,
+                       finished, err_word, stream);
 }

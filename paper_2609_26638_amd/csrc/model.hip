@@ -47,6 +47,24 @@ __global__ void embed_rows_kernel(const T* __restrict__ embed, int H, int vocab,
   for (int i = threadIdx.x; i < H; i += blockDim.x) x[(size_t)mrow * H + i] = to_f(e[i]);
 }
 
+// Two-forward round, between the forwards (appendix "Self-Speculative
+// Decoding and KV-Cache Update", item Draft forward): a0 = top-1 of the
+// boundary row, d_j = top-1 of mask row j (j = 1..B), and the causal KV the
+// draft forward wrote for x0 is kept (kv_len + 1).  Finished sequences keep
+// their state.  am: [S, B + 1].
+__global__ void round_draft_kernel(int S, int B, const int32_t* __restrict__ am,
+                                   const int32_t* __restrict__ finished, int32_t* __restrict__ kv_len,
+                                   int32_t* __restrict__ lead, int32_t* __restrict__ draft,
+                                   int draft_width) {
+  const int s = blockIdx.x * blockDim.x + threadIdx.x;
+  if (s >= S) return;
+  const int R = B + 1;
+  lead[s] = am[(size_t)s * R];
+  if (finished[s]) return;
+  for (int j = 0; j < B; ++j) draft[(size_t)s * draft_width + j] = am[(size_t)s * R + 1 + j];
+  kv_len[s] += 1;
+}
+
 // out[m, :] = x[m, :] / sqrt(mean(x^2) + eps) * g   (one workgroup per row)
 template <typename T>
 __global__ void __launch_bounds__(256) rmsnorm_kernel(const float* __restrict__ x, const T* __restrict__ g,
@@ -533,7 +551,7 @@ __global__ void __launch_bounds__(256) gemm_f32_kernel(const float* __restrict__
 // host orchestration
 // ---------------------------------------------------------------------------
 struct StepLayout {
-  size_t x, h, hsel, q, k, v, att, gate, up, act, logits, am, acc, attn_ws, total, attn_bytes,
+  size_t x, h, hsel, q, k, v, att, gate, up, act, logits, am, acc, lead, attn_ws, total, attn_bytes,
       attn_counters, gemm_part, gemm_part_bytes, gemm_counters, n_gemm_counters;
 };
 
@@ -600,6 +618,7 @@ static StepLayout step_layout(const dvs_model* m, int S, int n_causal, int n_mas
   L.logits = off; off += al(logit_rows * (size_t)m->vocab * 4);
   L.am = off; off += al(logit_rows * 4);
   L.acc = off; off += al((size_t)S * 4);
+  L.lead = off; off += al((size_t)S * 4);
   L.attn_bytes = dvs_attn_workspace_bytes(S, n_causal, n_mask, m->n_heads, m->n_kv_heads,
                                           m->head_dim, max_pages, chunk_keys, m->dtype);
   L.attn_counters = attn_counter_bytes(S, n_causal + n_mask, m->n_heads, m->n_kv_heads,
@@ -758,6 +777,50 @@ static int run_step(const dvs_model* m, const dvs_state* st, int n_causal, int n
                    st->finished, st->err_word, stream);
 }
 
+// The paper's two-forward round: draft forward over [x0, [M] x B], then a
+// causal verify forward over [a0, d_1..d_B] from position L + 1 (its K/V
+// overwrites the draft's mask-row slots), then acceptance against d_1..d_B
+// and the commit of a0, d_1..d_A, a_{A+1}.  Both forwards carry B + 1 rows.
+template <typename T>
+static int run_round(const dvs_model* m, const dvs_state* st, int B, int chunk_keys,
+                     const StepLayout& L, char* ws, float* logits_out, int32_t* argmax_out,
+                     int32_t* accept_out, hipStream_t stream) {
+  const int S = st->S, R = B + 1, M = S * R;
+  float* logits = logits_out ? logits_out : (float*)(ws + L.logits);
+  int32_t* am = argmax_out ? argmax_out : (int32_t*)(ws + L.am);
+  int32_t* acc = accept_out ? accept_out : (int32_t*)(ws + L.acc);
+  int32_t* lead = (int32_t*)(ws + L.lead);
+  int rc;
+  // draft forward
+  hipLaunchKernelGGL(embed_rows_kernel<T>, dim3(M), dim3(256), 0, stream, (const T*)m->embed,
+                     m->hidden, m->vocab, R, 1, st->boundary, st->draft, st->draft_width,
+                     (float*)(ws + L.x));
+  if ((rc = launch_status("literal_round(embed)"))) return rc;
+  if ((rc = forward_layers<T>(m, st, 1, B, chunk_keys, L, ws, stream))) return rc;
+  if ((rc = gemm(L, ws, m->dtype, ws + L.h, m->lm_head, M, m->vocab, m->hidden, logits, 1, 0, stream)))
+    return rc;
+  rc = argmax_accept(logits, DVS_F32, S, R, m->vocab, 1, st->draft, st->draft_width, am, acc,
+                     st->err_word, stream);
+  if (rc) return rc;
+  hipLaunchKernelGGL(round_draft_kernel, dim3((S + 255) / 256), dim3(256), 0, stream, S, B, am,
+                     st->finished, st->kv_len, lead, st->draft, st->draft_width);
+  if ((rc = launch_status("literal_round(draft)"))) return rc;
+  // verify forward
+  hipLaunchKernelGGL(embed_rows_kernel<T>, dim3(M), dim3(256), 0, stream, (const T*)m->embed,
+                     m->hidden, m->vocab, R, R, lead, st->draft, st->draft_width, (float*)(ws + L.x));
+  if ((rc = launch_status("literal_round(embed)"))) return rc;
+  if ((rc = forward_layers<T>(m, st, R, 0, chunk_keys, L, ws, stream))) return rc;
+  if ((rc = gemm(L, ws, m->dtype, ws + L.h, m->lm_head, M, m->vocab, m->hidden, logits, 1, 0, stream)))
+    return rc;
+  rc = argmax_accept(logits, DVS_F32, S, R, m->vocab, R, st->draft, st->draft_width, am, acc,
+                     st->err_word, stream);
+  if (rc) return rc;
+  return kv_commit_round(S, B, lead, acc, am, st->kv_len, st->page_table, st->num_pages,
+                         st->max_pages, st->free_stack, st->free_top, st->num_pool_pages,
+                         st->boundary, st->draft, st->draft_width, st->out_tokens, st->out_count,
+                         st->max_new, st->eos_id, st->finished, st->err_word, stream);
+}
+
 template <typename T>
 static int run_prefill(const dvs_model* m, const dvs_state* st, int P, int n_mask,
                        const int32_t* tokens, const float* x_prefix, int chunk_keys,
@@ -830,6 +893,40 @@ extern "C" int draft_verify_step(const dvs_model* m, const dvs_state* st, int32_
                             argmax_out, accept_out, s);
   return run_step<float>(m, st, n_causal, n_mask, chunk_keys, L, (char*)workspace, logits_out,
                          argmax_out, accept_out, s);
+}
+
+extern "C" int literal_round(const dvs_model* m, const dvs_state* st, int32_t B,
+                             int32_t chunk_keys, float* logits_out, int32_t* argmax_out,
+                             int32_t* accept_out, void* workspace, size_t ws_bytes, void* stream) {
+  clear_error();
+  DVS_CHECK_ARG(model_ok(m), "literal_round: invalid model description");
+  DVS_CHECK_ARG(st && st->S >= 1 && st->kv_len && st->page_table && st->num_pages &&
+                    st->free_stack && st->free_top && st->boundary && st->out_tokens &&
+                    st->out_count && st->finished,
+                "literal_round: invalid state description");
+  DVS_CHECK_ARG(B >= 1, "literal_round: need B >= 1");
+  DVS_CHECK_ARG(st->draft && st->draft_width >= B, "literal_round: draft narrower than B");
+  for (int l = 0; l < m->n_layers; ++l) {
+    const dvs_layer& ly = m->layers[l];
+    DVS_CHECK_ARG(ly.wq && ly.wk && ly.wv && ly.wo && ly.g_attn && ly.k_pool && ly.v_pool,
+                  "literal_round: layer %d incomplete", l);
+    DVS_CHECK_ARG(m->ffn == 0 || (ly.g_mlp && ly.w_gate && ly.w_up && ly.w_down),
+                  "literal_round: layer %d MLP incomplete", l);
+  }
+  DVS_CHECK_SUPPORTED(m->head_dim == 64 || m->head_dim == 96 || m->head_dim == 128,
+                      "literal_round: head_dim %d", m->head_dim);
+  const StepLayout L = step_layout(m, st->S, B + 1, 0, st->max_pages, chunk_keys,
+                                   (size_t)st->S * (B + 1));
+  if (!workspace || ws_bytes < L.total) {
+    set_error("literal_round: workspace needs %zu bytes, got %zu", L.total, ws_bytes);
+    return DVS_EWORKSPACE;
+  }
+  hipStream_t s = (hipStream_t)stream;
+  if (m->dtype == DVS_BF16)
+    return run_round<__bf16>(m, st, B, chunk_keys, L, (char*)workspace, logits_out, argmax_out,
+                             accept_out, s);
+  return run_round<float>(m, st, B, chunk_keys, L, (char*)workspace, logits_out, argmax_out,
+                          accept_out, s);
 }
 
 extern "C" size_t dvs_prefill_workspace_bytes(const dvs_model* m, int32_t S, int32_t P,

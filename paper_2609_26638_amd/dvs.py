@@ -38,6 +38,9 @@ _SIGS = {
     "kv_commit": ([_c_int, _c_int, _c_int, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_int, _c_ptr,
                    _c_ptr, _c_int, _c_ptr, _c_ptr, _c_int, _c_ptr, _c_ptr, _c_int, _c_int, _c_ptr,
                    _c_ptr, _c_ptr], _c_int),
+    "kv_commit_round": ([_c_int, _c_int, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_int,
+                         _c_ptr, _c_ptr, _c_int, _c_ptr, _c_ptr, _c_int, _c_ptr, _c_ptr, _c_int,
+                         _c_int, _c_ptr, _c_ptr, _c_ptr], _c_int),
 }
 
 class DvsLayer(ctypes.Structure):
@@ -67,6 +70,9 @@ _SIGS["dvs_step_workspace_bytes"] = ([ctypes.POINTER(DvsModel), _c_int, _c_int, 
                                       _c_int], _c_size)
 _SIGS["draft_verify_step"] = ([ctypes.POINTER(DvsModel), ctypes.POINTER(DvsState), _c_int, _c_int,
                                _c_int, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_size, _c_ptr], _c_int)
+
+_SIGS["literal_round"] = ([ctypes.POINTER(DvsModel), ctypes.POINTER(DvsState), _c_int, _c_int,
+                           _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_size, _c_ptr], _c_int)
 
 _SIGS["dvs_prefill_workspace_bytes"] = ([ctypes.POINTER(DvsModel), _c_int, _c_int, _c_int, _c_int,
                                          _c_int], _c_size)
@@ -297,6 +303,28 @@ def kv_commit(st: DeviceState, accept_len, argmax, n_causal: int, n_mask: int,
     _check(rc, "kv_commit")
 
 
+def kv_commit_round(st: DeviceState, B: int, lead, accept_len, argmax, eos_id: int = -1,
+                    max_new: int | None = None, stream=None):
+    """Commit of the two-forward round: a0 (lead), d_1..d_A, a_{A+1}."""
+    S = st.kv_len.shape[0]
+    _dev(lead, torch.int32, "lead", 1)
+    _dev(accept_len, torch.int32, "accept_len", 1)
+    _dev(argmax, torch.int32, "argmax", 2)
+    if argmax.shape != (S, B + 1):
+        raise DvsError("argmax must be [S, B + 1]")
+    cap = st.out_tokens.shape[1]
+    max_new = cap if max_new is None else min(int(max_new), cap)
+    if max_new != cap:
+        raise DvsError("max_new must equal the out_tokens row length")
+    rc = lib().kv_commit_round(S, B, _ptr(lead), _ptr(accept_len), _ptr(argmax), _ptr(st.kv_len),
+                               _ptr(st.page_table), _ptr(st.num_pages), st.max_pages,
+                               _ptr(st.free_stack), _ptr(st.free_top), st.pool_pages,
+                               _ptr(st.boundary), _ptr(st.draft), st.draft.shape[1],
+                               _ptr(st.out_tokens), _ptr(st.out_count), max_new, int(eos_id),
+                               _ptr(st.finished), _ptr(st.err), _stream(stream))
+    _check(rc, "kv_commit_round")
+
+
 # ---------------------------------------------------------------------------
 # whole-step decoder
 # ---------------------------------------------------------------------------
@@ -381,6 +409,26 @@ def draft_verify_step(model: DeviceModel, st: DeviceState, n_causal: int, n_mask
                                  _ptr(accept_out), _ptr(model.ws.buf), model.ws.nbytes,
                                  _stream(stream))
     _check(rc, "draft_verify_step")
+
+
+def literal_round(model: DeviceModel, st: DeviceState, B: int, chunk_keys: int = 0,
+                  eos_id: int = -1, logits_out=None, argmax_out=None, accept_out=None, stream=None):
+    """One round of the paper's two-forward decoding (draft forward, verify
+    forward, commit of a0, d_1..d_A, a_{A+1}) on the device."""
+    S = st.kv_len.shape[0]
+    need = model.workspace_bytes(S, B + 1, 0, st.max_pages, chunk_keys)
+    if need == 0:
+        raise DvsError("literal_round: invalid configuration")
+    if model.ws is None or model.ws.nbytes < need:
+        model.ws = Workspace(need, device=st.kv_len.device)
+    for t, name in ((logits_out, "logits_out"), (argmax_out, "argmax_out"), (accept_out, "accept_out")):
+        if t is not None:
+            _dev(t, torch.float32 if name == "logits_out" else torch.int32, name)
+    sd = _state_desc(st, eos_id)
+    rc = lib().literal_round(ctypes.byref(model.desc), ctypes.byref(sd), int(B), int(chunk_keys),
+                             _ptr(logits_out), _ptr(argmax_out), _ptr(accept_out),
+                             _ptr(model.ws.buf), model.ws.nbytes, _stream(stream))
+    _check(rc, "literal_round")
 
 
 def prefill(model: DeviceModel, st: DeviceState, P: int, n_mask: int, prefix_tokens=None,

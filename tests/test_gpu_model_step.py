@@ -1,5 +1,6 @@
 """GPU: draft_verify_step (decoder layers + hot path) against the oracle, and
-GPU self-speculative decoding == GPU greedy AR decoding, token for token."""
+GPU self-speculative decoding == GPU greedy AR decoding, token for token;
+the same for the paper's two-forward round (literal_round)."""
 import numpy as np
 import pytest
 import torch
@@ -60,6 +61,95 @@ def test_tiny_fp32_single_layer_step_matches_oracle():
     # the appended window K/V (first layer's pools) agree with the oracle
     kp = dm.k_pools[0].cpu().numpy()
     np.testing.assert_allclose(kp, om.k_pools[0], rtol=1e-4, atol=1e-6)
+
+
+def _widen_draft(host, width):
+    """The two-forward round keeps d_1..d_B in the draft array: width >= B."""
+    h = host.copy()
+    d = np.zeros((h.draft.shape[0], width), np.int32)
+    d[:, :h.draft.shape[1]] = h.draft
+    h.draft = d
+    return h
+
+
+def test_tiny_fp32_literal_round_matches_oracle():
+    w, ai = synth.tiny_step_inputs(0)
+    B, V = ai.n_causal, w.V
+    host = _widen_draft(ai.state, B)
+    om = OracleModel(w, [ai.k_pool], [ai.v_pool])
+    st_ref = host.copy()
+    lg_d, lg_v, am_v, A_ref, err = om.literal_round(st_ref, B)
+    assert err == 0
+    dm = dvs.DeviceModel(w, [ai.k_pool], [ai.v_pool], "f32")
+    st = dvs.DeviceState(host)
+    logits = torch.empty((B + 1, V), dtype=torch.float32, device="cuda")
+    am = torch.empty((1, B + 1), dtype=torch.int32, device="cuda")
+    acc = torch.empty((1,), dtype=torch.int32, device="cuda")
+    dvs.literal_round(dm, st, B, logits_out=logits, argmax_out=am, accept_out=acc)
+    torch.cuda.synchronize()
+    assert int(st.err.item()) == 0
+    got = st.to_host(host)
+    # draft forward: the GPU's a0 and d_1..d_B are the oracle's (every top-2
+    # margin of these rows is far above the fp32 logit error for this seed)
+    srt = np.sort(lg_d, axis=-1)
+    assert np.all(srt[..., -1] - srt[..., -2] > 4 * LOGIT_TOL_F32 * np.abs(lg_d).max(axis=-1))
+    np.testing.assert_array_equal(got.draft[:, :B], st_ref.draft[:, :B])
+    a0 = got.out_tokens[:, host.out_count[0]]
+    np.testing.assert_array_equal(a0, st_ref.out_tokens[:, host.out_count[0]])
+    # verify forward on the same window: logits within the fp32 tolerance
+    lg = logits.cpu().numpy().reshape(1, B + 1, V)
+    assert max_rel_err(lg.astype(np.float64), lg_v) <= LOGIT_TOL_F32
+    # replay: acceptance and the round's commit on the GPU's own top-1 are
+    # bit-exact, and so is the resulting state
+    am_gpu = am.cpu().numpy()
+    np.testing.assert_array_equal(am_gpu, od.top1_rows(lg.astype(np.float64)))
+    replay = host.copy()
+    replay.draft[:, :B] = got.draft[:, :B]
+    replay.kv_len += 1
+    A_gpu = od.accept(am_gpu, replay.draft, B + 1)
+    np.testing.assert_array_equal(acc.cpu().numpy(), A_gpu)
+    assert od.kv_commit(replay, A_gpu, am_gpu, B + 1, 0, lead=a0, window=B + 2) == 0
+    _states_equal(st, replay)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_literal_round_equals_greedy_ar_on_gpu(dtype):
+    """The paper's two-forward round commits a0, d_1..d_A, a_{A+1} per round;
+    its committed stream equals greedy AR bit for bit on the GPU."""
+    B, N, CH = 8, 40, 64
+    w, base, kps, vps = _small_model(4, dtype)
+    S = base.S
+    host = _widen_draft(base.state, B)
+    host.out_tokens = np.full((S, 256), -1, np.int32)
+    rng = np.random.default_rng(2)
+    host.boundary[:] = rng.integers(0, w.V, size=S)
+    ar_m = dvs.DeviceModel(w, _dev_pools(kps, dtype), _dev_pools(vps, dtype), dtype)
+    ar_st = dvs.DeviceState(host)
+    for _ in range(N):
+        dvs.draft_verify_step(ar_m, ar_st, 1, 0, chunk_keys=CH)
+    torch.cuda.synchronize()
+    assert int(ar_st.err.item()) == 0
+    ar = ar_st.to_host(host)
+    lr_m = dvs.DeviceModel(w, _dev_pools(kps, dtype), _dev_pools(vps, dtype), dtype)
+    lr_st = dvs.DeviceState(host)
+    acc = torch.empty((S,), dtype=torch.int32, device="cuda")
+    rounds = 0
+    while int(lr_st.out_count.min().item()) < N:
+        before = lr_st.out_count.clone()
+        dvs.literal_round(lr_m, lr_st, B, chunk_keys=CH, accept_out=acc)
+        rounds += 1
+        # each round commits a0, the accepted drafts and a_{A+1}: A + 2 tokens
+        assert torch.equal(lr_st.out_count - before, acc + 2)
+        assert rounds <= N
+    torch.cuda.synchronize()
+    assert int(lr_st.err.item()) == 0
+    lr = lr_st.to_host(host)
+    for s in range(S):
+        n = min(int(lr.out_count[s]), int(ar.out_count[s]))
+        assert n >= N
+        np.testing.assert_array_equal(lr.out_tokens[s, :n], ar.out_tokens[s, :n])
+        # every committed token but the boundary holds KV
+        assert lr.kv_len[s] - lr.out_count[s] == host.kv_len[s] - host.out_count[s]
 
 
 def _small_model(seed, dtype, n_layers=2, ffn=512, L=(37, 300, 129), std=0.08):
@@ -234,15 +324,17 @@ def test_prefill_matches_oracle_small():
 
 
 def _run_stack(si, dtype, mode, chunk):
-    """prefill then AR (mode 'ar') or fused steps until max_new tokens; returns
-    the host state, the number of steps and the device seconds of the loop."""
+    """prefill then AR (mode 'ar'), fused steps ('fused') or two-forward rounds
+    ('literal') until max_new tokens; returns the host state, the number of
+    steps and the device seconds of the loop."""
     w = si.weights
     pool = si.state.pool_pages
     L = w.n_layers
     kps = [torch.zeros((pool, w.Hkv, 16, w.D), dtype=torch.bfloat16, device="cuda") for _ in range(L)]
     vps = [torch.zeros((pool, w.Hkv, w.D, 16), dtype=torch.bfloat16, device="cuda") for _ in range(L)]
     dm = dvs.DeviceModel(w, kps, vps, dtype)
-    st = dvs.DeviceState(si.state)
+    host = _widen_draft(si.state, si.B) if mode == "literal" else si.state
+    st = dvs.DeviceState(host)
     dvs.prefill(dm, st, si.P, si.B, prefix_tokens=torch.from_numpy(si.prefix_tokens()).cuda(),
                 x_prefix=torch.from_numpy(si.x_prefix()).cuda(), chunk_keys=chunk)
     torch.cuda.synchronize()
@@ -253,6 +345,8 @@ def _run_stack(si, dtype, mode, chunk):
         for _ in range(16):
             if mode == "ar":
                 dvs.draft_verify_step(dm, st, 1, 0, chunk_keys=chunk)
+            elif mode == "literal":
+                dvs.literal_round(dm, st, si.B, chunk_keys=chunk)
             else:
                 dvs.draft_verify_step(dm, st, si.B, si.B, chunk_keys=chunk)
             steps += 1
@@ -261,7 +355,7 @@ def _run_stack(si, dtype, mode, chunk):
     e1.record()
     torch.cuda.synchronize()
     assert int(st.err.item()) == 0
-    return st.to_host(si.state), steps, e0.elapsed_time(e1) / 1e3
+    return st.to_host(host), steps, e0.elapsed_time(e1) / 1e3
 
 
 def test_decoder_stack_selfspec_equals_ar():
@@ -278,3 +372,7 @@ def test_decoder_stack_selfspec_equals_ar():
     np.testing.assert_array_equal(ar.out_count, [si.max_new] * 8)
     np.testing.assert_array_equal(ss.out_count, [si.max_new] * 8)
     np.testing.assert_array_equal(ss.out_tokens, ar.out_tokens)
+    lr, lr_rounds, lr_s = _run_stack(si, "bf16", "literal", 256)
+    print(f"[stack] two-forward rounds {lr_rounds} rounds {lr_s:.2f} s", flush=True)
+    np.testing.assert_array_equal(lr.out_count, [si.max_new] * 8)
+    np.testing.assert_array_equal(lr.out_tokens, ar.out_tokens)
