@@ -155,6 +155,39 @@ def test_commit_random_steps_match_oracle(seed):
         _assert_state_equal(dev, st)
 
 
+@pytest.mark.parametrize("seed", [0, 1])
+def test_commit_round_random_steps_match_oracle(seed):
+    """kv_commit_round (two-forward round: lead a0, then d_1..d_A, a_{A+1};
+    kv_len already counts x0; pages for the next B + 2 window) against the
+    oracle over random rounds, with EOS stops, budget truncation and
+    finished sequences."""
+    rng = np.random.default_rng(100 + seed)
+    S, B, V = 29, 5, 7
+    L = rng.integers(0, 300, size=S)
+    st = synth.make_paged_state(rng, L, B + 2, max_pages=64, scatter=True, slack=0.3,
+                                extra_pages=20, n_causal=B + 1, max_new=60)
+    dev = _dev_state(st)
+    for step in range(25):
+        am = rng.integers(0, V, size=(S, B + 1)).astype(np.int32)
+        lead = rng.integers(0, V, size=S).astype(np.int32)
+        live = st.finished == 0
+        # the draft forward's effect: d_1..d_B written, x0's KV kept
+        d = np.where(rng.random((S, B)) < 0.8, am[:, :B], rng.integers(0, V, size=(S, B)))
+        st.draft[live] = d[live]
+        st.kv_len[live] += 1
+        dev.draft.copy_(torch.from_numpy(st.draft))
+        dev.kv_len.copy_(torch.from_numpy(st.kv_len))
+        A = od.accept(am, st.draft, B + 1)
+        eos = 4 if step > 10 else -1
+        e = od.kv_commit(st, A, am, B + 1, 0, eos_id=eos, lead=lead, window=B + 2)
+        dvs.kv_commit_round(dev, B, torch.from_numpy(lead).cuda(), torch.from_numpy(A).cuda(),
+                            torch.from_numpy(am).cuda(), eos_id=eos)
+        torch.cuda.synchronize()
+        assert e == int(dev.err.item()) == 0
+        _assert_state_equal(dev, st)
+    assert st.finished.sum() > 0
+
+
 def test_commit_switching_window_size_pushes_pages():
     rng = np.random.default_rng(3)
     S = 9
