@@ -124,7 +124,8 @@ def run_decoder_stack(args):
     """The 16-layer bf16 decoder stack (hidden 1536, 16/4 heads, head_dim 96,
     SwiGLU 4096, vocab 65536; random weights): 8 sequences with 1024 vision
     embeddings + 64 prompt tokens are prefilled, then decoded with fused
-    self-speculative steps (B = 16) and, separately, with greedy AR steps.
+    self-speculative steps (B = 16) and, separately, with greedy AR steps and
+    with the paper's two-forward rounds (draft forward + verify forward).
     Reports end-to-end committed tokens/s of both (HIP events around the
     timed steps, prefill excluded) and, for the dominant cost, the HBM bytes a
     forward must move (all weights once, plus the KV cache read per layer)."""
@@ -146,19 +147,29 @@ def run_decoder_stack(args):
     mats = w.wq + w.wk + w.wv + w.wo + w.w_gate + w.w_up + w.w_down + [w.lm_head]
     weight_bytes = sum(int(np.prod(a.shape)) * 2 for a in mats)
     res = {}
-    for mode, (nc, nm) in (("fused", (si.B, si.B)), ("ar", (1, 0))):
-        st = dvs.DeviceState(si.state)
+    # the two-forward round keeps d_1..d_B in the draft array
+    wide = si.state.copy()
+    wide.draft = np.zeros((wide.draft.shape[0], si.B), np.int32)
+
+    def step(st, mode, nc, nm):
+        if mode == "literal":
+            dvs.literal_round(dm, st, si.B, chunk_keys=chunk)
+        else:
+            dvs.draft_verify_step(dm, st, nc, nm, chunk_keys=chunk)
+
+    for mode, (nc, nm) in (("fused", (si.B, si.B)), ("ar", (1, 0)), ("literal", (si.B + 1, 0))):
+        st = dvs.DeviceState(wide if mode == "literal" else si.state)
         dvs.prefill(dm, st, si.P, si.B, prefix_tokens=torch.from_numpy(si.prefix_tokens()).cuda(),
                     x_prefix=torch.from_numpy(si.x_prefix()).cuda(), chunk_keys=chunk)
         for _ in range(args.warmup):
-            dvs.draft_verify_step(dm, st, nc, nm, chunk_keys=chunk)
+            step(st, mode, nc, nm)
         torch.cuda.synchronize()
         c0 = int(st.out_count.sum().item())
         kv0 = int(st.kv_len.sum().item())
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record()
         for _ in range(args.steps):
-            dvs.draft_verify_step(dm, st, nc, nm, chunk_keys=chunk)
+            step(st, mode, nc, nm)
         e1.record()
         torch.cuda.synchronize()
         if int(st.err.item()):
@@ -167,7 +178,8 @@ def run_decoder_stack(args):
         ms = e0.elapsed_time(e1) / args.steps
         toks = int(st.out_count.sum().item()) - c0
         kv_mean = (kv0 + int(st.kv_len.sum().item())) / 2
-        step_bytes = weight_bytes + kv_mean * w.n_layers * w.Hkv * w.D * 2 * 2
+        fwd = 2 if mode == "literal" else 1          # forwards per step
+        step_bytes = fwd * (weight_bytes + kv_mean * w.n_layers * w.Hkv * w.D * 2 * 2)
         res[mode] = {"ms_per_step": round(ms, 4), "tokens_per_step": round(toks / args.steps, 3),
                      "tokens_per_s": round(toks / (ms * args.steps / 1e3), 1),
                      "hbm_bytes_per_step": int(step_bytes),
@@ -187,8 +199,10 @@ def run_decoder_stack(args):
                      "kernel": "whole fused step (weights once + KV per layer)",
                      "algorithmic_bytes": f["hbm_bytes_per_step"]},
         "ar": res["ar"],
+        "two_forward_round": res["literal"],
         "note": "random weights accept almost no drafts, so the fused step commits about one "
-                "token per sequence; its time is what a trained model's step would cost",
+                "token per sequence and the two-forward round about two; their times are what a "
+                "trained model's step would cost",
         "input_gen_s": round(t_gen, 1),
     }
     print(json.dumps(line), flush=True)
