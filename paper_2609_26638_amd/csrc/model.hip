@@ -233,7 +233,8 @@ __global__ void __launch_bounds__(256) gemm_bf16_kernel(const __bf16* __restrict
 // sum_k A[m, k] W[n, k].  The weights are streamed once; the row count is
 // small (8..256 window rows) or a long prefill.
 // ---------------------------------------------------------------------------
-constexpr int GK_MAXSPLIT = 32;
+constexpr int GK_MAXSPLIT = 4;     // logical K splits (bounds the partial traffic)
+constexpr int GK_SPLIT_ROWS = 256; // calls of at most this many rows run one split per workgroup
 
 // ---------------------------------------------------------------------------
 // gemm_rt_kernel<MT>: C[M, N] = A[M, K] W[N, K]^T (bf16 operands, fp32
@@ -244,11 +245,11 @@ constexpr int GK_MAXSPLIT = 32;
 //     p_0 + p_1 + ... + p_{KS-1}      (fp32, in this order)
 // where p_s is the MFMA accumulation of split s over its 16-wide k-steps in
 // order.  Two mappings compute exactly that, whatever the row count:
-//   * split per workgroup (calls of at most 32 rows): p_s is published with
-//     write-through stores and the last workgroup of the column block adds
-//     the splits in order;
-//   * all splits in one workgroup (longer calls): the running ordered sum
-//     stays in registers.
+//   * split per workgroup (calls of at most 256 rows, the decode steps): p_s
+//     of a (row tile, column block) is published with write-through stores
+//     and the last workgroup of that tile adds the splits in order;
+//   * all splits in one workgroup (longer calls, prefill): the running
+//     ordered sum stays in registers.
 // A fused step's causal rows are therefore bit-identical to AR steps.
 //
 // Waves: MT = 32 -> 1 x 4 (each wave 32 rows x 32 columns); MT >= 64 ->
@@ -283,11 +284,12 @@ __global__ void __launch_bounds__(256, 1) gemm_rt_kernel(
   const int nb = blockIdx.x % NBK;
   const int rest = blockIdx.x / NBK;
   const int n0 = nb * RT_NT;
-  // split-per-workgroup: blockIdx selects (column block, split), one row tile;
+  // split-per-workgroup: blockIdx selects (column block, split, row tile);
   // otherwise (column block, row tile) and every split
-  const int s_first = split_per_wg ? rest : 0;
-  const int s_end = split_per_wg ? rest + 1 : KS;
-  const int m0 = split_per_wg ? 0 : rest * MT;
+  const int rt = split_per_wg ? rest / KS : rest;
+  const int s_first = split_per_wg ? rest % KS : 0;
+  const int s_end = split_per_wg ? s_first + 1 : KS;
+  const int m0 = rt * MT;
   const int kc = K / KS;
   const int wr = WIDE ? (w >> 1) : 0, wc = WIDE ? (w & 1) : w;
   const int row_w = wr * (MT / (WIDE ? 2 : 1));   // first tile row of the wave
@@ -442,9 +444,11 @@ __global__ void __launch_bounds__(256, 1) gemm_rt_kernel(
     write_out(sum);
     return;
   }
-  if constexpr (MT == 32) {   // the host uses one split per workgroup only with 32-row tiles
-    // split per workgroup (MT == 32, m0 == 0): publish p_s, count in; the last
-    // workgroup of the column block adds the splits in order
+  if constexpr (MT <= 64) {   // the host uses one split per workgroup with 32- and 64-row tiles
+    // split per workgroup: publish p_s of this (row tile, column block), count
+    // in; the last workgroup of the tile adds the splits in order
+    const int n_rt = (M + MT - 1) / MT;
+    int32_t* cnt = counters + (size_t)nb * n_rt + rt;
 #pragma unroll
     for (int a = 0; a < RG; ++a)
 #pragma unroll
@@ -452,7 +456,7 @@ __global__ void __launch_bounds__(256, 1) gemm_rt_kernel(
         const int n = n0 + col_w + b * 32 + l32;
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
-          const int mrow = row_w + a * 32 + 8 * (i >> 2) + 4 * hh + (i & 3);
+          const int mrow = m0 + row_w + a * 32 + 8 * (i >> 2) + 4 * hh + (i & 3);
           if (mrow < M && n < N)
             __hip_atomic_store(part + ((size_t)s_first * M + mrow) * N + n, sum[a][b][i], __ATOMIC_RELAXED,
                                __HIP_MEMORY_SCOPE_AGENT);
@@ -461,40 +465,42 @@ __global__ void __launch_bounds__(256, 1) gemm_rt_kernel(
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     if (tid == 0)
-      s_last = __hip_atomic_fetch_add(&counters[nb], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == KS - 1;
+      s_last = __hip_atomic_fetch_add(cnt, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == KS - 1;
     __syncthreads();
     if (!s_last) return;
-    if (tid == 0) __hip_atomic_store(&counters[nb], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (tid == 0) __hip_atomic_store(cnt, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     f32x16 tot[RG][CG];
 #pragma unroll
     for (int a = 0; a < RG; ++a)
 #pragma unroll
       for (int b = 0; b < CG; ++b) tot[a][b] = f32x16{};
-    // (MT == 32 here: one 32 x 32 tile per wave) splits are loaded SPB at a
-    // time, every load of a batch issued before any is added, then added in
-    // split order
-    constexpr int SPB = 8;
-    const int n = n0 + col_w + l32;
-    for (int sp0 = 0; sp0 < KS; sp0 += SPB) {
-      float v[SPB][16];
+    // the splits' partials, GK_MAXSPLIT of them at most, are loaded together
+    // (every load issued before any is added), then added in split order
+    static_assert(GK_MAXSPLIT <= 4, "one batch of split partials");
 #pragma unroll
-      for (int q = 0; q < SPB; ++q) {
-        const int sp = min(sp0 + q, KS - 1);
+    for (int a = 0; a < RG; ++a)
 #pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const int mrow = row_w + 8 * (i >> 2) + 4 * hh + (i & 3);
-          const int mr = min(mrow, M - 1), nn = min(n, N - 1);
-          v[q][i] = __hip_atomic_load(part + ((size_t)sp * M + mr) * N + nn, __ATOMIC_RELAXED,
-                                      __HIP_MEMORY_SCOPE_AGENT);
+      for (int b = 0; b < CG; ++b) {
+        const int n = n0 + col_w + b * 32 + l32;
+        float v[GK_MAXSPLIT][16];
+#pragma unroll
+        for (int q = 0; q < GK_MAXSPLIT; ++q) {
+          const int sp = min(q, KS - 1);
+#pragma unroll
+          for (int i = 0; i < 16; ++i) {
+            const int mrow = m0 + row_w + a * 32 + 8 * (i >> 2) + 4 * hh + (i & 3);
+            const int mr = min(mrow, M - 1), nn = min(n, N - 1);
+            v[q][i] = __hip_atomic_load(part + ((size_t)sp * M + mr) * N + nn, __ATOMIC_RELAXED,
+                                        __HIP_MEMORY_SCOPE_AGENT);
+          }
         }
+#pragma unroll
+        for (int q = 0; q < GK_MAXSPLIT; ++q)
+          if (q < KS) {
+#pragma unroll
+            for (int i = 0; i < 16; ++i) tot[a][b][i] += v[q][i];
+          }
       }
-#pragma unroll
-      for (int q = 0; q < SPB; ++q)
-        if (sp0 + q < KS) {
-#pragma unroll
-          for (int i = 0; i < 16; ++i) tot[0][0][i] += v[q][i];
-        }
-    }
     write_out(tot);
   }
   }
@@ -555,10 +561,12 @@ struct StepLayout {
       attn_counters, gemm_part, gemm_part_bytes, gemm_counters, n_gemm_counters;
 };
 
-// Logical K splits of a bf16 GEMM: enough 128-column blocks x splits to
-// fill the chip when each split is a workgroup, a split being a multiple of
-// 64 of K.  A function of (N, K) only, so that row results do not depend on
-// the row count.
+// Logical K splits of a bf16 GEMM: up to GK_MAXSPLIT, enough for 128-column
+// blocks x splits to fill the chip when each split is a workgroup, a split
+// being a multiple of 64 of K.  A function of (N, K) only, so that row results
+// do not depend on the row count.  (Few splits: the partials of a 256-row
+// call cost KS x 256 x 4 bytes per weight column against 2 K bytes of
+// weights.)
 static int gemm_ksplit(int N, int K) {
   if (K % 64 != 0) return 1;
   static_assert(GK_MAXSPLIT >= 1, "split bound");
@@ -631,11 +639,13 @@ static StepLayout step_layout(const dvs_model* m, int S, int n_causal, int n_mas
                               {(int)M, m->ffn, H}, {(int)M, H, m->ffn}, {(int)logit_rows, m->vocab, H}};
     size_t part = 0, cnt = 0;
     for (const auto& sh : shapes) {
-      if (sh[1] <= 0 || sh[0] > 32) continue;   // only calls of <= 32 rows publish split partials
+      // only calls of <= GK_SPLIT_ROWS rows publish split partials
+      if (sh[1] <= 0 || sh[0] > GK_SPLIT_ROWS) continue;
       const int ksp = gemm_ksplit(sh[1], sh[2]);
       if (ksp > 1) {
+        const size_t mt = sh[0] <= 32 ? 32 : 64;
         part = std::max(part, (size_t)ksp * sh[0] * sh[1] * 4);
-        cnt = std::max(cnt, (size_t)(sh[1] + RT_NT - 1) / RT_NT);
+        cnt = std::max(cnt, (size_t)(sh[1] + RT_NT - 1) / RT_NT * ((sh[0] + mt - 1) / mt));
       }
     }
     L.gemm_part = off; off += al(part); L.gemm_part_bytes = part;
@@ -654,16 +664,18 @@ static int gemm(const StepLayout& L, char* ws, int dtype, const void* A, const v
   if (dtype == DVS_BF16 && K % 64 == 0) {
     const int ksp = gemm_ksplit(N, K);
     const int nb = (N + RT_NT - 1) / RT_NT;
-    const bool split_wg = M <= 32 && ksp > 1;
-    if (split_wg && ((size_t)ksp * M * N * 4 > L.gemm_part_bytes || (size_t)nb > L.n_gemm_counters)) {
+    const bool split_wg = M <= GK_SPLIT_ROWS && ksp > 1;
+    int mt = split_wg ? (M <= 32 ? 32 : 64) : (M <= 32 ? 32 : gemm_rows_per_tile(M, N));
+    if (mt == 256 && ksp > 1) mt = 128;   // the 256-row tile keeps no running split sum
+    const long long n_rt = (M + mt - 1) / mt;
+    if (split_wg && ((size_t)ksp * M * N * 4 > L.gemm_part_bytes ||
+                     (size_t)nb * n_rt > L.n_gemm_counters)) {
       set_error("draft_verify_step: GEMM split workspace too small");
       return DVS_EWORKSPACE;
     }
     float* part = (float*)(ws + L.gemm_part);
     int32_t* cnt = (int32_t*)(ws + L.gemm_counters);
-    int mt = M <= 32 ? 32 : gemm_rows_per_tile(M, N);
-    if (mt == 256 && ksp > 1) mt = 128;   // the 256-row tile keeps no running split sum
-    const long long grid = split_wg ? (long long)nb * ksp : (long long)nb * ((M + mt - 1) / mt);
+    const long long grid = split_wg ? (long long)nb * ksp * n_rt : (long long)nb * n_rt;
     DVS_CHECK_SUPPORTED(grid < (1LL << 31), "draft_verify_step: GEMM grid too large");
     const dim3 g((unsigned)grid), blk(256);
     const __bf16* a = (const __bf16*)A;
