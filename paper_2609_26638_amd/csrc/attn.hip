@@ -972,12 +972,12 @@ __global__ void __launch_bounds__(NP * 128, 1) attn_bf16_pc_kernel(AttnParams p)
       };
       const size_t slot = (size_t)it * p.max_segs + kseg;
       // Merge of a split item by its last workgroup, all 512 threads: rows'
-      // segment weights exp2(m_c - M) / sum_c exp2(m_c - M) l_c go to LDS
+      // segment weights exp2(m_c - M) l_c / sum_c exp2(m_c - M) l_c go to LDS
       // (the K ring is idle by then), then every thread combines whole runs
       // of 4 output columns of one row, in segment order, with batched
       // coherent loads, and stores them as 8 bf16 bytes.
       auto merge_all = [&]() {
-        const float* pob = p.part_o + (size_t)it * p.max_segs * (NC * OREG);
+        const uint32_t* pob = (const uint32_t*)(p.part_o + (size_t)it * p.max_segs * (NC * OREG));
         const float* pmlb = p.part_ml + (size_t)it * p.max_segs * (2 * RPWG);
         float* s_w = (float*)kring;   // [BAL_MAX_SEGS][RPWG]
         if (tid < RPWG) {
@@ -1000,7 +1000,7 @@ __global__ void __launch_bounds__(NP * 128, 1) attn_bf16_pc_kernel(AttnParams p)
           const float inv = lt > 0.f ? 1.f / lt : 0.f;
 #pragma unroll
           for (int c = 0; c < BAL_MAX_SEGS; ++c)
-            if (c < nseg) s_w[c * RPWG + tid] = __builtin_amdgcn_exp2f(mv[c] - Ms) * inv;
+            if (c < nseg) s_w[c * RPWG + tid] = __builtin_amdgcn_exp2f(mv[c] - Ms) * lv[c] * inv;
         }
         __syncthreads();
         // thread -> (row lane ct of the partial layout, half of its 4-column runs)
@@ -1008,7 +1008,7 @@ __global__ void __launch_bounds__(NP * 128, 1) attn_bf16_pc_kernel(AttnParams p)
         const int half = tid / NC;
         const int mkp = ct >> 6, mlane = ct & 63, ml32 = mlane & 31, mhh = mlane >> 5;
         constexpr int NQ = 2 * DG * 4;           // 4-column runs per row lane
-        constexpr int QB = 4;                    // runs per batch
+        constexpr int QB = (NQ / 2) % 8 == 0 ? 8 : 4;   // runs per batch (two words each)
         static_assert((NQ / 2) % QB == 0, "merge batches");
 #pragma unroll 1
         for (int q0 = 0; q0 < NQ / 2; q0 += QB) {
@@ -1022,14 +1022,14 @@ __global__ void __launch_bounds__(NP * 128, 1) attn_bf16_pc_kernel(AttnParams p)
             // opaque offset: the addresses are formed here, not hoisted
             int off = c * (NC * OREG) + ct;
             asm volatile("" : "+v"(off));
-            float v[QB][4];
+            uint32_t v[QB][2];
 #pragma unroll
             for (int b = 0; b < QB; ++b) {
               const int q = half + 2 * (q0 + b);     // run index: g, dg, i4
-              const int base_i = (q >> 2) * 16 + (q & 3) * 4;   // (g * DG + dg) * 16 + 4 * i4
+              const int base_w = (q >> 2) * 8 + (q & 3) * 2;   // (g * DG + dg) * 8 + 2 * i4
 #pragma unroll
-              for (int j = 0; j < 4; ++j)
-                v[b][j] = __hip_atomic_load(pob + off + (base_i + j) * NC, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+              for (int j = 0; j < 2; ++j)
+                v[b][j] = __hip_atomic_load(pob + off + (base_w + j) * NC, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             }
 #pragma unroll
             for (int b = 0; b < QB; ++b) {
@@ -1037,7 +1037,8 @@ __global__ void __launch_bounds__(NP * 128, 1) attn_bf16_pc_kernel(AttnParams p)
               const int g = q / (DG * 4);
               const float wc = s_w[c * RPWG + mkp * 64 + g * 32 + ml32];
 #pragma unroll
-              for (int j = 0; j < 4; ++j) acc[b][j] += wc * v[b][j];
+              for (int j = 0; j < 4; ++j)
+                acc[b][j] += wc * __uint_as_float((j & 1) ? (v[b][j >> 1] & 0xffff0000u) : (v[b][j >> 1] << 16));
             }
           }
 #pragma unroll
@@ -1427,7 +1428,9 @@ __global__ void __launch_bounds__(NP * 128, 1) attn_bf16_pc_kernel(AttnParams p)
           continue;
         }
         {
-          float* po = p.part_o + slot * (size_t)(NC * OREG);
+          // the segment's partial output O / l in bf16 (pairs of registers
+          // in one word), m and l in fp32
+          uint32_t* po = (uint32_t*)(p.part_o + slot * (size_t)(NC * OREG));
           if (hh == 0) {
             float* pml = p.part_ml + slot * (size_t)(2 * RPWG);
 #pragma unroll
@@ -1436,13 +1439,18 @@ __global__ void __launch_bounds__(NP * 128, 1) attn_bf16_pc_kernel(AttnParams p)
                                  __HIP_MEMORY_SCOPE_AGENT);
           }
 #pragma unroll
-          for (int g = 0; g < 2; ++g)
+          for (int g = 0; g < 2; ++g) {
+            const float inv = lrow[g] > 0.f ? 1.f / lrow[g] : 0.f;
 #pragma unroll
             for (int dg = 0; dg < DG; ++dg)
 #pragma unroll
-              for (int i = 0; i < 16; ++i)
-                __hip_atomic_store(po + ((g * DG + dg) * 16 + i) * NC + ct, o[g][dg][i], __ATOMIC_RELAXED,
+              for (int i = 0; i < 16; i += 2) {
+                const uint32_t w = __builtin_bit_cast(
+                    uint32_t, __builtin_convertvector(f32x2{o[g][dg][i] * inv, o[g][dg][i + 1] * inv}, bf16x2));
+                __hip_atomic_store(po + ((g * DG + dg) * 8 + i / 2) * NC + ct, w, __ATOMIC_RELAXED,
                                    __HIP_MEMORY_SCOPE_AGENT);
+              }
+          }
         }
         wait_vmcnt<0>();
         __syncthreads();                                       // F2

@@ -75,6 +75,7 @@ def test_attention_matches_oracle(case):
     out, d = _run(ai, chunk, err=err)
     ref, kp, vp = _oracle(ai)
     e = max_rel_err(to_f64(out), ref)
+    print(f"[err] {name}: max rel err {e:.3e}", flush=True)
     assert e <= TOL[dt], f"{name}: max rel err {e:.3e}"
     assert int(err.item()) == 0
     # the append wrote exactly the window's K/V (bit for bit, full pools)
@@ -175,8 +176,11 @@ def test_long_document_sampled_rows(long_doc):
                           ai.k_pool, ai.v_pool, ai.state.page_table, ai.state.kv_len,
                           ai.n_causal, ai.n_mask, ai.scale, sorted(samples),
                           decode=synth.bf16_to_f64)
+    worst = 0.0
     for key, v in ref.items():
         s, r, h = key
         e = max_rel_err(o[s, r, h][None], v[None])
+        worst = max(worst, e)
         assert e <= 2e-2, (key, e)
+    print(f"[err] long-document sampled rows: max rel err {worst:.3e}", flush=True)
     assert np.all(np.isfinite(o))
