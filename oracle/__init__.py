@@ -17,7 +17,9 @@ Plain, slow, float64 numpy written from the paper's definitions:
   specify are read as documented in ``model``), greedy AR decoding
   (Preliminaries, eq. ``eq:ar``) and fused self-speculative decoding, whose
   committed streams must coincide (appendix "AR-Equivalence and Equality
-  Testing", Argument).
+  Testing", Argument), the paper's two-forward round, and direct
+  block-diffusion decoding (appendix "Direct Block-Diffusion Decoding":
+  confidence-threshold reveal, cache-write forward, block commit).
 
 It shares no code with the HIP path and imports nothing from it.  Inputs come
 from the seeded generators, passed in as arrays.

@@ -49,6 +49,27 @@ the run starts with the lead token and, since the kept x0 is already in
 ``kv_len``, the new length is ``kv_len + k - 1``; the pages cover the next
 round's windows, ``[L', L' + B + 2)`` (``window = B + 2``).
 
+Direct block-diffusion decoding
+-------------------------------
+The appendix's diagnostic decoder ("Direct Block-Diffusion Decoding") fills
+one block of B positions after the boundary by repeated denoising: every
+forward runs over ``[x0, b_1..b_B]`` (1 causal row, B bidirectional block
+rows) where ``b_p`` is the revealed token or ``[M]``; the prediction for
+block position p is the top-1 of row p-1 (the shifted convention: position 1
+is predicted by the boundary row, the final position of the preceding
+block), its confidence the softmax probability of that top-1 token.  Every
+still-masked position whose confidence exceeds tau_c (strictly) is
+revealed; if none does, the single most confident masked position is
+(readings: ties go to the lowest position; only masked positions are
+candidates, revealed tokens never change).  When no position is masked, one
+more forward over ``[x0, b_1..b_{B-1}]`` as causal rows writes the block's KV
+without predicting anything, and the block ``b_1..b_B`` is committed: its
+last token is the new boundary, ``kv_len`` grows by B, and the pages cover
+the next denoising window ``[L', L' + B + 1)``.  A stop token truncates the
+committed run at that token and ends the sequence (the output is cut at its
+first EOS, and no later block is generated).  ``kv_commit`` takes the block
+as the explicit run of each sequence (``block_runs``).
+
 Top-1 rule: the maximum logit wins; among equal maxima the lowest vocabulary
 index wins; -0.0 and +0.0 are equal.  Non-finite logits are an error.
 
@@ -92,6 +113,49 @@ def top1_rows(logits: np.ndarray) -> np.ndarray:
     return out.reshape(lead)
 
 
+def top1_confidence(row: np.ndarray) -> tuple:
+    """(top-1 index, softmax probability of that token) of one logit row.
+
+    The probability of the largest logit z_m is exp(z_m) / sum_i exp(z_i)
+    = 1 / sum_i exp(z_i - z_m) (appendix "Direct Block-Diffusion Decoding":
+    a prediction's confidence is its token probability).
+    """
+    t = top1(row)
+    z = np.asarray(row, dtype=np.float64)
+    return t, float(1.0 / np.sum(np.exp(z - z[t])))
+
+
+def reveal(block: np.ndarray, am: np.ndarray, conf: np.ndarray, tau_c: float,
+           finished: np.ndarray) -> np.ndarray:
+    """One denoising step's reveal (appendix "Direct Block-Diffusion Decoding").
+
+    block [S, B] int: revealed token of position p (column p-1), or -1 while
+    masked.  am, conf [S, B]: top-1 and its confidence of window row p-1,
+    i.e. the prediction for position p.  Every masked position with
+    conf > tau_c is revealed; if there is none, the masked position of
+    largest confidence (lowest position among ties).  Finished sequences and
+    complete blocks are left alone.  Returns the new block.
+    """
+    out = block.copy()
+    S, B = block.shape
+    for s in range(S):
+        if finished[s]:
+            continue
+        masked = [p for p in range(B) if block[s, p] < 0]
+        if not masked:
+            continue
+        chosen = [p for p in masked if conf[s, p] > tau_c]
+        if not chosen:
+            best = masked[0]
+            for p in masked[1:]:
+                if conf[s, p] > conf[s, best]:
+                    best = p
+            chosen = [best]
+        for p in chosen:
+            out[s, p] = am[s, p]
+    return out
+
+
 def accept_length(a: np.ndarray, d: np.ndarray) -> int:
     """Longest k such that d_j == a_j for every j <= k (1-based j).
 
@@ -124,12 +188,16 @@ def committed_run(argmax_row: np.ndarray, draft_row: np.ndarray, A: int, lead=No
 
 def kv_commit(st, accept_len: np.ndarray, argmax: np.ndarray, n_causal: int, n_mask: int,
               eos_id: int = -1, max_new: int | None = None, page_size: int = 16,
-              lead: np.ndarray | None = None, window: int | None = None) -> int:
+              lead: np.ndarray | None = None, window: int | None = None,
+              block_runs: np.ndarray | None = None) -> int:
     """Apply one step's commit to ``st`` (a synth.PagedState-like object) in place.
 
     ``lead`` (two-forward round): per-sequence a0, committed first; the
     boundary's KV is then already in ``kv_len``.  ``window``: rows of the next
-    window the pages must cover (default n_causal + n_mask).
+    window the pages must cover (default n_causal + n_mask).  ``block_runs``
+    [S, n] (direct block diffusion): the whole row is each sequence's run,
+    in place of the accepted drafts and the verifier's token (accept_len and
+    argmax are then unused).
     Returns the error word (0 on success; on error ``st`` is unchanged).
     """
     S = st.kv_len.shape[0]
@@ -149,8 +217,11 @@ def kv_commit(st, accept_len: np.ndarray, argmax: np.ndarray, n_causal: int, n_m
     for s in range(S):
         if st.finished[s]:
             continue
-        run = committed_run(argmax[s], st.draft[s], int(accept_len[s]),
-                            None if lead is None else lead[s])
+        if block_runs is not None:
+            run = [int(t) for t in block_runs[s]]
+        else:
+            run = committed_run(argmax[s], st.draft[s], int(accept_len[s]),
+                                None if lead is None else lead[s])
         kept = []
         stop = False
         for tok in run:

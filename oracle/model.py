@@ -24,6 +24,11 @@ Decoders (all from a given committed state, see ``oracle.decode``):
 * ``fused_step`` one self-speculative step: window ``[x0, d_1..d_{B-1}]``
   (causal) followed by B ``[M]`` rows (bidirectional within the block);
   accept, commit, roll back (``oracle.decode``).
+* ``diffusion_block`` direct block-diffusion decoding of one block
+  (appendix "Direct Block-Diffusion Decoding", see ``oracle.decode``):
+  denoising forwards over ``[x0, b_1..b_B]`` until every position is
+  revealed, then a cache-write forward over ``[x0, b_1..b_{B-1}]`` and the
+  commit of the block.
 * ``prefill``   the prefix as causal rows, plus B ``[M]`` rows whose top-1
   tokens are the first draft; the last prefix row's top-1 is the first
   committed token and boundary (appendix item State: the initial boundary is
@@ -164,6 +169,44 @@ class OracleModel:
         err = odec.kv_commit(st, A, am_v, B + 1, 0, eos_id=eos_id, max_new=max_new,
                              page_size=self.page_size, lead=a0, window=B + 2)
         return logits_d, logits_v, am_v, A, err
+
+    def diffusion_denoise(self, st, block: np.ndarray, tau_c: float):
+        """One denoising forward over [x0, b_1..b_B] (1 causal row, B block
+        rows; -1 = [M]) and its reveal.  kv_len is unchanged.  Returns
+        (logits [S, B+1, V], top-1 [S, B], confidence [S, B], new block):
+        column p-1 of the last three is block position p, from row p-1."""
+        S, B = block.shape
+        tok = np.empty((S, B + 1), dtype=np.int64)
+        tok[:, 0] = st.boundary
+        tok[:, 1:] = np.where(block < 0, self.mask_id, block)
+        logits = self.forward(self.embed[tok], st, 1, B)
+        am = np.zeros((S, B), dtype=np.int32)
+        conf = np.zeros((S, B), dtype=np.float64)
+        for s in range(S):
+            for p in range(B):
+                am[s, p], conf[s, p] = odec.top1_confidence(logits[s, p])
+        return logits, am, conf, odec.reveal(block, am, conf, tau_c, st.finished)
+
+    def diffusion_block(self, st, B: int, tau_c: float, eos_id: int = -1, max_new=None):
+        """Decode one block by direct block diffusion.  Pages must cover
+        [L, L + B + 1) on entry (the commit leaves them so).  Returns
+        (block [S, B], denoising forwards, err); the block costs that many
+        forwards plus one cache-write forward."""
+        S = st.kv_len.shape[0]
+        block = np.full((S, B), -1, dtype=np.int64)
+        steps = 0
+        while np.any((block < 0).any(axis=1) & (st.finished == 0)):
+            _, _, _, block = self.diffusion_denoise(st, block, tau_c)
+            steps += 1
+            assert steps <= B, "a denoising step revealed nothing"
+        # cache-write forward: x0 and b_1..b_{B-1} as causal rows
+        tok = np.empty((S, B), dtype=np.int64)
+        tok[:, 0] = st.boundary
+        tok[:, 1:] = np.where(block[:, :B - 1] < 0, self.mask_id, block[:, :B - 1])
+        self.forward(self.embed[tok], st, B, 0)
+        err = odec.kv_commit(st, None, None, B, 0, eos_id=eos_id, max_new=max_new,
+                             page_size=self.page_size, window=B + 1, block_runs=block)
+        return block, steps, err
 
     def ar_step(self, st, eos_id: int = -1, max_new=None):
         """One greedy AR step: window [x0]; commits its top-1."""

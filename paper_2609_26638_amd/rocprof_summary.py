@@ -1,7 +1,12 @@
 """Summaries of rocprofv3 output for the profiles folder.
 
 * ``stats``: the kernel-trace statistics of a run (``--kernel-trace --stats``)
-  as a markdown table, with the command that produced them.
+  as a markdown table, with the command that produced them.  Given
+  ``--kernel``, ``--groups`` and ``--bench``, it also splits that kernel's
+  launches, in start order, into the bench's phases (warmup, the event-free
+  timed loop, the instrumented loop) and sets the average of the
+  instrumented loop beside the ``avg_ms`` the bench line printed in the
+  same process.
 * ``traffic``: HBM bytes per dispatch of one kernel from a ``--pmc FETCH_SIZE``
   run and a ``--pmc WRITE_SIZE`` run of ``bench.py --profile-attn N``.  Both
   counters are calibrated against the device-to-device copy of known size
@@ -50,6 +55,35 @@ def kernel_stats_md(stats, title, command, limit=12):
     return "\n".join(out) + "\n"
 
 
+def launch_groups_md(trace, kernel, groups, bench_line=None):
+    """Average duration of one kernel's launches, split in start order into
+    consecutive groups of the given sizes ((name, count) pairs; a count of
+    -1 takes the rest)."""
+    rows = [r for r in _rows(trace, "kernel_trace.csv") if kernel in r["Kernel_Name"]]
+    rows.sort(key=lambda r: int(r["Start_Timestamp"]))
+    us = [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3 for r in rows]
+    out = ["", f"Launches of `{kernel}` in start order, by phase of the run:", "",
+           "| phase | launches | avg us | min us | max us |", "|---|---|---|---|---|"]
+    i, avgs = 0, {}
+    for name, n in groups:
+        part = us[i:] if n < 0 else us[i:i + n]
+        i += len(part)
+        if not part:
+            continue
+        avgs[name] = sum(part) / len(part)
+        out.append(f"| {name} | {len(part)} | {avgs[name]:.1f} | {min(part):.1f} | {max(part):.1f} |")
+    if bench_line is not None:
+        avg = bench_line["roofline"]["avg_ms"] * 1e3
+        out += ["", f"The bench line printed by the same process: `avg_ms` = {avg:.1f} us "
+                f"(HIP events around each launch of the instrumented loop), "
+                f"`value` = {bench_line['value']:.0f} {bench_line['unit']}."]
+        last = list(avgs)[-1] if avgs else None
+        if last is not None:
+            out.append(f"Trace average of the same launches: {avgs[last]:.1f} us "
+                       f"({avgs[last] / avg:.3f} of the event figure).")
+    return "\n".join(out) + "\n"
+
+
 def per_dispatch(counter_dir, counter):
     """{dispatch id: (kernel name, value summed over the counter's instances)}"""
     acc = collections.OrderedDict()
@@ -71,6 +105,17 @@ def _meta(path):
     if meta is None:
         raise SystemExit("no profile_attn line in " + path)
     return meta
+
+
+def _bench_line(path):
+    line = None
+    for raw in open(path):
+        raw = raw.strip()
+        if raw.startswith("{") and '"roofline"' in raw:
+            line = json.loads(raw)
+    if line is None:
+        raise SystemExit("no bench line in " + path)
+    return line
 
 
 def traffic(fetch_dir, write_dir, kernel, copy_bytes):
@@ -139,6 +184,9 @@ def main():
     s.add_argument("--title", required=True)
     s.add_argument("--command", required=True)
     s.add_argument("--out", required=True)
+    s.add_argument("--kernel", help="substring of one kernel's name")
+    s.add_argument("--groups", help="phase=count,... of that kernel's launches (-1: the rest)")
+    s.add_argument("--bench", help="file whose last JSON line is the bench line of the same run")
     t = sub.add_parser("traffic")
     t.add_argument("--fetch", required=True, help="output directory of the FETCH_SIZE run")
     t.add_argument("--write", required=True, help="output directory of the WRITE_SIZE run")
@@ -171,8 +219,13 @@ def main():
         print(json.dumps(res["mean"]))
         return
     if a.cmd == "stats":
+        text = kernel_stats_md(a.stats, a.title, a.command)
+        if a.kernel and a.groups:
+            groups = [(g.split("=")[0], int(g.split("=")[1])) for g in a.groups.split(",")]
+            line = _bench_line(a.bench) if a.bench else None
+            text += launch_groups_md(a.stats, a.kernel, groups, line)
         with open(a.out, "w") as f:
-            f.write(kernel_stats_md(a.stats, a.title, a.command))
+            f.write(text)
         return
     meta = _meta(a.meta)
     tr = traffic(a.fetch, a.write, a.kernel, meta["copy_bytes"])
