@@ -60,6 +60,7 @@ extern "C" {
 #define DVS_ERR_MAX_PAGES 2       /* a sequence would exceed max_pages        */
 #define DVS_ERR_NONFINITE 4       /* a logit was NaN or infinite              */
 #define DVS_ERR_BAD_PAGE 8        /* a page id outside [0, num_pool_pages)    */
+#define DVS_ERR_OPEN_BLOCK 16     /* a block commit met a masked position     */
 
 #define DVS_PAGE_SIZE 16
 
@@ -136,6 +137,22 @@ int attn_hybrid_block(const void* q, const void* k_new, const void* v_new, void*
 int argmax_accept(const void* logits, int32_t dtype, int32_t S, int32_t R, int32_t V,
                   int32_t n_causal, const int32_t* draft, int32_t draft_width,
                   int32_t* argmax_out, int32_t* accept_len, int32_t* err_word, void* stream);
+
+/* ------------------------------------------------------------------------
+ * top1_confidence
+ *
+ * Top-1 and its softmax probability for every row (appendix "Direct
+ * Block-Diffusion Decoding": a prediction is revealed by its token
+ * probability):
+ *   argmax_out[r] = top-1 of logits[r, :] (the rule of argmax_accept);
+ *   conf_out[r]   = exp(z_max) / sum_i exp(z_i) = 1 / sum_i exp(z_i - z_max),
+ *                   fp32 arithmetic, one pass over the row.
+ *   logits [rows, V] DVS_F32 or DVS_BF16; argmax_out [rows] int32 and
+ *   conf_out [rows] fp32 (written); err_word: DVS_ERR_NONFINITE as in
+ *   argmax_accept (may be NULL).
+ * ---------------------------------------------------------------------- */
+int top1_confidence(const void* logits, int32_t dtype, int32_t rows, int32_t V,
+                    int32_t* argmax_out, float* conf_out, int32_t* err_word, void* stream);
 
 /* ------------------------------------------------------------------------
  * kv_commit
@@ -267,6 +284,26 @@ typedef struct dvs_state {
 
 size_t dvs_step_workspace_bytes(const dvs_model* m, int32_t S, int32_t n_causal, int32_t n_mask,
                                 int32_t max_pages, int32_t chunk_keys);
+/* ------------------------------------------------------------------------
+ * kv_commit_block
+ *
+ * The commit of one block of direct block-diffusion decoding (appendix
+ * "Direct Block-Diffusion Decoding"), after the cache-write forward over
+ * [x0, b_1..b_{B-1}].  Same as kv_commit except:
+ *   run      = b_1..b_B = block[s, 0..B-1] (all B positions revealed; a
+ *              negative token in the kept part of a live sequence's run sets
+ *              DVS_ERR_OPEN_BLOCK and nothing is changed);
+ *   kv_len[s] += k;  pages cover the next denoising window:
+ *              ceil((kv_len + B + 1) / 16);  draft is not changed.
+ *   block [S, B] int32 (read); other arrays as in kv_commit.
+ * Requirements: 1 <= S <= 1024, B >= 1.
+ * ---------------------------------------------------------------------- */
+int kv_commit_block(int32_t S, int32_t B, const int32_t* block, int32_t* kv_len,
+                    int32_t* page_table, int32_t* num_pages, int32_t max_pages,
+                    int32_t* free_stack, int32_t* free_top, int32_t num_pool_pages,
+                    int32_t* boundary, int32_t* out_tokens, int32_t* out_count, int32_t max_new,
+                    int32_t eos_id, int32_t* finished, int32_t* err_word, void* stream);
+
 
 int draft_verify_step(const dvs_model* m, const dvs_state* st, int32_t n_causal, int32_t n_mask,
                       int32_t chunk_keys, float* logits_out, int32_t* argmax_out,
@@ -297,6 +334,45 @@ int draft_verify_step(const dvs_model* m, const dvs_state* st, int32_t n_causal,
 int literal_round(const dvs_model* m, const dvs_state* st, int32_t B, int32_t chunk_keys,
                   float* logits_out, int32_t* argmax_out, int32_t* accept_out, void* workspace,
                   size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * diffusion_denoise / diffusion_block / dvs_diffusion_workspace_bytes
+ *
+ * Direct block-diffusion decoding (appendix "Direct Block-Diffusion
+ * Decoding"), with the layers of draft_verify_step.  block [S, B] int32
+ * holds the revealed token of block position p = 1..B in column p-1, or -1
+ * while masked.
+ *
+ * diffusion_denoise: one forward over [x0, b_1..b_B] at positions L .. L+B
+ *   (boundary row causal, block rows bidirectional, masked positions as
+ *   [M]); top-1 and confidence (top1_confidence) of every row; then for
+ *   every live sequence with masked positions: each masked position p whose
+ *   row p-1 has confidence > tau_c takes that row's top-1; if none does,
+ *   the masked position of largest confidence (lowest p among ties) does.
+ *   Revealed positions never change; kv_len is unchanged.  *n_open (device
+ *   int32, written) = number of live sequences whose block is still open.
+ *   logits_out [S*(B+1), vocab] fp32, argmax_out [S*(B+1)] int32,
+ *   conf_out [S*(B+1)] fp32 receive the forward's rows (each optional).
+ *   workspace: dvs_step_workspace_bytes(m, S, 1, B, ...) bytes suffice.
+ *
+ * diffusion_block: one whole block: fills block with -1, runs
+ *   diffusion_denoise until no live block is open (at most B forwards, each
+ *   followed by a 4-byte device-to-host read and a stream synchronisation),
+ *   then the cache-write forward over [x0, b_1..b_{B-1}] (B causal rows, no
+ *   LM head) and kv_commit_block.  *steps_out (host, optional) = denoising
+ *   forwards; the block cost *steps_out + 1 forwards.  Pages must cover
+ *   [L, L + B + 1) on entry (kv_commit_block leaves them so).  workspace:
+ *   dvs_diffusion_workspace_bytes(m, S, B, max_pages, chunk_keys) bytes.
+ * ---------------------------------------------------------------------- */
+size_t dvs_diffusion_workspace_bytes(const dvs_model* m, int32_t S, int32_t B, int32_t max_pages,
+                                     int32_t chunk_keys);
+int diffusion_denoise(const dvs_model* m, const dvs_state* st, int32_t B, float tau_c,
+                      int32_t* block, int32_t* n_open, int32_t chunk_keys, float* logits_out,
+                      int32_t* argmax_out, float* conf_out, void* workspace, size_t ws_bytes,
+                      void* stream);
+int diffusion_block(const dvs_model* m, const dvs_state* st, int32_t B, float tau_c,
+                    int32_t* block, int32_t chunk_keys, int32_t* steps_out, void* workspace,
+                    size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
  * dvs_prefill

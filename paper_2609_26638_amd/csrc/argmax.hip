@@ -127,6 +127,68 @@ __global__ void __launch_bounds__(256) argmax_kernel(const void* __restrict__ lo
   }
 }
 
+// Top-1 and its softmax probability (appendix "Direct Block-Diffusion
+// Decoding": a prediction's confidence is its token probability), in one
+// pass over the row: every thread keeps its first maximum m and the sum
+// sum_i exp(x_i - m) of what it has read, rescaled when m grows; the threads
+// then merge (m, sum, index) pairs, the lowest index among equal maxima.
+// conf = 1 / sum.  fp32 arithmetic; one workgroup per row.
+template <bool BF16>
+__global__ void __launch_bounds__(256) top1_conf_kernel(const void* __restrict__ logits, int V,
+                                                        int32_t* __restrict__ argmax_out,
+                                                        float* __restrict__ conf_out,
+                                                        int32_t* err) {
+  __shared__ float sm[4], ss[4];
+  __shared__ int si[4];
+  const size_t row = blockIdx.x;
+  const int tid = threadIdx.x;
+  const char* base = (const char*)logits + row * (size_t)V * (BF16 ? 2 : 4);
+  float m = -INFINITY, sum = 0.f, nf = 0.f;
+  int bi = 0x7fffffff;
+  for (int i = tid; i < V; i += 256) {
+    const float f = BF16 ? __uint_as_float((uint32_t)((const uint16_t*)base)[i] << 16)
+                         : ((const float*)base)[i];
+    nf = fmaf(f, 0.f, nf);
+    if (f > m) {
+      sum = sum * __expf(m - f) + 1.f;
+      m = f;
+      bi = i;
+    } else {
+      sum += __expf(f - m);
+    }
+  }
+  // wave merge
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    const float om = __shfl_xor(m, off);
+    const float os = __shfl_xor(sum, off);
+    const int oi = __shfl_xor(bi, off);
+    const float M = fmaxf(m, om);
+    const float a = m == -INFINITY ? 0.f : sum * __expf(m - M);
+    const float b = om == -INFINITY ? 0.f : os * __expf(om - M);
+    bi = (om > m || (om == m && oi < bi)) ? oi : bi;
+    m = M;
+    sum = a + b;
+  }
+  if ((tid & 63) == 0) { sm[tid >> 6] = m; ss[tid >> 6] = sum; si[tid >> 6] = bi; }
+  if (nf != nf) set_err(err, DVS_ERR_NONFINITE);
+  __syncthreads();
+  if (tid == 0) {
+    float M = sm[0], S = ss[0];
+    int I = si[0];
+    for (int w = 1; w < 4; ++w) {
+      const float nm = fmaxf(M, sm[w]);
+      const float a = M == -INFINITY ? 0.f : S * __expf(M - nm);
+      const float b = sm[w] == -INFINITY ? 0.f : ss[w] * __expf(sm[w] - nm);
+      if (sm[w] > M || (sm[w] == M && si[w] < I)) I = si[w];
+      M = nm;
+      S = a + b;
+    }
+    argmax_out[row] = I == 0x7fffffff ? 0 : I;
+    conf_out[row] = 1.f / S;
+  }
+}
+
 __global__ void accept_kernel(const int32_t* __restrict__ argmax_out, int S, int R, int n_causal,
                               const int32_t* __restrict__ draft, int draft_width,
                               int32_t* __restrict__ accept_len) {
@@ -143,6 +205,23 @@ __global__ void accept_kernel(const int32_t* __restrict__ argmax_out, int S, int
 }  // namespace dvs
 
 using namespace dvs;
+
+extern "C" int top1_confidence(const void* logits, int32_t dtype, int32_t rows, int32_t V,
+                               int32_t* argmax_out, float* conf_out, int32_t* err_word,
+                               void* stream) {
+  clear_error();
+  DVS_CHECK_ARG(logits && argmax_out && conf_out, "top1_confidence: NULL array argument");
+  DVS_CHECK_ARG(rows >= 1 && V >= 1, "top1_confidence: need rows, V >= 1");
+  DVS_CHECK_SUPPORTED(dtype == DVS_F32 || dtype == DVS_BF16, "top1_confidence: dtype %d", dtype);
+  hipStream_t st = (hipStream_t)stream;
+  if (dtype == DVS_BF16)
+    hipLaunchKernelGGL(top1_conf_kernel<true>, dim3((unsigned)rows), dim3(256), 0, st, logits, V,
+                       argmax_out, conf_out, err_word);
+  else
+    hipLaunchKernelGGL(top1_conf_kernel<false>, dim3((unsigned)rows), dim3(256), 0, st, logits, V,
+                       argmax_out, conf_out, err_word);
+  return launch_status("top1_confidence");
+}
 
 extern "C" int argmax_accept(const void* logits, int32_t dtype, int32_t S, int32_t R, int32_t V,
                              int32_t n_causal, const int32_t* draft, int32_t draft_width,

@@ -11,6 +11,12 @@
 // token: the run is a0, d_1..d_A, a_{A+1}, kv_len already counts the kept x0
 // (so kv_len += k - 1), and the pages cover the next round's windows.
 //
+// Direct block diffusion commits a whole block b_1..b_B through the same
+// kernel (no accept length): the run is the block, kv_len += k (the
+// cache-write forward wrote x0 and b_1..b_{B-1}), and the pages cover the
+// next denoising window of B + 1 rows.  A masked (negative) token in a live
+// block is an error.
+//
 // Pages: each sequence ends holding ceil((kv_len + W) / 16) pages, W the
 // window of the next call (R, or B + 2 in the two-forward round).  Two
 // exclusive scans over the sequences give every surplus page its slot on the
@@ -46,7 +52,7 @@ __device__ __forceinline__ int block_exclusive_scan(int v, int* sh, int& total) 
 struct CommitParams {
   int S, n_causal, n_mask, R, window, max_pages, pool_pages, draft_width, max_new, eos_id;
   const int32_t* lead;   // two-forward round: a0 per sequence, committed first (else NULL)
-  const int32_t* accept_len;
+  const int32_t* accept_len;   // NULL: the run is the first n_causal tokens of argmax
   const int32_t* argmax;
   int32_t* kv_len;
   int32_t* page_table;
@@ -87,7 +93,7 @@ __global__ void __launch_bounds__(COMMIT_THREADS) kv_commit_kernel(CommitParams 
     cnt = p.out_count[s];
     fin = p.finished[s] != 0;
     if (!fin) {
-      A = p.accept_len[s];
+      A = p.accept_len ? p.accept_len[s] : p.n_causal - 1;
       A = A < 0 ? 0 : (A > p.n_causal - 1 ? p.n_causal - 1 : A);
       // run = [a0,] d_1..d_A, a_{A+1} (last index jl); keep up to the first
       // stop token / budget.  Tokens are fetched RUN_CHUNK at a time
@@ -105,6 +111,7 @@ __global__ void __launch_bounds__(COMMIT_THREADS) kv_commit_kernel(CommitParams 
           if (cnt + k >= p.max_new) {
             stop = done = true;
           } else {
+            if (!p.accept_len && tk[u] < 0) atomicOr(&s_err, DVS_ERR_OPEN_BLOCK);
             ++k;
             last_tok = tk[u];
             if (p.eos_id >= 0 && tk[u] == p.eos_id) stop = done = true;
@@ -192,7 +199,7 @@ static int launch_commit(const char* who, int32_t S, int32_t n_causal, int32_t n
                          int32_t* draft, int32_t draft_width, int32_t* out_tokens,
                          int32_t* out_count, int32_t max_new, int32_t eos_id, int32_t* finished,
                          int32_t* err_word, void* stream) {
-  DVS_CHECK_ARG(accept_len && argmax && kv_len && page_table && num_pages && free_stack &&
+  DVS_CHECK_ARG(argmax && kv_len && page_table && num_pages && free_stack &&
                     free_top && boundary && out_tokens && out_count && finished,
                 "%s: NULL array argument", who);
   DVS_CHECK_ARG(S >= 1 && S <= COMMIT_THREADS, "%s: need 1 <= S <= %d", who, COMMIT_THREADS);
@@ -225,6 +232,7 @@ extern "C" int kv_commit(int32_t S, int32_t n_causal, int32_t n_mask, const int3
                          int32_t* out_count, int32_t max_new, int32_t eos_id, int32_t* finished,
                          int32_t* err_word, void* stream) {
   clear_error();
+  DVS_CHECK_ARG(accept_len != nullptr, "kv_commit: NULL accept_len");
   return launch_commit("kv_commit", S, n_causal, n_mask, n_causal + n_mask, nullptr, accept_len,
                        argmax, kv_len, page_table, num_pages, max_pages, free_stack, free_top,
                        num_pool_pages, boundary, draft, draft_width, out_tokens, out_count, max_new,
@@ -239,10 +247,27 @@ extern "C" int kv_commit_round(int32_t S, int32_t B, const int32_t* lead, const 
                                int32_t* out_count, int32_t max_new, int32_t eos_id,
                                int32_t* finished, int32_t* err_word, void* stream) {
   clear_error();
-  DVS_CHECK_ARG(lead != nullptr, "kv_commit_round: NULL lead");
+  DVS_CHECK_ARG(lead != nullptr && accept_len != nullptr, "kv_commit_round: NULL lead/accept_len");
   DVS_CHECK_ARG(B >= 1, "kv_commit_round: need B >= 1");
   return launch_commit("kv_commit_round", S, B + 1, 0, B + 2, lead, accept_len, argmax, kv_len,
                        page_table, num_pages, max_pages, free_stack, free_top, num_pool_pages,
                        boundary, draft, draft_width, out_tokens, out_count, max_new, eos_id,
                        finished, err_word, stream);
+}
+
+extern "C" int kv_commit_block(int32_t S, int32_t B, const int32_t* block, int32_t* kv_len,
+                               int32_t* page_table, int32_t* num_pages, int32_t max_pages,
+                               int32_t* free_stack, int32_t* free_top, int32_t num_pool_pages,
+                               int32_t* boundary, int32_t* out_tokens, int32_t* out_count,
+                               int32_t max_new, int32_t eos_id, int32_t* finished,
+                               int32_t* err_word, void* stream) {
+  clear_error();
+  DVS_CHECK_ARG(block != nullptr, "kv_commit_block: NULL block");
+  DVS_CHECK_ARG(B >= 1, "kv_commit_block: need B >= 1");
+  // run token j < B - 1 comes from the draft slot j, the last from argmax[B - 1]:
+  // both are the block row
+  return launch_commit("kv_commit_block", S, B, 0, B + 1, nullptr, nullptr, block, kv_len,
+                       page_table, num_pages, max_pages, free_stack, free_top, num_pool_pages,
+                       boundary, const_cast<int32_t*>(block), B, out_tokens, out_count, max_new,
+                       eos_id, finished, err_word, stream);
 }

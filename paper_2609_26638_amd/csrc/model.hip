@@ -37,11 +37,12 @@ template <typename T>
 __global__ void embed_rows_kernel(const T* __restrict__ embed, int H, int vocab, int R, int n_causal,
                                   const int32_t* __restrict__ boundary,
                                   const int32_t* __restrict__ draft, int draft_width,
-                                  float* __restrict__ x) {
+                                  const int32_t* __restrict__ block, float* __restrict__ x) {
   const int mrow = blockIdx.x;
   const int s = mrow / R, r = mrow - s * R;
   int tok = vocab;  // [M]
   if (r < n_causal) tok = (r == 0) ? boundary[s] : draft[(size_t)s * draft_width + (r - 1)];
+  else if (block) tok = block[(size_t)s * (R - n_causal) + (r - n_causal)];  // -1: [M]
   if (tok < 0 || tok > vocab) tok = vocab;
   const T* e = embed + (size_t)tok * H;
   for (int i = threadIdx.x; i < H; i += blockDim.x) x[(size_t)mrow * H + i] = to_f(e[i]);
@@ -63,6 +64,61 @@ __global__ void round_draft_kernel(int S, int B, const int32_t* __restrict__ am,
   if (finished[s]) return;
   for (int j = 0; j < B; ++j) draft[(size_t)s * draft_width + j] = am[(size_t)s * R + 1 + j];
   kv_len[s] += 1;
+}
+
+// Reveal of one denoising step (appendix "Direct Block-Diffusion
+// Decoding"): every masked block position p whose prediction (top-1 of
+// window row p-1) has confidence above tau_c takes that token; when no
+// position qualifies, the most confident masked one does (lowest position
+// among ties).  Revealed positions never change.  One 64-lane wave per
+// sequence, lane = position mod 64; a sequence whose block stays open adds
+// one to *n_open.  block: [S, B] (-1 = masked); am, conf: [S, B + 1].
+__global__ void __launch_bounds__(64) reveal_kernel(int B, float tau_c,
+                                                    const int32_t* __restrict__ am,
+                                                    const float* __restrict__ conf,
+                                                    const int32_t* __restrict__ finished,
+                                                    int32_t* __restrict__ block,
+                                                    int32_t* __restrict__ n_open) {
+  const int s = blockIdx.x, lane = threadIdx.x;
+  if (finished[s]) return;
+  int32_t* b = block + (size_t)s * B;
+  const int32_t* a = am + (size_t)s * (B + 1);
+  const float* c = conf + (size_t)s * (B + 1);
+  constexpr int NONE = 0x7fffffff;
+  int hits = 0, bp = NONE;
+  float bc = 0.f;
+  for (int p = lane; p < B; p += 64) {
+    if (b[p] >= 0) continue;
+    const float cp = c[p];
+    if (cp > tau_c) {
+      b[p] = a[p];
+      ++hits;
+    } else if (bp == NONE || cp > bc) {   // positions ascend: the first of equals stays
+      bc = cp;
+      bp = p;
+    }
+  }
+  if (!__any(hits)) {
+    // (larger confidence, then smaller position) over the wave
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+      const float oc = __shfl_xor(bc, off);
+      const int op = __shfl_xor(bp, off);
+      if (op != NONE && (bp == NONE || oc > bc || (oc == bc && op < bp))) {
+        bc = oc;
+        bp = op;
+      }
+    }
+    if (bp != NONE && (bp & 63) == lane) b[bp] = a[bp];
+  }
+  int left = 0;
+  for (int p = lane; p < B; p += 64) left |= b[p] < 0;
+  if (__any(left) && lane == 0) atomicAdd(n_open, 1);
+}
+
+__global__ void fill_words_kernel(int32_t* __restrict__ p, int n, int32_t v) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = v;
 }
 
 // out[m, :] = x[m, :] / sqrt(mean(x^2) + eps) * g   (one workgroup per row)
@@ -557,7 +613,8 @@ __global__ void __launch_bounds__(256) gemm_f32_kernel(const float* __restrict__
 // host orchestration
 // ---------------------------------------------------------------------------
 struct StepLayout {
-  size_t x, h, hsel, q, k, v, att, gate, up, act, logits, am, acc, lead, attn_ws, total, attn_bytes,
+  size_t x, h, hsel, q, k, v, att, gate, up, act, logits, am, conf, nopen, acc, lead, attn_ws, total,
+      attn_bytes,
       attn_counters, gemm_part, gemm_part_bytes, gemm_counters, n_gemm_counters;
 };
 
@@ -625,6 +682,8 @@ static StepLayout step_layout(const dvs_model* m, int S, int n_causal, int n_mas
   L.act = off; off += al(M * (size_t)m->ffn * es);
   L.logits = off; off += al(logit_rows * (size_t)m->vocab * 4);
   L.am = off; off += al(logit_rows * 4);
+  L.conf = off; off += al(logit_rows * 4);
+  L.nopen = off; off += al(4);
   L.acc = off; off += al((size_t)S * 4);
   L.lead = off; off += al((size_t)S * 4);
   L.attn_bytes = dvs_attn_workspace_bytes(S, n_causal, n_mask, m->n_heads, m->n_kv_heads,
@@ -774,7 +833,7 @@ static int run_step(const dvs_model* m, const dvs_state* st, int n_causal, int n
   int32_t* acc = accept_out ? accept_out : (int32_t*)(ws + L.acc);
   hipLaunchKernelGGL(embed_rows_kernel<T>, dim3(M), dim3(256), 0, stream, (const T*)m->embed,
                      m->hidden, m->vocab, R, n_causal, st->boundary, st->draft, st->draft_width,
-                     (float*)(ws + L.x));
+                     nullptr, (float*)(ws + L.x));
   int rc;
   if ((rc = launch_status("draft_verify_step(embed)"))) return rc;
   if ((rc = forward_layers<T>(m, st, n_causal, n_mask, chunk_keys, L, ws, stream))) return rc;
@@ -806,7 +865,7 @@ static int run_round(const dvs_model* m, const dvs_state* st, int B, int chunk_k
   // draft forward
   hipLaunchKernelGGL(embed_rows_kernel<T>, dim3(M), dim3(256), 0, stream, (const T*)m->embed,
                      m->hidden, m->vocab, R, 1, st->boundary, st->draft, st->draft_width,
-                     (float*)(ws + L.x));
+                     nullptr, (float*)(ws + L.x));
   if ((rc = launch_status("literal_round(embed)"))) return rc;
   if ((rc = forward_layers<T>(m, st, 1, B, chunk_keys, L, ws, stream))) return rc;
   if ((rc = gemm(L, ws, m->dtype, ws + L.h, m->lm_head, M, m->vocab, m->hidden, logits, 1, 0, stream)))
@@ -819,7 +878,8 @@ static int run_round(const dvs_model* m, const dvs_state* st, int B, int chunk_k
   if ((rc = launch_status("literal_round(draft)"))) return rc;
   // verify forward
   hipLaunchKernelGGL(embed_rows_kernel<T>, dim3(M), dim3(256), 0, stream, (const T*)m->embed,
-                     m->hidden, m->vocab, R, R, lead, st->draft, st->draft_width, (float*)(ws + L.x));
+                     m->hidden, m->vocab, R, R, lead, st->draft, st->draft_width, nullptr,
+                     (float*)(ws + L.x));
   if ((rc = launch_status("literal_round(embed)"))) return rc;
   if ((rc = forward_layers<T>(m, st, R, 0, chunk_keys, L, ws, stream))) return rc;
   if ((rc = gemm(L, ws, m->dtype, ws + L.h, m->lm_head, M, m->vocab, m->hidden, logits, 1, 0, stream)))
@@ -831,6 +891,52 @@ static int run_round(const dvs_model* m, const dvs_state* st, int B, int chunk_k
                          st->max_pages, st->free_stack, st->free_top, st->num_pool_pages,
                          st->boundary, st->draft, st->draft_width, st->out_tokens, st->out_count,
                          st->max_new, st->eos_id, st->finished, st->err_word, stream);
+}
+
+// One denoising forward of direct block diffusion: [x0, b_1..b_B] with the
+// boundary row causal and the block rows bidirectional (masked positions
+// carry [M]); top-1 and confidence of every row; the reveal.  kv_len is
+// unchanged (the window's K/V slots are rewritten by the next forward).
+template <typename T>
+static int run_denoise(const dvs_model* m, const dvs_state* st, int B, float tau_c,
+                       int32_t* block, int32_t* n_open, int chunk_keys, const StepLayout& L,
+                       char* ws, float* logits_out, int32_t* argmax_out, float* conf_out,
+                       hipStream_t stream) {
+  const int S = st->S, R = B + 1, M = S * R;
+  float* logits = logits_out ? logits_out : (float*)(ws + L.logits);
+  int32_t* am = argmax_out ? argmax_out : (int32_t*)(ws + L.am);
+  float* conf = conf_out ? conf_out : (float*)(ws + L.conf);
+  hipLaunchKernelGGL(embed_rows_kernel<T>, dim3(M), dim3(256), 0, stream, (const T*)m->embed,
+                     m->hidden, m->vocab, R, 1, st->boundary, st->draft, st->draft_width, block,
+                     (float*)(ws + L.x));
+  int rc;
+  if ((rc = launch_status("diffusion_denoise(embed)"))) return rc;
+  if ((rc = forward_layers<T>(m, st, 1, B, chunk_keys, L, ws, stream))) return rc;
+  if ((rc = gemm(L, ws, m->dtype, ws + L.h, m->lm_head, M, m->vocab, m->hidden, logits, 1, 0, stream)))
+    return rc;
+  if ((rc = top1_confidence(logits, DVS_F32, M, m->vocab, am, conf, st->err_word, stream))) return rc;
+  hipLaunchKernelGGL(zero_words_kernel, dim3(1), dim3(256), 0, stream, n_open, 1);
+  hipLaunchKernelGGL(reveal_kernel, dim3(S), dim3(64), 0, stream, B, tau_c, am, conf,
+                     st->finished, block, n_open);
+  return launch_status("diffusion_denoise(reveal)");
+}
+
+// The block's cache-write forward (x0 and b_1..b_{B-1} as causal rows, no
+// LM head) and its commit.
+template <typename T>
+static int run_block_commit(const dvs_model* m, const dvs_state* st, int B, const int32_t* block,
+                            int chunk_keys, const StepLayout& L, char* ws, hipStream_t stream) {
+  const int S = st->S, M = S * B;
+  hipLaunchKernelGGL(embed_rows_kernel<T>, dim3(M), dim3(256), 0, stream, (const T*)m->embed,
+                     m->hidden, m->vocab, B, B, st->boundary, block, B, nullptr,
+                     (float*)(ws + L.x));
+  int rc;
+  if ((rc = launch_status("diffusion_block(embed)"))) return rc;
+  if ((rc = forward_layers<T>(m, st, B, 0, chunk_keys, L, ws, stream))) return rc;
+  return kv_commit_block(S, B, block, st->kv_len, st->page_table, st->num_pages, st->max_pages,
+                         st->free_stack, st->free_top, st->num_pool_pages, st->boundary,
+                         st->out_tokens, st->out_count, st->max_new, st->eos_id, st->finished,
+                         st->err_word, stream);
 }
 
 template <typename T>
@@ -975,4 +1081,97 @@ extern "C" int dvs_prefill(const dvs_model* m, const dvs_state* st, int32_t P, i
                                (char*)workspace, logits_out, s);
   return run_prefill<float>(m, st, P, n_mask, prefix_tokens, x_prefix, chunk_keys, L,
                             (char*)workspace, logits_out, s);
+}
+
+static int check_model_state(const dvs_model* m, const dvs_state* st, const char* who) {
+  DVS_CHECK_ARG(model_ok(m), "%s: invalid model description", who);
+  DVS_CHECK_ARG(st && st->S >= 1 && st->kv_len && st->page_table && st->num_pages &&
+                    st->free_stack && st->free_top && st->boundary && st->out_tokens &&
+                    st->out_count && st->finished,
+                "%s: invalid state description", who);
+  for (int l = 0; l < m->n_layers; ++l) {
+    const dvs_layer& ly = m->layers[l];
+    DVS_CHECK_ARG(ly.wq && ly.wk && ly.wv && ly.wo && ly.g_attn && ly.k_pool && ly.v_pool,
+                  "%s: layer %d incomplete", who, l);
+    DVS_CHECK_ARG(m->ffn == 0 || (ly.g_mlp && ly.w_gate && ly.w_up && ly.w_down),
+                  "%s: layer %d MLP incomplete", who, l);
+  }
+  DVS_CHECK_SUPPORTED(m->head_dim == 64 || m->head_dim == 96 || m->head_dim == 128,
+                      "%s: head_dim %d", who, m->head_dim);
+  return DVS_OK;
+}
+
+extern "C" size_t dvs_diffusion_workspace_bytes(const dvs_model* m, int32_t S, int32_t B,
+                                                int32_t max_pages, int32_t chunk_keys) {
+  if (!model_ok(m) || S < 1 || B < 1 || max_pages < 1) return 0;
+  return std::max(step_layout(m, S, 1, B, max_pages, chunk_keys, (size_t)S * (B + 1)).total,
+                  step_layout(m, S, B, 0, max_pages, chunk_keys, 0).total);
+}
+
+extern "C" int diffusion_denoise(const dvs_model* m, const dvs_state* st, int32_t B, float tau_c,
+                                 int32_t* block, int32_t* n_open, int32_t chunk_keys,
+                                 float* logits_out, int32_t* argmax_out, float* conf_out,
+                                 void* workspace, size_t ws_bytes, void* stream) {
+  clear_error();
+  int rc = check_model_state(m, st, "diffusion_denoise");
+  if (rc) return rc;
+  DVS_CHECK_ARG(B >= 1 && block && n_open, "diffusion_denoise: need B >= 1, block, n_open");
+  const StepLayout L = step_layout(m, st->S, 1, B, st->max_pages, chunk_keys,
+                                   (size_t)st->S * (B + 1));
+  if (!workspace || ws_bytes < L.total) {
+    set_error("diffusion_denoise: workspace needs %zu bytes, got %zu", L.total, ws_bytes);
+    return DVS_EWORKSPACE;
+  }
+  hipStream_t s = (hipStream_t)stream;
+  if (m->dtype == DVS_BF16)
+    return run_denoise<__bf16>(m, st, B, tau_c, block, n_open, chunk_keys, L, (char*)workspace,
+                               logits_out, argmax_out, conf_out, s);
+  return run_denoise<float>(m, st, B, tau_c, block, n_open, chunk_keys, L, (char*)workspace,
+                            logits_out, argmax_out, conf_out, s);
+}
+
+extern "C" int diffusion_block(const dvs_model* m, const dvs_state* st, int32_t B, float tau_c,
+                               int32_t* block, int32_t chunk_keys, int32_t* steps_out,
+                               void* workspace, size_t ws_bytes, void* stream) {
+  clear_error();
+  int rc = check_model_state(m, st, "diffusion_block");
+  if (rc) return rc;
+  DVS_CHECK_ARG(B >= 1 && block, "diffusion_block: need B >= 1 and a block array");
+  const int S = st->S;
+  const StepLayout Ld = step_layout(m, S, 1, B, st->max_pages, chunk_keys, (size_t)S * (B + 1));
+  const StepLayout Lc = step_layout(m, S, B, 0, st->max_pages, chunk_keys, 0);
+  const size_t need = std::max(Ld.total, Lc.total);
+  if (!workspace || ws_bytes < need) {
+    set_error("diffusion_block: workspace needs %zu bytes, got %zu", need, ws_bytes);
+    return DVS_EWORKSPACE;
+  }
+  hipStream_t s = (hipStream_t)stream;
+  char* ws = (char*)workspace;
+  int32_t* n_open = (int32_t*)(ws + Ld.nopen);
+  hipLaunchKernelGGL(fill_words_kernel, dim3((S * B + 255) / 256), dim3(256), 0, s, block, S * B,
+                     -1);
+  if ((rc = launch_status("diffusion_block(fill)"))) return rc;
+  // every step reveals at least one position of every open block
+  int steps = 0, open = 1;
+  while (open && steps < B) {
+    rc = m->dtype == DVS_BF16
+             ? run_denoise<__bf16>(m, st, B, tau_c, block, n_open, chunk_keys, Ld, ws, nullptr,
+                                   nullptr, nullptr, s)
+             : run_denoise<float>(m, st, B, tau_c, block, n_open, chunk_keys, Ld, ws, nullptr,
+                                  nullptr, nullptr, s);
+    if (rc) return rc;
+    ++steps;
+    if (hipMemcpyAsync(&open, n_open, sizeof(int32_t), hipMemcpyDeviceToHost, s) != hipSuccess ||
+        hipStreamSynchronize(s) != hipSuccess) {
+      set_error("diffusion_block: reading the open-block count failed");
+      return DVS_EHIP;
+    }
+  }
+  if (open) {
+    set_error("diffusion_block: %d blocks still open after %d steps", open, steps);
+    return DVS_EHIP;
+  }
+  if (steps_out) *steps_out = steps;
+  return m->dtype == DVS_BF16 ? run_block_commit<__bf16>(m, st, B, block, chunk_keys, Lc, ws, s)
+                              : run_block_commit<float>(m, st, B, block, chunk_keys, Lc, ws, s);
 }

@@ -41,6 +41,10 @@ _SIGS = {
     "kv_commit_round": ([_c_int, _c_int, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_int,
                          _c_ptr, _c_ptr, _c_int, _c_ptr, _c_ptr, _c_int, _c_ptr, _c_ptr, _c_int,
                          _c_int, _c_ptr, _c_ptr, _c_ptr], _c_int),
+    "top1_confidence": ([_c_ptr, _c_int, _c_int, _c_int, _c_ptr, _c_ptr, _c_ptr, _c_ptr], _c_int),
+    "kv_commit_block": ([_c_int, _c_int, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_int, _c_ptr, _c_ptr,
+                         _c_int, _c_ptr, _c_ptr, _c_ptr, _c_int, _c_int, _c_ptr, _c_ptr, _c_ptr],
+                        _c_int),
 }
 
 class DvsLayer(ctypes.Structure):
@@ -73,6 +77,15 @@ _SIGS["draft_verify_step"] = ([ctypes.POINTER(DvsModel), ctypes.POINTER(DvsState
 
 _SIGS["literal_round"] = ([ctypes.POINTER(DvsModel), ctypes.POINTER(DvsState), _c_int, _c_int,
                            _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_size, _c_ptr], _c_int)
+
+_SIGS["dvs_diffusion_workspace_bytes"] = ([ctypes.POINTER(DvsModel), _c_int, _c_int, _c_int,
+                                           _c_int], _c_size)
+_SIGS["diffusion_denoise"] = ([ctypes.POINTER(DvsModel), ctypes.POINTER(DvsState), _c_int, _c_f32,
+                               _c_ptr, _c_ptr, _c_int, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_size,
+                               _c_ptr], _c_int)
+_SIGS["diffusion_block"] = ([ctypes.POINTER(DvsModel), ctypes.POINTER(DvsState), _c_int, _c_f32,
+                             _c_ptr, _c_int, ctypes.POINTER(ctypes.c_int32), _c_ptr, _c_size,
+                             _c_ptr], _c_int)
 
 _SIGS["dvs_prefill_workspace_bytes"] = ([ctypes.POINTER(DvsModel), _c_int, _c_int, _c_int, _c_int,
                                          _c_int], _c_size)
@@ -244,6 +257,28 @@ def argmax_accept(logits, n_causal: int, draft, argmax_out=None, accept_len=None
     return argmax_out, accept_len
 
 
+def top1_confidence(logits, argmax_out=None, conf_out=None, err=None, stream=None):
+    """logits [..., V] (f32/bf16) -> (top-1 [...] int32, softmax probability of it [...] f32)."""
+    if logits.device.type != "cuda" or not logits.is_contiguous():
+        raise DvsError("logits must be a contiguous device tensor")
+    lead, V = logits.shape[:-1], logits.shape[-1]
+    rows = int(np.prod(lead)) if len(lead) else 1
+    if argmax_out is None:
+        argmax_out = torch.empty(lead, dtype=torch.int32, device=logits.device)
+    if conf_out is None:
+        conf_out = torch.empty(lead, dtype=torch.float32, device=logits.device)
+    _dev(argmax_out, torch.int32, "argmax_out")
+    _dev(conf_out, torch.float32, "conf_out")
+    if argmax_out.numel() != rows or conf_out.numel() != rows:
+        raise DvsError("argmax_out / conf_out must have one entry per row")
+    if err is not None:
+        _dev(err, torch.int32, "err", 1)
+    rc = lib().top1_confidence(_ptr(logits), _dtype_code(logits), rows, V, _ptr(argmax_out),
+                               _ptr(conf_out), _ptr(err), _stream(stream))
+    _check(rc, "top1_confidence")
+    return argmax_out, conf_out
+
+
 # ---------------------------------------------------------------------------
 # commit / rollback over a device-resident decode state
 # ---------------------------------------------------------------------------
@@ -323,6 +358,26 @@ def kv_commit_round(st: DeviceState, B: int, lead, accept_len, argmax, eos_id: i
                                _ptr(st.out_tokens), _ptr(st.out_count), max_new, int(eos_id),
                                _ptr(st.finished), _ptr(st.err), _stream(stream))
     _check(rc, "kv_commit_round")
+
+
+def kv_commit_block(st: DeviceState, block, eos_id: int = -1, max_new: int | None = None,
+                    stream=None):
+    """Commit of one direct block-diffusion block: b_1..b_B (block [S, B])."""
+    S = st.kv_len.shape[0]
+    _dev(block, torch.int32, "block", 2)
+    if block.shape[0] != S:
+        raise DvsError("block must be [S, B]")
+    cap = st.out_tokens.shape[1]
+    max_new = cap if max_new is None else min(int(max_new), cap)
+    if max_new != cap:
+        raise DvsError("max_new must equal the out_tokens row length")
+    rc = lib().kv_commit_block(S, block.shape[1], _ptr(block), _ptr(st.kv_len),
+                               _ptr(st.page_table), _ptr(st.num_pages), st.max_pages,
+                               _ptr(st.free_stack), _ptr(st.free_top), st.pool_pages,
+                               _ptr(st.boundary), _ptr(st.out_tokens), _ptr(st.out_count),
+                               max_new, int(eos_id), _ptr(st.finished), _ptr(st.err),
+                               _stream(stream))
+    _check(rc, "kv_commit_block")
 
 
 # ---------------------------------------------------------------------------
@@ -429,6 +484,64 @@ def literal_round(model: DeviceModel, st: DeviceState, B: int, chunk_keys: int =
                              _ptr(logits_out), _ptr(argmax_out), _ptr(accept_out),
                              _ptr(model.ws.buf), model.ws.nbytes, _stream(stream))
     _check(rc, "literal_round")
+
+
+def diffusion_denoise(model: DeviceModel, st: DeviceState, block, tau_c: float, n_open=None,
+                      chunk_keys: int = 0, eos_id: int = -1, logits_out=None, argmax_out=None,
+                      conf_out=None, stream=None):
+    """One denoising forward of direct block diffusion and its reveal; block
+    [S, B] int32 (-1 = masked) is updated in place.  Returns n_open (a device
+    int32 [1]: live sequences whose block is still open)."""
+    S = st.kv_len.shape[0]
+    _dev(block, torch.int32, "block", 2)
+    B = block.shape[1]
+    if block.shape[0] != S:
+        raise DvsError("block must be [S, B]")
+    need = model.workspace_bytes(S, 1, B, st.max_pages, chunk_keys)
+    if need == 0:
+        raise DvsError("diffusion_denoise: invalid configuration")
+    if model.ws is None or model.ws.nbytes < need:
+        model.ws = Workspace(need, device=st.kv_len.device)
+    if n_open is None:
+        n_open = torch.empty(1, dtype=torch.int32, device=st.kv_len.device)
+    _dev(n_open, torch.int32, "n_open", 1)
+    for t, name, dt in ((logits_out, "logits_out", torch.float32),
+                        (argmax_out, "argmax_out", torch.int32), (conf_out, "conf_out", torch.float32)):
+        if t is not None:
+            _dev(t, dt, name)
+    sd = _state_desc(st, eos_id)
+    rc = lib().diffusion_denoise(ctypes.byref(model.desc), ctypes.byref(sd), int(B), float(tau_c),
+                                 _ptr(block), _ptr(n_open), int(chunk_keys), _ptr(logits_out),
+                                 _ptr(argmax_out), _ptr(conf_out), _ptr(model.ws.buf),
+                                 model.ws.nbytes, _stream(stream))
+    _check(rc, "diffusion_denoise")
+    return n_open
+
+
+def diffusion_block(model: DeviceModel, st: DeviceState, B: int, tau_c: float, block=None,
+                    chunk_keys: int = 0, eos_id: int = -1, stream=None):
+    """Decode and commit one block by direct block diffusion.  Returns
+    (block [S, B] int32, denoising forwards); the block cost one more
+    forward (the cache write)."""
+    S = st.kv_len.shape[0]
+    need = int(lib().dvs_diffusion_workspace_bytes(ctypes.byref(model.desc), S, int(B),
+                                                   st.max_pages, int(chunk_keys)))
+    if need == 0:
+        raise DvsError("diffusion_block: invalid configuration")
+    if model.ws is None or model.ws.nbytes < need:
+        model.ws = Workspace(need, device=st.kv_len.device)
+    if block is None:
+        block = torch.empty((S, B), dtype=torch.int32, device=st.kv_len.device)
+    _dev(block, torch.int32, "block", 2)
+    if tuple(block.shape) != (S, B):
+        raise DvsError("block must be [S, B]")
+    steps = ctypes.c_int32(0)
+    sd = _state_desc(st, eos_id)
+    rc = lib().diffusion_block(ctypes.byref(model.desc), ctypes.byref(sd), int(B), float(tau_c),
+                               _ptr(block), int(chunk_keys), ctypes.byref(steps),
+                               _ptr(model.ws.buf), model.ws.nbytes, _stream(stream))
+    _check(rc, "diffusion_block")
+    return block, int(steps.value)
 
 
 def prefill(model: DeviceModel, st: DeviceState, P: int, n_mask: int, prefix_tokens=None,
