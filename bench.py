@@ -120,12 +120,18 @@ def cpu_baseline(ai, li, n_seq: int):
     return tokens / dt, threads, desc, dt
 
 
+# confidence threshold of the direct block-diffusion figure (one of the
+# thresholds, 0.7 / 0.9 / 0.95 / 0.99, the paper reports its diffusion mode at)
+DIFFUSION_TAU_C = 0.9
+
+
 def run_decoder_stack(args):
     """The 16-layer bf16 decoder stack (hidden 1536, 16/4 heads, head_dim 96,
     SwiGLU 4096, vocab 65536; random weights): 8 sequences with 1024 vision
     embeddings + 64 prompt tokens are prefilled, then decoded with fused
-    self-speculative steps (B = 16) and, separately, with greedy AR steps and
-    with the paper's two-forward rounds (draft forward + verify forward).
+    self-speculative steps (B = 16) and, separately, with greedy AR steps,
+    with the paper's two-forward rounds (draft forward + verify forward) and
+    with direct block diffusion (one block of B per step).
     Reports end-to-end committed tokens/s of both (HIP events around the
     timed steps, prefill excluded) and, for the dominant cost, the HBM bytes a
     forward must move (all weights once, plus the KV cache read per layer)."""
@@ -152,13 +158,19 @@ def run_decoder_stack(args):
     wide.draft = np.zeros((wide.draft.shape[0], si.B), np.int32)
 
     def step(st, mode, nc, nm):
+        """One step of the mode; returns the forwards it ran."""
         if mode == "literal":
             dvs.literal_round(dm, st, si.B, chunk_keys=chunk)
-        else:
-            dvs.draft_verify_step(dm, st, nc, nm, chunk_keys=chunk)
+            return 2
+        if mode == "diffusion":
+            _, steps = dvs.diffusion_block(dm, st, si.B, DIFFUSION_TAU_C, chunk_keys=chunk)
+            return steps + 1
+        dvs.draft_verify_step(dm, st, nc, nm, chunk_keys=chunk)
+        return 1
 
-    for mode, (nc, nm) in (("fused", (si.B, si.B)), ("ar", (1, 0)), ("literal", (si.B + 1, 0))):
-        st = dvs.DeviceState(wide if mode == "literal" else si.state)
+    for mode, (nc, nm) in (("fused", (si.B, si.B)), ("ar", (1, 0)), ("literal", (si.B + 1, 0)),
+                           ("diffusion", (1, si.B))):
+        st = dvs.DeviceState(wide if mode in ("literal", "diffusion") else si.state)
         dvs.prefill(dm, st, si.P, si.B, prefix_tokens=torch.from_numpy(si.prefix_tokens()).cuda(),
                     x_prefix=torch.from_numpy(si.x_prefix()).cuda(), chunk_keys=chunk)
         for _ in range(args.warmup):
@@ -168,8 +180,9 @@ def run_decoder_stack(args):
         kv0 = int(st.kv_len.sum().item())
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record()
+        n_fwd = 0
         for _ in range(args.steps):
-            step(st, mode, nc, nm)
+            n_fwd += step(st, mode, nc, nm)
         e1.record()
         torch.cuda.synchronize()
         if int(st.err.item()):
@@ -178,12 +191,18 @@ def run_decoder_stack(args):
         ms = e0.elapsed_time(e1) / args.steps
         toks = int(st.out_count.sum().item()) - c0
         kv_mean = (kv0 + int(st.kv_len.sum().item())) / 2
-        fwd = 2 if mode == "literal" else 1          # forwards per step
+        fwd = n_fwd / args.steps                      # forwards per step
         step_bytes = fwd * (weight_bytes + kv_mean * w.n_layers * w.Hkv * w.D * 2 * 2)
         res[mode] = {"ms_per_step": round(ms, 4), "tokens_per_step": round(toks / args.steps, 3),
                      "tokens_per_s": round(toks / (ms * args.steps / 1e3), 1),
+                     "forwards_per_step": round(fwd, 3),
                      "hbm_bytes_per_step": int(step_bytes),
                      "hbm_gbs": round(step_bytes / (ms / 1e3) / 1e9, 1)}
+        if mode == "diffusion":
+            # the paper's diffusion TPF: tokens per sequence over the forwards
+            # that reveal tokens (the cache-write forwards excluded)
+            res[mode]["tokens_per_denoising_forward"] = round(
+                toks / st.kv_len.shape[0] / (n_fwd - args.steps), 3)
     f = res["fused"]
     line = {
         "metric": "committed tokens/sec per GPU, 16-layer decoder stack (self-speculative fused step)",
@@ -200,9 +219,12 @@ def run_decoder_stack(args):
                      "algorithmic_bytes": f["hbm_bytes_per_step"]},
         "ar": res["ar"],
         "two_forward_round": res["literal"],
+        "direct_diffusion": dict(res["diffusion"], tau_c=DIFFUSION_TAU_C),
         "note": "random weights accept almost no drafts, so the fused step commits about one "
                 "token per sequence and the two-forward round about two; their times are what a "
-                "trained model's step would cost",
+                "trained model's step would cost.  Direct diffusion: a step is one block of B "
+                "tokens; random weights are never confident, so a block reveals one position per "
+                "denoising forward (B + 1 forwards per block)",
         "input_gen_s": round(t_gen, 1),
     }
     print(json.dumps(line), flush=True)
