@@ -70,6 +70,14 @@ committed run at that token and ends the sequence (the output is cut at its
 first EOS, and no later block is generated).  ``kv_commit`` takes the block
 as the explicit run of each sequence (``block_runs``).
 
+Multi-step drafting (experiments, "Draft Schedule": a draft-side
+threshold tau_d sets how many denoising forwards build the draft) is the
+two-forward round with its draft refined like a diffusion block: the B + 1
+predictions of the draft window are revealed with ``reveal`` at tau_d, and
+revealed a0, d_1..d_{B-1} are fed back as the inputs of mask rows 1..B (a
+reading: d_B, predicted by the last row, has no input slot but is revealed
+like the others).  tau_d = 0 is the one-shot draft.
+
 Top-1 rule: the maximum logit wins; among equal maxima the lowest vocabulary
 index wins; -0.0 and +0.0 are equal.  Non-finite logits are an error.
 

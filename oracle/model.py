@@ -143,21 +143,45 @@ class OracleModel:
                              page_size=self.page_size)
         return logits, am, A, err
 
-    def literal_round(self, st, B: int, eos_id: int = -1, max_new=None):
+    def literal_round(self, st, B: int, eos_id: int = -1, max_new=None, tau_d=None):
         """The paper's two-forward round (appendix "Self-Speculative Decoding
         and KV-Cache Update"); see oracle.decode.  Pages must cover
         [L, L + B + 2).  Returns (draft logits, verify logits, verify top-1,
-        accept_len, err)."""
+        accept_len, err).
+
+        tau_d (experiments, "Draft Schedule"): the draft is refined over
+        several forwards instead of one.  The B + 1 predictions of the draft
+        window (a0 from the boundary row, d_j from mask row j) are revealed
+        like a diffusion block (``decode.reveal`` with threshold tau_d);
+        revealed a0, d_1..d_{B-1} replace the [M] inputs of mask rows 1..B in
+        the next draft forward (d_B has no input slot).  ``self.draft_steps``
+        records the draft forwards of the last call; tau_d = None is the
+        one-shot draft (one forward)."""
         S = st.kv_len.shape[0]
         live = st.finished == 0
-        # draft forward: [x0, [M] x B]; a0 from the boundary row, d_j from mask row j
-        tok = np.empty((S, B + 1), dtype=np.int64)
-        tok[:, 0] = st.boundary
-        tok[:, 1:] = self.mask_id
-        logits_d = self.forward(self.embed[tok], st, 1, B)
-        am_d = odec.top1_rows(logits_d)
-        a0 = am_d[:, 0].copy()
-        st.draft[live, :B] = am_d[live, 1:B + 1]
+        # draft forward(s): [x0, [M] x B] (revealed tokens in place of [M])
+        block = np.full((S, B + 1), -1, dtype=np.int64)
+        steps = 0
+        while True:
+            tok = np.empty((S, B + 1), dtype=np.int64)
+            tok[:, 0] = st.boundary
+            tok[:, 1:] = np.where(block[:, :B] < 0, self.mask_id, block[:, :B])
+            logits_d = self.forward(self.embed[tok], st, 1, B)
+            steps += 1
+            if tau_d is None:
+                block = odec.top1_rows(logits_d).astype(np.int64)
+                break
+            am = np.zeros((S, B + 1), dtype=np.int32)
+            conf = np.zeros((S, B + 1), dtype=np.float64)
+            for s in range(S):
+                for r in range(B + 1):
+                    am[s, r], conf[s, r] = odec.top1_confidence(logits_d[s, r])
+            block = odec.reveal(block, am, conf, tau_d, st.finished)
+            if not np.any((block < 0).any(axis=1) & live):
+                break
+        self.draft_steps = steps
+        a0 = block[:, 0].copy()
+        st.draft[live, :B] = block[live, 1:B + 1]
         st.kv_len[live] += 1                      # x0's causal KV is kept
         # verify forward: [a0, d_1..d_B] under causal attention from L + 1
         tok_v = np.empty((S, B + 1), dtype=np.int64)

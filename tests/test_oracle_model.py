@@ -207,3 +207,39 @@ def test_tpf_identity_against_printed_table():
     for row in g["rows"]:
         # the paper prints one decimal: the identity must agree to that digit
         assert abs((row["accepted"] + 2) / 2 - row["tpf"]) <= 0.05 + 1e-12, row
+
+
+@pytest.mark.parametrize("seed,B,tau_d", [(30, 4, 0.05), (31, 3, 0.3), (32, 6, 1.01)])
+def test_refined_draft_round_stream_equals_greedy_ar(seed, B, tau_d):
+    """Multi-step drafting (experiments, "Draft Schedule") changes only the
+    draft, so the committed stream is still greedy AR's; a refinement takes
+    1..B+1 draft forwards and reveals at least one prediction per forward."""
+    m, st = _prefilled(seed, B=B, n_causal=B + 1)
+    n = 24
+    ar = _ar_tokens(m, st, n)
+    ms, ss = _clone(m), st.copy()
+    while min(ss.out_count) < n + 1:
+        _, _, _, A, err = ms.literal_round(ss, B, tau_d=tau_d)
+        assert err == 0
+        assert 1 <= ms.draft_steps <= B + 1
+        if tau_d > 1:
+            assert ms.draft_steps == B + 1
+    for s in range(ss.kv_len.shape[0]):
+        got = list(ss.out_tokens[s, :ss.out_count[s]])
+        L = min(len(got), len(ar[s]))
+        assert got[:L] == ar[s][:L]
+
+
+def test_refined_draft_with_zero_threshold_is_one_shot():
+    B = 5
+    m, st = _prefilled(33, B=B, n_causal=B + 1)
+    a, sa = _clone(m), st.copy()
+    b, sb = _clone(m), st.copy()
+    for _ in range(3):
+        _, lv_a, _, A_a, _ = a.literal_round(sa, B)
+        _, lv_b, _, A_b, _ = b.literal_round(sb, B, tau_d=0.0)
+        assert b.draft_steps == 1
+        np.testing.assert_array_equal(A_a, A_b)
+        np.testing.assert_array_equal(lv_a, lv_b)
+        np.testing.assert_array_equal(sa.draft, sb.draft)
+        np.testing.assert_array_equal(sa.out_tokens, sb.out_tokens)
