@@ -375,6 +375,29 @@ int diffusion_block(const dvs_model* m, const dvs_state* st, int32_t B, float ta
                     size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
+ * literal_round_refined
+ *
+ * literal_round with a multi-step draft (experiments, "Draft Schedule": a
+ * draft-side confidence threshold tau_d sets how many denoising forwards
+ * build the draft).  The B + 1 predictions of the draft window [x0, b_1..b_B]
+ * (a0 from the boundary row, d_j from row j) are revealed like a diffusion
+ * block (the rule of diffusion_denoise, threshold tau_d); revealed a0,
+ * d_1..d_{B-1} replace the [M] inputs of rows 1..B in the next draft forward
+ * (d_B has no input slot).  When every live draft is complete (at most
+ * B + 1 forwards, each followed by a 4-byte device-to-host read and a stream
+ * synchronisation), the round continues as literal_round steps 2 and 3.
+ * tau_d = 0 gives the one-shot draft of literal_round.  *draft_steps_out
+ * (host, optional) = draft forwards; the round cost *draft_steps_out + 1
+ * forwards.  Arguments, page and output conventions as literal_round;
+ * workspace: the larger of dvs_step_workspace_bytes(m, S, 1, B, ...) and
+ * dvs_step_workspace_bytes(m, S, B + 1, 0, ...).
+ * ---------------------------------------------------------------------- */
+int literal_round_refined(const dvs_model* m, const dvs_state* st, int32_t B, float tau_d,
+                          int32_t chunk_keys, float* logits_out, int32_t* argmax_out,
+                          int32_t* accept_out, int32_t* draft_steps_out, void* workspace,
+                          size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
  * dvs_prefill
  *
  * Prefill of a fresh sequence (appendix item State: the first boundary token

@@ -37,12 +37,13 @@ template <typename T>
 __global__ void embed_rows_kernel(const T* __restrict__ embed, int H, int vocab, int R, int n_causal,
                                   const int32_t* __restrict__ boundary,
                                   const int32_t* __restrict__ draft, int draft_width,
-                                  const int32_t* __restrict__ block, float* __restrict__ x) {
+                                  const int32_t* __restrict__ block, int block_stride,
+                                  float* __restrict__ x) {
   const int mrow = blockIdx.x;
   const int s = mrow / R, r = mrow - s * R;
   int tok = vocab;  // [M]
   if (r < n_causal) tok = (r == 0) ? boundary[s] : draft[(size_t)s * draft_width + (r - 1)];
-  else if (block) tok = block[(size_t)s * (R - n_causal) + (r - n_causal)];  // -1: [M]
+  else if (block) tok = block[(size_t)s * block_stride + (r - n_causal)];  // -1: [M]
   if (tok < 0 || tok > vocab) tok = vocab;
   const T* e = embed + (size_t)tok * H;
   for (int i = threadIdx.x; i < H; i += blockDim.x) x[(size_t)mrow * H + i] = to_f(e[i]);
@@ -72,8 +73,10 @@ __global__ void round_draft_kernel(int S, int B, const int32_t* __restrict__ am,
 // position qualifies, the most confident masked one does (lowest position
 // among ties).  Revealed positions never change.  One 64-lane wave per
 // sequence, lane = position mod 64; a sequence whose block stays open adds
-// one to *n_open.  block: [S, B] (-1 = masked); am, conf: [S, B + 1].
-__global__ void __launch_bounds__(64) reveal_kernel(int B, float tau_c,
+// one to *n_open.  block: [S, B] (-1 = masked); am, conf: [S, R], R > B-1
+// (row p-1 predicts position p).  The refined draft of the two-forward round
+// uses B = R: its last prediction has no input slot.
+__global__ void __launch_bounds__(64) reveal_kernel(int B, int R, float tau_c,
                                                     const int32_t* __restrict__ am,
                                                     const float* __restrict__ conf,
                                                     const int32_t* __restrict__ finished,
@@ -82,8 +85,8 @@ __global__ void __launch_bounds__(64) reveal_kernel(int B, float tau_c,
   const int s = blockIdx.x, lane = threadIdx.x;
   if (finished[s]) return;
   int32_t* b = block + (size_t)s * B;
-  const int32_t* a = am + (size_t)s * (B + 1);
-  const float* c = conf + (size_t)s * (B + 1);
+  const int32_t* a = am + (size_t)s * R;
+  const float* c = conf + (size_t)s * R;
   constexpr int NONE = 0x7fffffff;
   int hits = 0, bp = NONE;
   float bc = 0.f;
@@ -613,7 +616,8 @@ __global__ void __launch_bounds__(256) gemm_f32_kernel(const float* __restrict__
 // host orchestration
 // ---------------------------------------------------------------------------
 struct StepLayout {
-  size_t x, h, hsel, q, k, v, att, gate, up, act, logits, am, conf, nopen, acc, lead, attn_ws, total,
+  size_t x, h, hsel, q, k, v, att, gate, up, act, logits, am, conf, nopen, blk, acc, lead, attn_ws,
+      total,
       attn_bytes,
       attn_counters, gemm_part, gemm_part_bytes, gemm_counters, n_gemm_counters;
 };
@@ -684,6 +688,7 @@ static StepLayout step_layout(const dvs_model* m, int S, int n_causal, int n_mas
   L.am = off; off += al(logit_rows * 4);
   L.conf = off; off += al(logit_rows * 4);
   L.nopen = off; off += al(4);
+  L.blk = off; off += al(M * 4);
   L.acc = off; off += al((size_t)S * 4);
   L.lead = off; off += al((size_t)S * 4);
   L.attn_bytes = dvs_attn_workspace_bytes(S, n_causal, n_mask, m->n_heads, m->n_kv_heads,
@@ -833,7 +838,7 @@ static int run_step(const dvs_model* m, const dvs_state* st, int n_causal, int n
   int32_t* acc = accept_out ? accept_out : (int32_t*)(ws + L.acc);
   hipLaunchKernelGGL(embed_rows_kernel<T>, dim3(M), dim3(256), 0, stream, (const T*)m->embed,
                      m->hidden, m->vocab, R, n_causal, st->boundary, st->draft, st->draft_width,
-                     nullptr, (float*)(ws + L.x));
+                     nullptr, 0, (float*)(ws + L.x));
   int rc;
   if ((rc = launch_status("draft_verify_step(embed)"))) return rc;
   if ((rc = forward_layers<T>(m, st, n_causal, n_mask, chunk_keys, L, ws, stream))) return rc;
@@ -865,7 +870,7 @@ static int run_round(const dvs_model* m, const dvs_state* st, int B, int chunk_k
   // draft forward
   hipLaunchKernelGGL(embed_rows_kernel<T>, dim3(M), dim3(256), 0, stream, (const T*)m->embed,
                      m->hidden, m->vocab, R, 1, st->boundary, st->draft, st->draft_width,
-                     nullptr, (float*)(ws + L.x));
+                     nullptr, 0, (float*)(ws + L.x));
   if ((rc = launch_status("literal_round(embed)"))) return rc;
   if ((rc = forward_layers<T>(m, st, 1, B, chunk_keys, L, ws, stream))) return rc;
   if ((rc = gemm(L, ws, m->dtype, ws + L.h, m->lm_head, M, m->vocab, m->hidden, logits, 1, 0, stream)))
@@ -878,7 +883,7 @@ static int run_round(const dvs_model* m, const dvs_state* st, int B, int chunk_k
   if ((rc = launch_status("literal_round(draft)"))) return rc;
   // verify forward
   hipLaunchKernelGGL(embed_rows_kernel<T>, dim3(M), dim3(256), 0, stream, (const T*)m->embed,
-                     m->hidden, m->vocab, R, R, lead, st->draft, st->draft_width, nullptr,
+                     m->hidden, m->vocab, R, R, lead, st->draft, st->draft_width, nullptr, 0,
                      (float*)(ws + L.x));
   if ((rc = launch_status("literal_round(embed)"))) return rc;
   if ((rc = forward_layers<T>(m, st, R, 0, chunk_keys, L, ws, stream))) return rc;
@@ -897,8 +902,10 @@ static int run_round(const dvs_model* m, const dvs_state* st, int B, int chunk_k
 // boundary row causal and the block rows bidirectional (masked positions
 // carry [M]); top-1 and confidence of every row; the reveal.  kv_len is
 // unchanged (the window's K/V slots are rewritten by the next forward).
+// npos: block positions, B (direct diffusion) or B + 1 (the refined draft of
+// the two-forward round, whose last prediction has no input slot).
 template <typename T>
-static int run_denoise(const dvs_model* m, const dvs_state* st, int B, float tau_c,
+static int run_denoise(const dvs_model* m, const dvs_state* st, int B, int npos, float tau_c,
                        int32_t* block, int32_t* n_open, int chunk_keys, const StepLayout& L,
                        char* ws, float* logits_out, int32_t* argmax_out, float* conf_out,
                        hipStream_t stream) {
@@ -908,7 +915,7 @@ static int run_denoise(const dvs_model* m, const dvs_state* st, int B, float tau
   float* conf = conf_out ? conf_out : (float*)(ws + L.conf);
   hipLaunchKernelGGL(embed_rows_kernel<T>, dim3(M), dim3(256), 0, stream, (const T*)m->embed,
                      m->hidden, m->vocab, R, 1, st->boundary, st->draft, st->draft_width, block,
-                     (float*)(ws + L.x));
+                     npos, (float*)(ws + L.x));
   int rc;
   if ((rc = launch_status("diffusion_denoise(embed)"))) return rc;
   if ((rc = forward_layers<T>(m, st, 1, B, chunk_keys, L, ws, stream))) return rc;
@@ -916,7 +923,7 @@ static int run_denoise(const dvs_model* m, const dvs_state* st, int B, float tau
     return rc;
   if ((rc = top1_confidence(logits, DVS_F32, M, m->vocab, am, conf, st->err_word, stream))) return rc;
   hipLaunchKernelGGL(zero_words_kernel, dim3(1), dim3(256), 0, stream, n_open, 1);
-  hipLaunchKernelGGL(reveal_kernel, dim3(S), dim3(64), 0, stream, B, tau_c, am, conf,
+  hipLaunchKernelGGL(reveal_kernel, dim3(S), dim3(64), 0, stream, npos, R, tau_c, am, conf,
                      st->finished, block, n_open);
   return launch_status("diffusion_denoise(reveal)");
 }
@@ -928,7 +935,7 @@ static int run_block_commit(const dvs_model* m, const dvs_state* st, int B, cons
                             int chunk_keys, const StepLayout& L, char* ws, hipStream_t stream) {
   const int S = st->S, M = S * B;
   hipLaunchKernelGGL(embed_rows_kernel<T>, dim3(M), dim3(256), 0, stream, (const T*)m->embed,
-                     m->hidden, m->vocab, B, B, st->boundary, block, B, nullptr,
+                     m->hidden, m->vocab, B, B, st->boundary, block, B, nullptr, 0,
                      (float*)(ws + L.x));
   int rc;
   if ((rc = launch_status("diffusion_block(embed)"))) return rc;
@@ -937,6 +944,64 @@ static int run_block_commit(const dvs_model* m, const dvs_state* st, int B, cons
                          st->free_stack, st->free_top, st->num_pool_pages, st->boundary,
                          st->out_tokens, st->out_count, st->max_new, st->eos_id, st->finished,
                          st->err_word, stream);
+}
+
+// The two-forward round with a refined draft: draft forwards over
+// [x0, b_1..b_B] until every one of the B + 1 predictions (a0, d_1..d_B) is
+// revealed at threshold tau_d (b_p: revealed prediction p, else [M]); then
+// the verify forward and commit of run_round.  Ld and Lv (layouts of the
+// (1, B) and (B + 1, 0) windows) agree below the attention workspace, where
+// the block and the lead tokens live.
+template <typename T>
+static int run_round_refined(const dvs_model* m, const dvs_state* st, int B, float tau_d,
+                             int chunk_keys, const StepLayout& Ld, const StepLayout& Lv, char* ws,
+                             float* logits_out, int32_t* argmax_out, int32_t* accept_out,
+                             int* draft_steps, hipStream_t stream) {
+  const int S = st->S, R = B + 1, M = S * R;
+  int32_t* blk = (int32_t*)(ws + Ld.blk);
+  int32_t* n_open = (int32_t*)(ws + Ld.nopen);
+  int32_t* lead = (int32_t*)(ws + Lv.lead);
+  hipLaunchKernelGGL(fill_words_kernel, dim3((M + 255) / 256), dim3(256), 0, stream, blk, M, -1);
+  int rc;
+  if ((rc = launch_status("literal_round_refined(fill)"))) return rc;
+  int steps = 0, open = 1;
+  while (open && steps < R) {
+    if ((rc = run_denoise<T>(m, st, B, R, tau_d, blk, n_open, chunk_keys, Ld, ws, nullptr, nullptr,
+                             nullptr, stream)))
+      return rc;
+    ++steps;
+    if (hipMemcpyAsync(&open, n_open, sizeof(int32_t), hipMemcpyDeviceToHost, stream) != hipSuccess ||
+        hipStreamSynchronize(stream) != hipSuccess) {
+      set_error("literal_round_refined: reading the open-draft count failed");
+      return DVS_EHIP;
+    }
+  }
+  if (open) {
+    set_error("literal_round_refined: %d drafts still open after %d forwards", open, steps);
+    return DVS_EHIP;
+  }
+  if (draft_steps) *draft_steps = steps;
+  hipLaunchKernelGGL(round_draft_kernel, dim3((S + 255) / 256), dim3(256), 0, stream, S, B, blk,
+                     st->finished, st->kv_len, lead, st->draft, st->draft_width);
+  if ((rc = launch_status("literal_round_refined(draft)"))) return rc;
+  float* logits = logits_out ? logits_out : (float*)(ws + Lv.logits);
+  int32_t* am = argmax_out ? argmax_out : (int32_t*)(ws + Lv.am);
+  int32_t* acc = accept_out ? accept_out : (int32_t*)(ws + Lv.acc);
+  hipLaunchKernelGGL(embed_rows_kernel<T>, dim3(M), dim3(256), 0, stream, (const T*)m->embed,
+                     m->hidden, m->vocab, R, R, lead, st->draft, st->draft_width, nullptr, 0,
+                     (float*)(ws + Lv.x));
+  if ((rc = launch_status("literal_round_refined(embed)"))) return rc;
+  if ((rc = forward_layers<T>(m, st, R, 0, chunk_keys, Lv, ws, stream))) return rc;
+  if ((rc = gemm(Lv, ws, m->dtype, ws + Lv.h, m->lm_head, M, m->vocab, m->hidden, logits, 1, 0,
+                 stream)))
+    return rc;
+  rc = argmax_accept(logits, DVS_F32, S, R, m->vocab, R, st->draft, st->draft_width, am, acc,
+                     st->err_word, stream);
+  if (rc) return rc;
+  return kv_commit_round(S, B, lead, acc, am, st->kv_len, st->page_table, st->num_pages,
+                         st->max_pages, st->free_stack, st->free_top, st->num_pool_pages,
+                         st->boundary, st->draft, st->draft_width, st->out_tokens, st->out_count,
+                         st->max_new, st->eos_id, st->finished, st->err_word, stream);
 }
 
 template <typename T>
@@ -1124,9 +1189,9 @@ extern "C" int diffusion_denoise(const dvs_model* m, const dvs_state* st, int32_
   }
   hipStream_t s = (hipStream_t)stream;
   if (m->dtype == DVS_BF16)
-    return run_denoise<__bf16>(m, st, B, tau_c, block, n_open, chunk_keys, L, (char*)workspace,
-                               logits_out, argmax_out, conf_out, s);
-  return run_denoise<float>(m, st, B, tau_c, block, n_open, chunk_keys, L, (char*)workspace,
+    return run_denoise<__bf16>(m, st, B, B, tau_c, block, n_open, chunk_keys, L,
+                               (char*)workspace, logits_out, argmax_out, conf_out, s);
+  return run_denoise<float>(m, st, B, B, tau_c, block, n_open, chunk_keys, L, (char*)workspace,
                             logits_out, argmax_out, conf_out, s);
 }
 
@@ -1155,9 +1220,9 @@ extern "C" int diffusion_block(const dvs_model* m, const dvs_state* st, int32_t 
   int steps = 0, open = 1;
   while (open && steps < B) {
     rc = m->dtype == DVS_BF16
-             ? run_denoise<__bf16>(m, st, B, tau_c, block, n_open, chunk_keys, Ld, ws, nullptr,
+             ? run_denoise<__bf16>(m, st, B, B, tau_c, block, n_open, chunk_keys, Ld, ws, nullptr,
                                    nullptr, nullptr, s)
-             : run_denoise<float>(m, st, B, tau_c, block, n_open, chunk_keys, Ld, ws, nullptr,
+             : run_denoise<float>(m, st, B, B, tau_c, block, n_open, chunk_keys, Ld, ws, nullptr,
                                   nullptr, nullptr, s);
     if (rc) return rc;
     ++steps;
@@ -1174,4 +1239,33 @@ extern "C" int diffusion_block(const dvs_model* m, const dvs_state* st, int32_t 
   if (steps_out) *steps_out = steps;
   return m->dtype == DVS_BF16 ? run_block_commit<__bf16>(m, st, B, block, chunk_keys, Lc, ws, s)
                               : run_block_commit<float>(m, st, B, block, chunk_keys, Lc, ws, s);
+}
+
+extern "C" int literal_round_refined(const dvs_model* m, const dvs_state* st, int32_t B,
+                                     float tau_d, int32_t chunk_keys, float* logits_out,
+                                     int32_t* argmax_out, int32_t* accept_out,
+                                     int32_t* draft_steps_out, void* workspace, size_t ws_bytes,
+                                     void* stream) {
+  clear_error();
+  int rc = check_model_state(m, st, "literal_round_refined");
+  if (rc) return rc;
+  DVS_CHECK_ARG(B >= 1, "literal_round_refined: need B >= 1");
+  DVS_CHECK_ARG(st->draft && st->draft_width >= B, "literal_round_refined: draft narrower than B");
+  const int S = st->S;
+  const StepLayout Ld = step_layout(m, S, 1, B, st->max_pages, chunk_keys, (size_t)S * (B + 1));
+  const StepLayout Lv = step_layout(m, S, B + 1, 0, st->max_pages, chunk_keys, (size_t)S * (B + 1));
+  const size_t need = std::max(Ld.total, Lv.total);
+  if (!workspace || ws_bytes < need) {
+    set_error("literal_round_refined: workspace needs %zu bytes, got %zu", need, ws_bytes);
+    return DVS_EWORKSPACE;
+  }
+  int steps = 0;
+  hipStream_t s = (hipStream_t)stream;
+  rc = m->dtype == DVS_BF16
+           ? run_round_refined<__bf16>(m, st, B, tau_d, chunk_keys, Ld, Lv, (char*)workspace,
+                                       logits_out, argmax_out, accept_out, &steps, s)
+           : run_round_refined<float>(m, st, B, tau_d, chunk_keys, Ld, Lv, (char*)workspace,
+                                      logits_out, argmax_out, accept_out, &steps, s);
+  if (draft_steps_out) *draft_steps_out = steps;
+  return rc;
 }

@@ -87,6 +87,10 @@ _SIGS["diffusion_block"] = ([ctypes.POINTER(DvsModel), ctypes.POINTER(DvsState),
                              _c_ptr, _c_int, ctypes.POINTER(ctypes.c_int32), _c_ptr, _c_size,
                              _c_ptr], _c_int)
 
+_SIGS["literal_round_refined"] = ([ctypes.POINTER(DvsModel), ctypes.POINTER(DvsState), _c_int,
+                                   _c_f32, _c_int, _c_ptr, _c_ptr, _c_ptr,
+                                   ctypes.POINTER(ctypes.c_int32), _c_ptr, _c_size, _c_ptr], _c_int)
+
 _SIGS["dvs_prefill_workspace_bytes"] = ([ctypes.POINTER(DvsModel), _c_int, _c_int, _c_int, _c_int,
                                          _c_int], _c_size)
 _SIGS["dvs_prefill"] = ([ctypes.POINTER(DvsModel), ctypes.POINTER(DvsState), _c_int, _c_int, _c_ptr,
@@ -484,6 +488,31 @@ def literal_round(model: DeviceModel, st: DeviceState, B: int, chunk_keys: int =
                              _ptr(logits_out), _ptr(argmax_out), _ptr(accept_out),
                              _ptr(model.ws.buf), model.ws.nbytes, _stream(stream))
     _check(rc, "literal_round")
+
+
+def literal_round_refined(model: DeviceModel, st: DeviceState, B: int, tau_d: float,
+                          chunk_keys: int = 0, eos_id: int = -1, logits_out=None, argmax_out=None,
+                          accept_out=None, stream=None) -> int:
+    """The two-forward round with its draft refined at threshold tau_d over
+    several draft forwards; returns the number of draft forwards."""
+    S = st.kv_len.shape[0]
+    need = max(model.workspace_bytes(S, 1, B, st.max_pages, chunk_keys),
+               model.workspace_bytes(S, B + 1, 0, st.max_pages, chunk_keys))
+    if need == 0:
+        raise DvsError("literal_round_refined: invalid configuration")
+    if model.ws is None or model.ws.nbytes < need:
+        model.ws = Workspace(need, device=st.kv_len.device)
+    for t, name in ((logits_out, "logits_out"), (argmax_out, "argmax_out"), (accept_out, "accept_out")):
+        if t is not None:
+            _dev(t, torch.float32 if name == "logits_out" else torch.int32, name)
+    steps = ctypes.c_int32(0)
+    sd = _state_desc(st, eos_id)
+    rc = lib().literal_round_refined(ctypes.byref(model.desc), ctypes.byref(sd), int(B),
+                                     float(tau_d), int(chunk_keys), _ptr(logits_out),
+                                     _ptr(argmax_out), _ptr(accept_out), ctypes.byref(steps),
+                                     _ptr(model.ws.buf), model.ws.nbytes, _stream(stream))
+    _check(rc, "literal_round_refined")
+    return int(steps.value)
 
 
 def diffusion_denoise(model: DeviceModel, st: DeviceState, block, tau_c: float, n_open=None,

@@ -188,3 +188,83 @@ def test_block_commit_rejects_open_block():
     torch.cuda.synchronize()
     assert int(st.err.item()) & 16
     _states_equal(st, host)
+
+
+def _top2_margin_ok(logits):
+    srt = np.sort(logits, axis=-1)
+    return bool(np.all(srt[..., -1] - srt[..., -2] > 4 * LOGIT_TOL_F32 * np.abs(logits).max(axis=-1)))
+
+
+def test_refined_draft_round_matches_oracle(monkeypatch):
+    """literal_round_refined (multi-step drafting) against the oracle's round
+    with the same tau_d: draft forwards, drafts and the committed state.
+    Every reveal decision of the oracle is recorded to check its margin."""
+    B = 6
+    margin = [np.inf]
+    reveal = od.reveal
+
+    def recording_reveal(block, am, conf, tau_c, finished):
+        for s in range(block.shape[0]):
+            m = conf[s][block[s] < 0]
+            if finished[s] or not m.size:
+                continue
+            margin[0] = min(margin[0], float(np.min(np.abs(m - tau_c))))
+            if np.all(m <= tau_c) and m.size > 1:
+                t2 = np.sort(m)[-2:]
+                margin[0] = min(margin[0], float(t2[1] - t2[0]) + float(t2[1] == t2[0]))
+        return reveal(block, am, conf, tau_c, finished)
+
+    monkeypatch.setattr(od, "reveal", recording_reveal)
+    w, host, kps, vps = _model_and_state("f32", B, seed=15)
+    host.draft = np.zeros((host.kv_len.shape[0], B), np.int32)
+    om = OracleModel(w, kps, vps)
+    probe = OracleModel(w, kps, vps)
+    lg0 = probe.forward(probe.embed[np.concatenate(
+        [host.boundary[:, None], np.full((host.kv_len.shape[0], B), probe.mask_id)], 1)],
+        host.copy(), 1, B)
+    c = np.sort([od.top1_confidence(r)[1] for r in lg0.reshape(-1, w.V)])
+    i = int(0.5 * len(c))
+    tau = float(np.float32(0.5 * (c[i] + c[i + 1])))
+    dm = dvs.DeviceModel(w, _dev_pools(kps, "f32"), _dev_pools(vps, "f32"), "f32")
+    st = dvs.DeviceState(host)
+    ref = host.copy()
+    for rnd in range(2):
+        lg_d, lg_v, _, _, err = om.literal_round(ref, B, tau_d=tau)
+        assert err == 0
+        assert _top2_margin_ok(lg_d) and _top2_margin_ok(lg_v)
+        steps = dvs.literal_round_refined(dm, st, B, tau)
+        torch.cuda.synchronize()
+        assert int(st.err.item()) == 0
+        print(f"[round {rnd}] tau_d={tau:.4g} draft forwards gpu {steps} oracle {om.draft_steps}")
+        assert steps == om.draft_steps
+        _states_equal(st, ref)
+    print(f"[margin] smallest reveal margin {margin[0]:.3e}")
+    assert margin[0] > 1e-4 * tau
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_refined_draft_round_equals_greedy_ar_on_gpu(dtype):
+    B, N, CH, TAU = 8, 32, 64, 0.05
+    w, host, kps, vps = _model_and_state(dtype, B)
+    host.draft = np.zeros((host.kv_len.shape[0], B), np.int32)
+    ar_m = dvs.DeviceModel(w, _dev_pools(kps, dtype), _dev_pools(vps, dtype), dtype)
+    ar_st = dvs.DeviceState(host)
+    for _ in range(N):
+        dvs.draft_verify_step(ar_m, ar_st, 1, 0, chunk_keys=CH)
+    rm = dvs.DeviceModel(w, _dev_pools(kps, dtype), _dev_pools(vps, dtype), dtype)
+    rs = dvs.DeviceState(host)
+    rounds, multi = 0, 0
+    while int(rs.out_count.min().item()) < N:
+        steps = dvs.literal_round_refined(rm, rs, B, TAU, chunk_keys=CH)
+        assert 1 <= steps <= B + 1
+        multi += steps > 1
+        rounds += 1
+        assert rounds <= N
+    torch.cuda.synchronize()
+    assert int(ar_st.err.item()) == 0 and int(rs.err.item()) == 0
+    ar, rr = ar_st.to_host(host), rs.to_host(host)
+    for s in range(host.kv_len.shape[0]):
+        n = min(int(rr.out_count[s]), int(ar.out_count[s]))
+        assert n >= N
+        np.testing.assert_array_equal(rr.out_tokens[s, :n], ar.out_tokens[s, :n])
+    assert multi >= 1
