@@ -120,8 +120,9 @@ def cpu_baseline(ai, li, n_seq: int):
     return tokens / dt, threads, desc, dt
 
 
-# confidence threshold of the direct block-diffusion figure (one of the
-# thresholds, 0.7 / 0.9 / 0.95 / 0.99, the paper reports its diffusion mode at)
+# confidence threshold of the direct block-diffusion and refined-draft figures
+# (one of the thresholds, 0.7 / 0.9 / 0.95 / 0.99, the paper reports its
+# diffusion mode at)
 DIFFUSION_TAU_C = 0.9
 
 
@@ -130,8 +131,9 @@ def run_decoder_stack(args):
     SwiGLU 4096, vocab 65536; random weights): 8 sequences with 1024 vision
     embeddings + 64 prompt tokens are prefilled, then decoded with fused
     self-speculative steps (B = 16) and, separately, with greedy AR steps,
-    with the paper's two-forward rounds (draft forward + verify forward) and
-    with direct block diffusion (one block of B per step).
+    with the paper's two-forward rounds (draft forward + verify forward), the
+    same rounds with a multi-step draft (threshold tau_d) and with direct
+    block diffusion (one block of B per step).
     Reports end-to-end committed tokens/s of both (HIP events around the
     timed steps, prefill excluded) and, for the dominant cost, the HBM bytes a
     forward must move (all weights once, plus the KV cache read per layer)."""
@@ -165,12 +167,14 @@ def run_decoder_stack(args):
         if mode == "diffusion":
             _, steps = dvs.diffusion_block(dm, st, si.B, DIFFUSION_TAU_C, chunk_keys=chunk)
             return steps + 1
+        if mode == "refined":
+            return dvs.literal_round_refined(dm, st, si.B, DIFFUSION_TAU_C, chunk_keys=chunk) + 1
         dvs.draft_verify_step(dm, st, nc, nm, chunk_keys=chunk)
         return 1
 
     for mode, (nc, nm) in (("fused", (si.B, si.B)), ("ar", (1, 0)), ("literal", (si.B + 1, 0)),
-                           ("diffusion", (1, si.B))):
-        st = dvs.DeviceState(wide if mode in ("literal", "diffusion") else si.state)
+                           ("diffusion", (1, si.B)), ("refined", (si.B + 1, 0))):
+        st = dvs.DeviceState(wide if mode in ("literal", "diffusion", "refined") else si.state)
         dvs.prefill(dm, st, si.P, si.B, prefix_tokens=torch.from_numpy(si.prefix_tokens()).cuda(),
                     x_prefix=torch.from_numpy(si.x_prefix()).cuda(), chunk_keys=chunk)
         for _ in range(args.warmup):
@@ -220,11 +224,13 @@ def run_decoder_stack(args):
         "ar": res["ar"],
         "two_forward_round": res["literal"],
         "direct_diffusion": dict(res["diffusion"], tau_c=DIFFUSION_TAU_C),
+        "refined_draft_round": dict(res["refined"], tau_d=DIFFUSION_TAU_C),
         "note": "random weights accept almost no drafts, so the fused step commits about one "
                 "token per sequence and the two-forward round about two; their times are what a "
                 "trained model's step would cost.  Direct diffusion: a step is one block of B "
                 "tokens; random weights are never confident, so a block reveals one position per "
-                "denoising forward (B + 1 forwards per block)",
+                "denoising forward (B + 1 forwards per block), and a refined draft takes B + 1 draft "
+                "forwards",
         "input_gen_s": round(t_gen, 1),
     }
     print(json.dumps(line), flush=True)

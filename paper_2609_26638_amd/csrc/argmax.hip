@@ -132,12 +132,15 @@ __global__ void __launch_bounds__(256) argmax_kernel(const void* __restrict__ lo
 // pass over the row: every thread keeps its first maximum m and the sum
 // sum_i exp(x_i - m) of what it has read, rescaled when m grows; the threads
 // then merge (m, sum, index) pairs, the lowest index among equal maxima.
-// conf = 1 / sum.  fp32 arithmetic; one workgroup per row.
+// conf = 1 / sum.  fp32 arithmetic; one workgroup per row, 16-byte loads
+// with UNR in flight per thread as in argmax_kernel.
 template <bool BF16>
 __global__ void __launch_bounds__(256) top1_conf_kernel(const void* __restrict__ logits, int V,
                                                         int32_t* __restrict__ argmax_out,
                                                         float* __restrict__ conf_out,
                                                         int32_t* err) {
+  constexpr int EPV = BF16 ? 8 : 4;   // elements per 16-byte vector
+  constexpr int UNR = 8;              // vectors in flight per thread
   __shared__ float sm[4], ss[4];
   __shared__ int si[4];
   const size_t row = blockIdx.x;
@@ -145,18 +148,63 @@ __global__ void __launch_bounds__(256) top1_conf_kernel(const void* __restrict__
   const char* base = (const char*)logits + row * (size_t)V * (BF16 ? 2 : 4);
   float m = -INFINITY, sum = 0.f, nf = 0.f;
   int bi = 0x7fffffff;
-  for (int i = tid; i < V; i += 256) {
-    const float f = BF16 ? __uint_as_float((uint32_t)((const uint16_t*)base)[i] << 16)
-                         : ((const float*)base)[i];
+  // elementwise update, in increasing index order per thread
+  auto visit = [&](float f, int i) {
     nf = fmaf(f, 0.f, nf);
     if (f > m) {
-      sum = sum * __expf(m - f) + 1.f;
+      sum = (m == -INFINITY ? 0.f : sum * __expf(m - f)) + 1.f;
       m = f;
       bi = i;
-    } else {
+    } else if (m != -INFINITY) {
       sum += __expf(f - m);
     }
+  };
+  // vectorised body (16-byte aligned rows): per batch of UNR vectors, the
+  // batch maximum first (one rescale of the running sum per batch), then the
+  // batch's terms
+  const bool aligned = ((((uintptr_t)base) & 15) == 0);
+  const int nvec = aligned ? V / EPV : 0;
+  int v0 = 0;
+  for (; v0 + UNR * 256 <= nvec; v0 += UNR * 256) {
+    u32x4 buf[UNR];
+#pragma unroll
+    for (int u = 0; u < UNR; ++u) buf[u] = ((const u32x4*)base)[v0 + u * 256 + tid];
+    float bm = -INFINITY;
+#pragma unroll
+    for (int u = 0; u < UNR; ++u)
+#pragma unroll
+      for (int e = 0; e < EPV; ++e) {
+        const float x = elem_f<BF16>(buf[u], e);
+        bm = fmaxf(bm, x);
+        nf = fmaf(x, 0.f, nf);
+      }
+    if (bm > m) {
+      int at = 0x7fffffff;
+#pragma unroll
+      for (int u = UNR - 1; u >= 0; --u)
+#pragma unroll
+        for (int e = EPV - 1; e >= 0; --e)
+          if (elem_f<BF16>(buf[u], e) == bm) at = (v0 + u * 256 + tid) * EPV + e;
+      sum = m == -INFINITY ? 0.f : sum * __expf(m - bm);
+      m = bm;
+      bi = at;
+    }
+    if (m != -INFINITY) {
+#pragma unroll
+      for (int u = 0; u < UNR; ++u)
+#pragma unroll
+        for (int e = 0; e < EPV; ++e) sum += __expf(elem_f<BF16>(buf[u], e) - m);
+    }
   }
+  for (int vi = v0 + tid; vi < nvec; vi += 256) {
+    const u32x4 x = ((const u32x4*)base)[vi];
+#pragma unroll
+    for (int e = 0; e < EPV; ++e) visit(elem_f<BF16>(x, e), vi * EPV + e);
+  }
+  for (int i = nvec * EPV + tid; i < V; i += 256)
+    visit(BF16 ? __uint_as_float((uint32_t)((const uint16_t*)base)[i] << 16)
+               : ((const float*)base)[i],
+          i);
   // wave merge
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) {
