@@ -196,12 +196,35 @@ def run_decoder_stack(args):
         toks = int(st.out_count.sum().item()) - c0
         kv_mean = (kv0 + int(st.kv_len.sum().item())) / 2
         fwd = n_fwd / args.steps                      # forwards per step
+        graph = None
+        if mode in ("fused", "ar", "literal"):
+            # the same step captured once into a HIP graph and replayed (its
+            # inputs are all in device memory, so a replay is the next step)
+            g = dvs.capture(lambda: step(st, mode, nc, nm))
+            g.replay()
+            torch.cuda.synchronize()
+            gc0 = int(st.out_count.sum().item())
+            e0.record()
+            for _ in range(args.steps):
+                g.replay()
+            e1.record()
+            torch.cuda.synchronize()
+            if int(st.err.item()):
+                print(json.dumps({"error": f"device error word {int(st.err.item())}"}))
+                sys.exit(1)
+            gms = e0.elapsed_time(e1) / args.steps
+            gtoks = int(st.out_count.sum().item()) - gc0
+            graph = {"ms_per_step": round(gms, 4),
+                     "tokens_per_s": round(gtoks / (gms * args.steps / 1e3), 1)}
+            del g
         step_bytes = fwd * (weight_bytes + kv_mean * w.n_layers * w.Hkv * w.D * 2 * 2)
         res[mode] = {"ms_per_step": round(ms, 4), "tokens_per_step": round(toks / args.steps, 3),
                      "tokens_per_s": round(toks / (ms * args.steps / 1e3), 1),
                      "forwards_per_step": round(fwd, 3),
                      "hbm_bytes_per_step": int(step_bytes),
                      "hbm_gbs": round(step_bytes / (ms / 1e3) / 1e9, 1)}
+        if graph is not None:
+            res[mode]["hip_graph"] = graph
         if mode == "diffusion":
             # the paper's diffusion TPF: tokens per sequence over the forwards
             # that reveal tokens (the cache-write forwards excluded)
@@ -221,6 +244,7 @@ def run_decoder_stack(args):
                      "frac": round(f["hbm_gbs"] / HBM_PEAK_GBS, 4), "traffic": None,
                      "kernel": "whole fused step (weights once + KV per layer)",
                      "algorithmic_bytes": f["hbm_bytes_per_step"]},
+        "fused_hip_graph": res["fused"].get("hip_graph"),
         "ar": res["ar"],
         "two_forward_round": res["literal"],
         "direct_diffusion": dict(res["diffusion"], tau_c=DIFFUSION_TAU_C),

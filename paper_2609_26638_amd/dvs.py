@@ -490,6 +490,23 @@ def literal_round(model: DeviceModel, st: DeviceState, B: int, chunk_keys: int =
     _check(rc, "literal_round")
 
 
+def capture(fn) -> "torch.cuda.CUDAGraph":
+    """Record the launches of ``fn`` (calls of this module that only enqueue:
+    draft_verify_step, literal_round, attn_hybrid_block, argmax_accept, the
+    commits; not diffusion_block or literal_round_refined, which read a count
+    back from the device) into a HIP graph.  ``replay()`` re-runs them on the
+    buffers' current contents: every input of a step (kv_len, pages, boundary,
+    draft, ...) is read from device memory, so a replay is the next step.
+    The library clears its counters with kernels, never with a memset node.
+    Workspaces must be allocated before the capture (one eager call does it)
+    and must not be replaced (by a call needing a larger one) while the
+    graph is replayed."""
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        fn()
+    return g
+
+
 def literal_round_refined(model: DeviceModel, st: DeviceState, B: int, tau_d: float,
                           chunk_keys: int = 0, eos_id: int = -1, logits_out=None, argmax_out=None,
                           accept_out=None, stream=None) -> int:
