@@ -78,6 +78,21 @@ revealed a0, d_1..d_{B-1} are fed back as the inputs of mask rows 1..B (a
 reading: d_B, predicted by the last row, has no input slot but is revealed
 like the others).  tau_d = 0 is the one-shot draft.
 
+Stochastic acceptance
+---------------------
+Under sampling, the draft is accepted by the standard acceptance-rejection
+rule of speculative decoding, which keeps the committed tokens distributed
+as the verifier's own samples (Preliminaries, "Speculative Decoding"; the
+rule is that of Leviathan et al. 2023 and Chen et al. 2023).  For the
+two-forward round at temperature T: p_j = softmax(z_j / T) of verify row
+j-1 and q_j = softmax of draft row j; a0 is sampled from the boundary row
+(the verifier's own distribution), d_j from q_j; d_j is accepted while
+``u_j * q_j(d_j) < p_j(d_j)`` (probability min(1, p/q)); at the first
+rejection the token is sampled from ``max(0, p_j - q_j)`` (normalised), and
+after B acceptances from p_{B+1}.  Every random number is an input.
+Sampling from weights w with a uniform u takes the smallest index whose
+running sum (index order) exceeds ``u * sum(w)``.
+
 Top-1 rule: the maximum logit wins; among equal maxima the lowest vocabulary
 index wins; -0.0 and +0.0 are equal.  Non-finite logits are an error.
 
@@ -162,6 +177,37 @@ def reveal(block: np.ndarray, am: np.ndarray, conf: np.ndarray, tau_c: float,
         for p in chosen:
             out[s, p] = am[s, p]
     return out
+
+
+def softmax_t(z: np.ndarray, T: float) -> np.ndarray:
+    """softmax(z / T) of one row, float64."""
+    z = np.asarray(z, dtype=np.float64)
+    w = np.exp((z - z.max()) / T)
+    return w / w.sum()
+
+
+def sample_index(w: np.ndarray, u: float) -> int:
+    """Inverse-CDF sample: the smallest i with w_0 + ... + w_i > u * sum(w)
+    (w >= 0, not all zero; 0 <= u < 1)."""
+    c = np.cumsum(np.asarray(w, dtype=np.float64))
+    i = int(np.searchsorted(c, u * c[-1], side="right"))
+    return min(i, len(c) - 1)
+
+
+def stochastic_accept(p: np.ndarray, q: np.ndarray, d: np.ndarray, u_acc: np.ndarray) -> int:
+    """A = number of leading drafts accepted: d_j (j = 1..B) is accepted
+    while u_acc[j-1] * q[j-1, d_j] < p[j-1, d_j].  p, q: [B, V]."""
+    A = 0
+    for j in range(len(d)):
+        if not (u_acc[j] * q[j, d[j]] < p[j, d[j]]):
+            break
+        A = j + 1
+    return A
+
+
+def resample_weights(p: np.ndarray, q: np.ndarray | None) -> np.ndarray:
+    """max(0, p - q) after a rejection, p itself after full acceptance."""
+    return p.copy() if q is None else np.maximum(p - q, 0.0)
 
 
 def accept_length(a: np.ndarray, d: np.ndarray) -> int:

@@ -194,6 +194,43 @@ class OracleModel:
                              page_size=self.page_size, lead=a0, window=B + 2)
         return logits_d, logits_v, am_v, A, err
 
+    def sampled_round(self, st, B: int, T: float, u: np.ndarray, eos_id: int = -1,
+                      max_new=None):
+        """The two-forward round under sampling at temperature T with the
+        standard acceptance-rejection rule (see oracle.decode).  u [S, 2B + 2]
+        uniforms: u[:, 0] samples a0, u[:, j] samples d_j (j = 1..B),
+        u[:, B + j] tests d_j, u[:, 2B + 1] samples the final token.  Pages
+        must cover [L, L + B + 2).  Returns (draft logits, verify logits, A,
+        final tokens, err)."""
+        S = st.kv_len.shape[0]
+        live = st.finished == 0
+        tok = np.empty((S, B + 1), dtype=np.int64)
+        tok[:, 0] = st.boundary
+        tok[:, 1:] = self.mask_id
+        logits_d = self.forward(self.embed[tok], st, 1, B)
+        q = np.array([[odec.softmax_t(logits_d[s, r], T) for r in range(B + 1)] for s in range(S)])
+        drafted = np.array([[odec.sample_index(q[s, r], u[s, r]) for r in range(B + 1)]
+                            for s in range(S)], dtype=np.int64)
+        a0 = drafted[:, 0].copy()
+        st.draft[live, :B] = drafted[live, 1:]
+        st.kv_len[live] += 1
+        tok_v = np.empty((S, B + 1), dtype=np.int64)
+        tok_v[:, 0] = a0
+        tok_v[:, 1:] = st.draft[:, :B]
+        logits_v = self.forward(self.embed[tok_v], st, B + 1, 0)
+        A = np.zeros(S, dtype=np.int32)
+        final = np.zeros(S, dtype=np.int32)
+        am = np.zeros((S, B + 1), dtype=np.int32)
+        for s in range(S):
+            p = np.array([odec.softmax_t(logits_v[s, r], T) for r in range(B + 1)])
+            A[s] = odec.stochastic_accept(p[:B], q[s, 1:], st.draft[s, :B], u[s, B + 1:2 * B + 1])
+            w = odec.resample_weights(p[A[s]], None if A[s] == B else q[s, A[s] + 1])
+            final[s] = odec.sample_index(w, u[s, 2 * B + 1])
+            am[s, A[s]] = final[s]
+        err = odec.kv_commit(st, A, am, B + 1, 0, eos_id=eos_id, max_new=max_new,
+                             page_size=self.page_size, lead=a0, window=B + 2)
+        return logits_d, logits_v, A, final, err
+
     def diffusion_denoise(self, st, block: np.ndarray, tau_c: float):
         """One denoising forward over [x0, b_1..b_B] (1 causal row, B block
         rows; -1 = [M]) and its reveal.  kv_len is unchanged.  Returns
