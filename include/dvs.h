@@ -398,6 +398,34 @@ int literal_round_refined(const dvs_model* m, const dvs_state* st, int32_t B, fl
                           size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
+ * literal_round_sampled / dvs_sampled_round_workspace_bytes
+ *
+ * literal_round under sampling at temperature T, with the standard
+ * acceptance-rejection rule of speculative decoding, which keeps the
+ * committed tokens distributed as the verifier's own samples (Preliminaries,
+ * "Speculative Decoding").  Each row's distribution is softmax(z / T) (fp32).
+ *   1. draft forward over [x0, [M] x B]: a0 is sampled from the boundary
+ *      row with u[s, 0] (the verifier's own distribution at L + 1) and d_j
+ *      from mask row j (q_j) with u[s, j], j = 1..B; x0's KV is kept;
+ *   2. verify forward over [a0, d_1..d_B]: p_j from row j-1;
+ *   3. d_j is accepted while u[s, B + j] * q_j(d_j) < p_j(d_j); A = number
+ *      accepted; the final token is sampled with u[s, 2B + 1] from
+ *      max(0, p_{A+1} - q_{A+1}) (normalised) if A < B, else from p_{B+1};
+ *      kv_commit_round commits a0, d_1..d_A and the final token.
+ * Sampling from weights w with uniform u takes the smallest index whose
+ * running sum (index order) exceeds u * sum(w).
+ *   u [S, 2B + 2] fp32 uniforms in [0, 1) (device, read; the caller draws
+ *   them); temperature > 0.  logits_out [S*(B+1), vocab] (verify logits) and
+ *   accept_out [S] are optional.  Pages as literal_round.  workspace:
+ *   dvs_sampled_round_workspace_bytes(m, S, B, max_pages, chunk_keys).
+ * ---------------------------------------------------------------------- */
+size_t dvs_sampled_round_workspace_bytes(const dvs_model* m, int32_t S, int32_t B,
+                                         int32_t max_pages, int32_t chunk_keys);
+int literal_round_sampled(const dvs_model* m, const dvs_state* st, int32_t B, float temperature,
+                          const float* u, int32_t chunk_keys, float* logits_out,
+                          int32_t* accept_out, void* workspace, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
  * dvs_prefill
  *
  * Prefill of a fresh sequence (appendix item State: the first boundary token

@@ -31,6 +31,16 @@ void clear_error();
 // Launch status after hipLaunchKernelGGL.
 int launch_status(const char* what);
 
+// Sampled two-forward round (sample.hip).
+int launch_row_stats(const float* logits, int rows, int V, float invT, float2* stats,
+                     int32_t* err, hipStream_t st);
+int launch_sample_rows(const float* logits, const float2* stats, int V, float invT,
+                       const float* u, int u_stride, int S, int R, int32_t* tok, hipStream_t st);
+int launch_accept_final(int S, int B, int V, float invT, const float* zv, const float2* sv,
+                        const float* zd, const float2* sd, const int32_t* draft, int draft_width,
+                        const float* u, int u_stride, int32_t* accept_len, int32_t* am,
+                        hipStream_t st);
+
 // Bytes at the start of an attention workspace that hold the split-merge
 // counters (zero between calls) for the given call shape.
 size_t attn_counter_bytes(int S, int R, int Hq, int Hkv, int D, int max_pages, int chunk_keys,

@@ -1004,6 +1004,55 @@ static int run_round_refined(const dvs_model* m, const dvs_state* st, int B, flo
                          st->max_new, st->eos_id, st->finished, st->err_word, stream);
 }
 
+// The two-forward round under sampling at temperature T (stochastic
+// acceptance): the draft forward's rows are sampled (a0 from the boundary
+// row, d_j from mask row j) with u[s, 0..B]; the verify forward's rows give
+// p_j; acceptance and the final sample use u[s, B+1..2B+1].  Draft logits and
+// both rows' statistics live past the larger of the two forwards' layouts.
+template <typename T>
+static int run_round_sampled(const dvs_model* m, const dvs_state* st, int B, float T_,
+                             const float* u, int chunk_keys, const StepLayout& Ld,
+                             const StepLayout& Lv, size_t extra, char* ws, float* logits_out,
+                             int32_t* accept_out, hipStream_t stream) {
+  const int S = st->S, R = B + 1, M = S * R, V = m->vocab, us = 2 * B + 2;
+  const float invT = 1.f / T_;
+  float* zd = (float*)(ws + extra);
+  float2* sd = (float2*)(ws + extra + al((size_t)M * V * 4));
+  float2* sv = sd + M;
+  float* zv = logits_out ? logits_out : (float*)(ws + Lv.logits);
+  int32_t* tok = (int32_t*)(ws + Lv.am);
+  int32_t* acc = accept_out ? accept_out : (int32_t*)(ws + Lv.acc);
+  int32_t* lead = (int32_t*)(ws + Lv.lead);
+  int rc;
+  hipLaunchKernelGGL(embed_rows_kernel<T>, dim3(M), dim3(256), 0, stream, (const T*)m->embed,
+                     m->hidden, V, R, 1, st->boundary, st->draft, st->draft_width, nullptr, 0,
+                     (float*)(ws + Ld.x));
+  if ((rc = launch_status("literal_round_sampled(embed)"))) return rc;
+  if ((rc = forward_layers<T>(m, st, 1, B, chunk_keys, Ld, ws, stream))) return rc;
+  if ((rc = gemm(Ld, ws, m->dtype, ws + Ld.h, m->lm_head, M, V, m->hidden, zd, 1, 0, stream)))
+    return rc;
+  if ((rc = launch_row_stats(zd, M, V, invT, sd, st->err_word, stream))) return rc;
+  if ((rc = launch_sample_rows(zd, sd, V, invT, u, us, S, R, tok, stream))) return rc;
+  hipLaunchKernelGGL(round_draft_kernel, dim3((S + 255) / 256), dim3(256), 0, stream, S, B, tok,
+                     st->finished, st->kv_len, lead, st->draft, st->draft_width);
+  if ((rc = launch_status("literal_round_sampled(draft)"))) return rc;
+  hipLaunchKernelGGL(embed_rows_kernel<T>, dim3(M), dim3(256), 0, stream, (const T*)m->embed,
+                     m->hidden, V, R, R, lead, st->draft, st->draft_width, nullptr, 0,
+                     (float*)(ws + Lv.x));
+  if ((rc = launch_status("literal_round_sampled(embed)"))) return rc;
+  if ((rc = forward_layers<T>(m, st, R, 0, chunk_keys, Lv, ws, stream))) return rc;
+  if ((rc = gemm(Lv, ws, m->dtype, ws + Lv.h, m->lm_head, M, V, m->hidden, zv, 1, 0, stream)))
+    return rc;
+  if ((rc = launch_row_stats(zv, M, V, invT, sv, st->err_word, stream))) return rc;
+  if ((rc = launch_accept_final(S, B, V, invT, zv, sv, zd, sd, st->draft, st->draft_width, u, us,
+                                acc, tok, stream)))
+    return rc;
+  return kv_commit_round(S, B, lead, acc, tok, st->kv_len, st->page_table, st->num_pages,
+                         st->max_pages, st->free_stack, st->free_top, st->num_pool_pages,
+                         st->boundary, st->draft, st->draft_width, st->out_tokens, st->out_count,
+                         st->max_new, st->eos_id, st->finished, st->err_word, stream);
+}
+
 template <typename T>
 static int run_prefill(const dvs_model* m, const dvs_state* st, int P, int n_mask,
                        const int32_t* tokens, const float* x_prefix, int chunk_keys,
@@ -1268,4 +1317,48 @@ extern "C" int literal_round_refined(const dvs_model* m, const dvs_state* st, in
                                       logits_out, argmax_out, accept_out, &steps, s);
   if (draft_steps_out) *draft_steps_out = steps;
   return rc;
+}
+
+// Workspace of the sampled round: the larger of the two forwards' layouts,
+// then the draft logits [S(B+1), V] fp32 and two [S(B+1)] float2 statistics.
+static size_t sampled_extra(const dvs_model* m, int S, int B, int max_pages, int chunk_keys,
+                            StepLayout* Ld, StepLayout* Lv) {
+  *Ld = step_layout(m, S, 1, B, max_pages, chunk_keys, (size_t)S * (B + 1));
+  *Lv = step_layout(m, S, B + 1, 0, max_pages, chunk_keys, (size_t)S * (B + 1));
+  return al(std::max(Ld->total, Lv->total));
+}
+
+extern "C" size_t dvs_sampled_round_workspace_bytes(const dvs_model* m, int32_t S, int32_t B,
+                                                    int32_t max_pages, int32_t chunk_keys) {
+  if (!model_ok(m) || S < 1 || B < 1 || max_pages < 1) return 0;
+  StepLayout Ld, Lv;
+  const size_t M = (size_t)S * (B + 1);
+  return sampled_extra(m, S, B, max_pages, chunk_keys, &Ld, &Lv) + al(M * m->vocab * 4) +
+         2 * al(M * 8);
+}
+
+extern "C" int literal_round_sampled(const dvs_model* m, const dvs_state* st, int32_t B,
+                                     float temperature, const float* u, int32_t chunk_keys,
+                                     float* logits_out, int32_t* accept_out, void* workspace,
+                                     size_t ws_bytes, void* stream) {
+  clear_error();
+  int rc = check_model_state(m, st, "literal_round_sampled");
+  if (rc) return rc;
+  DVS_CHECK_ARG(B >= 1 && u, "literal_round_sampled: need B >= 1 and uniforms");
+  DVS_CHECK_ARG(temperature > 0.f && temperature < 1e30f,
+                "literal_round_sampled: temperature must be positive and finite");
+  DVS_CHECK_ARG(st->draft && st->draft_width >= B, "literal_round_sampled: draft narrower than B");
+  const size_t need = dvs_sampled_round_workspace_bytes(m, st->S, B, st->max_pages, chunk_keys);
+  if (!workspace || ws_bytes < need) {
+    set_error("literal_round_sampled: workspace needs %zu bytes, got %zu", need, ws_bytes);
+    return DVS_EWORKSPACE;
+  }
+  StepLayout Ld, Lv;
+  const size_t extra = sampled_extra(m, st->S, B, st->max_pages, chunk_keys, &Ld, &Lv);
+  hipStream_t s = (hipStream_t)stream;
+  return m->dtype == DVS_BF16
+             ? run_round_sampled<__bf16>(m, st, B, temperature, u, chunk_keys, Ld, Lv, extra,
+                                         (char*)workspace, logits_out, accept_out, s)
+             : run_round_sampled<float>(m, st, B, temperature, u, chunk_keys, Ld, Lv, extra,
+                                        (char*)workspace, logits_out, accept_out, s);
 }

@@ -91,6 +91,12 @@ _SIGS["literal_round_refined"] = ([ctypes.POINTER(DvsModel), ctypes.POINTER(DvsS
                                    _c_f32, _c_int, _c_ptr, _c_ptr, _c_ptr,
                                    ctypes.POINTER(ctypes.c_int32), _c_ptr, _c_size, _c_ptr], _c_int)
 
+_SIGS["dvs_sampled_round_workspace_bytes"] = ([ctypes.POINTER(DvsModel), _c_int, _c_int, _c_int,
+                                               _c_int], _c_size)
+_SIGS["literal_round_sampled"] = ([ctypes.POINTER(DvsModel), ctypes.POINTER(DvsState), _c_int,
+                                   _c_f32, _c_ptr, _c_int, _c_ptr, _c_ptr, _c_ptr, _c_size,
+                                   _c_ptr], _c_int)
+
 _SIGS["dvs_prefill_workspace_bytes"] = ([ctypes.POINTER(DvsModel), _c_int, _c_int, _c_int, _c_int,
                                          _c_int], _c_size)
 _SIGS["dvs_prefill"] = ([ctypes.POINTER(DvsModel), ctypes.POINTER(DvsState), _c_int, _c_int, _c_ptr,
@@ -530,6 +536,33 @@ def literal_round_refined(model: DeviceModel, st: DeviceState, B: int, tau_d: fl
                                      _ptr(model.ws.buf), model.ws.nbytes, _stream(stream))
     _check(rc, "literal_round_refined")
     return int(steps.value)
+
+
+def literal_round_sampled(model: DeviceModel, st: DeviceState, B: int, temperature: float, u,
+                          chunk_keys: int = 0, eos_id: int = -1, logits_out=None,
+                          accept_out=None, stream=None):
+    """The two-forward round under sampling (stochastic acceptance); u is a
+    device float32 [S, 2B + 2] of uniforms in [0, 1)."""
+    S = st.kv_len.shape[0]
+    _dev(u, torch.float32, "u", 2)
+    if tuple(u.shape) != (S, 2 * B + 2):
+        raise DvsError("u must be [S, 2B + 2]")
+    need = int(lib().dvs_sampled_round_workspace_bytes(ctypes.byref(model.desc), S, int(B),
+                                                       st.max_pages, int(chunk_keys)))
+    if need == 0:
+        raise DvsError("literal_round_sampled: invalid configuration")
+    if model.ws is None or model.ws.nbytes < need:
+        model.ws = Workspace(need, device=st.kv_len.device)
+    if logits_out is not None:
+        _dev(logits_out, torch.float32, "logits_out")
+    if accept_out is not None:
+        _dev(accept_out, torch.int32, "accept_out", 1)
+    sd = _state_desc(st, eos_id)
+    rc = lib().literal_round_sampled(ctypes.byref(model.desc), ctypes.byref(sd), int(B),
+                                     float(temperature), _ptr(u), int(chunk_keys),
+                                     _ptr(logits_out), _ptr(accept_out), _ptr(model.ws.buf),
+                                     model.ws.nbytes, _stream(stream))
+    _check(rc, "literal_round_sampled")
 
 
 def diffusion_denoise(model: DeviceModel, st: DeviceState, block, tau_c: float, n_open=None,
