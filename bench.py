@@ -126,14 +126,20 @@ def cpu_baseline(ai, li, n_seq: int):
 DIFFUSION_TAU_C = 0.9
 
 
+# temperature of the sampled-round figure (stochastic acceptance)
+SAMPLING_T = 1.0
+
+
 def run_decoder_stack(args):
     """The 16-layer bf16 decoder stack (hidden 1536, 16/4 heads, head_dim 96,
     SwiGLU 4096, vocab 65536; random weights): 8 sequences with 1024 vision
     embeddings + 64 prompt tokens are prefilled, then decoded with fused
     self-speculative steps (B = 16) and, separately, with greedy AR steps,
     with the paper's two-forward rounds (draft forward + verify forward), the
-    same rounds with a multi-step draft (threshold tau_d) and with direct
-    block diffusion (one block of B per step).
+    same rounds with a multi-step draft (threshold tau_d), the same rounds
+    under sampling with stochastic acceptance (T = 1, uniforms drawn on the
+    device inside the timed loop) and with direct block diffusion (one block
+    of B per step).
     Reports end-to-end committed tokens/s of both (HIP events around the
     timed steps, prefill excluded) and, for the dominant cost, the HBM bytes a
     forward must move (all weights once, plus the KV cache read per layer)."""
@@ -155,6 +161,8 @@ def run_decoder_stack(args):
     mats = w.wq + w.wk + w.wv + w.wo + w.w_gate + w.w_up + w.w_down + [w.lm_head]
     weight_bytes = sum(int(np.prod(a.shape)) * 2 for a in mats)
     res = {}
+    # uniforms of the sampled round, drawn on the device per round
+    gen = torch.Generator(device="cuda").manual_seed(0)
     # the two-forward round keeps d_1..d_B in the draft array
     wide = si.state.copy()
     wide.draft = np.zeros((wide.draft.shape[0], si.B), np.int32)
@@ -169,12 +177,18 @@ def run_decoder_stack(args):
             return steps + 1
         if mode == "refined":
             return dvs.literal_round_refined(dm, st, si.B, DIFFUSION_TAU_C, chunk_keys=chunk) + 1
+        if mode == "sampled":
+            u = torch.rand((st.kv_len.shape[0], 2 * si.B + 2), device="cuda", generator=gen)
+            dvs.literal_round_sampled(dm, st, si.B, SAMPLING_T, u, chunk_keys=chunk)
+            return 2
         dvs.draft_verify_step(dm, st, nc, nm, chunk_keys=chunk)
         return 1
 
     for mode, (nc, nm) in (("fused", (si.B, si.B)), ("ar", (1, 0)), ("literal", (si.B + 1, 0)),
-                           ("diffusion", (1, si.B)), ("refined", (si.B + 1, 0))):
-        st = dvs.DeviceState(wide if mode in ("literal", "diffusion", "refined") else si.state)
+                           ("diffusion", (1, si.B)), ("refined", (si.B + 1, 0)),
+                           ("sampled", (si.B + 1, 0))):
+        st = dvs.DeviceState(wide if mode in ("literal", "diffusion", "refined", "sampled")
+                             else si.state)
         dvs.prefill(dm, st, si.P, si.B, prefix_tokens=torch.from_numpy(si.prefix_tokens()).cuda(),
                     x_prefix=torch.from_numpy(si.x_prefix()).cuda(), chunk_keys=chunk)
         for _ in range(args.warmup):
@@ -249,6 +263,7 @@ def run_decoder_stack(args):
         "two_forward_round": res["literal"],
         "direct_diffusion": dict(res["diffusion"], tau_c=DIFFUSION_TAU_C),
         "refined_draft_round": dict(res["refined"], tau_d=DIFFUSION_TAU_C),
+        "sampled_round": dict(res["sampled"], temperature=SAMPLING_T),
         "note": "random weights accept almost no drafts, so the fused step commits about one "
                 "token per sequence and the two-forward round about two; their times are what a "
                 "trained model's step would cost.  Direct diffusion: a step is one block of B "
