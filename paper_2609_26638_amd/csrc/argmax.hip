@@ -11,10 +11,11 @@
 // Acceptance (method "Self-Speculative Decoding"; appendix item Accept):
 // a_j = top1(row j-1); A = longest prefix of the draft with d_j == a_j.
 //
-// The argmax is a pure HBM stream: one workgroup per row, 16-byte loads with
-// 16 in flight per thread (8 read 3.4% slower, 32 twice as slow), about two
-// vector instructions per element (max3 chain, NaN/infinity probe),
-// wavefront shuffles, then LDS across waves.
+// The argmax is a pure HBM stream: one workgroup of 512 threads per row,
+// 16-byte loads with 8 in flight per thread (interleaved A/B: 256 threads
+// with 8 or 16 in flight read 5% / 2% slower, 512 with 16 17% slower), about
+// two vector instructions per element (max3 chain, NaN/infinity probe),
+// wavefront shuffles, then LDS across the eight waves.
 #include "dvs_common.h"
 
 namespace dvs {
@@ -47,12 +48,12 @@ __device__ __forceinline__ float elem_f(const u32x4& x, int e) {
 }
 
 template <bool BF16>
-__global__ void __launch_bounds__(256) argmax_kernel(const void* __restrict__ logits, int V,
+__global__ void __launch_bounds__(512) argmax_kernel(const void* __restrict__ logits, int V,
                                                      int32_t* __restrict__ argmax_out,
                                                      int32_t* err) {
   constexpr int EPV = BF16 ? 8 : 4;   // elements per 16-byte vector
-  constexpr int UNR = 16;             // vectors in flight per thread
-  __shared__ uint64_t sred[4];
+  constexpr int UNR = 8;              // vectors in flight per thread
+  __shared__ uint64_t sred[8];
   const size_t row = blockIdx.x;
   const int tid = threadIdx.x;
   const char* base = (const char*)logits + row * (size_t)V * (BF16 ? 2 : 4);
@@ -70,10 +71,10 @@ __global__ void __launch_bounds__(256) argmax_kernel(const void* __restrict__ lo
   const bool aligned = ((((uintptr_t)base) & 15) == 0);
   const int nvec = aligned ? V / EPV : 0;
   int v0 = 0;
-  for (; v0 + UNR * 256 <= nvec; v0 += UNR * 256) {
+  for (; v0 + UNR * 512 <= nvec; v0 += UNR * 512) {
     u32x4 buf[UNR];
 #pragma unroll
-    for (int u = 0; u < UNR; ++u) buf[u] = ((const u32x4*)base)[v0 + u * 256 + tid];
+    for (int u = 0; u < UNR; ++u) buf[u] = ((const u32x4*)base)[v0 + u * 512 + tid];
     float bm = -INFINITY;
 #pragma unroll
     for (int u = 0; u < UNR; ++u)
@@ -89,12 +90,12 @@ __global__ void __launch_bounds__(256) argmax_kernel(const void* __restrict__ lo
       for (int u = UNR - 1; u >= 0; --u)
 #pragma unroll
         for (int e = EPV - 1; e >= 0; --e)
-          if (elem_f<BF16>(buf[u], e) == bm) at = (v0 + u * 256 + tid) * EPV + e;
+          if (elem_f<BF16>(buf[u], e) == bm) at = (v0 + u * 512 + tid) * EPV + e;
       best = bm;
       bi = at;
     }
   }
-  for (int vi = v0 + tid; vi < nvec; vi += 256) {
+  for (int vi = v0 + tid; vi < nvec; vi += 512) {
     const u32x4 x = ((const u32x4*)base)[vi];
 #pragma unroll
     for (int e = 0; e < EPV; ++e) {
@@ -104,7 +105,7 @@ __global__ void __launch_bounds__(256) argmax_kernel(const void* __restrict__ lo
     }
   }
   // scalar tail (and the whole row when unaligned)
-  for (int i = nvec * EPV + tid; i < V; i += 256) {
+  for (int i = nvec * EPV + tid; i < V; i += 512) {
     const float f = BF16 ? __uint_as_float((uint32_t)((const uint16_t*)base)[i] << 16)
                          : ((const float*)base)[i];
     nf = fmaf(f, 0.f, nf);
@@ -123,7 +124,7 @@ __global__ void __launch_bounds__(256) argmax_kernel(const void* __restrict__ lo
   __syncthreads();
   if (tid == 0) {
     uint64_t b = sred[0];
-    for (int i = 1; i < 4; ++i) b = sred[i] > b ? sred[i] : b;
+    for (int i = 1; i < 8; ++i) b = sred[i] > b ? sred[i] : b;
     argmax_out[row] = 0x7fffffff - (int)(uint32_t)(b & 0xffffffffu);
   }
 }
@@ -287,10 +288,10 @@ extern "C" int argmax_accept(const void* logits, int32_t dtype, int32_t S, int32
   DVS_CHECK_SUPPORTED(rows < (1LL << 31), "argmax_accept: too many rows");
   hipStream_t st = (hipStream_t)stream;
   if (dtype == DVS_BF16)
-    hipLaunchKernelGGL(argmax_kernel<true>, dim3((unsigned)rows), dim3(256), 0, st, logits, V,
+    hipLaunchKernelGGL(argmax_kernel<true>, dim3((unsigned)rows), dim3(512), 0, st, logits, V,
                        argmax_out, err_word);
   else
-    hipLaunchKernelGGL(argmax_kernel<false>, dim3((unsigned)rows), dim3(256), 0, st, logits, V,
+    hipLaunchKernelGGL(argmax_kernel<false>, dim3((unsigned)rows), dim3(512), 0, st, logits, V,
                        argmax_out, err_word);
   int rc = launch_status("argmax_accept(argmax)");
   if (rc) return rc;
