@@ -308,7 +308,7 @@ class ModelWeights:
     wk: list
     wv: list
     wo: list
-    g_attn: list                  # RMSNorm gains (unit)
+    g_attn: list                  # RMSNorm gains, N(1, gain_std)
     g_mlp: list
     w_gate: list
     w_up: list
@@ -324,7 +324,8 @@ class ModelWeights:
 
 
 def make_model_weights(seed: int, V: int, H: int, Hq: int, Hkv: int, D: int,
-                       n_layers: int, ffn: int, std: float = 0.02) -> ModelWeights:
+                       n_layers: int, ffn: int, std: float = 0.02,
+                       gain_std: float = 0.1) -> ModelWeights:
     ss = np.random.SeedSequence([seed, 0x3E16])
     rngs = [np.random.Generator(np.random.PCG64(c)) for c in ss.spawn(4 + 7 * n_layers)]
     it = iter(rngs)
@@ -346,12 +347,18 @@ def make_model_weights(seed: int, V: int, H: int, Hq: int, Hkv: int, D: int,
             for _ in range(3):
                 next(it)
     lm = _normal(next(it), (H, V), std)
-    ones = [np.ones(H, np.float32) for _ in range(n_layers)]
+    # RMSNorm gains: N(1, gain_std) per element (a trained model's gains are
+    # not all one; distinct gains make a swapped or dropped gain visible).
+    gss = np.random.SeedSequence([seed, 0x6A1E])
+    g_rng = [np.random.Generator(np.random.PCG64(c)) for c in gss.spawn(2 * n_layers + 1)]
+    g_attn = [_normal(g_rng[2 * l], (H,), gain_std, mean=1.0) for l in range(n_layers)]
+    g_mlp = [_normal(g_rng[2 * l + 1], (H,), gain_std, mean=1.0) for l in range(n_layers)]
+    g_final = _normal(g_rng[-1], (H,), gain_std, mean=1.0)
     return ModelWeights(V=V, H=H, Hq=Hq, Hkv=Hkv, D=D, n_layers=n_layers, ffn=ffn,
                         embed=emb, wq=wq, wk=wk, wv=wv, wo=wo,
-                        g_attn=ones, g_mlp=[o.copy() for o in ones],
+                        g_attn=g_attn, g_mlp=g_mlp,
                         w_gate=wg, w_up=wu, w_down=wd,
-                        g_final=np.ones(H, np.float32), lm_head=lm)
+                        g_final=g_final, lm_head=lm)
 
 
 # ----------------------------------------------------------------------------
