@@ -53,6 +53,17 @@ constexpr int BAL_MAX_SEGS = 9;        // balanced mode: segments per item (boun
 constexpr int BAL_MAX_SEQS = 1024;     // balanced mode: sequences per call
 constexpr float RESCALE_LOG2 = 8.f;
 
+// Partial slot of segment k of a split item whose segment 0 is held by
+// workgroup wg0.  Aligned chunks: one slot per (item, chunk).  Balanced
+// shares: an item's segments sit in consecutive workgroups, and a workgroup
+// holds at most two segments of split items -- the continuation of an item
+// begun earlier (its first segment, k > 0) and the start of an item that runs
+// on past its share (its last segment, k == 0) -- so two slots per
+// workgroup suffice, whatever the length mix.
+__device__ __forceinline__ size_t part_slot(int balanced, int it, int max_segs, int wg0, int k) {
+  return balanced ? (size_t)(wg0 + k) * 2 + (k == 0 ? 1 : 0) : (size_t)it * max_segs + k;
+}
+
 struct AttnParams {
   const void* q;
   const void* k_new;
@@ -701,7 +712,8 @@ __global__ void __launch_bounds__(NW * 64, 1) attn_bf16_kernel(AttnParams p) {
     // Publish the partial with write-through (agent-coherent) stores, wait for
     // them, then count in; the workgroup that completes the item merges with
     // coherent loads.  No L2-wide write-back or invalidate is needed.
-    const size_t slot = (size_t)it * p.max_segs + k;
+    const int wg0 = (int)blockIdx.x - k;
+    const size_t slot = part_slot(p.balanced, it, p.max_segs, wg0, k);
     {
       float* po = p.part_o + slot * (size_t)(NT * NREG);
       float* pml = p.part_ml + slot * (size_t)(NT * 2);
@@ -716,13 +728,15 @@ __global__ void __launch_bounds__(NW * 64, 1) attn_bf16_kernel(AttnParams p) {
     }
     wait_vmcnt<0>();
     __syncthreads();
+    // The count-in is a release (the partials written by every thread of the
+    // workgroup, ordered before it by the barrier, become visible at agent
+    // scope first) and an acquire (the last workgroup's loads below see every
+    // other workgroup's partials; the barrier extends it to all its threads).
     if (tid == 0)
-      s_flag[0] = (__hip_atomic_fetch_add(&p.counters[it], 1, __ATOMIC_RELAXED,
+      s_flag[0] = (__hip_atomic_fetch_add(&p.counters[it], 1, __ATOMIC_ACQ_REL,
                                           __HIP_MEMORY_SCOPE_AGENT) == nseg - 1);
     __syncthreads();
     if (!s_flag[0]) continue;
-    const float* pob = p.part_o + (size_t)it * p.max_segs * (NT * NREG);
-    const float* pmlb = p.part_ml + (size_t)it * p.max_segs * (NT * 2);
     // Partials are read with coherent loads; every batch is issued in full
     // before any of it is used, so the loads overlap instead of each one
     // waiting for the previous.
@@ -731,8 +745,8 @@ __global__ void __launch_bounds__(NW * 64, 1) attn_bf16_kernel(AttnParams p) {
       float mv[8];
 #pragma unroll
       for (int j = 0; j < 8; ++j)
-        mv[j] = __hip_atomic_load(pmlb + (size_t)min(c0 + j, nseg - 1) * NT * 2 + tid, __ATOMIC_RELAXED,
-                                  __HIP_MEMORY_SCOPE_AGENT);
+        mv[j] = __hip_atomic_load(p.part_ml + part_slot(p.balanced, it, p.max_segs, wg0, min(c0 + j, nseg - 1)) * (NT * 2) + tid,
+                                  __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 #pragma unroll
       for (int j = 0; j < 8; ++j) M = fmaxf(M, mv[j]);   // repeats of the last segment are harmless
     }
@@ -742,8 +756,9 @@ __global__ void __launch_bounds__(NW * 64, 1) attn_bf16_kernel(AttnParams p) {
     for (int dg = 0; dg < DG; ++dg) acc[dg] = f32x16{};
     float lt = 0.f;
     for (int c = 0; c < nseg; ++c) {
-      const float* src_ml = pmlb + (size_t)c * NT * 2;
-      const float* src = pob + (size_t)c * NT * NREG;
+      const size_t sc = part_slot(p.balanced, it, p.max_segs, wg0, c);
+      const float* src_ml = p.part_ml + sc * (NT * 2);
+      const float* src = p.part_o + sc * (NT * NREG);
       float pv[NREG];
 #pragma unroll
       for (int i = 0; i < NREG; ++i)
@@ -970,24 +985,24 @@ __global__ void __launch_bounds__(NP * 128, 1) attn_bf16_pc_kernel(AttnParams p)
         fill_window_tile<D, NP * 128>(tidw, t0, pg_lo, L, T, s, R, p.Hkv, kvh, rt == 0, s_pages, kpb, vpb, knb,
                                       vnb, kring, vring);
       };
-      const size_t slot = (size_t)it * p.max_segs + kseg;
+      const int wg0 = owner(0);
+      const size_t slot = part_slot(1, it, p.max_segs, wg0, kseg);
       // Merge of a split item by its last workgroup, all 512 threads: rows'
       // segment weights exp2(m_c - M) l_c / sum_c exp2(m_c - M) l_c go to LDS
       // (the K ring is idle by then), then every thread combines whole runs
       // of 4 output columns of one row, in segment order, with batched
       // coherent loads, and stores them as 8 bf16 bytes.
       auto merge_all = [&]() {
-        const uint32_t* pob = (const uint32_t*)(p.part_o + (size_t)it * p.max_segs * (NC * OREG));
-        const float* pmlb = p.part_ml + (size_t)it * p.max_segs * (2 * RPWG);
+        const uint32_t* pob = (const uint32_t*)p.part_o;
         float* s_w = (float*)kring;   // [BAL_MAX_SEGS][RPWG]
         if (tid < RPWG) {
           float mv[BAL_MAX_SEGS], lv[BAL_MAX_SEGS];
 #pragma unroll
           for (int c = 0; c < BAL_MAX_SEGS; ++c) {
             const int cc = min(c, nseg - 1);
-            mv[c] = __hip_atomic_load(pmlb + (size_t)cc * (2 * RPWG) + tid, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            lv[c] = __hip_atomic_load(pmlb + (size_t)cc * (2 * RPWG) + RPWG + tid, __ATOMIC_RELAXED,
-                                      __HIP_MEMORY_SCOPE_AGENT);
+            const float* src = p.part_ml + part_slot(1, it, p.max_segs, wg0, cc) * (2 * RPWG);
+            mv[c] = __hip_atomic_load(src + tid, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            lv[c] = __hip_atomic_load(src + RPWG + tid, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
           }
           float M = -INFINITY;
 #pragma unroll
@@ -1020,7 +1035,7 @@ __global__ void __launch_bounds__(NP * 128, 1) attn_bf16_pc_kernel(AttnParams p)
 #pragma unroll 1
           for (int c = 0; c < nseg; ++c) {
             // opaque offset: the addresses are formed here, not hoisted
-            int off = c * (NC * OREG) + ct;
+            int off = (int)part_slot(1, it, p.max_segs, wg0, c) * (NC * OREG / 2) + ct;
             asm volatile("" : "+v"(off));
             uint32_t v[QB][2];
 #pragma unroll
@@ -1190,7 +1205,7 @@ __global__ void __launch_bounds__(NP * 128, 1) attn_bf16_pc_kernel(AttnParams p)
         wait_vmcnt<0>();
         __syncthreads();                                     // F2
         if (tid == 0)
-          s_flag[0] = (__hip_atomic_fetch_add(&p.counters[it], 1, __ATOMIC_RELAXED,
+          s_flag[0] = (__hip_atomic_fetch_add(&p.counters[it], 1, __ATOMIC_ACQ_REL,
                                               __HIP_MEMORY_SCOPE_AGENT) == nseg - 1);
         __syncthreads();                                     // F3
         if (s_flag[0]) {
@@ -1430,7 +1445,7 @@ __global__ void __launch_bounds__(NP * 128, 1) attn_bf16_pc_kernel(AttnParams p)
         {
           // the segment's partial output O / l in bf16 (pairs of registers
           // in one word), m and l in fp32
-          uint32_t* po = (uint32_t*)(p.part_o + slot * (size_t)(NC * OREG));
+          uint32_t* po = (uint32_t*)p.part_o + slot * (size_t)(NC * OREG / 2);
           if (hh == 0) {
             float* pml = p.part_ml + slot * (size_t)(2 * RPWG);
 #pragma unroll
@@ -1638,12 +1653,20 @@ static AttnPlan plan_attn(int S, int R, int Hq, int Hkv, int D, int max_pages, i
     pl.grid = pl.n_chunks_max * pl.n_items;
   }
   const int NT = pl.nw * 64;
-  const size_t slots = (size_t)pl.n_items * pl.max_segs;
+  // partial slots: two per workgroup in the balanced split, one per (item,
+  // chunk) in the aligned one (part_slot)
+  const size_t slots = pl.balanced ? (size_t)2 * pl.grid : (size_t)pl.n_items * pl.max_segs;
   if (dtype == DVS_BF16) {
+    // per slot: m and l of every query row (fp32), and O -- fp32 per thread
+    // and register in attn_bf16_kernel, O / l as bf16 pairs per consumer
+    // thread in the producer/consumer kernel (4 pairs, 256 rows)
+    const size_t ml_b = pl.pc ? (size_t)2 * 256 * sizeof(float) : (size_t)NT * 2 * sizeof(float);
+    const size_t o_b = pl.pc ? (size_t)256 * (2 * (D / 32) * 16) * 2
+                             : (size_t)NT * (D / 32) * 16 * sizeof(float);
     pl.off_counters = 0;
     pl.off_ml = align256((size_t)pl.n_items * sizeof(int32_t));
-    pl.off_o = pl.off_ml + align256(slots * NT * 2 * sizeof(float));
-    pl.bytes = pl.off_o + align256(slots * NT * (size_t)(D / 32) * 16 * sizeof(float));
+    pl.off_o = pl.off_ml + align256(slots * ml_b);
+    pl.bytes = pl.off_o + align256(slots * o_b);
   } else {
     pl.bytes = 256;
   }

@@ -523,8 +523,10 @@ __global__ void __launch_bounds__(256, 1) gemm_rt_kernel(
       }
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
+    // release of this workgroup's partials (ordered before it by the
+    // barrier) and, for the last workgroup, acquire of the others'
     if (tid == 0)
-      s_last = __hip_atomic_fetch_add(cnt, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == KS - 1;
+      s_last = __hip_atomic_fetch_add(cnt, 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT) == KS - 1;
     __syncthreads();
     if (!s_last) return;
     if (tid == 0) __hip_atomic_store(cnt, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
