@@ -117,6 +117,34 @@ int attn_hybrid_block(const void* q, const void* k_new, const void* v_new, void*
                       int32_t* err_word, void* workspace, size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
+ * attn_hybrid_block_noalloc
+ *
+ * For callers that cannot allocate device memory: code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc.  The same
+ * computation, arguments and error behaviour as attn_hybrid_block, without
+ * the workspace: the split partials and counters live in a device array of
+ * DVS_ATTN_SCRATCH_BYTES inside the library, one per GPU, held from the
+ * library's first use on that GPU until the process ends.  The call
+ * allocates nothing (no hipMalloc, hipFree or allocating library routine);
+ * it clears the counters it uses with a kernel on `stream` first.
+ *   - A shape whose attn_hybrid_block workspace (dvs_attn_workspace_bytes)
+ *     exceeds DVS_ATTN_SCRATCH_BYTES is rejected with DVS_EWORKSPACE before
+ *     anything is launched; the fp32 path needs no scratch.
+ *   - Every call on one GPU shares that GPU's array: calls that overlap in
+ *     time on one GPU (other streams, other host threads) race and give
+ *     wrong results; serialise them.
+ *   - DVS_EHIP if the array's device address cannot be obtained.
+ * ---------------------------------------------------------------------- */
+#define DVS_ATTN_SCRATCH_BYTES (64u << 20)
+
+int attn_hybrid_block_noalloc(const void* q, const void* k_new, const void* v_new, void* k_pool,
+                              void* v_pool, const int32_t* page_table, const int32_t* kv_len,
+                              int32_t S, int32_t n_causal, int32_t n_mask, int32_t Hq,
+                              int32_t Hkv, int32_t D, int32_t max_pages, int32_t num_pool_pages,
+                              float softmax_scale, int32_t dtype, int32_t chunk_keys, void* out,
+                              int32_t* err_word, void* stream);
+
+/* ------------------------------------------------------------------------
  * argmax_accept
  *
  * Top-1 over the vocabulary for every window row, then greedy acceptance

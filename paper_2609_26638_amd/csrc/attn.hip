@@ -41,6 +41,8 @@
 // fp32 path: a plain per-(sequence, row, head) workgroup, fp32 throughout.
 #include <math.h>
 
+#include <mutex>
+
 #include "dvs_common.h"
 
 namespace dvs {
@@ -1590,6 +1592,11 @@ __global__ void __launch_bounds__(256) attn_f32_kernel(AttnParams p) {
 // ---------------------------------------------------------------------------
 // host side
 // ---------------------------------------------------------------------------
+__global__ void attn_zero_kernel(int32_t* __restrict__ p, int n) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = 0;
+}
+
 struct AttnPlan {
   int nw, rows_total, rows_per_wg, n_row_tiles, n_items, balanced, pc;
   int chunk_tiles, n_chunks_max, share_min, max_segs, grid;
@@ -1710,15 +1717,17 @@ extern "C" size_t dvs_attn_workspace_bytes(int32_t S, int32_t n_causal, int32_t 
   return plan_attn(S, n_causal + n_mask, Hq, Hkv, D, max_pages, chunk_keys, dtype).bytes;
 }
 
-extern "C" int attn_hybrid_block(const void* q, const void* k_new, const void* v_new,
-                                 void* k_pool, void* v_pool, const int32_t* page_table,
-                                 const int32_t* kv_len, int32_t S, int32_t n_causal,
-                                 int32_t n_mask, int32_t Hq, int32_t Hkv, int32_t D,
-                                 int32_t max_pages, int32_t num_pool_pages, float softmax_scale,
-                                 int32_t dtype, int32_t chunk_keys, void* out,
-                                 int32_t* err_word, void* workspace, size_t ws_bytes,
-                                 void* stream) {
-  clear_error();
+// Host check and launch shared by attn_hybrid_block and
+// attn_hybrid_block_noalloc.  `scratch_cap` > 0 marks the scratch-array
+// variant: the workspace is the library's own array of that many bytes, and
+// the split counters are cleared by a kernel at the start of every call.
+static int attn_launch(const void* q, const void* k_new, const void* v_new, void* k_pool,
+                       void* v_pool, const int32_t* page_table, const int32_t* kv_len, int32_t S,
+                       int32_t n_causal, int32_t n_mask, int32_t Hq, int32_t Hkv, int32_t D,
+                       int32_t max_pages, int32_t num_pool_pages, float softmax_scale,
+                       int32_t dtype, int32_t chunk_keys, void* out, int32_t* err_word,
+                       void* workspace, size_t ws_bytes, void* stream, size_t scratch_cap,
+                       bool check_only = false) {
   DVS_CHECK_ARG(q && k_new && v_new && k_pool && v_pool && page_table && kv_len && out,
                 "attn_hybrid_block: NULL array argument");
   DVS_CHECK_ARG(S >= 1 && n_causal >= 0 && n_mask >= 0 && n_causal + n_mask >= 1,
@@ -1733,6 +1742,12 @@ extern "C" int attn_hybrid_block(const void* q, const void* k_new, const void* v
   DVS_CHECK_SUPPORTED(D == 64 || D == 96 || D == 128, "attn_hybrid_block: head_dim %d", D);
   const int R = n_causal + n_mask;
   AttnPlan pl = plan_attn(S, R, Hq, Hkv, D, max_pages, chunk_keys, dtype);
+  if (scratch_cap > 0 && dtype == DVS_BF16 && pl.bytes > scratch_cap) {
+    set_error("attn_hybrid_block_noalloc: this shape needs %zu bytes of scratch, the library's "
+              "array holds %zu (use attn_hybrid_block with a workspace)", pl.bytes, scratch_cap);
+    return DVS_EWORKSPACE;
+  }
+  if (check_only) return DVS_OK;
   if (dtype == DVS_BF16 && (!workspace || ws_bytes < pl.bytes)) {
     set_error("attn_hybrid_block: workspace needs %zu bytes, got %zu", pl.bytes, ws_bytes);
     return DVS_EWORKSPACE;
@@ -1754,6 +1769,11 @@ extern "C" int attn_hybrid_block(const void* q, const void* k_new, const void* v
     prm.part_ml = (float*)(ws + pl.off_ml);
     prm.part_o = (float*)(ws + pl.off_o);
     DVS_CHECK_SUPPORTED((long long)pl.grid < (1LL << 31), "attn_hybrid_block: grid too large");
+    if (scratch_cap > 0) {
+      // the array keeps the previous call's contents: clear the counters
+      const int nw = (int)((pl.off_ml - pl.off_counters) / sizeof(int32_t));
+      hipLaunchKernelGGL(attn_zero_kernel, dim3((nw + 255) / 256), dim3(256), 0, st, prm.counters, nw);
+    }
     if (D == 128) launch_bf16<128>(pl, prm, st);
     else if (D == 96) launch_bf16<96>(pl, prm, st);
     else launch_bf16<64>(pl, prm, st);
@@ -1765,4 +1785,78 @@ extern "C" int attn_hybrid_block(const void* q, const void* k_new, const void* v
     else hipLaunchKernelGGL(attn_f32_kernel<64>, dim3(grid), dim3(256), 0, st, prm);
   }
   return launch_status("attn_hybrid_block");
+}
+
+extern "C" int attn_hybrid_block(const void* q, const void* k_new, const void* v_new,
+                                 void* k_pool, void* v_pool, const int32_t* page_table,
+                                 const int32_t* kv_len, int32_t S, int32_t n_causal,
+                                 int32_t n_mask, int32_t Hq, int32_t Hkv, int32_t D,
+                                 int32_t max_pages, int32_t num_pool_pages, float softmax_scale,
+                                 int32_t dtype, int32_t chunk_keys, void* out,
+                                 int32_t* err_word, void* workspace, size_t ws_bytes,
+                                 void* stream) {
+  clear_error();
+  return attn_launch(q, k_new, v_new, k_pool, v_pool, page_table, kv_len, S, n_causal, n_mask,
+                     Hq, Hkv, D, max_pages, num_pool_pages, softmax_scale, dtype, chunk_keys, out,
+                     err_word, workspace, ws_bytes, stream, 0);
+}
+
+// ---------------------------------------------------------------------------
+// attn_hybrid_block_noalloc: the same call with the library's own scratch
+// array as its workspace, for callers that cannot allocate device memory.
+// `scratch` is a device-side symbol: host code never passes its name to a
+// kernel; it uses the address hipGetSymbolAddress gives for the current
+// device, looked up once per device on that device's first call.
+// ---------------------------------------------------------------------------
+static __device__ __align__(256) char scratch[DVS_ATTN_SCRATCH_BYTES];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+}  // namespace
+
+static int scratch_for_current_device(void** out_ptr) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) {
+    set_error("attn_hybrid_block_noalloc: no current device (or device id >= %d)", kMaxDevices);
+    return DVS_EHIP;
+  }
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !ptr) {
+      set_error("attn_hybrid_block_noalloc: hipGetSymbolAddress failed on device %d: %s", dev,
+                hipGetErrorString(e));
+      return DVS_EHIP;
+    }
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out_ptr = g_scratch_ptr[dev];
+  return DVS_OK;
+}
+
+extern "C" int attn_hybrid_block_noalloc(const void* q, const void* k_new, const void* v_new,
+                                         void* k_pool, void* v_pool, const int32_t* page_table,
+                                         const int32_t* kv_len, int32_t S, int32_t n_causal,
+                                         int32_t n_mask, int32_t Hq, int32_t Hkv, int32_t D,
+                                         int32_t max_pages, int32_t num_pool_pages,
+                                         float softmax_scale, int32_t dtype, int32_t chunk_keys,
+                                         void* out, int32_t* err_word, void* stream) {
+  clear_error();
+  // every argument and the scratch size are checked before anything is
+  // launched or the device array is looked up
+  int rc = attn_launch(q, k_new, v_new, k_pool, v_pool, page_table, kv_len, S, n_causal, n_mask,
+                       Hq, Hkv, D, max_pages, num_pool_pages, softmax_scale, dtype, chunk_keys,
+                       out, err_word, nullptr, 0, stream, DVS_ATTN_SCRATCH_BYTES, true);
+  if (rc != DVS_OK) return rc;
+  void* ws = nullptr;
+  if (dtype == DVS_BF16) {
+    rc = scratch_for_current_device(&ws);
+    if (rc != DVS_OK) return rc;
+  }
+  return attn_launch(q, k_new, v_new, k_pool, v_pool, page_table, kv_len, S, n_causal, n_mask,
+                     Hq, Hkv, D, max_pages, num_pool_pages, softmax_scale, dtype, chunk_keys, out,
+                     err_word, ws, DVS_ATTN_SCRATCH_BYTES, stream, DVS_ATTN_SCRATCH_BYTES);
 }

@@ -33,6 +33,8 @@ _SIGS = {
     "dvs_attn_workspace_bytes": ([_c_int] * 9, _c_size),
     "attn_hybrid_block": ([_c_ptr] * 7 + [_c_int] * 8 + [_c_f32, _c_int, _c_int, _c_ptr, _c_ptr,
                                                           _c_ptr, _c_size, _c_ptr], _c_int),
+    "attn_hybrid_block_noalloc": ([_c_ptr] * 7 + [_c_int] * 8 + [_c_f32, _c_int, _c_int, _c_ptr,
+                                                                  _c_ptr, _c_ptr], _c_int),
     "argmax_accept": ([_c_ptr, _c_int, _c_int, _c_int, _c_int, _c_int, _c_ptr, _c_int, _c_ptr,
                        _c_ptr, _c_ptr, _c_ptr], _c_int),
     "kv_commit": ([_c_int, _c_int, _c_int, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_int, _c_ptr,
@@ -196,6 +198,51 @@ class Workspace:
             self.buf = torch.zeros(int(nbytes), dtype=torch.uint8, device=self.buf.device)
             self.shape = None
         return self
+
+
+def _attn_args(q, k_new, v_new, k_pool, v_pool, page_table, kv_len, n_causal, n_mask, out, err):
+    """Shape and dtype checks shared by the two attention entry points."""
+    dt = q.dtype
+    _dev(q, dt, "q", 4)
+    S, R, Hq, D = q.shape
+    _dev(k_new, dt, "k_new", 4)
+    _dev(v_new, dt, "v_new", 4)
+    Hkv = k_new.shape[2]
+    if tuple(k_new.shape) != (S, R, Hkv, D) or tuple(v_new.shape) != (S, R, Hkv, D):
+        raise DvsError("k_new / v_new must be [S, R, Hkv, D]")
+    _dev(k_pool, dt, "k_pool", 4)
+    _dev(v_pool, dt, "v_pool", 4)
+    P = k_pool.shape[0]
+    if tuple(k_pool.shape) != (P, Hkv, 16, D) or tuple(v_pool.shape) != (P, Hkv, D, 16):
+        raise DvsError("pools must be k [P,Hkv,16,D] and v [P,Hkv,D,16]")
+    _dev(page_table, torch.int32, "page_table", 2)
+    _dev(kv_len, torch.int32, "kv_len", 1)
+    if page_table.shape[0] != S or kv_len.shape[0] != S:
+        raise DvsError("page_table / kv_len must have S rows")
+    if R != n_causal + n_mask:
+        raise DvsError("R must equal n_causal + n_mask")
+    if out is None:
+        out = torch.empty_like(q)
+    _dev(out, dt, "out", 4)
+    if err is not None:
+        _dev(err, torch.int32, "err", 1)
+    return S, R, Hq, Hkv, D, P, page_table.shape[1], out
+
+
+def attn_hybrid_block_noalloc(q, k_new, v_new, k_pool, v_pool, page_table, kv_len, n_causal: int,
+                              n_mask: int, softmax_scale: float, out=None, err=None,
+                              chunk_keys: int = 0, stream=None):
+    """attn_hybrid_block with the library's own scratch array as workspace (the C
+    call allocates nothing; ``out`` is allocated here when not given)."""
+    S, R, Hq, Hkv, D, P, max_pages, out = _attn_args(q, k_new, v_new, k_pool, v_pool, page_table,
+                                                     kv_len, n_causal, n_mask, out, err)
+    rc = lib().attn_hybrid_block_noalloc(_ptr(q), _ptr(k_new), _ptr(v_new), _ptr(k_pool),
+                                         _ptr(v_pool), _ptr(page_table), _ptr(kv_len), S, n_causal,
+                                         n_mask, Hq, Hkv, D, max_pages, P, float(softmax_scale),
+                                         _dtype_code(q), int(chunk_keys), _ptr(out), _ptr(err),
+                                         _stream(stream))
+    _check(rc, "attn_hybrid_block_noalloc")
+    return out
 
 
 def attn_hybrid_block(q, k_new, v_new, k_pool, v_pool, page_table, kv_len, n_causal: int,

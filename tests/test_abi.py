@@ -75,3 +75,18 @@ def test_host_validation_rejects_bad_arguments():
     rc = L.kv_commit(2, 4, 2, *([fake] * 5), 4, fake, fake, 8, fake, fake, 3, fake, fake, 8,
                      -1, fake, nul, nul)
     assert rc == -1                                   # mask rows fewer than the draft width
+
+
+@needs_lib
+def test_noalloc_rejects_oversized_shape_before_any_hip_call():
+    """attn_hybrid_block_noalloc checks the shape against its scratch array
+    first: an oversized call fails on the host, with nothing launched."""
+    L = dvs.lib()
+    fake = ctypes.c_void_p(0x1000)
+    # 64 sequences, 64 rows, aligned 64-key chunks over 1030 pages: > 64 MiB
+    rc = L.attn_hybrid_block_noalloc(*([fake] * 7), 64, 32, 32, 16, 4, 128, 1030, 8, 0.1, 1, 64,
+                                     fake, None, None)
+    assert rc == -4 and b"scratch" in L.dvs_last_error()
+    rc = L.attn_hybrid_block_noalloc(*([fake] * 7), 1, 2, 2, 6, 4, 64, 4, 4, 0.1, 1, 0, fake,
+                                     None, None)
+    assert rc == -1                                   # Hq % Hkv (checked before the device lookup)
