@@ -47,6 +47,25 @@ __device__ __forceinline__ float elem_f(const u32x4& x, int e) {
   }
 }
 
+// A row with no value above -inf (every value -inf or NaN): the top-1 is the
+// lowest index holding -inf (the largest comparable value), or 0 when every
+// value is NaN, so the result is always a vocabulary index.  Block-wide scan
+// (NT threads); runs only for such rows, which also set DVS_ERR_NONFINITE.
+template <bool BF16, int NT>
+__device__ __forceinline__ int first_neg_inf(const char* base, int V, int tid, int* s_first) {
+  if (tid == 0) *s_first = 0x7fffffff;
+  __syncthreads();
+  int first = 0x7fffffff;
+  for (int i = tid; i < V; i += NT) {
+    const float f = BF16 ? __uint_as_float((uint32_t)((const uint16_t*)base)[i] << 16)
+                         : ((const float*)base)[i];
+    if (f == -INFINITY) { first = i; break; }
+  }
+  if (first != 0x7fffffff) atomicMin(s_first, first);
+  __syncthreads();
+  return *s_first == 0x7fffffff ? 0 : *s_first;
+}
+
 template <bool BF16>
 __global__ void __launch_bounds__(512) argmax_kernel(const void* __restrict__ logits, int V,
                                                      int32_t* __restrict__ argmax_out,
@@ -54,6 +73,7 @@ __global__ void __launch_bounds__(512) argmax_kernel(const void* __restrict__ lo
   constexpr int EPV = BF16 ? 8 : 4;   // elements per 16-byte vector
   constexpr int UNR = 8;              // vectors in flight per thread
   __shared__ uint64_t sred[8];
+  __shared__ int s_first;
   const size_t row = blockIdx.x;
   const int tid = threadIdx.x;
   const char* base = (const char*)logits + row * (size_t)V * (BF16 ? 2 : 4);
@@ -122,9 +142,12 @@ __global__ void __launch_bounds__(512) argmax_kernel(const void* __restrict__ lo
   if ((tid & 63) == 0) sred[tid >> 6] = bp;
   if (nonfinite) set_err(err, DVS_ERR_NONFINITE);
   __syncthreads();
-  if (tid == 0) {
-    uint64_t b = sred[0];
-    for (int i = 1; i < 8; ++i) b = sred[i] > b ? sred[i] : b;
+  uint64_t b = sred[0];
+  for (int i = 1; i < 8; ++i) b = sred[i] > b ? sred[i] : b;
+  if (b == 0) {   // no value above -inf anywhere in the row (uniform branch)
+    const int i0 = first_neg_inf<BF16, 512>(base, V, tid, &s_first);
+    if (tid == 0) argmax_out[row] = i0;
+  } else if (tid == 0) {
     argmax_out[row] = 0x7fffffff - (int)(uint32_t)(b & 0xffffffffu);
   }
 }
@@ -145,6 +168,7 @@ __global__ void __launch_bounds__(256) top1_conf_kernel(const void* __restrict__
   constexpr int UNR = 8;              // vectors in flight per thread
   __shared__ float sm[4], ss[4];
   __shared__ int si[4];
+  __shared__ int s_first;
   const size_t row = blockIdx.x;
   const int tid = threadIdx.x;
   const char* base = (const char*)logits + row * (size_t)V * (BF16 ? 2 : 4);
@@ -223,6 +247,15 @@ __global__ void __launch_bounds__(256) top1_conf_kernel(const void* __restrict__
   if ((tid & 63) == 0) { sm[tid >> 6] = m; ss[tid >> 6] = sum; si[tid >> 6] = bi; }
   if (nf != nf) set_err(err, DVS_ERR_NONFINITE);
   __syncthreads();
+  if (si[0] == 0x7fffffff && si[1] == 0x7fffffff && si[2] == 0x7fffffff && si[3] == 0x7fffffff) {
+    // no value above -inf anywhere in the row (uniform branch)
+    const int i0 = first_neg_inf<BF16, 256>(base, V, tid, &s_first);
+    if (tid == 0) {
+      argmax_out[row] = i0;
+      conf_out[row] = 0.f;
+    }
+    return;
+  }
   if (tid == 0) {
     float M = sm[0], S = ss[0];
     int I = si[0];
@@ -234,7 +267,7 @@ __global__ void __launch_bounds__(256) top1_conf_kernel(const void* __restrict__
       M = nm;
       S = a + b;
     }
-    argmax_out[row] = I == 0x7fffffff ? 0 : I;
+    argmax_out[row] = I;
     conf_out[row] = 1.f / S;
   }
 }
@@ -278,7 +311,7 @@ extern "C" int argmax_accept(const void* logits, int32_t dtype, int32_t S, int32
                              int32_t* argmax_out, int32_t* accept_len, int32_t* err_word,
                              void* stream) {
   clear_error();
-  DVS_CHECK_ARG(logits && argmax_out && accept_len, "argmax_accept: NULL array argument");
+  DVS_CHECK_ARG(logits && argmax_out, "argmax_accept: NULL array argument");
   DVS_CHECK_ARG(S >= 1 && R >= 1 && V >= 1, "argmax_accept: need S, R, V >= 1");
   DVS_CHECK_ARG(n_causal >= 1 && n_causal <= R, "argmax_accept: need 1 <= n_causal <= R");
   DVS_CHECK_ARG(draft_width >= n_causal - 1, "argmax_accept: draft_width < n_causal - 1");
@@ -294,7 +327,7 @@ extern "C" int argmax_accept(const void* logits, int32_t dtype, int32_t S, int32
     hipLaunchKernelGGL(argmax_kernel<false>, dim3((unsigned)rows), dim3(512), 0, st, logits, V,
                        argmax_out, err_word);
   int rc = launch_status("argmax_accept(argmax)");
-  if (rc) return rc;
+  if (rc || !accept_len) return rc;
   hipLaunchKernelGGL(accept_kernel, dim3((S + 255) / 256), dim3(256), 0, st, argmax_out, S, R,
                      n_causal, draft, draft_width, accept_len);
   return launch_status("argmax_accept(accept)");

@@ -76,6 +76,44 @@ def test_argmax_nonfinite_flagged_long_bf16_row(bits):
     assert err & dvs.ERR_NONFINITE
 
 
+def _expected_degenerate(row):
+    """The header's rule for a row with no value above -inf: the lowest index
+    holding -inf, or 0 when every value is NaN (NaN never wins)."""
+    idx = np.flatnonzero(row == -np.inf)
+    return int(idx[0]) if idx.size else 0
+
+
+@pytest.mark.parametrize("dtype,V", [("f32", 777), ("bf16", 65536), ("bf16", 37), ("f32", 16384)])
+def test_argmax_rows_without_a_finite_value_give_vocabulary_indices(dtype, V):
+    """All -inf, all NaN, NaN then -inf, and a row whose only non-NaN values
+    are -inf deep inside it: every result is an index in [0, V) by the rule
+    above, and every such row raises DVS_ERR_NONFINITE.  A row with NaNs
+    among finite values takes the top-1 of the finite values."""
+    x = np.full((1, 5, V), -np.inf, np.float32)
+    x[0, 1] = np.nan
+    x[0, 2, :3] = np.nan
+    x[0, 3] = np.nan
+    x[0, 3, V - 2] = -np.inf
+    x[0, 4] = np.random.default_rng(8).standard_normal(V).astype(np.float32)
+    x[0, 4, ::7] = np.nan
+    x[0, 4, V // 2 + 3] = 9.0
+    xx = synth.f32_to_bf16_bits(x) if dtype == "bf16" else x
+    for r in range(4):   # each degenerate row alone, to see its own flag
+        am, _, err = _argmax(xx[:, r:r + 1], dtype, 1, np.zeros((1, 0), np.int32))
+        assert int(am[0, 0]) == _expected_degenerate(x[0, r]), r
+        assert err & dvs.ERR_NONFINITE
+    am, _, err = _argmax(xx, dtype, 1, np.zeros((1, 0), np.int32))
+    assert [int(v) for v in am[0]] == [0, 0, 3, V - 2, V // 2 + 3]
+    lg = to_dev(xx.reshape(5, V), dtype)
+    top = torch.zeros(5, dtype=torch.int32, device="cuda")
+    conf = torch.zeros(5, dtype=torch.float32, device="cuda")
+    e2 = torch.zeros(1, dtype=torch.int32, device="cuda")
+    dvs.top1_confidence(lg, top, conf, err=e2)
+    torch.cuda.synchronize()
+    assert top.cpu().tolist() == [0, 0, 3, V - 2, V // 2 + 3]
+    assert int(e2.item()) & dvs.ERR_NONFINITE
+
+
 def test_argmax_ties_in_vectorized_path_bf16():
     """Equal maxima planted at two positions of 65536-wide rows: in one 16-byte
     vector, in one thread's batch, across threads, across batches, at the row
@@ -153,6 +191,38 @@ def test_commit_random_steps_match_oracle(seed):
         torch.cuda.synchronize()
         assert e == int(dev.err.item())
         _assert_state_equal(dev, st)
+
+
+@pytest.mark.parametrize("seed,B", [(0, 6), (1, 32), (2, 17)])
+def test_accept_commit_random_steps_match_oracle(seed, B):
+    """accept_commit (acceptance inside the commit kernel) against the
+    oracle's accept then kv_commit over random steps: drafts that match the
+    top-1 with probability 0.9 (long accepted runs at B = 32: four run
+    chunks), EOS stops, budget truncation, finished sequences."""
+    rng = np.random.default_rng(200 + seed)
+    S, V = 41, 9
+    R = 2 * B
+    L = rng.integers(0, 300, size=S)
+    # pool: enough free pages for every sequence to reach its 200-token budget
+    st = synth.make_paged_state(rng, L, R, max_pages=96, scatter=True, slack=0.3,
+                                extra_pages=S * 14, n_causal=B, max_new=200)
+    dev = _dev_state(st)
+    accepted = []
+    for step in range(25):
+        am = rng.integers(0, V, size=(S, R)).astype(np.int32)
+        st.draft[:] = np.where(rng.random((S, B - 1)) < 0.9, am[:, :B - 1], st.draft)
+        dev.draft.copy_(torch.from_numpy(st.draft))
+        A = od.accept(am, st.draft, B)
+        live = st.finished == 0
+        eos = 4 if step > 15 else -1
+        e = od.kv_commit(st, A, am, B, B, eos_id=eos)
+        got_A = dvs.accept_commit(dev, torch.from_numpy(am).cuda(), B, B, eos_id=eos)
+        torch.cuda.synchronize()
+        assert e == int(dev.err.item()) == 0
+        np.testing.assert_array_equal(got_A.cpu().numpy(), np.where(live, A, 0))
+        _assert_state_equal(dev, st)
+        accepted.extend(A[live].tolist())
+    assert max(accepted) == B - 1 and st.finished.sum() > 0
 
 
 @pytest.mark.parametrize("seed", [0, 1])
