@@ -90,9 +90,13 @@ const char* dvs_last_error(void);
  *   v_pool  [num_pool_pages, Hkv, D, 16]  paged V cache, head-dim-major (updated)
  *   page_table [S, max_pages] int32, kv_len [S] int32 (read only)
  *   out     [S, R, Hq, D]     attention output, same dtype as q
- *   chunk_keys   key-range split per workgroup (multiple of 64; 0 = auto).
- *                Chunks start at absolute positions that are multiples of it,
- *                so a row's arithmetic does not depend on the other rows.
+ *   chunk_keys   key-range split per workgroup (multiple of 64), or 0 for
+ *                the balanced split.  Chunks start at absolute positions that
+ *                are multiples of it, so a row's arithmetic does not depend on
+ *                the other rows (a causal row equals an AR call bit for bit).
+ *                0: the items' tiles are shared out evenly over the chip,
+ *                whatever the length mix; a row's rounding then depends on
+ *                the call's other rows, which drops that bit-equality.
  *   err_word     int32 device word (may be NULL): DVS_ERR_MAX_PAGES if
  *                L + R > max_pages * 16, DVS_ERR_BAD_PAGE for a page id
  *                outside the pool; such sequences are skipped.
@@ -157,9 +161,14 @@ int attn_hybrid_block_noalloc(const void* q, const void* k_new, const void* v_ne
  *
  *   logits   [S, R, V]  DVS_F32 or DVS_BF16
  *   draft    [S, draft_width] int32; draft_width >= n_causal - 1
- *   argmax_out [S, R] int32, accept_len [S] int32 (written)
- *   err_word  DVS_ERR_NONFINITE if any logit is NaN/Inf (the argmax of such
- *             a row is still written, by bit-pattern order).  May be NULL.
+ *   argmax_out [S, R] int32, accept_len [S] int32 (written); accept_len
+ *             may be NULL: then only the top-1 is computed (for
+ *             accept_commit, which accepts inside the commit kernel)
+ *   err_word  DVS_ERR_NONFINITE if any logit is NaN/Inf.  May be NULL.  Such
+ *             a row still gets a vocabulary index: NaN values never win, so
+ *             the top-1 is taken over the other values; a row with no value
+ *             above -inf gives the lowest index holding -inf, or 0 when every
+ *             value is NaN.
  * Requirements: 1 <= n_causal <= R, V >= 1.
  * ---------------------------------------------------------------------- */
 int argmax_accept(const void* logits, int32_t dtype, int32_t S, int32_t R, int32_t V,
@@ -177,7 +186,8 @@ int argmax_accept(const void* logits, int32_t dtype, int32_t S, int32_t R, int32
  *                   fp32 arithmetic, one pass over the row.
  *   logits [rows, V] DVS_F32 or DVS_BF16; argmax_out [rows] int32 and
  *   conf_out [rows] fp32 (written); err_word: DVS_ERR_NONFINITE as in
- *   argmax_accept (may be NULL).
+ *   argmax_accept (may be NULL); a row with no value above -inf gets the
+ *   index rule of argmax_accept and confidence 0.
  * ---------------------------------------------------------------------- */
 int top1_confidence(const void* logits, int32_t dtype, int32_t rows, int32_t V,
                     int32_t* argmax_out, float* conf_out, int32_t* err_word, void* stream);
@@ -218,6 +228,25 @@ int kv_commit(int32_t S, int32_t n_causal, int32_t n_mask, const int32_t* accept
               int32_t* boundary, int32_t* draft, int32_t draft_width, int32_t* out_tokens,
               int32_t* out_count, int32_t max_new, int32_t eos_id, int32_t* finished,
               int32_t* err_word, void* stream);
+
+/* ------------------------------------------------------------------------
+ * accept_commit
+ *
+ * Acceptance, commit and KV rollback in one kernel (method "Self-Speculative
+ * Decoding"; appendix items Accept, Cache update, Next round): for every
+ * live sequence, A = largest k <= n_causal-1 with draft[s, j-1] ==
+ * argmax[s, j-1] for every j <= k (the rule of argmax_accept), written to
+ * accept_out[s] (0 for finished sequences; accept_out may be NULL); then
+ * exactly kv_commit with that A.  Arguments, layouts, errors and
+ * requirements as kv_commit, with argmax from argmax_accept (which may then
+ * skip its own acceptance: accept_len = NULL).
+ * ---------------------------------------------------------------------- */
+int accept_commit(int32_t S, int32_t n_causal, int32_t n_mask, const int32_t* argmax,
+                  int32_t* accept_out, int32_t* kv_len, int32_t* page_table, int32_t* num_pages,
+                  int32_t max_pages, int32_t* free_stack, int32_t* free_top,
+                  int32_t num_pool_pages, int32_t* boundary, int32_t* draft, int32_t draft_width,
+                  int32_t* out_tokens, int32_t* out_count, int32_t max_new, int32_t eos_id,
+                  int32_t* finished, int32_t* err_word, void* stream);
 
 /* ------------------------------------------------------------------------
  * kv_commit_round

@@ -25,6 +25,11 @@
 // logical pages ascending), so the result is independent of thread timing.
 // Feasibility is decided before anything is written: on failure the whole
 // state is left untouched and the error bit is set.
+//
+// accept_commit runs the acceptance in the same kernel: each thread first
+// finds its sequence's longest accepted prefix A (draft against the
+// verifier's top-1), then commits as above -- one launch for accept, commit
+// and rollback.
 #include "dvs_common.h"
 
 namespace dvs {
@@ -53,6 +58,8 @@ struct CommitParams {
   int S, n_causal, n_mask, R, window, max_pages, pool_pages, draft_width, max_new, eos_id;
   const int32_t* lead;   // two-forward round: a0 per sequence, committed first (else NULL)
   const int32_t* accept_len;   // NULL: the run is the first n_causal tokens of argmax
+  int accept_here;             // 1: A computed in this kernel from argmax and draft
+  int32_t* accept_out;         // accept_here: A per sequence (may be NULL)
   const int32_t* argmax;
   int32_t* kv_len;
   int32_t* page_table;
@@ -92,8 +99,30 @@ __global__ void __launch_bounds__(COMMIT_THREADS) kv_commit_kernel(CommitParams 
     n = p.num_pages[s];
     cnt = p.out_count[s];
     fin = p.finished[s] != 0;
+    if (!fin && p.accept_here) {
+      // longest prefix with d_j == a_j = argmax[s, j-1], j <= n_causal - 1,
+      // compared RUN_CHUNK positions at a time (independent loads first)
+      const int nd = p.n_causal - 1;
+      bool go = true;
+      for (int j0 = 0; j0 < nd && go; j0 += RUN_CHUNK) {
+        int dv[RUN_CHUNK], av[RUN_CHUNK];
+#pragma unroll
+        for (int u = 0; u < RUN_CHUNK; ++u) {
+          const int j = min(j0 + u, nd - 1);
+          dv[u] = p.draft[(size_t)s * p.draft_width + j];
+          av[u] = p.argmax[(size_t)s * p.R + j];
+        }
+#pragma unroll
+        for (int u = 0; u < RUN_CHUNK; ++u) {
+          if (!go || j0 + u >= nd) continue;
+          if (dv[u] == av[u]) A = j0 + u + 1;
+          else go = false;
+        }
+      }
+    }
+    if (live_seq && p.accept_here && p.accept_out) p.accept_out[s] = fin ? 0 : A;
     if (!fin) {
-      A = p.accept_len ? p.accept_len[s] : p.n_causal - 1;
+      if (!p.accept_here) A = p.accept_len ? p.accept_len[s] : p.n_causal - 1;
       A = A < 0 ? 0 : (A > p.n_causal - 1 ? p.n_causal - 1 : A);
       // run = [a0,] d_1..d_A, a_{A+1} (last index jl); keep up to the first
       // stop token / budget.  Tokens are fetched RUN_CHUNK at a time
@@ -193,6 +222,7 @@ using namespace dvs;
 
 static int launch_commit(const char* who, int32_t S, int32_t n_causal, int32_t n_mask,
                          int32_t window, const int32_t* lead, const int32_t* accept_len,
+                         int accept_here, int32_t* accept_out,
                          const int32_t* argmax, int32_t* kv_len, int32_t* page_table,
                          int32_t* num_pages, int32_t max_pages, int32_t* free_stack,
                          int32_t* free_top, int32_t num_pool_pages, int32_t* boundary,
@@ -216,7 +246,8 @@ static int launch_commit(const char* who, int32_t S, int32_t n_causal, int32_t n
   p.lead = lead;
   p.max_pages = max_pages; p.pool_pages = num_pool_pages; p.draft_width = draft_width;
   p.max_new = max_new; p.eos_id = eos_id;
-  p.accept_len = accept_len; p.argmax = argmax; p.kv_len = kv_len; p.page_table = page_table;
+  p.accept_len = accept_len; p.accept_here = accept_here; p.accept_out = accept_out;
+  p.argmax = argmax; p.kv_len = kv_len; p.page_table = page_table;
   p.num_pages = num_pages; p.free_stack = free_stack; p.free_top = free_top;
   p.boundary = boundary; p.draft = draft; p.out_tokens = out_tokens; p.out_count = out_count;
   p.finished = finished; p.err = err_word;
@@ -234,7 +265,7 @@ extern "C" int kv_commit(int32_t S, int32_t n_causal, int32_t n_mask, const int3
   clear_error();
   DVS_CHECK_ARG(accept_len != nullptr, "kv_commit: NULL accept_len");
   return launch_commit("kv_commit", S, n_causal, n_mask, n_causal + n_mask, nullptr, accept_len,
-                       argmax, kv_len, page_table, num_pages, max_pages, free_stack, free_top,
+                       0, nullptr, argmax, kv_len, page_table, num_pages, max_pages, free_stack, free_top,
                        num_pool_pages, boundary, draft, draft_width, out_tokens, out_count, max_new,
                        eos_id, finished, err_word, stream);
 }
@@ -249,7 +280,8 @@ extern "C" int kv_commit_round(int32_t S, int32_t B, const int32_t* lead, const 
   clear_error();
   DVS_CHECK_ARG(lead != nullptr && accept_len != nullptr, "kv_commit_round: NULL lead/accept_len");
   DVS_CHECK_ARG(B >= 1, "kv_commit_round: need B >= 1");
-  return launch_commit("kv_commit_round", S, B + 1, 0, B + 2, lead, accept_len, argmax, kv_len,
+  return launch_commit("kv_commit_round", S, B + 1, 0, B + 2, lead, accept_len, 0, nullptr,
+                       argmax, kv_len,
                        page_table, num_pages, max_pages, free_stack, free_top, num_pool_pages,
                        boundary, draft, draft_width, out_tokens, out_count, max_new, eos_id,
                        finished, err_word, stream);
@@ -266,8 +298,24 @@ extern "C" int kv_commit_block(int32_t S, int32_t B, const int32_t* block, int32
   DVS_CHECK_ARG(B >= 1, "kv_commit_block: need B >= 1");
   // run token j < B - 1 comes from the draft slot j, the last from argmax[B - 1]:
   // both are the block row
-  return launch_commit("kv_commit_block", S, B, 0, B + 1, nullptr, nullptr, block, kv_len,
+  return launch_commit("kv_commit_block", S, B, 0, B + 1, nullptr, nullptr, 0, nullptr, block,
+                       kv_len,
                        page_table, num_pages, max_pages, free_stack, free_top, num_pool_pages,
                        boundary, const_cast<int32_t*>(block), B, out_tokens, out_count, max_new,
                        eos_id, finished, err_word, stream);
+}
+
+extern "C" int accept_commit(int32_t S, int32_t n_causal, int32_t n_mask, const int32_t* argmax,
+                             int32_t* accept_out, int32_t* kv_len, int32_t* page_table,
+                             int32_t* num_pages, int32_t max_pages, int32_t* free_stack,
+                             int32_t* free_top, int32_t num_pool_pages, int32_t* boundary,
+                             int32_t* draft, int32_t draft_width, int32_t* out_tokens,
+                             int32_t* out_count, int32_t max_new, int32_t eos_id, int32_t* finished,
+                             int32_t* err_word, void* stream) {
+  clear_error();
+  DVS_CHECK_ARG(draft || n_causal == 1, "accept_commit: NULL draft");
+  return launch_commit("accept_commit", S, n_causal, n_mask, n_causal + n_mask, nullptr, nullptr,
+                       1, accept_out, argmax, kv_len, page_table, num_pages, max_pages,
+                       free_stack, free_top, num_pool_pages, boundary, draft, draft_width,
+                       out_tokens, out_count, max_new, eos_id, finished, err_word, stream);
 }

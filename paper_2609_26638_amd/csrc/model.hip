@@ -7,7 +7,7 @@
 // then per layer: RMSNorm -> Q/K/V projections -> rotary positions at
 // kv_len + r -> attn_hybrid_block (appends the window's K/V) -> O projection
 // + residual -> [RMSNorm -> SwiGLU MLP + residual], final RMSNorm, LM head,
-// and the hot-path tail argmax_accept -> kv_commit.
+// and the hot-path tail argmax_accept -> accept_commit.
 //
 // Every matrix product is C[m, n] = sum_k A[m, k] * W[n, k] with weights laid
 // out [out, in] so both MFMA operands are contiguous along k.  One wave owns
@@ -846,13 +846,14 @@ static int run_step(const dvs_model* m, const dvs_state* st, int n_causal, int n
   if ((rc = forward_layers<T>(m, st, n_causal, n_mask, chunk_keys, L, ws, stream))) return rc;
   if ((rc = gemm(L, ws, m->dtype, ws + L.h, m->lm_head, M, m->vocab, m->hidden, logits, 1, 0, stream)))
     return rc;
-  rc = argmax_accept(logits, DVS_F32, S, R, m->vocab, n_causal, st->draft, st->draft_width, am, acc,
-                     st->err_word, stream);
+  rc = argmax_accept(logits, DVS_F32, S, R, m->vocab, n_causal, st->draft, st->draft_width, am,
+                     nullptr, st->err_word, stream);
   if (rc) return rc;
-  return kv_commit(S, n_causal, n_mask, acc, am, st->kv_len, st->page_table, st->num_pages,
-                   st->max_pages, st->free_stack, st->free_top, st->num_pool_pages, st->boundary,
-                   st->draft, st->draft_width, st->out_tokens, st->out_count, st->max_new, st->eos_id,
-                   st->finished, st->err_word, stream);
+  // acceptance inside the commit kernel
+  return accept_commit(S, n_causal, n_mask, am, acc, st->kv_len, st->page_table, st->num_pages,
+                       st->max_pages, st->free_stack, st->free_top, st->num_pool_pages,
+                       st->boundary, st->draft, st->draft_width, st->out_tokens, st->out_count,
+                       st->max_new, st->eos_id, st->finished, st->err_word, stream);
 }
 
 // The paper's two-forward round: draft forward over [x0, [M] x B], then a

@@ -25,6 +25,12 @@ ERR_BAD_PAGE = 8
 
 _lib = None
 
+# Model-level calls default to aligned 256-key attention chunks: a row's
+# arithmetic then does not depend on the call's other rows, so the
+# self-speculative stream equals greedy AR bit for bit.  chunk_keys = 0 (the
+# balanced split) fills the chip better but drops that guarantee.
+MODEL_CHUNK_KEYS = 256
+
 _c_int, _c_ptr, _c_f32, _c_size = ctypes.c_int32, ctypes.c_void_p, ctypes.c_float, ctypes.c_size_t
 
 _SIGS = {
@@ -40,6 +46,9 @@ _SIGS = {
     "kv_commit": ([_c_int, _c_int, _c_int, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_int, _c_ptr,
                    _c_ptr, _c_int, _c_ptr, _c_ptr, _c_int, _c_ptr, _c_ptr, _c_int, _c_int, _c_ptr,
                    _c_ptr, _c_ptr], _c_int),
+    "accept_commit": ([_c_int, _c_int, _c_int, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_int,
+                       _c_ptr, _c_ptr, _c_int, _c_ptr, _c_ptr, _c_int, _c_ptr, _c_ptr, _c_int,
+                       _c_int, _c_ptr, _c_ptr, _c_ptr], _c_int),
     "kv_commit_round": ([_c_int, _c_int, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_int,
                          _c_ptr, _c_ptr, _c_int, _c_ptr, _c_ptr, _c_int, _c_ptr, _c_ptr, _c_int,
                          _c_int, _c_ptr, _c_ptr, _c_ptr], _c_int),
@@ -294,17 +303,21 @@ def attn_hybrid_block(q, k_new, v_new, k_pool, v_pool, page_table, kv_len, n_cau
 # ---------------------------------------------------------------------------
 
 def argmax_accept(logits, n_causal: int, draft, argmax_out=None, accept_len=None, err=None,
-                  stream=None):
-    """logits [S,R,V] (f32/bf16), draft [S,W] int32 -> (argmax [S,R], accept_len [S])."""
+                  stream=None, accept: bool = True):
+    """logits [S,R,V] (f32/bf16), draft [S,W] int32 -> (argmax [S,R], accept_len [S]).
+    accept=False: top-1 only (accept_len is None), for accept_commit."""
     _dev(logits, logits.dtype, "logits", 3)
     S, R, V = logits.shape
     _dev(draft, torch.int32, "draft", 2)
     if argmax_out is None:
         argmax_out = torch.empty((S, R), dtype=torch.int32, device=logits.device)
-    if accept_len is None:
+    if accept and accept_len is None:
         accept_len = torch.empty((S,), dtype=torch.int32, device=logits.device)
+    if not accept:
+        accept_len = None
     _dev(argmax_out, torch.int32, "argmax_out", 2)
-    _dev(accept_len, torch.int32, "accept_len", 1)
+    if accept_len is not None:
+        _dev(accept_len, torch.int32, "accept_len", 1)
     if err is not None:
         _dev(err, torch.int32, "err", 1)
     rc = lib().argmax_accept(_ptr(logits), _dtype_code(logits), S, R, V, n_causal, _ptr(draft),
@@ -373,6 +386,26 @@ class DeviceState:
             setattr(h, f, getattr(self, f).cpu().numpy().copy())
         h.free_top = int(self.free_top.item())
         return h
+
+
+def accept_commit(st: DeviceState, argmax, n_causal: int, n_mask: int, accept_out=None,
+                  eos_id: int = -1, stream=None):
+    """Acceptance, commit and rollback in one kernel; returns accept_out [S] int32."""
+    S = st.kv_len.shape[0]
+    _dev(argmax, torch.int32, "argmax", 2)
+    if argmax.shape != (S, n_causal + n_mask):
+        raise DvsError("argmax must be [S, n_causal + n_mask]")
+    if accept_out is None:
+        accept_out = torch.empty((S,), dtype=torch.int32, device=argmax.device)
+    _dev(accept_out, torch.int32, "accept_out", 1)
+    rc = lib().accept_commit(S, n_causal, n_mask, _ptr(argmax), _ptr(accept_out), _ptr(st.kv_len),
+                             _ptr(st.page_table), _ptr(st.num_pages), st.max_pages,
+                             _ptr(st.free_stack), _ptr(st.free_top), st.pool_pages,
+                             _ptr(st.boundary), _ptr(st.draft), st.draft.shape[1],
+                             _ptr(st.out_tokens), _ptr(st.out_count), st.out_tokens.shape[1],
+                             int(eos_id), _ptr(st.finished), _ptr(st.err), _stream(stream))
+    _check(rc, "accept_commit")
+    return accept_out
 
 
 def kv_commit(st: DeviceState, accept_len, argmax, n_causal: int, n_mask: int,
@@ -488,7 +521,7 @@ class DeviceModel:
         self.V, self.H = w.V, w.H
         self.ws = None
 
-    def workspace_bytes(self, S, n_causal, n_mask, max_pages, chunk_keys=0) -> int:
+    def workspace_bytes(self, S, n_causal, n_mask, max_pages, chunk_keys=MODEL_CHUNK_KEYS) -> int:
         return int(lib().dvs_step_workspace_bytes(ctypes.byref(self.desc), S, n_causal, n_mask,
                                                   max_pages, chunk_keys))
 
@@ -503,7 +536,7 @@ def _state_desc(st: DeviceState, eos_id: int) -> DvsState:
 
 
 def draft_verify_step(model: DeviceModel, st: DeviceState, n_causal: int, n_mask: int,
-                      chunk_keys: int = 0, eos_id: int = -1, logits_out=None, argmax_out=None,
+                      chunk_keys: int = MODEL_CHUNK_KEYS, eos_id: int = -1, logits_out=None, argmax_out=None,
                       accept_out=None, stream=None):
     """One fused step (or an AR step with n_causal=1, n_mask=0) on the device."""
     S = st.kv_len.shape[0]
@@ -523,7 +556,7 @@ def draft_verify_step(model: DeviceModel, st: DeviceState, n_causal: int, n_mask
     _check(rc, "draft_verify_step")
 
 
-def literal_round(model: DeviceModel, st: DeviceState, B: int, chunk_keys: int = 0,
+def literal_round(model: DeviceModel, st: DeviceState, B: int, chunk_keys: int = MODEL_CHUNK_KEYS,
                   eos_id: int = -1, logits_out=None, argmax_out=None, accept_out=None, stream=None):
     """One round of the paper's two-forward decoding (draft forward, verify
     forward, commit of a0, d_1..d_A, a_{A+1}) on the device."""
@@ -561,7 +594,7 @@ def capture(fn) -> "torch.cuda.CUDAGraph":
 
 
 def literal_round_refined(model: DeviceModel, st: DeviceState, B: int, tau_d: float,
-                          chunk_keys: int = 0, eos_id: int = -1, logits_out=None, argmax_out=None,
+                          chunk_keys: int = MODEL_CHUNK_KEYS, eos_id: int = -1, logits_out=None, argmax_out=None,
                           accept_out=None, stream=None) -> int:
     """The two-forward round with its draft refined at threshold tau_d over
     several draft forwards; returns the number of draft forwards."""
@@ -586,7 +619,7 @@ def literal_round_refined(model: DeviceModel, st: DeviceState, B: int, tau_d: fl
 
 
 def literal_round_sampled(model: DeviceModel, st: DeviceState, B: int, temperature: float, u,
-                          chunk_keys: int = 0, eos_id: int = -1, logits_out=None,
+                          chunk_keys: int = MODEL_CHUNK_KEYS, eos_id: int = -1, logits_out=None,
                           accept_out=None, stream=None):
     """The two-forward round under sampling (stochastic acceptance); u is a
     device float32 [S, 2B + 2] of uniforms in [0, 1)."""
@@ -613,7 +646,7 @@ def literal_round_sampled(model: DeviceModel, st: DeviceState, B: int, temperatu
 
 
 def diffusion_denoise(model: DeviceModel, st: DeviceState, block, tau_c: float, n_open=None,
-                      chunk_keys: int = 0, eos_id: int = -1, logits_out=None, argmax_out=None,
+                      chunk_keys: int = MODEL_CHUNK_KEYS, eos_id: int = -1, logits_out=None, argmax_out=None,
                       conf_out=None, stream=None):
     """One denoising forward of direct block diffusion and its reveal; block
     [S, B] int32 (-1 = masked) is updated in place.  Returns n_open (a device
@@ -645,7 +678,7 @@ def diffusion_denoise(model: DeviceModel, st: DeviceState, block, tau_c: float, 
 
 
 def diffusion_block(model: DeviceModel, st: DeviceState, B: int, tau_c: float, block=None,
-                    chunk_keys: int = 0, eos_id: int = -1, stream=None):
+                    chunk_keys: int = MODEL_CHUNK_KEYS, eos_id: int = -1, stream=None):
     """Decode and commit one block by direct block diffusion.  Returns
     (block [S, B] int32, denoising forwards); the block cost one more
     forward (the cache write)."""
@@ -671,7 +704,7 @@ def diffusion_block(model: DeviceModel, st: DeviceState, B: int, tau_c: float, b
 
 
 def prefill(model: DeviceModel, st: DeviceState, P: int, n_mask: int, prefix_tokens=None,
-            x_prefix=None, chunk_keys: int = 0, eos_id: int = -1, logits_out=None, stream=None):
+            x_prefix=None, chunk_keys: int = MODEL_CHUNK_KEYS, eos_id: int = -1, logits_out=None, stream=None):
     """Prefill P prefix rows (token ids and/or given fp32 embeddings) plus
     n_mask mask rows; sets kv_len, boundary, first draft and first token."""
     S = st.kv_len.shape[0]
