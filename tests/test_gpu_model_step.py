@@ -376,3 +376,70 @@ def test_decoder_stack_selfspec_equals_ar():
     print(f"[stack] two-forward rounds {lr_rounds} rounds {lr_s:.2f} s", flush=True)
     np.testing.assert_array_equal(lr.out_count, [si.max_new] * 8)
     np.testing.assert_array_equal(lr.out_tokens, ar.out_tokens)
+
+
+def test_decoder_stack_replay_with_ar_drafts():
+    """The 16-layer bf16 stack with full acceptances: every third fused step
+    the device draft is overwritten with the greedy-AR continuation, so the
+    step must accept all B - 1 drafts (A = B - 1) at the stack's own shape.
+    Every step's GPU top-1 is replayed through the oracle's accept and commit
+    (appendix items Accept and Cache update), which must reproduce the GPU's
+    accepted lengths, committed tokens, lengths, page tables and free stack
+    bit for bit; the final stream equals greedy AR."""
+    print("[stack] generating the 16-layer stack", flush=True)
+    si = synth.decoder_stack_inputs()
+    ar, _, _ = _run_stack(si, "bf16", "ar", 256)
+    print("[stack] AR reference done", flush=True)
+    w, B, S = si.weights, si.B, 8
+    pool = si.state.pool_pages
+    kps = [torch.zeros((pool, w.Hkv, 16, w.D), dtype=torch.bfloat16, device="cuda")
+           for _ in range(w.n_layers)]
+    vps = [torch.zeros((pool, w.Hkv, w.D, 16), dtype=torch.bfloat16, device="cuda")
+           for _ in range(w.n_layers)]
+    dm = dvs.DeviceModel(w, kps, vps, "bf16")
+    st = dvs.DeviceState(si.state)
+    dvs.prefill(dm, st, si.P, B, prefix_tokens=torch.from_numpy(si.prefix_tokens()).cuda(),
+                x_prefix=torch.from_numpy(si.x_prefix()).cuda(), chunk_keys=256)
+    am = torch.empty((S, 2 * B), dtype=torch.int32, device="cuda")
+    acc = torch.empty(S, dtype=torch.int32, device="cuda")
+    forced_full = 0
+    steps = 0
+    while True:
+        before = st.to_host(si.state)
+        if before.finished.min() == 1:
+            break
+        forced = steps % 3 == 2
+        if forced:
+            d = np.zeros((S, B - 1), np.int32)
+            for s in range(S):
+                c = int(before.out_count[s])
+                tail = ar.out_tokens[s, c:c + B - 1]
+                d[s, :tail.size] = tail
+            st.draft.copy_(torch.from_numpy(d).cuda())
+            before.draft = d
+        dvs.draft_verify_step(dm, st, B, B, chunk_keys=256, argmax_out=am, accept_out=acc)
+        torch.cuda.synchronize()
+        assert int(st.err.item()) == 0
+        got_am = am.cpu().numpy()
+        got_A = acc.cpu().numpy()
+        ref_A = od.accept(got_am, before.draft, B)
+        np.testing.assert_array_equal(got_A, ref_A)
+        ref = before.copy()
+        assert od.kv_commit(ref, ref_A, got_am, B, B) == 0
+        _states_equal(st, ref)
+        after = st.to_host(si.state)
+        assert after.free_top == ref.free_top
+        np.testing.assert_array_equal(after.free_stack[:after.free_top], ref.free_stack[:ref.free_top])
+        if forced:
+            for s in range(S):
+                c = int(before.out_count[s])
+                if not before.finished[s] and c + B - 1 <= si.max_new:
+                    assert got_A[s] == B - 1, (steps, s, got_A[s])
+                    forced_full += 1
+        steps += 1
+        assert steps <= 2 * si.max_new
+    print(f"[stack] {steps} steps, {forced_full} full acceptances", flush=True)
+    assert forced_full >= 8 * 10
+    host = st.to_host(si.state)
+    np.testing.assert_array_equal(host.out_count, [si.max_new] * S)
+    np.testing.assert_array_equal(host.out_tokens, ar.out_tokens)

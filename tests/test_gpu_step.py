@@ -50,3 +50,64 @@ def test_batched_serving_step_matches_oracle():
                           samples, decode=synth.bf16_to_f64)
     for (s, r, h), v in ref.items():
         assert max_rel_err(o[s, r, h][None], v[None]) <= 2e-2, (s, r, h)
+
+
+def test_long_document_step_matches_oracle():
+    """The benchmark's step, once, on the 64-sequence KV 4k-16k workload (B = 32,
+    64 window rows, vocabulary 65536, balanced attention split): argmax of all
+    64 x 64 rows, accepted lengths (draft width 31), committed tokens, kv_len,
+    page tables and the free stack bit for bit against the oracle; attention
+    within 2e-2 on a causal row and a mask row of every (sequence, KV head)
+    item the kernel splits and merges (512 output vectors and more)."""
+    print("[step] generating the 64-sequence KV 4k-16k workload", flush=True)
+    ai, li = synth.long_document_inputs()
+    B, S, R, Hkv = ai.n_causal, ai.S, ai.R, ai.Hkv
+    G = ai.Hq // Hkv
+    host = ai.state.copy()
+    host.out_tokens = np.full((S, 256), -1, np.int32)
+    d = dev_attn(ai)
+    st = dvs.DeviceState(host)
+    logits = to_dev(li.logits, "bf16")
+    out = dvs.attn_hybrid_block(d["q"], d["k_new"], d["v_new"], d["k_pool"], d["v_pool"],
+                                st.page_table, st.kv_len, B, B, ai.scale, err=st.err,
+                                chunk_keys=0)
+    am, A = dvs.argmax_accept(logits, B, st.draft, err=st.err)
+    dvs.kv_commit(st, A, am, B, B)
+    torch.cuda.synchronize()
+    assert int(st.err.item()) == 0
+    print("[step] integers", flush=True)
+    # bf16 -> fp32 widening is exact, so the oracle's comparisons see the same values
+    ref_am = od.top1_rows(synth.bf16_to_f32(li.logits))
+    np.testing.assert_array_equal(am.cpu().numpy(), ref_am)
+    ref_A = od.accept(ref_am, host.draft, B)
+    np.testing.assert_array_equal(A.cpu().numpy(), ref_A)
+    # long accepted runs: the commit moves runs of up to B tokens
+    assert ref_A.max() == B - 1 and 12.0 < ref_A.mean() < 17.0
+    ref_st = host.copy()
+    assert od.kv_commit(ref_st, ref_A, ref_am, B, B) == 0
+    got = st.to_host(ref_st)
+    for f in ("kv_len", "page_table", "num_pages", "boundary", "draft", "out_tokens",
+              "out_count", "finished"):
+        np.testing.assert_array_equal(getattr(got, f), getattr(ref_st, f), err_msg=f)
+    assert got.free_top == ref_st.free_top
+    np.testing.assert_array_equal(got.free_stack[:got.free_top], ref_st.free_stack[:ref_st.free_top])
+    print("[step] attention on every (sequence, KV head) item", flush=True)
+    rng = np.random.default_rng(9)
+    samples = set()
+    for s in range(S):
+        for g in range(Hkv):
+            for r in (int(rng.integers(0, B)), int(rng.integers(B, R))):
+                samples.add((s, r, g * G + int(rng.integers(0, G))))
+        samples.add((s, B - 1, int(rng.integers(0, ai.Hq))))      # the last causal row
+        samples.add((s, R - 1, int(rng.integers(0, ai.Hq))))      # the last mask row
+    assert len(samples) >= 512
+    ref = oa.attn_sampled(ai.as_f64("q"), ai.as_f64("k_new"), ai.as_f64("v_new"), ai.k_pool,
+                          ai.v_pool, ai.state.page_table, ai.state.kv_len, B, B, ai.scale,
+                          sorted(samples), decode=synth.bf16_to_f64)
+    o = to_f64(out)
+    worst = 0.0
+    for (s, r, h), v in ref.items():
+        e = max_rel_err(o[s, r, h][None], v[None])
+        worst = max(worst, e)
+        assert e <= 2e-2, (s, r, h, e)
+    print(f"[err] long-document step: {len(ref)} vectors, max rel err {worst:.3e}", flush=True)
