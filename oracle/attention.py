@@ -41,6 +41,51 @@ def visible_hi(L: int, n_causal: int, n_mask: int) -> np.ndarray:
     return hi
 
 
+def visible_mask(L: int, n_causal: int, n_mask: int, group: int = 0) -> np.ndarray:
+    """Visibility [R, L + R] of the window rows over key positions, with the
+    mask rows cut into groups of ``group`` rows (0: one group of n_mask).
+
+    Causal row r sees keys <= L + r.  With G = n_mask / group groups, the
+    rows of mask group g see the whole cache, the causal rows
+    0 .. n_causal - G + g and the rows of their own group (bidirectionally).
+    One group (G = 1) is the hybrid mask of ``visible_hi``.  With
+    G = n_causal, group g is the draft block of the continuation that keeps
+    the causal rows 0..g: the per-acceptance drafts of the structured-mask
+    AR-diffusion hybrids the paper cites in its related work.
+    """
+    R = n_causal + n_mask
+    group = n_mask if group == 0 else group
+    vis = np.zeros((R, L + R), dtype=bool)
+    vis[:, :L] = True
+    for r in range(n_causal):
+        vis[r, L:L + r + 1] = True
+    if n_mask:
+        n_groups = n_mask // group
+        assert n_groups * group == n_mask and (n_groups == 1 or n_groups <= n_causal)
+        for r in range(n_causal, R):
+            g = (r - n_causal) // group
+            vis[r, L:L + n_causal - n_groups + g + 1] = True
+            lo = L + n_causal + g * group
+            vis[r, lo:lo + group] = True
+    return vis
+
+
+def window_positions(L: int, n_causal: int, n_mask: int, group: int = 0) -> np.ndarray:
+    """Sequence position of every window row: L + r for causal rows; row i of
+    mask group g sits right after the last causal row the group sees, at
+    L + (n_causal - G + g) + 1 + i (one group: L + r)."""
+    R = n_causal + n_mask
+    group = n_mask if group == 0 else max(group, 1)
+    pos = np.empty(R, dtype=np.int64)
+    pos[:n_causal] = L + np.arange(n_causal)
+    if n_mask:
+        n_groups = n_mask // group
+        for r in range(n_causal, R):
+            g, i = divmod(r - n_causal, group)
+            pos[r] = L + (n_causal - n_groups + g) + 1 + i
+    return pos
+
+
 def gather_cache(pool: np.ndarray, page_row: np.ndarray, L: int, page_size: int,
                  slot_last: bool = False, decode=None) -> np.ndarray:
     """Dense [L, Hkv, D] view of a sequence's first L cached positions.
@@ -98,10 +143,30 @@ def attend_rows(q: np.ndarray, keys: np.ndarray, vals: np.ndarray, hi: np.ndarra
     return out
 
 
+def attend_rows_vis(q: np.ndarray, keys: np.ndarray, vals: np.ndarray, vis: np.ndarray,
+                    scale: float) -> np.ndarray:
+    """attend_rows with an explicit visibility vis [R, T] over key positions."""
+    R, Hq, D = q.shape
+    T, Hkv, _ = keys.shape
+    G = Hq // Hkv
+    out = np.zeros((R, Hq, D), dtype=np.float64)
+    for r in range(R):
+        for h in range(Hq):
+            g = h // G
+            s = scale * (keys[:, g, :] @ q[r, h, :])
+            s = np.where(vis[r], s, -np.inf)
+            s = s - s.max()
+            w = np.exp(s)
+            w = w / w.sum()
+            out[r, h, :] = w @ vals[:, g, :]
+    return out
+
+
 def attn_hybrid_block(q, k_new, v_new, k_pool, v_pool, page_table, kv_len,
                       n_causal: int, n_mask: int, scale: float, page_size: int = 16,
-                      seqs=None):
-    """Append the window's K/V to the pools, then attend with the hybrid mask.
+                      seqs=None, group: int = 0):
+    """Append the window's K/V to the pools, then attend with the hybrid mask
+    (``group`` > 0: the grouped mask of ``visible_mask``).
 
     All float inputs are float64 arrays: q [S,R,Hq,D], k_new/v_new [S,R,Hkv,D],
     k_pool [P,Hkv,page_size,D], v_pool [P,Hkv,D,page_size] (both modified in
@@ -117,7 +182,11 @@ def attn_hybrid_block(q, k_new, v_new, k_pool, v_pool, page_table, kv_len,
         append_block(v_pool, page_table[s], L, v_new[s], page_size, slot_last=True)
         keys = gather_cache(k_pool, page_table[s], L + R, page_size)
         vals = gather_cache(v_pool, page_table[s], L + R, page_size, slot_last=True)
-        out[s] = attend_rows(q[s], keys, vals, visible_hi(L, n_causal, n_mask), scale)
+        if group and group != n_mask:
+            out[s] = attend_rows_vis(q[s], keys, vals, visible_mask(L, n_causal, n_mask, group),
+                                     scale)
+        else:
+            out[s] = attend_rows(q[s], keys, vals, visible_hi(L, n_causal, n_mask), scale)
     return out
 
 

@@ -243,7 +243,7 @@ def committed_run(argmax_row: np.ndarray, draft_row: np.ndarray, A: int, lead=No
 def kv_commit(st, accept_len: np.ndarray, argmax: np.ndarray, n_causal: int, n_mask: int,
               eos_id: int = -1, max_new: int | None = None, page_size: int = 16,
               lead: np.ndarray | None = None, window: int | None = None,
-              block_runs: np.ndarray | None = None) -> int:
+              block_runs: np.ndarray | None = None, draft_group: int = 0) -> int:
     """Apply one step's commit to ``st`` (a synth.PagedState-like object) in place.
 
     ``lead`` (two-forward round): per-sequence a0, committed first; the
@@ -251,7 +251,9 @@ def kv_commit(st, accept_len: np.ndarray, argmax: np.ndarray, n_causal: int, n_m
     window the pages must cover (default n_causal + n_mask).  ``block_runs``
     [S, n] (direct block diffusion): the whole row is each sequence's run,
     in place of the accepted drafts and the verifier's token (accept_len and
-    argmax are then unused).
+    argmax are then unused).  ``draft_group`` > 0 (per-acceptance drafts): the
+    mask rows are n_causal groups of that many rows, and the next draft comes
+    from group A (the continuation that kept exactly the accepted drafts).
     Returns the error word (0 on success; on error ``st`` is unchanged).
     """
     S = st.kv_len.shape[0]
@@ -294,7 +296,8 @@ def kv_commit(st, accept_len: np.ndarray, argmax: np.ndarray, n_causal: int, n_m
             new_bound[s] = kept[-1]
         if n_mask > 0:
             W = st.draft.shape[1]
-            new_draft[s] = argmax[s, n_causal:n_causal + W]
+            first = n_causal + (int(accept_len[s]) * draft_group if draft_group else 0)
+            new_draft[s] = argmax[s, first:first + W]
         new_fin[s] = 1 if stop else 0
 
     need = np.array([(int(new_len[s]) + R + page_size - 1) // page_size for s in range(S)],

@@ -98,14 +98,18 @@ class OracleModel:
     def mask_id(self) -> int:
         return self.V
 
-    def forward(self, x: np.ndarray, st, n_causal: int, n_mask: int) -> np.ndarray:
-        """Rows x [S, R, H] (already embedded) at positions kv_len[s] + r.
+    def forward(self, x: np.ndarray, st, n_causal: int, n_mask: int,
+                group: int = 0) -> np.ndarray:
+        """Rows x [S, R, H] (already embedded) at positions kv_len[s] + r
+        (``group`` > 0: mask rows in groups, at the positions of
+        ``attention.window_positions``, attending with the grouped mask).
 
-        Appends every layer's window K/V to the pools and returns logits
-        [S, R, V].
+        Appends every layer's window K/V to the pools (window row r at slot
+        kv_len[s] + r) and returns logits [S, R, V].
         """
         S, R, _ = x.shape
-        pos = st.kv_len[:, None].astype(np.int64) + np.arange(R)[None, :]
+        pos = np.stack([oattn.window_positions(int(L), n_causal, n_mask, group)
+                        for L in st.kv_len])
         scale = 1.0 / np.sqrt(self.D)
         for l in range(self.n_layers):
             h = rmsnorm(x, self.g_attn[l], self.eps)
@@ -116,7 +120,7 @@ class OracleModel:
             k = rope(k, pos, self.theta)
             o = oattn.attn_hybrid_block(q, k, v, self.k_pools[l], self.v_pools[l],
                                         st.page_table, st.kv_len, n_causal, n_mask, scale,
-                                        self.page_size)
+                                        self.page_size, group=group)
             x = x + o.reshape(S, R, self.Hq * self.D) @ self.wo[l]
             if self.ffn:
                 h2 = rmsnorm(x, self.g_mlp[l], self.eps)
@@ -141,6 +145,28 @@ class OracleModel:
         A = odec.accept(am, st.draft, B)
         err = odec.kv_commit(st, A, am, B, B, eos_id=eos_id, max_new=max_new,
                              page_size=self.page_size)
+        return logits, am, A, err
+
+    def multidraft_step(self, st, B: int, eos_id: int = -1, max_new=None):
+        """One self-speculative step with a draft per possible acceptance
+        (the structured-mask AR-diffusion hybrid the paper cites in its
+        related work): window [x0, d_1..d_{B-1}] (causal) followed by B groups
+        of B [M] rows.  Group k assumes A = k: its rows sit right after d_k
+        (at L + k + 1 + i, the first standing in for the unknown a_{k+1}),
+        see the cache, the causal rows 0..k and their own group.  After
+        acceptance A the next draft is group A's top-1 (rows 0..B-2 of the
+        group), so it is conditioned on the accepted tokens only.  Pages must
+        cover [L, L + B + B*B).  Returns (logits, argmax, accept_len, err)."""
+        S = st.kv_len.shape[0]
+        tok = np.empty((S, B + B * B), dtype=np.int64)
+        tok[:, 0] = st.boundary
+        tok[:, 1:B] = st.draft[:, :B - 1]
+        tok[:, B:] = self.mask_id
+        logits = self.forward(self.embed[tok], st, B, B * B, group=B)
+        am = odec.top1_rows(logits)
+        A = odec.accept(am, st.draft, B)
+        err = odec.kv_commit(st, A, am, B, B * B, eos_id=eos_id, max_new=max_new,
+                             page_size=self.page_size, draft_group=B)
         return logits, am, A, err
 
     def literal_round(self, st, B: int, eos_id: int = -1, max_new=None, tau_d=None):
