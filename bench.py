@@ -198,13 +198,27 @@ def run_decoder_stack(args):
             u = torch.rand((st.kv_len.shape[0], 2 * si.B + 2), device="cuda", generator=gen)
             dvs.literal_round_sampled(dm, st, si.B, SAMPLING_T, u, chunk_keys=chunk)
             return 2
+        if mode == "multidraft":
+            dvs.multidraft_step(dm, st, si.B, chunk_keys=chunk)
+            return 1
         dvs.draft_verify_step(dm, st, nc, nm, chunk_keys=chunk)
         return 1
 
+    # the multi-draft step's window is B + B*B rows: a state whose pages cover it
+    md_state = synth.stack_state(3, si.state.kv_len.shape[0], si.P, si.B, si.max_new,
+                                 si.B + si.B * si.B)
     for mode, (nc, nm) in (("fused", (si.B, si.B)), ("ar", (1, 0)), ("literal", (si.B + 1, 0)),
                            ("diffusion", (1, si.B)), ("refined", (si.B + 1, 0)),
-                           ("sampled", (si.B + 1, 0))):
-        st = dvs.DeviceState(wide if mode in ("literal", "diffusion", "refined", "sampled")
+                           ("sampled", (si.B + 1, 0)), ("multidraft", (si.B, si.B * si.B))):
+        if mode == "multidraft" and md_state.pool_pages > pool:
+            pool = md_state.pool_pages
+            kps = [torch.zeros((pool, w.Hkv, 16, w.D), dtype=torch.bfloat16, device="cuda")
+                   for _ in range(w.n_layers)]
+            vps = [torch.zeros((pool, w.Hkv, w.D, 16), dtype=torch.bfloat16, device="cuda")
+                   for _ in range(w.n_layers)]
+            dm = dvs.DeviceModel(w, kps, vps, "bf16")
+        st = dvs.DeviceState(md_state if mode == "multidraft" else
+                             wide if mode in ("literal", "diffusion", "refined", "sampled")
                              else si.state)
         dvs.prefill(dm, st, si.P, si.B, prefix_tokens=torch.from_numpy(si.prefix_tokens()).cuda(),
                     x_prefix=torch.from_numpy(si.x_prefix()).cuda(), chunk_keys=chunk)
@@ -281,6 +295,7 @@ def run_decoder_stack(args):
         "direct_diffusion": dict(res["diffusion"], tau_c=DIFFUSION_TAU_C),
         "refined_draft_round": dict(res["refined"], tau_d=DIFFUSION_TAU_C),
         "sampled_round": dict(res["sampled"], temperature=SAMPLING_T),
+        "multidraft_step": dict(res["multidraft"], window_rows=si.B + si.B * si.B),
         "note": "random weights accept almost no drafts, so the fused step commits about one "
                 "token per sequence and the two-forward round about two; their times are what a "
                 "trained model's step would cost.  Direct diffusion: a step is one block of B "

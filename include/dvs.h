@@ -121,6 +121,29 @@ int attn_hybrid_block(const void* q, const void* k_new, const void* v_new, void*
                       int32_t* err_word, void* workspace, size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
+ * attn_hybrid_block_grouped
+ *
+ * attn_hybrid_block with the mask rows cut into groups of mask_group rows
+ * (0: one group, which is attn_hybrid_block).  With G = n_mask / mask_group
+ * groups (G <= n_causal), row i of mask group g sees the cache, the causal
+ * rows 0 .. n_causal - G + g and, bidirectionally, the rows of its own group
+ * (window slots [L + n_causal + g*mask_group, L + n_causal + (g+1)*mask_group));
+ * causal rows are unchanged.  With G = n_causal = B and B rows per group,
+ * group k is the draft block of the continuation that keeps the causal rows
+ * 0..k: one draft per possible acceptance length, the structured-mask
+ * AR-diffusion hybrid the paper cites in its related work (multidraft_step).
+ * The window's K/V is appended at [L, L + R) in row order as before; query
+ * positions (rotary) are the caller's.  Workspace as attn_hybrid_block.
+ * ---------------------------------------------------------------------- */
+int attn_hybrid_block_grouped(const void* q, const void* k_new, const void* v_new, void* k_pool,
+                              void* v_pool, const int32_t* page_table, const int32_t* kv_len,
+                              int32_t S, int32_t n_causal, int32_t n_mask, int32_t mask_group,
+                              int32_t Hq, int32_t Hkv, int32_t D, int32_t max_pages,
+                              int32_t num_pool_pages, float softmax_scale, int32_t dtype,
+                              int32_t chunk_keys, void* out, int32_t* err_word, void* workspace,
+                              size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
  * attn_hybrid_block_noalloc
  *
  * For callers that cannot allocate device memory: code under HIP graph
@@ -240,8 +263,14 @@ int kv_commit(int32_t S, int32_t n_causal, int32_t n_mask, const int32_t* accept
  * exactly kv_commit with that A.  Arguments, layouts, errors and
  * requirements as kv_commit, with argmax from argmax_accept (which may then
  * skip its own acceptance: accept_len = NULL).
+ *   draft_group  0: the next draft is the mask rows' top-1, as kv_commit;
+ *                > 0: the mask rows are n_causal groups of draft_group rows
+ *                (attn_hybrid_block_grouped) and the next draft is group A's:
+ *                draft[s, j-1] = argmax[s, n_causal + A*draft_group + j - 1].
+ *                Needs n_mask == n_causal * draft_group >= draft_width.
  * ---------------------------------------------------------------------- */
-int accept_commit(int32_t S, int32_t n_causal, int32_t n_mask, const int32_t* argmax,
+int accept_commit(int32_t S, int32_t n_causal, int32_t n_mask, int32_t draft_group,
+                  const int32_t* argmax,
                   int32_t* accept_out, int32_t* kv_len, int32_t* page_table, int32_t* num_pages,
                   int32_t max_pages, int32_t* free_stack, int32_t* free_top,
                   int32_t num_pool_pages, int32_t* boundary, int32_t* draft, int32_t draft_width,
@@ -365,6 +394,33 @@ int kv_commit_block(int32_t S, int32_t B, const int32_t* block, int32_t* kv_len,
 int draft_verify_step(const dvs_model* m, const dvs_state* st, int32_t n_causal, int32_t n_mask,
                       int32_t chunk_keys, float* logits_out, int32_t* argmax_out,
                       int32_t* accept_out, void* workspace, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * multidraft_step
+ *
+ * draft_verify_step with one draft block per possible acceptance length:
+ * the window is the B causal rows [x0, d_1..d_{B-1}] followed by B groups
+ * of B mask rows (R = B + B*B).  Group k assumes A = k: its rows sit at
+ * positions L + k + 1 + i (i = 0..B-1; the first stands in for the
+ * not-yet-known a_{k+1}, as the paper's draft forward puts [M] where a0
+ * will be), attend to the cache, the causal rows 0..k and their own group
+ * (attn_hybrid_block_grouped), and predict the tokens after d_1..d_k,
+ * a_{k+1}.  Acceptance and commit are draft_verify_step's, except that the
+ * next draft is group A's top-1 (accept_commit with draft_group = B), so it
+ * is conditioned on the accepted drafts only -- never on a rejected one.
+ * This is the structured-mask AR-diffusion hybrid of the paper's related
+ * work, applied to the fused step; B = 1 is the fused step.  Group k's
+ * outputs equal the mask rows of a fused call that verifies only x0,
+ * d_1..d_k (n_causal = k + 1).
+ * Pages must cover [L, L + B + B*B) (accept_commit leaves them so for the
+ * next call); draft_width B - 1 or B.  logits_out [S*(B + B*B), vocab],
+ * argmax_out [S*(B + B*B)], accept_out [S] optional as draft_verify_step.
+ * workspace: dvs_step_workspace_bytes(m, S, B, B*B, max_pages, chunk_keys).
+ * With chunk_keys > 0 every committed token equals greedy AR's bit for bit.
+ * ---------------------------------------------------------------------- */
+int multidraft_step(const dvs_model* m, const dvs_state* st, int32_t B, int32_t chunk_keys,
+                    float* logits_out, int32_t* argmax_out, int32_t* accept_out,
+                    void* workspace, size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
  * literal_round

@@ -86,9 +86,32 @@ struct AttnParams {
   int n_chunks_max;  // aligned: grid rows
   int share_min;     // balanced: minimum tiles per workgroup
   int max_segs;      // partial slots per item
+  int group;         // mask rows per group (0: one block of n_mask rows)
+  int n_groups;      // n_mask / group
   float scale_log2;
   float scale;
 };
+
+// Second visible interval of window row r (beside keys <= hi): the slots of
+// its own mask group when the mask rows come in groups.  Row i of mask group
+// g sees the cache, the causal rows 0 .. n_causal - n_groups + g (so hi =
+// L + n_causal - n_groups + g) and the slots [lo2, hi2] of its group.  Empty
+// (lo2 > hi2) for causal rows and for one group, where hi covers the whole
+// window.
+struct Vis2 {
+  int lo2, hi2;
+};
+__device__ __forceinline__ Vis2 group_interval(const AttnParams& p, int L, int r) {
+  if (p.group == 0 || r < p.n_causal) return Vis2{1 << 30, -1};
+  const int g = (r - p.n_causal) / p.group;
+  const int lo = L + p.n_causal + g * p.group;
+  return Vis2{lo, lo + p.group - 1};
+}
+__device__ __forceinline__ int row_hi(const AttnParams& p, int L, int r) {
+  if (r < p.n_causal) return L + r;
+  if (p.group == 0) return L + p.R - 1;
+  return L + p.n_causal - p.n_groups + (r - p.n_causal) / p.group;
+}
 
 // ---------------------------------------------------------------------------
 // LDS layouts of one 64-key tile (bf16)
@@ -512,7 +535,7 @@ __global__ void __launch_bounds__(NW * 64, 1) attn_bf16_kernel(AttnParams p) {
     const bool rvalid = n < p.rows_total;
     const int r = n / p.G;
     const int h = kvh * p.G + (n - r * p.G);
-    const int hi = !rvalid ? -1 : (r < p.n_causal ? L + r : T - 1);
+    const int hi = !rvalid ? -1 : row_hi(p, L, r);
     bf16x8 qf[KS];
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks)
@@ -555,12 +578,13 @@ __global__ void __launch_bounds__(NW * 64, 1) attn_bf16_kernel(AttnParams p) {
           sacc[kg] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[ks & 1][kg], qf[ks], sacc[kg], 0, 0, 0);
       }
       if (masked) {
+        const Vis2 v2 = rvalid ? group_interval(p, L, r) : Vis2{1 << 30, -1};
 #pragma unroll
         for (int kg = 0; kg < KG; ++kg)
 #pragma unroll
           for (int i = 0; i < 16; ++i) {
             const int key = key0 + kg * 32 + 16 * (i >> 3) + 8 * hh + (i & 7);
-            if (key > hi) sacc[kg][i] = -INFINITY;
+            if (key > hi && (key < v2.lo2 || key > v2.hi2)) sacc[kg][i] = -INFINITY;
           }
       }
       // tile max: a tree over the lane's 16*KG scores, then lane^32
@@ -958,7 +982,7 @@ __global__ void __launch_bounds__(NP * 128, 1) attn_bf16_pc_kernel(AttnParams p)
         rvalid[g] = n < p.rows_total;
         rr[g] = n / p.G;
         hq[g] = kvh * p.G + (n - rr[g] * p.G);
-        hi[g] = !rvalid[g] ? -1 : (rr[g] < p.n_causal ? L + rr[g] : T - 1);
+        hi[g] = !rvalid[g] ? -1 : row_hi(p, L, rr[g]);
       }
 
       auto stage_pages = [&](int ja, int jb) {
@@ -1125,12 +1149,13 @@ __global__ void __launch_bounds__(NP * 128, 1) attn_bf16_pc_kernel(AttnParams p)
 #pragma unroll
           for (int g = 0; g < 2; ++g) {
             if (masked) {
+              const Vis2 v2 = rvalid[g] ? group_interval(p, L, rr[g]) : Vis2{1 << 30, -1};
 #pragma unroll
               for (int kg = 0; kg < 2; ++kg)
 #pragma unroll
                 for (int i = 0; i < 16; ++i) {
                   const int key = key0 + kg * 32 + 16 * (i >> 3) + 8 * hh + (i & 7);
-                  if (key > hi[g]) sacc[g][kg][i] = -INFINITY;
+                  if (key > hi[g] && (key < v2.lo2 || key > v2.hi2)) sacc[g][kg][i] = -INFINITY;
                 }
             }
             // tile max: two running max3 chains (one per 32-key group); a
@@ -1504,7 +1529,9 @@ __global__ void __launch_bounds__(256) attn_f32_kernel(AttnParams p) {
     if (r == 0 && h == 0 && tid == 0) set_err(p.err, DVS_ERR_MAX_PAGES);
     return;
   }
-  const int hi = r < p.n_causal ? L + r : T - 1;
+  const int hi = row_hi(p, L, r);
+  const Vis2 v2 = group_interval(p, L, r);
+  const int hend = v2.hi2 > hi ? v2.hi2 : hi;   // last visible key
   const float* q = (const float*)p.q;
   const float* kn = (const float*)p.k_new;
   const float* vn = (const float*)p.v_new;
@@ -1529,10 +1556,10 @@ __global__ void __launch_bounds__(256) attn_f32_kernel(AttnParams p) {
 
   float m = -INFINITY, l = 0.f, acc = 0.f;
   bool bad = false;
-  for (int t0 = 0; t0 <= hi; t0 += 256) {
+  for (int t0 = 0; t0 <= hend; t0 += 256) {
     const int k = t0 + tid;
     float sc = -INFINITY;
-    if (k <= hi) {
+    if (k <= hi || (k >= v2.lo2 && k <= v2.hi2)) {
       const float* krow = nullptr;
       if (k < L) {
         const int pg = pt[k >> 4];
@@ -1568,7 +1595,7 @@ __global__ void __launch_bounds__(256) attn_f32_kernel(AttnParams p) {
     m = mnew;
     if (tid < D) {
       float a = acc * alpha;
-      const int nk = min(256, hi + 1 - t0);
+      const int nk = min(256, hend + 1 - t0);
       for (int j = 0; j < nk; ++j) {
         const int kk = t0 + j;
         float vv;
@@ -1727,7 +1754,7 @@ static int attn_launch(const void* q, const void* k_new, const void* v_new, void
                        int32_t max_pages, int32_t num_pool_pages, float softmax_scale,
                        int32_t dtype, int32_t chunk_keys, void* out, int32_t* err_word,
                        void* workspace, size_t ws_bytes, void* stream, size_t scratch_cap,
-                       bool check_only = false) {
+                       bool check_only = false, int32_t mask_group = 0) {
   DVS_CHECK_ARG(q && k_new && v_new && k_pool && v_pool && page_table && kv_len && out,
                 "attn_hybrid_block: NULL array argument");
   DVS_CHECK_ARG(S >= 1 && n_causal >= 0 && n_mask >= 0 && n_causal + n_mask >= 1,
@@ -1740,6 +1767,11 @@ static int attn_launch(const void* q, const void* k_new, const void* v_new, void
                 "attn_hybrid_block: chunk_keys must be a multiple of 64 and <= %d", MAX_CHUNK_KEYS);
   DVS_CHECK_SUPPORTED(dtype == DVS_F32 || dtype == DVS_BF16, "attn_hybrid_block: dtype %d", dtype);
   DVS_CHECK_SUPPORTED(D == 64 || D == 96 || D == 128, "attn_hybrid_block: head_dim %d", D);
+  DVS_CHECK_ARG(mask_group >= 0 && (mask_group == 0 || n_mask % mask_group == 0),
+                "attn_hybrid_block: mask_group must divide n_mask");
+  const int n_groups = mask_group > 0 ? n_mask / mask_group : 1;
+  DVS_CHECK_ARG(n_groups <= 1 || n_groups <= n_causal,
+                "attn_hybrid_block: %d mask groups need as many causal rows", n_groups);
   const int R = n_causal + n_mask;
   AttnPlan pl = plan_attn(S, R, Hq, Hkv, D, max_pages, chunk_keys, dtype);
   if (scratch_cap > 0 && dtype == DVS_BF16 && pl.bytes > scratch_cap) {
@@ -1760,6 +1792,8 @@ static int attn_launch(const void* q, const void* k_new, const void* v_new, void
   prm.rows_total = pl.rows_total; prm.n_row_tiles = pl.n_row_tiles; prm.n_items = pl.n_items;
   prm.balanced = pl.balanced; prm.chunk_tiles = pl.chunk_tiles;
   prm.n_chunks_max = pl.n_chunks_max; prm.share_min = pl.share_min; prm.max_segs = pl.max_segs;
+  prm.group = n_groups > 1 ? mask_group : 0;
+  prm.n_groups = n_groups;
   prm.scale = softmax_scale;
   prm.scale_log2 = softmax_scale * 1.4426950408889634f;
   hipStream_t st = (hipStream_t)stream;
@@ -1799,6 +1833,21 @@ extern "C" int attn_hybrid_block(const void* q, const void* k_new, const void* v
   return attn_launch(q, k_new, v_new, k_pool, v_pool, page_table, kv_len, S, n_causal, n_mask,
                      Hq, Hkv, D, max_pages, num_pool_pages, softmax_scale, dtype, chunk_keys, out,
                      err_word, workspace, ws_bytes, stream, 0);
+}
+
+extern "C" int attn_hybrid_block_grouped(const void* q, const void* k_new, const void* v_new,
+                                         void* k_pool, void* v_pool, const int32_t* page_table,
+                                         const int32_t* kv_len, int32_t S, int32_t n_causal,
+                                         int32_t n_mask, int32_t mask_group, int32_t Hq,
+                                         int32_t Hkv, int32_t D, int32_t max_pages,
+                                         int32_t num_pool_pages, float softmax_scale,
+                                         int32_t dtype, int32_t chunk_keys, void* out,
+                                         int32_t* err_word, void* workspace, size_t ws_bytes,
+                                         void* stream) {
+  clear_error();
+  return attn_launch(q, k_new, v_new, k_pool, v_pool, page_table, kv_len, S, n_causal, n_mask,
+                     Hq, Hkv, D, max_pages, num_pool_pages, softmax_scale, dtype, chunk_keys, out,
+                     err_word, workspace, ws_bytes, stream, 0, false, mask_group);
 }
 
 // ---------------------------------------------------------------------------

@@ -60,6 +60,7 @@ struct CommitParams {
   const int32_t* accept_len;   // NULL: the run is the first n_causal tokens of argmax
   int accept_here;             // 1: A computed in this kernel from argmax and draft
   int32_t* accept_out;         // accept_here: A per sequence (may be NULL)
+  int draft_group;             // > 0: next draft from mask group A (groups of this many rows)
   const int32_t* argmax;
   int32_t* kv_len;
   int32_t* page_table;
@@ -205,7 +206,8 @@ __global__ void __launch_bounds__(COMMIT_THREADS) kv_commit_kernel(CommitParams 
           int tk[RUN_CHUNK];
 #pragma unroll
           for (int u = 0; u < RUN_CHUNK; ++u)
-            tk[u] = p.argmax[(size_t)s * p.R + p.n_causal + min(j0 + u, p.draft_width - 1)];
+            tk[u] = p.argmax[(size_t)s * p.R + p.n_causal + A * p.draft_group +
+                             min(j0 + u, p.draft_width - 1)];
 #pragma unroll
           for (int u = 0; u < RUN_CHUNK; ++u)
             if (j0 + u < p.draft_width) p.draft[(size_t)s * p.draft_width + j0 + u] = tk[u];
@@ -222,7 +224,7 @@ using namespace dvs;
 
 static int launch_commit(const char* who, int32_t S, int32_t n_causal, int32_t n_mask,
                          int32_t window, const int32_t* lead, const int32_t* accept_len,
-                         int accept_here, int32_t* accept_out,
+                         int accept_here, int32_t* accept_out, int32_t draft_group,
                          const int32_t* argmax, int32_t* kv_len, int32_t* page_table,
                          int32_t* num_pages, int32_t max_pages, int32_t* free_stack,
                          int32_t* free_top, int32_t num_pool_pages, int32_t* boundary,
@@ -246,7 +248,11 @@ static int launch_commit(const char* who, int32_t S, int32_t n_causal, int32_t n
   p.lead = lead;
   p.max_pages = max_pages; p.pool_pages = num_pool_pages; p.draft_width = draft_width;
   p.max_new = max_new; p.eos_id = eos_id;
+  DVS_CHECK_ARG(draft_group >= 0 && (draft_group == 0 ||
+                                     (n_mask == n_causal * draft_group && draft_group >= draft_width)),
+                "%s: mask rows must be n_causal groups of draft_group >= draft_width rows", who);
   p.accept_len = accept_len; p.accept_here = accept_here; p.accept_out = accept_out;
+  p.draft_group = draft_group;
   p.argmax = argmax; p.kv_len = kv_len; p.page_table = page_table;
   p.num_pages = num_pages; p.free_stack = free_stack; p.free_top = free_top;
   p.boundary = boundary; p.draft = draft; p.out_tokens = out_tokens; p.out_count = out_count;
@@ -265,7 +271,7 @@ extern "C" int kv_commit(int32_t S, int32_t n_causal, int32_t n_mask, const int3
   clear_error();
   DVS_CHECK_ARG(accept_len != nullptr, "kv_commit: NULL accept_len");
   return launch_commit("kv_commit", S, n_causal, n_mask, n_causal + n_mask, nullptr, accept_len,
-                       0, nullptr, argmax, kv_len, page_table, num_pages, max_pages, free_stack, free_top,
+                       0, nullptr, 0, argmax, kv_len, page_table, num_pages, max_pages, free_stack, free_top,
                        num_pool_pages, boundary, draft, draft_width, out_tokens, out_count, max_new,
                        eos_id, finished, err_word, stream);
 }
@@ -280,7 +286,7 @@ extern "C" int kv_commit_round(int32_t S, int32_t B, const int32_t* lead, const 
   clear_error();
   DVS_CHECK_ARG(lead != nullptr && accept_len != nullptr, "kv_commit_round: NULL lead/accept_len");
   DVS_CHECK_ARG(B >= 1, "kv_commit_round: need B >= 1");
-  return launch_commit("kv_commit_round", S, B + 1, 0, B + 2, lead, accept_len, 0, nullptr,
+  return launch_commit("kv_commit_round", S, B + 1, 0, B + 2, lead, accept_len, 0, nullptr, 0,
                        argmax, kv_len,
                        page_table, num_pages, max_pages, free_stack, free_top, num_pool_pages,
                        boundary, draft, draft_width, out_tokens, out_count, max_new, eos_id,
@@ -298,15 +304,15 @@ extern "C" int kv_commit_block(int32_t S, int32_t B, const int32_t* block, int32
   DVS_CHECK_ARG(B >= 1, "kv_commit_block: need B >= 1");
   // run token j < B - 1 comes from the draft slot j, the last from argmax[B - 1]:
   // both are the block row
-  return launch_commit("kv_commit_block", S, B, 0, B + 1, nullptr, nullptr, 0, nullptr, block,
-                       kv_len,
+  return launch_commit("kv_commit_block", S, B, 0, B + 1, nullptr, nullptr, 0, nullptr, 0,
+                       block, kv_len,
                        page_table, num_pages, max_pages, free_stack, free_top, num_pool_pages,
                        boundary, const_cast<int32_t*>(block), B, out_tokens, out_count, max_new,
                        eos_id, finished, err_word, stream);
 }
 
-extern "C" int accept_commit(int32_t S, int32_t n_causal, int32_t n_mask, const int32_t* argmax,
-                             int32_t* accept_out, int32_t* kv_len, int32_t* page_table,
+extern "C" int accept_commit(int32_t S, int32_t n_causal, int32_t n_mask, int32_t draft_group,
+                             const int32_t* argmax, int32_t* accept_out, int32_t* kv_len, int32_t* page_table,
                              int32_t* num_pages, int32_t max_pages, int32_t* free_stack,
                              int32_t* free_top, int32_t num_pool_pages, int32_t* boundary,
                              int32_t* draft, int32_t draft_width, int32_t* out_tokens,
@@ -315,7 +321,7 @@ extern "C" int accept_commit(int32_t S, int32_t n_causal, int32_t n_mask, const 
   clear_error();
   DVS_CHECK_ARG(draft || n_causal == 1, "accept_commit: NULL draft");
   return launch_commit("accept_commit", S, n_causal, n_mask, n_causal + n_mask, nullptr, nullptr,
-                       1, accept_out, argmax, kv_len, page_table, num_pages, max_pages,
+                       1, accept_out, draft_group, argmax, kv_len, page_table, num_pages, max_pages,
                        free_stack, free_top, num_pool_pages, boundary, draft, draft_width,
                        out_tokens, out_count, max_new, eos_id, finished, err_word, stream);
 }

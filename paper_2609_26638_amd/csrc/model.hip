@@ -142,11 +142,24 @@ __global__ void __launch_bounds__(256) rmsnorm_kernel(const float* __restrict__ 
     out[(size_t)mrow * H + i] = from_f<T>(xr[i] * inv * to_f(g[i]));
 }
 
-// rotate-half rotary embedding, in place, position kv_len[s] + r; angles in
-// double precision (positions reach thousands of radians).
+// Position of window row r relative to kv_len: r, except for mask rows cut
+// into groups of `group` rows (G = n_mask / group groups), where row i of
+// group g sits right after the last causal row the group sees:
+// n_causal - G + g + 1 + i (one group gives r again).
+__device__ __forceinline__ int window_offset(int r, int n_causal, int n_mask, int group) {
+  if (r < n_causal || group <= 0) return r;
+  const int n_groups = n_mask / group;
+  const int g = (r - n_causal) / group, i = (r - n_causal) - g * group;
+  return n_causal - n_groups + g + 1 + i;
+}
+
+// rotate-half rotary embedding, in place, at position kv_len[s] +
+// window_offset(r); angles in double precision (positions reach thousands
+// of radians).
 template <typename T>
 __global__ void rope_kernel(T* __restrict__ x, int M, int R, int nh, int D, double log2_theta,
-                            const int32_t* __restrict__ kv_len) {
+                            const int32_t* __restrict__ kv_len, int n_causal, int n_mask,
+                            int group) {
   const int half = D / 2;
   const long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x;
   if (idx >= (long long)M * nh * half) return;
@@ -154,7 +167,7 @@ __global__ void rope_kernel(T* __restrict__ x, int M, int R, int nh, int D, doub
   const long long mh = idx / half;
   const int mrow = (int)(mh / nh);
   const int s = mrow / R, r = mrow - s * R;
-  const double pos = (double)(kv_len[s] + r);
+  const double pos = (double)(kv_len[s] + window_offset(r, n_causal, n_mask, group));
   const double inv = exp2(-2.0 * i / D * log2_theta);
   double sn, cs;
   sincos(pos * inv, &sn, &cs);
@@ -766,7 +779,8 @@ static int gemm(const StepLayout& L, char* ws, int dtype, const void* A, const v
 // RMSNorm output in h.  The window is (n_causal, n_mask) rows per sequence.
 template <typename T>
 static int forward_layers(const dvs_model* m, const dvs_state* st, int n_causal, int n_mask,
-                          int chunk_keys, const StepLayout& L, char* ws, hipStream_t stream) {
+                          int chunk_keys, const StepLayout& L, char* ws, hipStream_t stream,
+                          int group = 0) {
   const int S = st->S, R = n_causal + n_mask, M = S * R;
   const int H = m->hidden, D = m->head_dim, Hq = m->n_heads, Hkv = m->n_kv_heads;
   const int dt = m->dtype;
@@ -803,14 +817,15 @@ static int forward_layers(const dvs_model* m, const dvs_state* st, int n_causal,
     if ((rc = gemm(L, ws, dt, h, ly.wv, M, Hkv * D, H, v, 0, 0, stream))) return rc;
     const long long nq = (long long)M * Hq * (D / 2), nk = (long long)M * Hkv * (D / 2);
     hipLaunchKernelGGL(rope_kernel<T>, dim3((unsigned)((nq + 255) / 256)), dim3(256), 0, stream, q, M,
-                       R, Hq, D, log2_theta, st->kv_len);
+                       R, Hq, D, log2_theta, st->kv_len, n_causal, n_mask, group);
     hipLaunchKernelGGL(rope_kernel<T>, dim3((unsigned)((nk + 255) / 256)), dim3(256), 0, stream, k, M,
-                       R, Hkv, D, log2_theta, st->kv_len);
+                       R, Hkv, D, log2_theta, st->kv_len, n_causal, n_mask, group);
     if ((rc = launch_status("draft_verify_step(rope)"))) return rc;
-    rc = attn_hybrid_block(q, k, v, ly.k_pool, ly.v_pool, st->page_table, st->kv_len, S, n_causal,
-                           n_mask, Hq, Hkv, D, st->max_pages, st->num_pool_pages,
-                           (float)(1.0 / sqrt((double)D)), dt, chunk_keys, att, st->err_word,
-                           ws + L.attn_ws, L.attn_bytes, stream);
+    rc = attn_hybrid_block_grouped(q, k, v, ly.k_pool, ly.v_pool, st->page_table, st->kv_len, S,
+                                   n_causal, n_mask, group, Hq, Hkv, D, st->max_pages,
+                                   st->num_pool_pages, (float)(1.0 / sqrt((double)D)), dt,
+                                   chunk_keys, att, st->err_word, ws + L.attn_ws, L.attn_bytes,
+                                   stream);
     if (rc) return rc;
     if ((rc = gemm(L, ws, dt, att, ly.wo, M, H, Hq * D, x, 1, 1, stream))) return rc;
     if (m->ffn > 0) {
@@ -833,7 +848,8 @@ static int forward_layers(const dvs_model* m, const dvs_state* st, int n_causal,
 template <typename T>
 static int run_step(const dvs_model* m, const dvs_state* st, int n_causal, int n_mask,
                     int chunk_keys, const StepLayout& L, char* ws, float* logits_out,
-                    int32_t* argmax_out, int32_t* accept_out, hipStream_t stream) {
+                    int32_t* argmax_out, int32_t* accept_out, hipStream_t stream,
+                    int group = 0) {
   const int S = st->S, R = n_causal + n_mask, M = S * R;
   float* logits = logits_out ? logits_out : (float*)(ws + L.logits);
   int32_t* am = argmax_out ? argmax_out : (int32_t*)(ws + L.am);
@@ -843,14 +859,14 @@ static int run_step(const dvs_model* m, const dvs_state* st, int n_causal, int n
                      nullptr, 0, (float*)(ws + L.x));
   int rc;
   if ((rc = launch_status("draft_verify_step(embed)"))) return rc;
-  if ((rc = forward_layers<T>(m, st, n_causal, n_mask, chunk_keys, L, ws, stream))) return rc;
+  if ((rc = forward_layers<T>(m, st, n_causal, n_mask, chunk_keys, L, ws, stream, group))) return rc;
   if ((rc = gemm(L, ws, m->dtype, ws + L.h, m->lm_head, M, m->vocab, m->hidden, logits, 1, 0, stream)))
     return rc;
   rc = argmax_accept(logits, DVS_F32, S, R, m->vocab, n_causal, st->draft, st->draft_width, am,
                      nullptr, st->err_word, stream);
   if (rc) return rc;
   // acceptance inside the commit kernel
-  return accept_commit(S, n_causal, n_mask, am, acc, st->kv_len, st->page_table, st->num_pages,
+  return accept_commit(S, n_causal, n_mask, group, am, acc, st->kv_len, st->page_table, st->num_pages,
                        st->max_pages, st->free_stack, st->free_top, st->num_pool_pages,
                        st->boundary, st->draft, st->draft_width, st->out_tokens, st->out_count,
                        st->max_new, st->eos_id, st->finished, st->err_word, stream);
@@ -1128,6 +1144,34 @@ extern "C" int draft_verify_step(const dvs_model* m, const dvs_state* st, int32_
                             argmax_out, accept_out, s);
   return run_step<float>(m, st, n_causal, n_mask, chunk_keys, L, (char*)workspace, logits_out,
                          argmax_out, accept_out, s);
+}
+
+static int check_model_state(const dvs_model* m, const dvs_state* st, const char* who);
+
+extern "C" int multidraft_step(const dvs_model* m, const dvs_state* st, int32_t B,
+                               int32_t chunk_keys, float* logits_out, int32_t* argmax_out,
+                               int32_t* accept_out, void* workspace, size_t ws_bytes,
+                               void* stream) {
+  clear_error();
+  DVS_CHECK_ARG(model_ok(m), "multidraft_step: invalid model description");
+  DVS_CHECK_ARG(B >= 1 && B <= 64, "multidraft_step: need 1 <= B <= 64");
+  int rc = check_model_state(m, st, "multidraft_step");
+  if (rc) return rc;
+  DVS_CHECK_ARG(st->draft_width >= B - 1 && st->draft_width <= B,
+                "multidraft_step: draft width must be B - 1 or B");
+  const int n_mask = B * B;
+  const StepLayout L = step_layout(m, st->S, B, n_mask, st->max_pages, chunk_keys,
+                                   (size_t)st->S * (B + n_mask));
+  if (!workspace || ws_bytes < L.total) {
+    set_error("multidraft_step: workspace needs %zu bytes, got %zu", L.total, ws_bytes);
+    return DVS_EWORKSPACE;
+  }
+  hipStream_t s = (hipStream_t)stream;
+  if (m->dtype == DVS_BF16)
+    return run_step<__bf16>(m, st, B, n_mask, chunk_keys, L, (char*)workspace, logits_out,
+                            argmax_out, accept_out, s, B);
+  return run_step<float>(m, st, B, n_mask, chunk_keys, L, (char*)workspace, logits_out, argmax_out,
+                         accept_out, s, B);
 }
 
 extern "C" int literal_round(const dvs_model* m, const dvs_state* st, int32_t B,

@@ -46,7 +46,7 @@ _SIGS = {
     "kv_commit": ([_c_int, _c_int, _c_int, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_int, _c_ptr,
                    _c_ptr, _c_int, _c_ptr, _c_ptr, _c_int, _c_ptr, _c_ptr, _c_int, _c_int, _c_ptr,
                    _c_ptr, _c_ptr], _c_int),
-    "accept_commit": ([_c_int, _c_int, _c_int, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_int,
+    "accept_commit": ([_c_int, _c_int, _c_int, _c_int, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_int,
                        _c_ptr, _c_ptr, _c_int, _c_ptr, _c_ptr, _c_int, _c_ptr, _c_ptr, _c_int,
                        _c_int, _c_ptr, _c_ptr, _c_ptr], _c_int),
     "kv_commit_round": ([_c_int, _c_int, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_int,
@@ -86,6 +86,11 @@ _SIGS["dvs_step_workspace_bytes"] = ([ctypes.POINTER(DvsModel), _c_int, _c_int, 
 _SIGS["draft_verify_step"] = ([ctypes.POINTER(DvsModel), ctypes.POINTER(DvsState), _c_int, _c_int,
                                _c_int, _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_size, _c_ptr], _c_int)
 
+_SIGS["multidraft_step"] = ([ctypes.POINTER(DvsModel), ctypes.POINTER(DvsState), _c_int, _c_int,
+                             _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_size, _c_ptr], _c_int)
+_SIGS["attn_hybrid_block_grouped"] = ([_c_ptr] * 7 + [_c_int] * 9 + [_c_f32, _c_int, _c_int,
+                                                                     _c_ptr, _c_ptr, _c_ptr,
+                                                                     _c_size, _c_ptr], _c_int)
 _SIGS["literal_round"] = ([ctypes.POINTER(DvsModel), ctypes.POINTER(DvsState), _c_int, _c_int,
                            _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_size, _c_ptr], _c_int)
 
@@ -389,7 +394,7 @@ class DeviceState:
 
 
 def accept_commit(st: DeviceState, argmax, n_causal: int, n_mask: int, accept_out=None,
-                  eos_id: int = -1, stream=None):
+                  eos_id: int = -1, draft_group: int = 0, stream=None):
     """Acceptance, commit and rollback in one kernel; returns accept_out [S] int32."""
     S = st.kv_len.shape[0]
     _dev(argmax, torch.int32, "argmax", 2)
@@ -398,7 +403,7 @@ def accept_commit(st: DeviceState, argmax, n_causal: int, n_mask: int, accept_ou
     if accept_out is None:
         accept_out = torch.empty((S,), dtype=torch.int32, device=argmax.device)
     _dev(accept_out, torch.int32, "accept_out", 1)
-    rc = lib().accept_commit(S, n_causal, n_mask, _ptr(argmax), _ptr(accept_out), _ptr(st.kv_len),
+    rc = lib().accept_commit(S, n_causal, n_mask, int(draft_group), _ptr(argmax), _ptr(accept_out), _ptr(st.kv_len),
                              _ptr(st.page_table), _ptr(st.num_pages), st.max_pages,
                              _ptr(st.free_stack), _ptr(st.free_top), st.pool_pages,
                              _ptr(st.boundary), _ptr(st.draft), st.draft.shape[1],
@@ -554,6 +559,48 @@ def draft_verify_step(model: DeviceModel, st: DeviceState, n_causal: int, n_mask
                                  _ptr(accept_out), _ptr(model.ws.buf), model.ws.nbytes,
                                  _stream(stream))
     _check(rc, "draft_verify_step")
+
+
+def multidraft_step(model: DeviceModel, st: DeviceState, B: int,
+                    chunk_keys: int = MODEL_CHUNK_KEYS, eos_id: int = -1, logits_out=None,
+                    argmax_out=None, accept_out=None, stream=None):
+    """One fused step with a draft block per possible acceptance (B groups of
+    B mask rows; the next draft comes from group A) on the device."""
+    S = st.kv_len.shape[0]
+    need = model.workspace_bytes(S, B, B * B, st.max_pages, chunk_keys)
+    if need == 0:
+        raise DvsError("multidraft_step: invalid configuration")
+    if model.ws is None or model.ws.nbytes < need:
+        model.ws = Workspace(need, device=st.kv_len.device)
+    for t, name in ((logits_out, "logits_out"), (argmax_out, "argmax_out"), (accept_out, "accept_out")):
+        if t is not None:
+            _dev(t, torch.float32 if name == "logits_out" else torch.int32, name)
+    sd = _state_desc(st, eos_id)
+    rc = lib().multidraft_step(ctypes.byref(model.desc), ctypes.byref(sd), B, int(chunk_keys),
+                               _ptr(logits_out), _ptr(argmax_out), _ptr(accept_out),
+                               _ptr(model.ws.buf), model.ws.nbytes, _stream(stream))
+    _check(rc, "multidraft_step")
+
+
+def attn_hybrid_block_grouped(q, k_new, v_new, k_pool, v_pool, page_table, kv_len, n_causal: int,
+                              n_mask: int, mask_group: int, softmax_scale: float, out=None,
+                              err=None, workspace=None, chunk_keys: int = 0, stream=None):
+    """attn_hybrid_block with the mask rows in groups of mask_group rows."""
+    S, R, Hq, Hkv, D, P, max_pages, out = _attn_args(q, k_new, v_new, k_pool, v_pool, page_table,
+                                                     kv_len, n_causal, n_mask, out, err)
+    code = _dtype_code(q)
+    need = attn_workspace_bytes(S, n_causal, n_mask, Hq, Hkv, D, max_pages, chunk_keys, code)
+    if workspace is None:
+        workspace = Workspace(need, device=q.device)
+    workspace.prepare(need, ("attn", S, R, Hq, Hkv, D, max_pages, int(chunk_keys), code))
+    rc = lib().attn_hybrid_block_grouped(_ptr(q), _ptr(k_new), _ptr(v_new), _ptr(k_pool),
+                                         _ptr(v_pool), _ptr(page_table), _ptr(kv_len), S, n_causal,
+                                         n_mask, int(mask_group), Hq, Hkv, D, max_pages, P,
+                                         float(softmax_scale), code, int(chunk_keys), _ptr(out),
+                                         _ptr(err), _ptr(workspace.buf), workspace.nbytes,
+                                         _stream(stream))
+    _check(rc, "attn_hybrid_block_grouped")
+    return out
 
 
 def literal_round(model: DeviceModel, st: DeviceState, B: int, chunk_keys: int = MODEL_CHUNK_KEYS,

@@ -429,6 +429,20 @@ class StackInputs:
         return x
 
 
+def stack_state(seed: int, S: int, P: int, B: int, max_new: int, window: int) -> PagedState:
+    """Fresh decode state for a prefix of P rows (kv_len = 0): pages for the
+    prefill and a window of `window` rows, scattered, and a pool with room
+    for max_new tokens of growth per sequence."""
+    ss = np.random.SeedSequence([seed, 0x5AC4])
+    r_pages = np.random.Generator(np.random.PCG64(ss.spawn(3)[2]))
+    max_pages = (P + max_new + window + PAGE_SIZE - 1) // PAGE_SIZE + 2
+    growth = S * ((max_new + window + PAGE_SIZE - 1) // PAGE_SIZE + 2)
+    st = make_paged_state(r_pages, np.full(S, P, dtype=np.int64), window, max_pages, scatter=True,
+                          slack=0.0, extra_pages=growth, n_causal=B, max_new=max_new)
+    st.kv_len[:] = 0
+    return st
+
+
 def decoder_stack_inputs(seed: int = 3, S: int = 8, n_layers: int = 16, H: int = 1536,
                          Hq: int = 16, Hkv: int = 4, D: int = 96, ffn: int = 4096, V: int = 65536,
                          n_vision: int = 1024, n_prompt: int = 64, B: int = 16,
@@ -437,14 +451,9 @@ def decoder_stack_inputs(seed: int = 3, S: int = 8, n_layers: int = 16, H: int =
     vision embeddings N(0, 1) plus uniform prompt tokens, block size B."""
     w = make_model_weights(seed, V, H, Hq, Hkv, D, n_layers, ffn, std=0.02)
     ss = np.random.SeedSequence([seed, 0x5AC4])
-    r_vis, r_prompt, r_pages = [np.random.Generator(np.random.PCG64(c)) for c in ss.spawn(3)]
+    r_vis, r_prompt, _ = [np.random.Generator(np.random.PCG64(c)) for c in ss.spawn(3)]
     vision = _normal(r_vis, (S, n_vision, H), 1.0)
     prompt = r_prompt.integers(0, V, size=(S, n_prompt)).astype(np.int32)
     P = n_vision + n_prompt
-    R = 2 * B
-    max_pages = (P + max_new + R + PAGE_SIZE - 1) // PAGE_SIZE + 2
-    growth = S * ((max_new + R + PAGE_SIZE - 1) // PAGE_SIZE + 2)
-    st = make_paged_state(r_pages, np.full(S, P, dtype=np.int64), R, max_pages, scatter=True,
-                          slack=0.0, extra_pages=growth, n_causal=B, max_new=max_new)
-    st.kv_len[:] = 0
+    st = stack_state(seed, S, P, B, max_new, 2 * B)
     return StackInputs(weights=w, vision=vision, prompt=prompt, state=st, B=B, max_new=max_new)

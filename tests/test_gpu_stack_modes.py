@@ -106,3 +106,37 @@ def test_stack_rounds_commit_the_ar_stream(stack, mode):
     assert int(st.err.item()) == 0
     _same_prefix(st.to_host(host), ar, N + 1)
     print(f"[stack-modes] {mode}: {rounds} rounds == AR", flush=True)
+
+
+def test_stack_multidraft_commits_the_ar_stream(stack):
+    """The per-acceptance multi-draft step at the stack's shape (B = 16: 16
+    causal rows and 16 groups of 16 mask rows, 272 window rows per
+    sequence): the first draft is the AR continuation, so the first step
+    accepts all 15 drafts, and the committed stream equals greedy AR."""
+    si = stack
+    ar = _ar_stream(si)
+    w, B = si.weights, si.B
+    pool_state = synth.stack_state(3, 8, si.P, B, si.max_new, B + B * B)
+    pool = pool_state.pool_pages
+    kps = [torch.zeros((pool, w.Hkv, 16, w.D), dtype=torch.bfloat16, device="cuda")
+           for _ in range(w.n_layers)]
+    vps = [torch.zeros((pool, w.Hkv, w.D, 16), dtype=torch.bfloat16, device="cuda")
+           for _ in range(w.n_layers)]
+    dm = dvs.DeviceModel(w, kps, vps, "bf16")
+    st = dvs.DeviceState(pool_state)
+    dvs.prefill(dm, st, si.P, B, prefix_tokens=torch.from_numpy(si.prefix_tokens()).cuda(),
+                x_prefix=torch.from_numpy(si.x_prefix()).cuda(), chunk_keys=CH)
+    st.draft.copy_(torch.from_numpy(np.ascontiguousarray(ar.out_tokens[:, 1:B])))
+    acc = torch.empty((8,), dtype=torch.int32, device="cuda")
+    dvs.multidraft_step(dm, st, B, chunk_keys=CH, accept_out=acc)
+    torch.cuda.synchronize()
+    assert acc.cpu().numpy().tolist() == [B - 1] * 8
+    steps = 1
+    while int(st.out_count.min().item()) < N + 1:
+        dvs.multidraft_step(dm, st, B, chunk_keys=CH)
+        steps += 1
+        assert steps <= N
+    torch.cuda.synchronize()
+    assert int(st.err.item()) == 0
+    _same_prefix(st.to_host(pool_state), ar, N + 1)
+    print(f"[stack-modes] multidraft: {steps} steps == AR", flush=True)
