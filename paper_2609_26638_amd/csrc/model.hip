@@ -157,11 +157,21 @@ __device__ __forceinline__ int window_offset(int r, int n_causal, int n_mask, in
 // window_offset(r); angles in double precision (positions reach thousands
 // of radians).
 template <typename T>
-__global__ void rope_kernel(T* __restrict__ x, int M, int R, int nh, int D, double log2_theta,
-                            const int32_t* __restrict__ kv_len, int n_causal, int n_mask,
-                            int group) {
+__global__ void rope_kernel(T* __restrict__ xq, int nhq, T* __restrict__ xk, int nhk, int M, int R,
+                            int D, double log2_theta, const int32_t* __restrict__ kv_len,
+                            int n_causal, int n_mask, int group) {
+  // one launch for the query and the key heads: indices below M*nhq*D/2
+  // rotate q, the rest k
   const int half = D / 2;
-  const long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  const long long nq = (long long)M * nhq * half;
+  T* x = xq;
+  int nh = nhq;
+  if (idx >= nq) {
+    idx -= nq;
+    x = xk;
+    nh = nhk;
+  }
   if (idx >= (long long)M * nh * half) return;
   const int i = (int)(idx % half);
   const long long mh = idx / half;
@@ -301,28 +311,284 @@ __global__ void __launch_bounds__(256) gemm_bf16_kernel(const __bf16* __restrict
 }
 
 // ---------------------------------------------------------------------------
-// bf16 GEMM for the decoder stack: C[m, n] (=, or += into the fp32 residual)
-// sum_k A[m, k] W[n, k].  The weights are streamed once; the row count is
-// small (8..256 window rows) or a long prefill.
+// bf16 GEMMs of the decoder stack.  C[m, n] = sum_k A[m, k] W[n, k] (bf16
+// operands, fp32 accumulation).
+//
+// Row invariance.  K is cut into KS logical splits (KS = 4 when K is a
+// multiple of 256, else 1; a function of K only).  Every output element is
+//     ((0 + p_0) + p_1) + ... + p_{KS-1}      (fp32, in this order)
+// where p_s is the in-order accumulation of v_mfma_f32_32x32x16_bf16 over the
+// 16-wide k-steps of split s (lane half hh holds k values 8*hh .. 8*hh+7 of a
+// step in both operands).  Both kernels below compute exactly that, so a
+// row's result never depends on how many rows a call carries: a fused step's
+// causal rows, a two-forward round's verify rows and AR rows agree bit for
+// bit.
+//   * gemm_ws_kernel (calls of at most WS_MAX_ROWS rows: every decode step
+//     of the benchmark shapes): wave s of a workgroup computes split s of a
+//     (row tile x 32 columns) tile straight from global memory and the four
+//     splits are added through LDS in order -- no partials leave the
+//     workgroup;
+//   * gemm_rt_kernel (longer calls: prefill, wide multi-draft windows): LDS-
+//     staged tiles of MT rows x 128 columns, the splits' products added to a
+//     running sum in registers.
 // ---------------------------------------------------------------------------
-constexpr int GK_MAXSPLIT = 4;     // logical K splits (bounds the partial traffic)
-constexpr int GK_SPLIT_ROWS = 256; // calls of at most this many rows run one split per workgroup
+constexpr int GK_SPLITS = 4;        // logical K splits when K % 256 == 0
+constexpr int WS_MAX_ROWS = 256;    // calls up to this many rows use gemm_ws_kernel
+
+static int gemm_ksplit(int K) { return K % (64 * GK_SPLITS) == 0 ? GK_SPLITS : 1; }
 
 // ---------------------------------------------------------------------------
-// gemm_rt_kernel<MT>: C[M, N] = A[M, K] W[N, K]^T (bf16 operands, fp32
-// accumulation), tiles of MT rows x 128 columns staged through LDS.
+// gemm_ws_kernel<MT>: weight-streaming GEMM for decode-step row counts.
 //
-// Row invariance.  K is cut into KS logical splits of kc = K / KS (a multiple
-// of 64), KS a function of (N, K) only.  Every output element is
-//     p_0 + p_1 + ... + p_{KS-1}      (fp32, in this order)
-// where p_s is the MFMA accumulation of split s over its 16-wide k-steps in
-// order.  Two mappings compute exactly that, whatever the row count:
-//   * split per workgroup (calls of at most 256 rows, the decode steps): p_s
-//     of a (row tile, column block) is published with write-through stores
-//     and the last workgroup of that tile adds the splits in order;
-//   * all splits in one workgroup (longer calls, prefill): the running
-//     ordered sum stays in registers.
-// A fused step's causal rows are therefore bit-identical to AR steps.
+// Workgroup = 4 waves = one (row tile of MT rows, 32-column block); wave s
+// computes split s (K/4 consecutive k) for the whole tile.  Each wave copies
+// its 32-wide K chunks (32 weight rows and MT rows of A, 64 bytes each)
+// with direct global -> LDS 16-byte loads, fully coalesced, into a private
+// 3-stage ring two chunks ahead of its products, and feeds the MFMAs from
+// there (no barriers between the waves until the split sums).  Each weight
+// element is read once per row tile; the row tiles of
+// a column block are dispatched back to back on one XCD (blockIdx mod 8), so
+// the second and later ones find the block's weights in that XCD's L2.
+// The splits meet in LDS and are added in order, then an epilogue writes the
+// tile:
+//   EPI_BF16       C (bf16) of the column block's segment (fused projections:
+//                  up to three weight matrices side by side, e.g. Wq|Wk|Wv,
+//                  each output into its own array);
+//   EPI_F32_ADD    C (fp32) += tile (the residual stream);
+//   EPI_F32        C (fp32) = tile (logits);
+//   EPI_SWIGLU     columns 0..15 of a block are gate rows, 16..31 the same up
+//                  rows: act = bf16(silu(bf16 gate) * bf16 up), 16 outputs per
+//                  row (the same roundings as separate gate, up and silu*up
+//                  passes);
+//   EPI_ARGMAX     per row the block's largest logit and its lowest index,
+//                  packed (order-preserving key, 0x7fffffff - index) for a
+//                  64-bit max (NaN never wins; non-finite values set
+//                  DVS_ERR_NONFINITE); argmax_rows_kernel takes the max over
+//                  a row's blocks, so the logits never reach memory.
+// ---------------------------------------------------------------------------
+enum { EPI_BF16 = 0, EPI_F32 = 1, EPI_F32_ADD = 2, EPI_SWIGLU = 3, EPI_ARGMAX = 4 };
+
+struct GemmSeg {
+  const __bf16* W;   // [n, K] rows of this segment
+  void* C;           // output of this segment, row stride = n (EPI_SWIGLU: the act array)
+  int n0, n;         // columns [n0, n0 + n) of the fused output
+};
+
+struct GemmArgs {
+  const __bf16* A;
+  int M, K, ncols;   // ncols: total output columns (EPI_SWIGLU: 2 * ffn)
+  GemmSeg seg[3];
+  int nseg, epi, n_rt;
+  uint64_t* part;    // EPI_ARGMAX: [M, ncols / 32]
+  int32_t* err;
+};
+
+__device__ __forceinline__ uint64_t pack_logit(float v, int idx, bool& nonfinite) {
+  uint32_t u = __float_as_uint(v);
+  if ((u & 0x7f800000u) == 0x7f800000u) nonfinite = true;
+  if (v != v) return 0;                        // NaN: never the top-1
+  if ((u & 0x7fffffffu) == 0) u = 0;           // -0 == +0
+  const uint32_t key = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+  return ((uint64_t)key << 32) | (uint32_t)(0x7fffffff - idx);
+}
+
+// s_waitcnt vmcnt(n) with the other counters untouched (gfx9 encoding).
+template <int N>
+__device__ __forceinline__ void ws_wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
+template <int MT>
+__global__ void __launch_bounds__(256, 2) gemm_ws_kernel(GemmArgs g) {
+  constexpr int RG = MT / 32;              // 32-row groups per wave
+  // ring stages per wave (deeper rings for the few-row calls measured no
+  // faster: the few-row calls are bound by their few workgroups)
+  constexpr int NS = 3;
+  constexpr int KC = 32;                   // k per chunk (64 bytes of a row)
+  constexpr int WB = 32 * 64;              // W part of a chunk: 32 rows
+  constexpr int CB = WB + MT * 64;         // chunk bytes (W rows, then A rows)
+  constexpr int NPL = (32 + MT) / 16;      // 1 KB copies per chunk and wave
+  static_assert(NPL * (NS - 1) < 64, "vmcnt range");
+  static_assert(4 * NS * CB >= GK_SPLITS * MT * 32 * 4, "the split sums reuse the rings");
+  __shared__ __attribute__((aligned(1024))) char s_ring[4 * NS * CB];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int l32 = lane & 31, hh = lane >> 5;
+  const int NB = (g.ncols + 31) / 32;
+  // XCD-aware order: blocks b, b + 8, b + 16, ... share an XCD; the row
+  // tiles of one column block are consecutive among them
+  const int x = blockIdx.x & 7, j = blockIdx.x >> 3;
+  const int cb = (j / g.n_rt) * 8 + x, rt = j % g.n_rt;
+  if (cb >= NB) return;
+  const int c0 = cb * 32, m0 = rt * MT;
+  char* ring = s_ring + w * NS * CB;
+
+  // Copies: instruction i of a chunk moves 1 KB, 16 rows of 64 bytes; lane L
+  // takes row 16i + L/4 and 16-byte chunk (L & 3) ^ sw(row), sw(row) =
+  // (row / 4) & 3, so LDS slot c of a row holds its chunk c ^ sw(row): the 16
+  // rows an MFMA operand read serves at once hit distinct banks.
+  const int crow = lane >> 2, cchk = lane & 3;
+  int si = 0;
+  const __bf16* wsrc[2];   // this lane's weight rows (tile rows 16i + L/4)
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int r = 16 * i + crow;
+    const __bf16* base;
+    bool valid;
+    int rowi;
+    if (g.epi == EPI_SWIGLU) {
+      rowi = cb * 16 + (r & 15);
+      valid = rowi < g.seg[0].n;
+      base = r < 16 ? g.seg[0].W : g.seg[1].W;
+    } else {
+      while (si + 1 < g.nseg && c0 >= g.seg[si + 1].n0) ++si;
+      rowi = c0 - g.seg[si].n0 + r;
+      valid = rowi < g.seg[si].n;
+      base = g.seg[si].W;
+    }
+    wsrc[i] = base + (size_t)(valid ? rowi : 0) * g.K + ((cchk ^ ((r >> 2) & 3)) << 3);
+  }
+  if (g.epi != EPI_SWIGLU)
+    while (si + 1 < g.nseg && c0 >= g.seg[si + 1].n0) ++si;
+  const __bf16* asrc[MT / 16];
+#pragma unroll
+  for (int i = 0; i < MT / 16; ++i) {
+    const int r = 16 * i + crow;
+    asrc[i] = g.A + (size_t)min(m0 + r, g.M - 1) * g.K + ((cchk ^ ((r >> 2) & 3)) << 3);
+  }
+  const int kq = g.K / GK_SPLITS;
+  const int kw = w * kq;               // this wave's split
+  const int nch = kq / KC;
+  auto issue = [&](int t) {
+    char* dst = ring + (t % NS) * CB;
+    const int k0 = kw + t * KC;
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+      __builtin_amdgcn_global_load_lds((const void*)(wsrc[i] + k0),
+                                       (__attribute__((address_space(3))) void*)(dst + i * 1024), 16, 0, 0);
+#pragma unroll
+    for (int i = 0; i < MT / 16; ++i)
+      __builtin_amdgcn_global_load_lds((const void*)(asrc[i] + k0),
+                                       (__attribute__((address_space(3))) void*)(dst + WB + i * 1024), 16, 0, 0);
+  };
+
+  f32x16 acc[RG];
+#pragma unroll
+  for (int a = 0; a < RG; ++a) acc[a] = f32x16{};
+  static_for<0, NS - 1>([&](auto c) {
+    if (decltype(c)::value < nch) issue(decltype(c)::value);
+  });
+  // chunk t complete while the `later` chunks after it may still be in flight
+  auto wait_chunk = [&](int later) {
+    static_for<0, NS>([&](auto c) {
+      constexpr int n = NS - 1 - decltype(c)::value;
+      if (later == n) ws_wait_vmcnt<n * NPL>();
+    });
+  };
+  for (int t = 0; t < nch; ++t) {
+    if (t + NS - 1 < nch) issue(t + NS - 1);
+    wait_chunk(min(NS - 1, nch - 1 - t));
+    const char* src = ring + (t % NS) * CB;
+    // every operand of the chunk from LDS first, then the products
+    bf16x8 bw[KC / 16], ba[KC / 16][RG];
+#pragma unroll
+    for (int ks = 0; ks < KC / 16; ++ks) {
+      const int q = 2 * ks + hh;   // the lane's 16-byte chunk of the row
+      bw[ks] = *(const bf16x8*)(src + l32 * 64 + ((q ^ ((l32 >> 2) & 3)) << 4));
+#pragma unroll
+      for (int a = 0; a < RG; ++a) {
+        const int r = a * 32 + l32;
+        ba[ks][a] = *(const bf16x8*)(src + WB + r * 64 + ((q ^ ((r >> 2) & 3)) << 4));
+      }
+    }
+#pragma unroll
+    for (int ks = 0; ks < KC / 16; ++ks)
+#pragma unroll
+      for (int a = 0; a < RG; ++a)
+        acc[a] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ba[ks][a], bw[ks], acc[a], 0, 0, 0);
+  }
+  // rows of W past the segment end were read from row 0: zero their columns
+  bool wvalid;
+  if (g.epi == EPI_SWIGLU) wvalid = cb * 16 + (l32 & 15) < g.seg[0].n;
+  else wvalid = c0 - g.seg[si].n0 + l32 < g.seg[si].n;
+
+  // splits in order through LDS (the rings are free once every wave is done)
+  __syncthreads();
+  float* s_red = (float*)s_ring;
+#pragma unroll
+  for (int a = 0; a < RG; ++a)
+#pragma unroll
+    for (int i = 0; i < 16; ++i)
+      s_red[w * (MT * 32) + (a * 32 + 8 * (i >> 2) + 4 * hh + (i & 3)) * 32 + l32] =
+          wvalid ? acc[a][i] : 0.f;
+  __syncthreads();
+  bool nonfinite = false;
+#pragma unroll
+  for (int e0 = 0; e0 < MT * 32; e0 += 256) {
+    const int e = e0 + tid;
+    const int r = e >> 5, c = e & 31;
+    float t = 0.f;
+#pragma unroll
+    for (int sp = 0; sp < GK_SPLITS; ++sp) t += s_red[sp * (MT * 32) + e];
+    const int row = m0 + r;
+    const bool rv = row < g.M;
+    if (g.epi == EPI_ARGMAX) {
+      const int col = c0 + c;
+      uint64_t kv = (rv && col < g.ncols) ? pack_logit(t, col, nonfinite) : 0;
+#pragma unroll
+      for (int off = 16; off > 0; off >>= 1) {
+        const uint32_t lo = __shfl_xor((uint32_t)kv, off);
+        const uint32_t hi = __shfl_xor((uint32_t)(kv >> 32), off);
+        const uint64_t o = ((uint64_t)hi << 32) | lo;
+        kv = o > kv ? o : kv;
+      }
+      if (c == 0 && rv) g.part[(size_t)row * NB + cb] = kv;
+    } else if (g.epi == EPI_SWIGLU) {
+      const float v = (float)(__bf16)t;             // gate or up, rounded as its own output
+      const float o = __shfl_xor(v, 16);
+      const int f = cb * 16 + c;
+      if (c < 16 && rv && f < g.seg[0].n) {
+        const float act = v / (1.0f + expf(-v)) * o;
+        ((__bf16*)g.seg[0].C)[(size_t)row * g.seg[0].n + f] = (__bf16)act;
+      }
+    } else {
+      const int col = c0 + c - g.seg[si].n0;
+      if (rv && col < g.seg[si].n) {
+        const size_t o = (size_t)row * g.seg[si].n + col;
+        if (g.epi == EPI_BF16) ((__bf16*)g.seg[si].C)[o] = (__bf16)t;
+        else if (g.epi == EPI_F32_ADD) ((float*)g.seg[si].C)[o] += t;
+        else ((float*)g.seg[si].C)[o] = t;
+      }
+    }
+  }
+  if (g.epi == EPI_ARGMAX && __any(nonfinite) && lane == 0) set_err(g.err, DVS_ERR_NONFINITE);
+}
+
+// Top-1 of each row from its column blocks' packed (key, index) maxima: one
+// wave per row, a 64-bit max, the lowest index among equal maxima; a row
+// whose values were all NaN gives 0.
+__global__ void __launch_bounds__(256) argmax_rows_kernel(const uint64_t* __restrict__ part, int M,
+                                                          int NB, int32_t* __restrict__ out) {
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (row >= M) return;
+  const uint64_t* p = part + (size_t)row * NB;
+  uint64_t b = 0;
+  for (int i = lane; i < NB; i += 64) b = p[i] > b ? p[i] : b;
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    const uint32_t lo = __shfl_xor((uint32_t)b, off);
+    const uint32_t hi = __shfl_xor((uint32_t)(b >> 32), off);
+    const uint64_t o = ((uint64_t)hi << 32) | lo;
+    b = o > b ? o : b;
+  }
+  if (lane == 0) out[row] = b == 0 ? 0 : 0x7fffffff - (int)(uint32_t)(b & 0xffffffffu);
+}
+
+// ---------------------------------------------------------------------------
+// gemm_rt_kernel<MT>: C[M, N] = A[M, K] W[N, K]^T for long calls, tiles of MT
+// rows x 128 columns staged through LDS; all KS splits of a tile in one
+// workgroup, each split's product added to a running sum in registers.
 //
 // Waves: MT = 32 -> 1 x 4 (each wave 32 rows x 32 columns); MT >= 64 ->
 // 2 x 2 (each wave MT/2 rows x 64 columns).  Per 64-wide K chunk all 256
@@ -338,8 +604,7 @@ constexpr int RT_KC = 64;    // K per LDS chunk
 template <int MT, bool SPLITS>
 __global__ void __launch_bounds__(256, 1) gemm_rt_kernel(
     const __bf16* __restrict__ A, const __bf16* __restrict__ W, int M, int N, int K, void* C,
-    int c_f32, int accumulate, int KS, int split_per_wg, float* __restrict__ part,
-    int32_t* __restrict__ counters) {
+    int c_f32, int accumulate, int KS, uint64_t* __restrict__ part, int32_t* err) {
   constexpr bool WIDE = MT >= 64;
   constexpr int RG = WIDE ? MT / 64 : 1;   // 32-row groups per wave
   constexpr int CG = WIDE ? 2 : 1;         // 32-column groups per wave
@@ -348,19 +613,13 @@ __global__ void __launch_bounds__(256, 1) gemm_rt_kernel(
   static_assert(A_LD >= 1 && W_LD >= 1, "tile / threads");
   __shared__ __attribute__((aligned(16))) char s_a[2][MT * RT_KC * 2];
   __shared__ __attribute__((aligned(16))) char s_w[2][RT_NT * RT_KC * 2];
-  __shared__ int s_last;
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int l32 = lane & 31, hh = lane >> 5;
   const int NBK = (N + RT_NT - 1) / RT_NT;
   const int nb = blockIdx.x % NBK;
-  const int rest = blockIdx.x / NBK;
+  const int rt = blockIdx.x / NBK;
   const int n0 = nb * RT_NT;
-  // split-per-workgroup: blockIdx selects (column block, split, row tile);
-  // otherwise (column block, row tile) and every split
-  const int rt = split_per_wg ? rest / KS : rest;
-  const int s_first = split_per_wg ? rest % KS : 0;
-  const int s_end = split_per_wg ? s_first + 1 : KS;
   const int m0 = rt * MT;
   const int kc = K / KS;
   const int wr = WIDE ? (w >> 1) : 0, wc = WIDE ? (w & 1) : w;
@@ -415,8 +674,8 @@ __global__ void __launch_bounds__(256, 1) gemm_rt_kernel(
   }
 
   const int nch = kc / RT_KC;
-  const int total = (s_end - s_first) * nch;
-  auto chunk_k0 = [&](int t) { return (s_first + t / nch) * kc + (t % nch) * RT_KC; };
+  const int total = KS * nch;
+  auto chunk_k0 = [&](int t) { return (t / nch) * kc + (t % nch) * RT_KC; };
   static_for<0, P - 1>([&](auto c) {
     constexpr int i = decltype(c)::value;
     load_chunk(chunk_k0(min(i, total - 1)), ra[i], rw[i]);
@@ -503,24 +762,12 @@ __global__ void __launch_bounds__(256, 1) gemm_rt_kernel(
         }
       }
   };
-  if constexpr (!SPLITS) {
-    // 0 + p_0, as in the split paths (keeps the sign of a zero sum alike)
-#pragma unroll
-    for (int a = 0; a < RG; ++a)
-#pragma unroll
-      for (int b = 0; b < CG; ++b) acc[a][b] = f32x16{} + acc[a][b];
-    write_out(acc);
-    return;
-  } else {
-  if (!split_per_wg || KS == 1) {
-    write_out(sum);
-    return;
-  }
-  if constexpr (MT <= 64) {   // the host uses one split per workgroup with 32- and 64-row tiles
-    // split per workgroup: publish p_s of this (row tile, column block), count
-    // in; the last workgroup of the tile adds the splits in order
-    const int n_rt = (M + MT - 1) / MT;
-    int32_t* cnt = counters + (size_t)nb * n_rt + rt;
+  // top-1 epilogue (part != NULL): per row and 32-column group the largest
+  // value and its lowest index, packed as gemm_ws_kernel's EPI_ARGMAX; the 32
+  // lanes of a lane half hold one row's 32 columns
+  auto write_top1 = [&](f32x16 (&v)[RG][CG]) {
+    const int NB = (N + 31) / 32;
+    bool nonfinite = false;
 #pragma unroll
     for (int a = 0; a < RG; ++a)
 #pragma unroll
@@ -529,54 +776,30 @@ __global__ void __launch_bounds__(256, 1) gemm_rt_kernel(
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
           const int mrow = m0 + row_w + a * 32 + 8 * (i >> 2) + 4 * hh + (i & 3);
-          if (mrow < M && n < N)
-            __hip_atomic_store(part + ((size_t)s_first * M + mrow) * N + n, sum[a][b][i], __ATOMIC_RELAXED,
-                               __HIP_MEMORY_SCOPE_AGENT);
+          uint64_t kv = (mrow < M && n < N) ? pack_logit(v[a][b][i], n, nonfinite) : 0;
+#pragma unroll
+          for (int off = 16; off > 0; off >>= 1) {
+            const uint32_t lo = __shfl_xor((uint32_t)kv, off);
+            const uint32_t hi = __shfl_xor((uint32_t)(kv >> 32), off);
+            const uint64_t o = ((uint64_t)hi << 32) | lo;
+            kv = o > kv ? o : kv;
+          }
+          if (l32 == 0 && mrow < M) part[(size_t)mrow * NB + (n0 + col_w + b * 32) / 32] = kv;
         }
       }
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
-    // release of this workgroup's partials (ordered before it by the
-    // barrier) and, for the last workgroup, acquire of the others'
-    if (tid == 0)
-      s_last = __hip_atomic_fetch_add(cnt, 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT) == KS - 1;
-    __syncthreads();
-    if (!s_last) return;
-    if (tid == 0) __hip_atomic_store(cnt, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    f32x16 tot[RG][CG];
+    if (__any(nonfinite) && lane == 0) set_err(err, DVS_ERR_NONFINITE);
+  };
+  if constexpr (!SPLITS) {
+    // 0 + p_0, as in the split paths (keeps the sign of a zero sum alike)
 #pragma unroll
     for (int a = 0; a < RG; ++a)
 #pragma unroll
-      for (int b = 0; b < CG; ++b) tot[a][b] = f32x16{};
-    // the splits' partials, GK_MAXSPLIT of them at most, are loaded together
-    // (every load issued before any is added), then added in split order
-    static_assert(GK_MAXSPLIT <= 4, "one batch of split partials");
-#pragma unroll
-    for (int a = 0; a < RG; ++a)
-#pragma unroll
-      for (int b = 0; b < CG; ++b) {
-        const int n = n0 + col_w + b * 32 + l32;
-        float v[GK_MAXSPLIT][16];
-#pragma unroll
-        for (int q = 0; q < GK_MAXSPLIT; ++q) {
-          const int sp = min(q, KS - 1);
-#pragma unroll
-          for (int i = 0; i < 16; ++i) {
-            const int mrow = m0 + row_w + a * 32 + 8 * (i >> 2) + 4 * hh + (i & 3);
-            const int mr = min(mrow, M - 1), nn = min(n, N - 1);
-            v[q][i] = __hip_atomic_load(part + ((size_t)sp * M + mr) * N + nn, __ATOMIC_RELAXED,
-                                        __HIP_MEMORY_SCOPE_AGENT);
-          }
-        }
-#pragma unroll
-        for (int q = 0; q < GK_MAXSPLIT; ++q)
-          if (q < KS) {
-#pragma unroll
-            for (int i = 0; i < 16; ++i) tot[a][b][i] += v[q][i];
-          }
-      }
-    write_out(tot);
-  }
+      for (int b = 0; b < CG; ++b) acc[a][b] = f32x16{} + acc[a][b];
+    if (part) write_top1(acc);
+    else write_out(acc);
+  } else {
+    if (part) write_top1(sum);
+    else write_out(sum);
   }
 }
 
@@ -631,31 +854,9 @@ __global__ void __launch_bounds__(256) gemm_f32_kernel(const float* __restrict__
 // host orchestration
 // ---------------------------------------------------------------------------
 struct StepLayout {
-  size_t x, h, hsel, q, k, v, att, gate, up, act, logits, am, conf, nopen, blk, acc, lead, attn_ws,
-      total,
-      attn_bytes,
-      attn_counters, gemm_part, gemm_part_bytes, gemm_counters, n_gemm_counters;
+  size_t x, h, hsel, q, k, v, att, gate, up, act, logits, am, conf, nopen, blk, acc, lead, part,
+      attn_ws, total, attn_bytes, attn_counters;
 };
-
-// Logical K splits of a bf16 GEMM: up to GK_MAXSPLIT, enough for 128-column
-// blocks x splits to fill the chip when each split is a workgroup, a split
-// being a multiple of 64 of K.  A function of (N, K) only, so that row results
-// do not depend on the row count.  (Few splits: the partials of a 256-row
-// call cost KS x 256 x 4 bytes per weight column against 2 K bytes of
-// weights.)
-static int gemm_ksplit(int N, int K) {
-  if (K % 64 != 0) return 1;
-  static_assert(GK_MAXSPLIT >= 1, "split bound");
-  const int nb = (N + RT_NT - 1) / RT_NT;
-  const int target = (256 + nb - 1) / nb;
-  if (target <= 1) return 1;
-  const int units = K / 64;
-  for (int d = target; d <= units && d <= GK_MAXSPLIT; ++d)
-    if (units % d == 0) return d;
-  for (int d = std::min(units, GK_MAXSPLIT); d > 1; --d)
-    if (units % d == 0) return d;
-  return 1;
-}
 
 // Rows per tile when all splits run in one workgroup (more than 32 rows):
 // the largest tile that still gives 256 workgroups, else 32.
@@ -706,65 +907,64 @@ static StepLayout step_layout(const dvs_model* m, int S, int n_causal, int n_mas
   L.blk = off; off += al(M * 4);
   L.acc = off; off += al((size_t)S * 4);
   L.lead = off; off += al((size_t)S * 4);
+  // the LM head's per-column-block maxima (fused top-1)
+  L.part = off; off += al(std::max(M, logit_rows) * (size_t)((m->vocab + 31) / 32) * 8);
   L.attn_bytes = dvs_attn_workspace_bytes(S, n_causal, n_mask, m->n_heads, m->n_kv_heads,
                                           m->head_dim, max_pages, chunk_keys, m->dtype);
   L.attn_counters = attn_counter_bytes(S, n_causal + n_mask, m->n_heads, m->n_kv_heads,
                                        m->head_dim, max_pages, chunk_keys, m->dtype);
   L.attn_ws = off; off += al(L.attn_bytes);
-  // split-K partials and counters of the largest bf16 GEMM of the call
-  if (m->dtype == DVS_BF16) {
-    const int H = m->hidden;
-    const int shapes[6][3] = {{(int)M, (int)qd, H}, {(int)M, (int)kd, H}, {(int)M, H, (int)qd},
-                              {(int)M, m->ffn, H}, {(int)M, H, m->ffn}, {(int)logit_rows, m->vocab, H}};
-    size_t part = 0, cnt = 0;
-    for (const auto& sh : shapes) {
-      // only calls of <= GK_SPLIT_ROWS rows publish split partials
-      if (sh[1] <= 0 || sh[0] > GK_SPLIT_ROWS) continue;
-      const int ksp = gemm_ksplit(sh[1], sh[2]);
-      if (ksp > 1) {
-        const size_t mt = sh[0] <= 32 ? 32 : 64;
-        part = std::max(part, (size_t)ksp * sh[0] * sh[1] * 4);
-        cnt = std::max(cnt, (size_t)(sh[1] + RT_NT - 1) / RT_NT * ((sh[0] + mt - 1) / mt));
-      }
-    }
-    L.gemm_part = off; off += al(part); L.gemm_part_bytes = part;
-    L.gemm_counters = off; off += al(cnt * 4); L.n_gemm_counters = cnt;
-  }
   L.total = off;
   return L;
+}
+
+static int launch_ws(GemmArgs& g, hipStream_t st) {
+  const int NB = (g.ncols + 31) / 32;
+  const int MT = g.M <= 32 ? 32 : 64;
+  g.n_rt = (g.M + MT - 1) / MT;
+  const long long grid = (long long)((NB + 7) / 8) * 8 * g.n_rt;
+  DVS_CHECK_SUPPORTED(grid < (1LL << 31), "draft_verify_step: GEMM grid too large");
+  if (MT == 32) hipLaunchKernelGGL(gemm_ws_kernel<32>, dim3((unsigned)grid), dim3(256), 0, st, g);
+  else hipLaunchKernelGGL(gemm_ws_kernel<64>, dim3((unsigned)grid), dim3(256), 0, st, g);
+  return launch_status("draft_verify_step(gemm)");
+}
+
+// gemm_ws_kernel serves a call when it computes the same splits as
+// gemm_rt_kernel would (bf16, K a multiple of 256) and the rows are few.
+static bool use_ws(int dtype, int M, int K) {
+  return dtype == DVS_BF16 && K % (64 * GK_SPLITS) == 0 && M <= WS_MAX_ROWS;
 }
 
 // C = A W^T (or C += for the fp32 residual).  `c_f32` selects an fp32 output
 // for bf16 models (residual stream, logits); fp32 models always write fp32.
 static int gemm(const StepLayout& L, char* ws, int dtype, const void* A, const void* W, int M,
                 int N, int K, void* C, int c_f32, int accumulate, hipStream_t st) {
+  (void)L; (void)ws;
   const int waves = (N + 31) / 32;
   const int blocks = (waves + 3) / 4;
+  if (use_ws(dtype, M, K)) {
+    GemmArgs g{};
+    g.A = (const __bf16*)A; g.M = M; g.K = K; g.ncols = N;
+    g.seg[0] = GemmSeg{(const __bf16*)W, C, 0, N};
+    g.nseg = 1;
+    g.epi = c_f32 ? (accumulate ? EPI_F32_ADD : EPI_F32) : EPI_BF16;
+    return launch_ws(g, st);
+  }
   if (dtype == DVS_BF16 && K % 64 == 0) {
-    const int ksp = gemm_ksplit(N, K);
-    const int nb = (N + RT_NT - 1) / RT_NT;
-    const bool split_wg = M <= GK_SPLIT_ROWS && ksp > 1;
-    int mt = split_wg ? (M <= 32 ? 32 : 64) : (M <= 32 ? 32 : gemm_rows_per_tile(M, N));
+    const int ksp = gemm_ksplit(K);
+    int mt = M <= 32 ? 32 : gemm_rows_per_tile(M, N);
     if (mt == 256 && ksp > 1) mt = 128;   // the 256-row tile keeps no running split sum
-    const long long n_rt = (M + mt - 1) / mt;
-    if (split_wg && ((size_t)ksp * M * N * 4 > L.gemm_part_bytes ||
-                     (size_t)nb * n_rt > L.n_gemm_counters)) {
-      set_error("draft_verify_step: GEMM split workspace too small");
-      return DVS_EWORKSPACE;
-    }
-    float* part = (float*)(ws + L.gemm_part);
-    int32_t* cnt = (int32_t*)(ws + L.gemm_counters);
-    const long long grid = split_wg ? (long long)nb * ksp * n_rt : (long long)nb * n_rt;
+    const int nb = (N + RT_NT - 1) / RT_NT;
+    const long long grid = (long long)nb * ((M + mt - 1) / mt);
     DVS_CHECK_SUPPORTED(grid < (1LL << 31), "draft_verify_step: GEMM grid too large");
     const dim3 g((unsigned)grid), blk(256);
     const __bf16* a = (const __bf16*)A;
     const __bf16* wt = (const __bf16*)W;
-    const int sw = split_wg ? 1 : 0;
     switch (mt) {
-      case 256: hipLaunchKernelGGL((gemm_rt_kernel<256, false>), g, blk, 0, st, a, wt, M, N, K, C, c_f32, accumulate, ksp, sw, part, cnt); break;
-      case 128: hipLaunchKernelGGL((gemm_rt_kernel<128, true>), g, blk, 0, st, a, wt, M, N, K, C, c_f32, accumulate, ksp, sw, part, cnt); break;
-      case 64: hipLaunchKernelGGL((gemm_rt_kernel<64, true>), g, blk, 0, st, a, wt, M, N, K, C, c_f32, accumulate, ksp, sw, part, cnt); break;
-      default: hipLaunchKernelGGL((gemm_rt_kernel<32, true>), g, blk, 0, st, a, wt, M, N, K, C, c_f32, accumulate, ksp, sw, part, cnt); break;
+      case 256: hipLaunchKernelGGL((gemm_rt_kernel<256, false>), g, blk, 0, st, a, wt, M, N, K, C, c_f32, accumulate, ksp, nullptr, nullptr); break;
+      case 128: hipLaunchKernelGGL((gemm_rt_kernel<128, true>), g, blk, 0, st, a, wt, M, N, K, C, c_f32, accumulate, ksp, nullptr, nullptr); break;
+      case 64: hipLaunchKernelGGL((gemm_rt_kernel<64, true>), g, blk, 0, st, a, wt, M, N, K, C, c_f32, accumulate, ksp, nullptr, nullptr); break;
+      default: hipLaunchKernelGGL((gemm_rt_kernel<32, true>), g, blk, 0, st, a, wt, M, N, K, C, c_f32, accumulate, ksp, nullptr, nullptr); break;
     }
   } else if (dtype == DVS_BF16)
     hipLaunchKernelGGL(gemm_bf16_kernel, dim3(blocks), dim3(256), 0, st, (const __bf16*)A,
@@ -773,6 +973,45 @@ static int gemm(const StepLayout& L, char* ws, int dtype, const void* A, const v
     hipLaunchKernelGGL(gemm_f32_kernel, dim3(blocks), dim3(256), 0, st, (const float*)A,
                        (const float*)W, M, N, K, (float*)C, accumulate);
   return launch_status("draft_verify_step(gemm)");
+}
+
+// LM head with the top-1 fused into its epilogue (no logits in memory), for
+// the rows in h; the result is argmax_kernel's (same values, same order).
+static int lm_head_top1(const dvs_model* m, const StepLayout& L, char* ws, const void* h, int M,
+                        int32_t* am, int32_t* err, hipStream_t st) {
+  GemmArgs g{};
+  g.A = (const __bf16*)h; g.M = M; g.K = m->hidden; g.ncols = m->vocab;
+  g.seg[0] = GemmSeg{(const __bf16*)m->lm_head, nullptr, 0, m->vocab};
+  g.nseg = 1;
+  g.epi = EPI_ARGMAX;
+  g.part = (uint64_t*)(ws + L.part);
+  g.err = err;
+  int rc;
+  if (M <= 32) {
+    rc = launch_ws(g, st);
+  } else {
+    // wide tiles: the rows of A are shared by 128 columns, the weights by
+    // up to 128 rows (32-column tiles would re-read A once per 32 columns)
+    const int N = m->vocab, K = m->hidden, ksp = gemm_ksplit(K);
+    int mt = gemm_rows_per_tile(M, N);
+    if (mt == 256 && ksp > 1) mt = 128;
+    const long long grid = (long long)((N + RT_NT - 1) / RT_NT) * ((M + mt - 1) / mt);
+    DVS_CHECK_SUPPORTED(grid < (1LL << 31), "draft_verify_step: GEMM grid too large");
+    const dim3 gr((unsigned)grid), blk(256);
+    const __bf16* a = (const __bf16*)h;
+    const __bf16* wt = (const __bf16*)m->lm_head;
+    switch (mt) {
+      case 256: hipLaunchKernelGGL((gemm_rt_kernel<256, false>), gr, blk, 0, st, a, wt, M, N, K, nullptr, 1, 0, ksp, g.part, err); break;
+      case 128: hipLaunchKernelGGL((gemm_rt_kernel<128, true>), gr, blk, 0, st, a, wt, M, N, K, nullptr, 1, 0, ksp, g.part, err); break;
+      default: hipLaunchKernelGGL((gemm_rt_kernel<64, true>), gr, blk, 0, st, a, wt, M, N, K, nullptr, 1, 0, ksp, g.part, err); break;
+    }
+    rc = launch_status("draft_verify_step(lm head)");
+  }
+  if (rc) return rc;
+  const int NB = (m->vocab + 31) / 32;
+  hipLaunchKernelGGL(argmax_rows_kernel, dim3((unsigned)((M + 3) / 4)), dim3(256), 0, st, g.part,
+                     M, NB, am);
+  return launch_status("draft_verify_step(lm head top-1)");
 }
 
 // The decoder stack on the rows in x (fp32, [M, hidden]); leaves the final
@@ -802,24 +1041,29 @@ static int forward_layers(const dvs_model* m, const dvs_state* st, int n_causal,
     hipLaunchKernelGGL(zero_words_kernel, dim3((nw + 255) / 256), dim3(256), 0, stream,
                        (int32_t*)(ws + L.attn_ws), nw);
   }
-  if (L.n_gemm_counters) {
-    const int nw = (int)L.n_gemm_counters;
-    hipLaunchKernelGGL(zero_words_kernel, dim3((nw + 255) / 256), dim3(256), 0, stream,
-                       (int32_t*)(ws + L.gemm_counters), nw);
-  }
   const double log2_theta = log2((double)m->rope_theta);
   for (int l = 0; l < m->n_layers; ++l) {
     const dvs_layer& ly = m->layers[l];
     hipLaunchKernelGGL(rmsnorm_kernel<T>, dim3(M), dim3(256), 0, stream, x, (const T*)ly.g_attn, H,
                        m->rms_eps, h);
-    if ((rc = gemm(L, ws, dt, h, ly.wq, M, Hq * D, H, q, 0, 0, stream))) return rc;
-    if ((rc = gemm(L, ws, dt, h, ly.wk, M, Hkv * D, H, k, 0, 0, stream))) return rc;
-    if ((rc = gemm(L, ws, dt, h, ly.wv, M, Hkv * D, H, v, 0, 0, stream))) return rc;
-    const long long nq = (long long)M * Hq * (D / 2), nk = (long long)M * Hkv * (D / 2);
-    hipLaunchKernelGGL(rope_kernel<T>, dim3((unsigned)((nq + 255) / 256)), dim3(256), 0, stream, q, M,
-                       R, Hq, D, log2_theta, st->kv_len, n_causal, n_mask, group);
-    hipLaunchKernelGGL(rope_kernel<T>, dim3((unsigned)((nk + 255) / 256)), dim3(256), 0, stream, k, M,
-                       R, Hkv, D, log2_theta, st->kv_len, n_causal, n_mask, group);
+    if (use_ws(dt, M, H)) {
+      // Q, K and V in one launch (the same splits as three separate calls)
+      GemmArgs g{};
+      g.A = (const __bf16*)h; g.M = M; g.K = H; g.ncols = (Hq + 2 * Hkv) * D;
+      g.seg[0] = GemmSeg{(const __bf16*)ly.wq, q, 0, Hq * D};
+      g.seg[1] = GemmSeg{(const __bf16*)ly.wk, k, Hq * D, Hkv * D};
+      g.seg[2] = GemmSeg{(const __bf16*)ly.wv, v, (Hq + Hkv) * D, Hkv * D};
+      g.nseg = 3;
+      g.epi = EPI_BF16;
+      if ((rc = launch_ws(g, stream))) return rc;
+    } else {
+      if ((rc = gemm(L, ws, dt, h, ly.wq, M, Hq * D, H, q, 0, 0, stream))) return rc;
+      if ((rc = gemm(L, ws, dt, h, ly.wk, M, Hkv * D, H, k, 0, 0, stream))) return rc;
+      if ((rc = gemm(L, ws, dt, h, ly.wv, M, Hkv * D, H, v, 0, 0, stream))) return rc;
+    }
+    const long long nqk = (long long)M * (Hq + Hkv) * (D / 2);
+    hipLaunchKernelGGL(rope_kernel<T>, dim3((unsigned)((nqk + 255) / 256)), dim3(256), 0, stream, q,
+                       Hq, k, Hkv, M, R, D, log2_theta, st->kv_len, n_causal, n_mask, group);
     if ((rc = launch_status("draft_verify_step(rope)"))) return rc;
     rc = attn_hybrid_block_grouped(q, k, v, ly.k_pool, ly.v_pool, st->page_table, st->kv_len, S,
                                    n_causal, n_mask, group, Hq, Hkv, D, st->max_pages,
@@ -831,12 +1075,23 @@ static int forward_layers(const dvs_model* m, const dvs_state* st, int n_causal,
     if (m->ffn > 0) {
       hipLaunchKernelGGL(rmsnorm_kernel<T>, dim3(M), dim3(256), 0, stream, x, (const T*)ly.g_mlp,
                          H, m->rms_eps, h);
-      if ((rc = gemm(L, ws, dt, h, ly.w_gate, M, m->ffn, H, gate, 0, 0, stream))) return rc;
-      if ((rc = gemm(L, ws, dt, h, ly.w_up, M, m->ffn, H, up, 0, 0, stream))) return rc;
-      const long long n = (long long)M * m->ffn;
-      hipLaunchKernelGGL(silu_mul_kernel<T>, dim3((unsigned)((n + 255) / 256)), dim3(256), 0,
-                         stream, gate, up, n, act);
-      if ((rc = launch_status("draft_verify_step(silu)"))) return rc;
+      if (use_ws(dt, M, H)) {
+        // gate and up in one launch, silu(gate) * up in its epilogue
+        GemmArgs g{};
+        g.A = (const __bf16*)h; g.M = M; g.K = H; g.ncols = 32 * ((m->ffn + 15) / 16);
+        g.seg[0] = GemmSeg{(const __bf16*)ly.w_gate, act, 0, m->ffn};
+        g.seg[1] = GemmSeg{(const __bf16*)ly.w_up, nullptr, 0, m->ffn};
+        g.nseg = 2;
+        g.epi = EPI_SWIGLU;
+        if ((rc = launch_ws(g, stream))) return rc;
+      } else {
+        if ((rc = gemm(L, ws, dt, h, ly.w_gate, M, m->ffn, H, gate, 0, 0, stream))) return rc;
+        if ((rc = gemm(L, ws, dt, h, ly.w_up, M, m->ffn, H, up, 0, 0, stream))) return rc;
+        const long long n = (long long)M * m->ffn;
+        hipLaunchKernelGGL(silu_mul_kernel<T>, dim3((unsigned)((n + 255) / 256)), dim3(256), 0,
+                           stream, gate, up, n, act);
+        if ((rc = launch_status("draft_verify_step(silu)"))) return rc;
+      }
       if ((rc = gemm(L, ws, dt, act, ly.w_down, M, H, m->ffn, x, 1, 1, stream))) return rc;
     }
   }
@@ -860,11 +1115,17 @@ static int run_step(const dvs_model* m, const dvs_state* st, int n_causal, int n
   int rc;
   if ((rc = launch_status("draft_verify_step(embed)"))) return rc;
   if ((rc = forward_layers<T>(m, st, n_causal, n_mask, chunk_keys, L, ws, stream, group))) return rc;
-  if ((rc = gemm(L, ws, m->dtype, ws + L.h, m->lm_head, M, m->vocab, m->hidden, logits, 1, 0, stream)))
-    return rc;
-  rc = argmax_accept(logits, DVS_F32, S, R, m->vocab, n_causal, st->draft, st->draft_width, am,
-                     nullptr, st->err_word, stream);
-  if (rc) return rc;
+  if (!logits_out && use_ws(m->dtype, M, m->hidden)) {
+    // top-1 in the LM head's epilogue: the logits never reach memory
+    if ((rc = lm_head_top1(m, L, ws, ws + L.h, M, am, st->err_word, stream))) return rc;
+  } else {
+    if ((rc = gemm(L, ws, m->dtype, ws + L.h, m->lm_head, M, m->vocab, m->hidden, logits, 1, 0,
+                   stream)))
+      return rc;
+    rc = argmax_accept(logits, DVS_F32, S, R, m->vocab, n_causal, st->draft, st->draft_width, am,
+                       nullptr, st->err_word, stream);
+    if (rc) return rc;
+  }
   // acceptance inside the commit kernel
   return accept_commit(S, n_causal, n_mask, group, am, acc, st->kv_len, st->page_table, st->num_pages,
                        st->max_pages, st->free_stack, st->free_top, st->num_pool_pages,
