@@ -735,22 +735,21 @@ __global__ void __launch_bounds__(NW * 64, 1) attn_bf16_kernel(AttnParams p) {
       write_out(o, lsum > 0.f ? 1.f / lsum : 0.f);
       continue;
     }
-    // Publish the partial with write-through (agent-coherent) stores, wait for
-    // them, then count in; the workgroup that completes the item merges with
-    // coherent loads.  No L2-wide write-back or invalidate is needed.
+    // Publish the partial (each thread's O values and its (m, l) contiguous),
+    // wait for the stores, then count in; the workgroup that completes the
+    // item merges.
     const int wg0 = (int)blockIdx.x - k;
     const size_t slot = part_slot(p.balanced, it, p.max_segs, wg0, k);
     {
-      float* po = p.part_o + slot * (size_t)(NT * NREG);
-      float* pml = p.part_ml + slot * (size_t)(NT * 2);
-      __hip_atomic_store(pml + tid, m, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      __hip_atomic_store(pml + NT + tid, lsum, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      float* po = p.part_o + slot * (size_t)(NT * NREG) + (size_t)tid * NREG;
+      float* pml = p.part_ml + slot * (size_t)(NT * 2) + (size_t)tid * 2;
+      *(f32x2*)pml = f32x2{m, lsum};
 #pragma unroll
       for (int dg = 0; dg < DG; ++dg)
 #pragma unroll
-        for (int i = 0; i < 16; ++i)
-          __hip_atomic_store(po + (dg * 16 + i) * NT + tid, o[dg][i], __ATOMIC_RELAXED,
-                             __HIP_MEMORY_SCOPE_AGENT);
+        for (int j = 0; j < 4; ++j)
+          *(f32x4*)(po + dg * 16 + 4 * j) =
+              f32x4{o[dg][4 * j], o[dg][4 * j + 1], o[dg][4 * j + 2], o[dg][4 * j + 3]};
     }
     wait_vmcnt<0>();
     __syncthreads();
@@ -763,40 +762,50 @@ __global__ void __launch_bounds__(NW * 64, 1) attn_bf16_kernel(AttnParams p) {
                                           __HIP_MEMORY_SCOPE_AGENT) == nseg - 1);
     __syncthreads();
     if (!s_flag[0]) continue;
-    // Partials are read with coherent loads; every batch is issued in full
-    // before any of it is used, so the loads overlap instead of each one
-    // waiting for the previous.
+    // Partials are read in batches issued in full before any of it is used,
+    // so the loads overlap instead of each one waiting for the previous.
+    auto ml_of = [&](int c) {
+      return *(const f32x2*)(p.part_ml + part_slot(p.balanced, it, p.max_segs, wg0, c) * (NT * 2) +
+                             (size_t)tid * 2);
+    };
     float M = -INFINITY;
     for (int c0 = 0; c0 < nseg; c0 += 8) {
-      float mv[8];
+      f32x2 mv[8];
 #pragma unroll
-      for (int j = 0; j < 8; ++j)
-        mv[j] = __hip_atomic_load(p.part_ml + part_slot(p.balanced, it, p.max_segs, wg0, min(c0 + j, nseg - 1)) * (NT * 2) + tid,
-                                  __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      for (int j = 0; j < 8; ++j) mv[j] = ml_of(min(c0 + j, nseg - 1));
 #pragma unroll
-      for (int j = 0; j < 8; ++j) M = fmaxf(M, mv[j]);   // repeats of the last segment are harmless
+      for (int j = 0; j < 8; ++j) M = fmaxf(M, mv[j][0]);   // repeats of the last segment are harmless
     }
     const float Ms = (M == -INFINITY) ? 0.f : M;
     f32x16 acc[DG];
 #pragma unroll
     for (int dg = 0; dg < DG; ++dg) acc[dg] = f32x16{};
     float lt = 0.f;
-    for (int c = 0; c < nseg; ++c) {
-      const size_t sc = part_slot(p.balanced, it, p.max_segs, wg0, c);
-      const float* src_ml = p.part_ml + sc * (NT * 2);
-      const float* src = p.part_o + sc * (NT * NREG);
-      float pv[NREG];
+    // SB segments per batch (two where the registers allow), added in
+    // segment order
+    constexpr int SB = NREG <= 48 ? 2 : 1;
+    for (int c0 = 0; c0 < nseg; c0 += SB) {
+      f32x4 pv[SB][NREG / 4];
+      f32x2 mlc[SB];
 #pragma unroll
-      for (int i = 0; i < NREG; ++i)
-        pv[i] = __hip_atomic_load(src + i * NT + tid, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      const float mc = __hip_atomic_load(src_ml + tid, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      const float lc = __hip_atomic_load(src_ml + NT + tid, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      const float wgt = __builtin_amdgcn_exp2f(mc - Ms);
-      lt += wgt * lc;
+      for (int b = 0; b < SB; ++b) {
+        const int c = min(c0 + b, nseg - 1);
+        const float* src = p.part_o + part_slot(p.balanced, it, p.max_segs, wg0, c) * (NT * NREG) +
+                           (size_t)tid * NREG;
 #pragma unroll
-      for (int dg = 0; dg < DG; ++dg)
+        for (int j = 0; j < NREG / 4; ++j) pv[b][j] = *(const f32x4*)(src + 4 * j);
+        mlc[b] = ml_of(c);
+      }
 #pragma unroll
-        for (int i = 0; i < 16; ++i) acc[dg][i] += wgt * pv[dg * 16 + i];
+      for (int b = 0; b < SB; ++b) {
+        if (c0 + b >= nseg) break;
+        const float wgt = __builtin_amdgcn_exp2f(mlc[b][0] - Ms);
+        lt += wgt * mlc[b][1];
+#pragma unroll
+        for (int dg = 0; dg < DG; ++dg)
+#pragma unroll
+          for (int i = 0; i < 16; ++i) acc[dg][i] += wgt * pv[b][(dg * 16 + i) / 4][i % 4];
+      }
     }
     write_out(acc, lt > 0.f ? 1.f / lt : 0.f);
     if (tid == 0) __hip_atomic_store(&p.counters[it], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);

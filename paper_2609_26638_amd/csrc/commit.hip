@@ -257,7 +257,10 @@ static int launch_commit(const char* who, int32_t S, int32_t n_causal, int32_t n
   p.num_pages = num_pages; p.free_stack = free_stack; p.free_top = free_top;
   p.boundary = boundary; p.draft = draft; p.out_tokens = out_tokens; p.out_count = out_count;
   p.finished = finished; p.err = err_word;
-  hipLaunchKernelGGL(kv_commit_kernel, dim3(1), dim3(COMMIT_THREADS), 0, (hipStream_t)stream, p);
+  // one thread per sequence, in whole waves: the block scans and barriers
+  // cost as many steps as the block has threads' log2
+  const int threads = ((S + 63) / 64) * 64;
+  hipLaunchKernelGGL(kv_commit_kernel, dim3(1), dim3(threads), 0, (hipStream_t)stream, p);
   return launch_status(who);
 }
 
