@@ -137,6 +137,101 @@ def cpu_baseline(ai, li, n_seq: int, threads: int):
     return tokens / dt, desc, dt
 
 
+def secondary_configs(steps: int):
+    """The smaller workloads, timed beside the headline one (each with its
+    own settling run first):
+      * one bf16 decoder-layer attention (1 sequence, KV 2048, 16/4 heads x
+        128, B = 16 -> 32 rows): latency of attn_hybrid_block with the
+        last-level cache flushed before every launch (a 512 MiB write), and
+        with it warm;
+      * the batched serving step (32 sequences, KV U[1024, 8192], B = 16,
+        vocab 65536, drafts match w.p. 0.9): committed tokens/s of the
+        single-layer step (attention, top-1, accept + commit)."""
+    import numpy as np
+    import torch
+    from paper_2609_26638_amd import dvs, synth
+
+    def dev(a):
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).cuda()
+
+    res = {}
+    # --- one decoder-layer attention, latency
+    ai = synth.one_layer_attn_inputs()
+    S, R, B = ai.S, ai.R, ai.n_causal
+    q, kn, vn, kp, vp = dev(ai.q), dev(ai.k_new), dev(ai.v_new), dev(ai.k_pool), dev(ai.v_pool)
+    st = dvs.DeviceState(ai.state)
+    out = torch.empty_like(q)
+    ws = dvs.Workspace(dvs.attn_workspace_bytes(S, B, B, ai.Hq, ai.Hkv, ai.D, ai.state.max_pages, 0))
+    flush = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
+
+    def attn():
+        dvs.attn_hybrid_block(q, kn, vn, kp, vp, st.page_table, st.kv_len, B, B, ai.scale, out=out,
+                              workspace=ws)
+    for _ in range(200):
+        attn()
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(2 * steps)]
+    for i in range(steps):          # cold: the cache flushed before each launch
+        flush.fill_(i & 0xff)
+        ev[i][0].record(); attn(); ev[i][1].record()
+    for i in range(steps, 2 * steps):   # warm: back to back
+        ev[i][0].record(); attn(); ev[i][1].record()
+    torch.cuda.synchronize()
+    cold = sum(a.elapsed_time(b) for a, b in ev[:steps]) / steps
+    warm = sum(a.elapsed_time(b) for a, b in ev[steps:]) / steps
+    nbytes = attn_algorithmic_bytes(ai.state.kv_len, S, R, ai.Hq, ai.Hkv, ai.D)
+    res["one_layer_attention"] = {
+        "workload": "1 sequence, KV 2048 (1536 vision + 512 text), 16q/4kv heads, head_dim 128, "
+                    "B=16 (32 rows), bf16",
+        "latency_us_llc_flushed": round(cold * 1e3, 2), "latency_us_warm": round(warm * 1e3, 2),
+        "algorithmic_bytes": nbytes,
+        "gbs_llc_flushed": round(nbytes / (cold / 1e3) / 1e9, 1)}
+    del flush, q, kn, vn, kp, vp, out, ws
+    # --- batched serving step, committed tokens/s
+    ai, li = synth.batched_serving_inputs()
+    S, R, B = ai.S, ai.R, ai.n_causal
+    q, kn, vn, kp, vp = dev(ai.q), dev(ai.k_new), dev(ai.v_new), dev(ai.k_pool), dev(ai.v_pool)
+    logits = dev(li.logits)
+    host = ai.state.copy()
+    host.out_tokens = np.full((S, 256), -1, np.int32)
+    pristine, st = dvs.DeviceState(host), dvs.DeviceState(host)
+    out = torch.empty_like(q)
+    am = torch.empty((S, R), dtype=torch.int32, device="cuda")
+    acc = torch.empty((S,), dtype=torch.int32, device="cuda")
+    ws = dvs.Workspace(dvs.attn_workspace_bytes(S, B, B, ai.Hq, ai.Hkv, ai.D, host.max_pages, 0))
+
+    def step():
+        st.copy_from(pristine)
+        dvs.attn_hybrid_block(q, kn, vn, kp, vp, st.page_table, st.kv_len, B, B, ai.scale,
+                              out=out, err=st.err, workspace=ws)
+        dvs.argmax_accept(logits, B, st.draft, argmax_out=am, err=st.err, accept=False)
+        dvs.accept_commit(st, am, B, B, accept_out=acc)
+    t0 = time.perf_counter()
+    while time.perf_counter() - t0 < 0.3:
+        for _ in range(25):
+            step()
+        torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        step()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    if int(st.err.item()):
+        raise RuntimeError(f"device error word {int(st.err.item())}")
+    toks = int((st.out_count - pristine.out_count).sum().item())
+    res["batched_serving_step"] = {
+        "workload": "32 sequences, KV U[1024,8192], 16q/4kv heads, head_dim 128, B=16 (32 rows), "
+                    "scattered 16-token pages, vocab 65536, drafts match top-1 w.p. 0.9; "
+                    "single-layer step",
+        "committed_tokens_per_s": round(toks / (ms / 1e3), 1), "ms_per_step": round(ms, 4),
+        "tokens_per_step": toks,
+        "attn_algorithmic_bytes": attn_algorithmic_bytes(ai.state.kv_len, S, R, ai.Hq, ai.Hkv, ai.D)}
+    return res
+
+
 # confidence threshold of the direct block-diffusion and refined-draft figures
 # (one of the thresholds, 0.7 / 0.9 / 0.95 / 0.99, the paper reports its
 # diffusion mode at)
@@ -318,6 +413,8 @@ def main():
                     help="untimed steps run back to back before the warmup, until the GPU's "
                          "power management has reached its sustained-load state")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-secondary", action="store_true",
+                    help="skip the one-layer latency and batched-serving figures")
     ap.add_argument("--workload", default="long-document", choices=["long-document", "decoder-stack"],
                     help="long-document: the single-layer step (the headline line); "
                          "decoder-stack: the 16-layer stack end to end")
@@ -516,6 +613,10 @@ def main():
         "settle": {"steps": settle_steps, "s": round(t_settle, 2)},
         "input_gen_s": round(t_gen, 1),
     }
+    if not args.no_secondary:
+        del logits, q, kn, vn, kp, vp, out, ws
+        torch.cuda.empty_cache()
+        line["other_configs"] = secondary_configs(max(args.steps, 20))
     if not args.no_cpu_baseline:
         model, n_aff, blas = host_cpu()
         rate1, desc, _ = cpu_baseline(ai, li, args.cpu_seqs, 1)

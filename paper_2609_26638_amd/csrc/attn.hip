@@ -51,7 +51,7 @@ constexpr int KT = 64;                 // keys per tile
 constexpr int NSTAGE = 4;              // LDS ring depth for cache tiles
 constexpr int SUB_TILES = 256;         // tiles whose page ids are staged at once
 constexpr int MAX_CHUNK_KEYS = 16384;
-constexpr int BAL_MAX_SEGS = 9;        // balanced mode: segments per item (bound)
+constexpr int BAL_MAX_SEGS = 16;       // balanced mode: segments per item (bound)
 constexpr int BAL_MAX_SEQS = 1024;     // balanced mode: sequences per call
 constexpr float RESCALE_LOG2 = 8.f;
 
