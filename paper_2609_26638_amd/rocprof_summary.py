@@ -3,10 +3,10 @@
 * ``stats``: the kernel-trace statistics of a run (``--kernel-trace --stats``)
   as a markdown table, with the command that produced them.  Given
   ``--kernel``, ``--groups`` and ``--bench``, it also splits that kernel's
-  launches, in start order, into the bench's phases (warmup, the event-free
-  timed loop, the instrumented loop) and sets the average of the
-  instrumented loop beside the ``avg_ms`` the bench line printed in the
-  same process.
+  launches, in start order, into the bench's phases (settling, warmup, the
+  event-free timed loop, the instrumented loop) and sets the trace's
+  averages of the timed and instrumented loops beside the ``avg_ms`` and
+  ``instrumented_avg_ms`` the bench line printed in the same process.
 * ``traffic``: HBM bytes per dispatch of one kernel from a ``--pmc FETCH_SIZE``
   run and a ``--pmc WRITE_SIZE`` run of ``bench.py --profile-attn N``.  Both
   counters are calibrated against the device-to-device copy of known size
@@ -73,14 +73,18 @@ def launch_groups_md(trace, kernel, groups, bench_line=None):
         avgs[name] = sum(part) / len(part)
         out.append(f"| {name} | {len(part)} | {avgs[name]:.1f} | {min(part):.1f} | {max(part):.1f} |")
     if bench_line is not None:
-        avg = bench_line["roofline"]["avg_ms"] * 1e3
-        out += ["", f"The bench line printed by the same process: `avg_ms` = {avg:.1f} us "
-                f"(HIP events around each launch of the instrumented loop), "
+        rl = bench_line["roofline"]
+        out += ["", "The bench line printed by the same process: "
                 f"`value` = {bench_line['value']:.0f} {bench_line['unit']}."]
-        last = list(avgs)[-1] if avgs else None
-        if last is not None:
-            out.append(f"Trace average of the same launches: {avgs[last]:.1f} us "
-                       f"({avgs[last] / avg:.3f} of the event figure).")
+        # avg_ms comes from the event-free timed loop (its step time less the
+        # other stages); instrumented_avg_ms from events around each launch
+        for key, phase, how in (("avg_ms", "timed", "timed loop, step time less the other stages"),
+                                ("instrumented_avg_ms", "instrumented",
+                                 "HIP events around each launch")):
+            if key in rl and phase in avgs:
+                ev = rl[key] * 1e3
+                out.append(f"`{key}` = {ev:.1f} us ({how}); the trace's {phase} launches "
+                           f"average {avgs[phase]:.1f} us ({avgs[phase] / ev:.3f} of it).")
     return "\n".join(out) + "\n"
 
 
