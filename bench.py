@@ -25,6 +25,7 @@ import argparse
 import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -38,10 +39,18 @@ ATTN_SOURCES = [os.path.join(ROOT, "paper_2609_26638_amd", "csrc", f)
                 for f in ("attn.hip", "dvs_common.h")]
 
 
+def _code_only(text: str) -> str:
+    """The source with comments removed and whitespace collapsed, so that a
+    comment edit does not count as a changed kernel."""
+    text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", " ", text)
+    return " ".join(text.split())
+
+
 def attn_source_hash() -> str:
     h = hashlib.sha256()
     for f in ATTN_SOURCES:
-        h.update(open(f, "rb").read())
+        h.update(_code_only(open(f).read()).encode())
     return h.hexdigest()[:16]
 
 

@@ -20,10 +20,13 @@
 //     touches only the lane's own row;
 //     O^T[d, row] += V^T P^T  A = V^T slice of the head-dim-major V tile,
 //                             B = P packed to bf16 straight from the scores.
-//   Cache tiles are copied HBM -> LDS with direct 16-byte loads through a
-//   3-stage ring; the tiles that reach the window go through registers (keys
-//   < L from the pool, [L, T) from k_new / v_new, appended to the pool by row
-//   tile 0, >= T zero).
+//   A workgroup first appends the window keys of its own tiles ([L, T) from
+//   k_new / v_new) to their pool slots; then every tile, cache or window, is
+//   copied HBM -> LDS with direct 16-byte loads through a 3-stage ring.  The
+//   tiles that reach L are masked; in the tile that runs past T the keys >= T
+//   read the sequence's last page again and their V values are zeroed before
+//   the products (their weights are zero, and a non-finite stale value would
+//   otherwise make them NaN).
 //
 //   Two ways to cut the work (both deterministic):
 //   * aligned (chunk_keys > 0): workgroup = one chunk of one item, chunks at
@@ -34,9 +37,11 @@
 //     workgroup takes an equal contiguous share, so the grid finishes together
 //     whatever the length mix; only shares that split an item publish
 //     partials.
-//   A split item's partials (m, l, O in fp32) are merged in segment order by
-//   the last workgroup to finish it (write-through stores, counter, coherent
-//   loads).
+//   A split item's partials ((m, l) in fp32; O in fp32, or as O/l in bf16 in
+//   the producer/consumer kernel) are merged in segment order by the last
+//   workgroup to count in; the count-in is an agent-scope acquire-release
+//   atomic add on the item's counter, which orders every workgroup's partial
+//   stores before the merging workgroup's loads.
 //
 // fp32 path: a plain per-(sequence, row, head) workgroup, fp32 throughout.
 #include <math.h>
@@ -175,145 +180,97 @@ __device__ __forceinline__ void wait_tiles(int tiles_after) {
 }
 
 // ---------------------------------------------------------------------------
-// A tile that reaches the window [L, T) or runs past T, staged through
-// registers into the K / V LDS tiles (kb, vb): keys < L from the pool,
-// [L, T) from k_new / v_new (and, when `append`, written to their pool
-// slots), >= T zero.  Every load of a thread is issued before any of its
-// stores (a pool append could alias a pool read as far as the compiler can
-// tell, which would otherwise serialize one memory round trip per element);
-// invalid elements read a harmless in-bounds address and are zeroed after.
+// Append the window keys [a, b) (L <= a < b <= T) of item (sequence s, KV
+// head kvh) to their pool slots: K rows from k_new, and in the head-dim-major
+// V pages one 32-byte row (the 16 slots of a page) per (page, head-dim
+// element), merged with the slots outside [a, b), which keep their values.
+// A workgroup appends exactly the keys of its own tiles before it streams
+// them, so the window tiles then go through the same direct loads as cache
+// tiles.  Tiles start at multiples of 64 keys, so every page belongs to one
+// tile, and workgroups of different row tiles of one item write identical
+// bytes.  Every load of a thread is issued before its stores (a pool store
+// could alias a pool load as far as the compiler can tell).  Slots whose page
+// id is invalid are skipped (the page staging reports them).
 // ---------------------------------------------------------------------------
 template <int D, int NT>
-__device__ __forceinline__ void fill_window_tile(int tid, int t0, int pg_lo, int L, int T, int s, int R,
-                                                 int Hkv, int kvh, bool append, const int* s_pages,
-                                                 char* __restrict__ kpb, char* __restrict__ vpb,
-                                                 const char* __restrict__ knb, const char* __restrict__ vnb,
-                                                 char* kb, char* vb) {
+__device__ __forceinline__ void append_window(int tid, int a, int b, int L, int s, int R, int Hkv,
+                                              int kvh, const int32_t* __restrict__ pt, int pool_pages,
+                                              char* __restrict__ kpb, char* __restrict__ vpb,
+                                              const char* __restrict__ knb,
+                                              const char* __restrict__ vnb) {
   constexpr int CPR = D / 8;
   constexpr int KROWB = D * 2;
   constexpr int PAGE_K = 16 * KROWB;
   constexpr int PAGE_V = D * 32;
-  constexpr int NKC = KT * CPR;              // 16-byte K chunks per tile (key-major)
-  constexpr int NVC = KT / 16 * D * 2;       // 16-byte V chunks of the LDS tile (8 keys of one head-dim row)
-  constexpr int NNC = KT * CPR;              // 16-byte v_new chunks (8 head-dim values of one key)
-  constexpr int NKI = (NKC + NT - 1) / NT, NVI = (NVC + NT - 1) / NT, NNI = (NNC + NT - 1) / NT;
-  // Per thread up to QB chunks of each kind per batch (one batch at 512
-  // threads); every global load of a batch is issued before any store.
-  //   K:  key rows, from the pool (key < L), k_new (< T) or zero.
-  //   V pool part: LDS chunk (head-dim row d, 8 keys) from the pool's
-  //       head-dim-major page when its keys are < L (element by element where
-  //       the chunk straddles L; its keys >= L are left to the next part).
-  //   V new part: a v_new chunk (one key, 8 head-dim values) for keys in
-  //       [L, T), zero for keys >= T, written to the 8 head-dim rows of the
-  //       key with 2-byte LDS stores (and appended to the pool the same way).
-  // The two V parts write disjoint bytes of the tile.
-  constexpr int QB = 2;
-  constexpr int NBK = (NKI + QB - 1) / QB, NBV = (NVI + QB - 1) / QB, NBN = (NNI + QB - 1) / QB;
-  constexpr int NB = NBK > NBV ? (NBK > NBN ? NBK : NBN) : (NBV > NBN ? NBV : NBN);
+  // K: (b - a) rows of CPR 16-byte chunks, two chunks per thread per batch
+  const int nk = (b - a) * CPR;
 #pragma unroll 1
-  for (int b = 0; b < NB; ++b) {
-    // ---- page ids (LDS), read together; index clamped into the array for
-    // chunks whose page is not used
-    int kpg[QB], vpg[QB], npg[QB];
+  for (int i0 = tid; i0 < nk; i0 += 2 * NT) {
+    u32x4 x[2];
+    int pg[2];
 #pragma unroll
-    for (int k = 0; k < QB; ++k) {
-      const int ck = tid + (b * QB + k) * NT;
-      kpg[k] = s_pages[min(max(((t0 + ck / CPR) >> 4) - pg_lo, 0), SUB_TILES * 4 - 1)];
-      const int cv = tid + (b * QB + k) * NT;
-      vpg[k] = s_pages[min(max(((t0 + (cv / (D * 2)) * 16) >> 4) - pg_lo, 0), SUB_TILES * 4 - 1)];
-      const int cn = tid + (b * QB + k) * NT;
-      npg[k] = s_pages[min(max(((t0 + cn / CPR) >> 4) - pg_lo, 0), SUB_TILES * 4 - 1)];
+    for (int e = 0; e < 2; ++e) {
+      const int i = i0 + e * NT;
+      const bool live = i < nk;
+      const int key = a + (live ? i / CPR : 0), cc = live ? i % CPR : 0;
+      pg[e] = live ? pt[key >> 4] : -1;
+      x[e] = *(const u32x4*)(knb + (((size_t)s * R + (key - L)) * Hkv + kvh) * KROWB + cc * 16);
     }
-    // ---- loads
-    u32x4 kv[QB], pv[QB], nv[QB];
-    uint16_t pe[QB][8];
 #pragma unroll
-    for (int k = 0; k < QB; ++k) {
-      {   // K
-        const int ci = tid + (b * QB + k) * NT;
-        const int key = t0 + ci / CPR, cc = ci % CPR;
-        const bool live = b * QB + k < NKI && ci < NKC;
-        const bool inpool = live && key < L, innew = live && key >= L && key < T;
-        const char* src = inpool ? kpb + ((size_t)kpg[k] * Hkv + kvh) * PAGE_K + (key & 15) * KROWB + cc * 16
-                                 : knb + (((size_t)s * R + (innew ? key - L : 0)) * Hkv + kvh) * KROWB + cc * 16;
-        const u32x4 x = *(const u32x4*)src;
-        kv[k] = (inpool || innew) ? x : u32x4{0, 0, 0, 0};
-      }
-      {   // V, pool part
-        const int ci = tid + (b * QB + k) * NT;
-        const int d = (ci >> 1) % D;
-        const int kbase = t0 + (ci / (D * 2)) * 16 + (ci & 1) * 8;
-        const bool live = b * QB + k < NVI && ci < NVC;
-        const char* vpage = vpb + ((size_t)vpg[k] * Hkv + kvh) * PAGE_V + d * 32 + (kbase & 15) * 2;
-        const bool whole = live && kbase + 8 <= L;
-        const u32x4 x = *(const u32x4*)(whole ? vpage : vnb);
-        pv[k] = x;
+    for (int e = 0; e < 2; ++e) {
+      const int i = i0 + e * NT;
+      if (i >= nk || pg[e] < 0 || pg[e] >= pool_pages) continue;
+      const int key = a + i / CPR, cc = i % CPR;
+      *(u32x4*)(kpb + ((size_t)pg[e] * Hkv + kvh) * PAGE_K + (key & 15) * KROWB + cc * 16) = x[e];
+    }
+  }
+  // V: pages [a / 16, (b - 1) / 16], one (page, head-dim element) row per thread
+  const int p0 = a >> 4;
+  const int nv = (((b - 1) >> 4) - p0 + 1) * D;
+#pragma unroll 1
+  for (int i = tid; i < nv; i += NT) {
+    const int pi = p0 + i / D, d = i % D;
+    const int pg = pt[pi];
+    if (pg < 0 || pg >= pool_pages) continue;
+    char* row = vpb + ((size_t)pg * Hkv + kvh) * PAGE_V + d * 32;
+    const int lo = max(a, pi * 16) - pi * 16, hi = min(b, pi * 16 + 16) - pi * 16;   // new slots [lo, hi)
+    u32x4 o0 = u32x4{0, 0, 0, 0}, o1 = u32x4{0, 0, 0, 0};
+    if (lo > 0 || hi < 16) {
+      o0 = *(const u32x4*)row;
+      o1 = *(const u32x4*)(row + 16);
+    }
+    uint16_t nvv[16];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {   // straddling chunk only (rare): keys < L
-          const bool el = live && !whole && kbase + e < L;
-          const uint16_t y = *(const uint16_t*)(el ? vpage + 2 * e : vnb);
-          pe[k][e] = y;
-        }
-      }
-      {   // V, new part
-        const int ci = tid + (b * QB + k) * NT;
-        const int key = t0 + ci / CPR, cc = ci % CPR;
-        const bool live = b * QB + k < NNI && ci < NNC && key >= L && key < T;
-        const u32x4 x = *(const u32x4*)(vnb + (((size_t)s * R + (live ? key - L : 0)) * Hkv + kvh) * KROWB + cc * 16);
-        nv[k] = live ? x : u32x4{0, 0, 0, 0};
+    for (int e = 0; e < 16; ++e) {
+      const int key = pi * 16 + (e >= lo && e < hi ? e : lo);
+      nvv[e] = *(const uint16_t*)(vnb + (((size_t)s * R + (key - L)) * Hkv + kvh) * KROWB + d * 2);
+    }
+    uint32_t w[8] = {o0[0], o0[1], o0[2], o0[3], o1[0], o1[1], o1[2], o1[3]};
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      if (e >= lo && e < hi) {
+        const int sh = 16 * (e & 1);
+        w[e >> 1] = (w[e >> 1] & ~(0xffffu << sh)) | ((uint32_t)nvv[e] << sh);
       }
     }
-    // ---- stores: LDS tiles, then the pool appends of keys in [L, T)
-#pragma unroll
-    for (int k = 0; k < QB; ++k) {
-      {   // K
-        const int ci = tid + (b * QB + k) * NT;
-        const int kk = ci / CPR, cc = ci % CPR;
-        const int key = t0 + kk;
-        if (b * QB + k < NKI && ci < NKC) {
-          *(u32x4*)(kb + kk * KROWB + ((cc ^ kswz<CPR>(kk)) << 4)) = kv[k];
-          if (append && key >= L && key < T)
-            *(u32x4*)(kpb + ((size_t)kpg[k] * Hkv + kvh) * PAGE_K + (key & 15) * KROWB + cc * 16) = kv[k];
-        }
-      }
-      {   // V, pool part
-        const int ci = tid + (b * QB + k) * NT;
-        const int tp = ci / (D * 2);
-        const int d = (ci >> 1) % D;
-        const int hc = ci & 1;
-        const int kbase = t0 + tp * 16 + hc * 8;
-        char* dst = vb + (tp * D + d) * 32 + ((hc ^ vswz(d)) << 4);
-        if (b * QB + k < NVI && ci < NVC) {
-          if (kbase + 8 <= L) {
-            *(u32x4*)dst = pv[k];
-          } else if (kbase < L) {
-#pragma unroll
-            for (int e = 0; e < 8; ++e)
-              if (kbase + e < L) *(uint16_t*)(dst + 2 * e) = pe[k][e];
-          }
-        }
-      }
-      {   // V, new part (keys >= L of the tile, zeros past T)
-        const int ci = tid + (b * QB + k) * NT;
-        const int kk = ci / CPR, cc = ci % CPR;
-        const int key = t0 + kk;
-        if (b * QB + k < NNI && ci < NNC && key >= L) {
-          const int tp = kk >> 4, kin = kk & 15;
-          const uint32_t w[4] = {nv[k][0], nv[k][1], nv[k][2], nv[k][3]};
-#pragma unroll
-          for (int j = 0; j < 8; ++j) {
-            const int d = cc * 8 + j;
-            const uint16_t v = (uint16_t)(w[j >> 1] >> (16 * (j & 1)));
-            *(uint16_t*)(vb + (tp * D + d) * 32 + ((((kin >> 3) ^ vswz(d)) << 4) | ((kin & 7) * 2))) = v;
-            if (append && key < T)
-              *(uint16_t*)(vpb + ((size_t)npg[k] * Hkv + kvh) * PAGE_V + d * 32 + (key & 15) * 2) = v;
-          }
-        }
-      }
-    }
+    *(u32x4*)row = u32x4{w[0], w[1], w[2], w[3]};
+    *(u32x4*)(row + 16) = u32x4{w[4], w[5], w[6], w[7]};
   }
 }
 
+// A V fragment of the 8 keys key0 .. key0 + 7 (bf16, in key order) with the
+// keys >= T zeroed: past T the pool holds whatever the slots last held (a
+// non-finite value there would turn its zero weight into NaN).
+__device__ __forceinline__ bf16x8 v_keys_below(const bf16x8& f, int key0, int T) {
+  const int nz = T - key0;
+  u32x4 w = __builtin_bit_cast(u32x4, f);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const uint32_t m = (2 * j + 1 < nz) ? 0xffffffffu : ((2 * j < nz) ? 0x0000ffffu : 0u);
+    w[j] &= m;
+  }
+  return __builtin_bit_cast(bf16x8, w);
+}
 
 __device__ __forceinline__ uint32_t lds_addr(const void* ptr) {
   return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)ptr;
@@ -631,33 +588,55 @@ __global__ void __launch_bounds__(NW * 64, 1) attn_bf16_kernel(AttnParams p) {
         pf[t] = __builtin_bit_cast(bf16x8, u32x4{pk[0], pk[1], pk[2], pk[3]});
       }
       lsum += (psum[0] + psum[1]) + (psum[2] + psum[3]);
-      // V fragments are read one k-step ahead of the MFMAs that use them
-      bf16x8 va[2][DG];
+      // V fragments are read one k-step ahead of the MFMAs that use them;
+      // in the tile that runs past T (TAIL), keys >= T are zeroed
+      auto pv = [&](auto tail) {
+        constexpr bool TAIL = decltype(tail)::value != 0;
+        bf16x8 va[2][DG];
 #pragma unroll
-      for (int dg = 0; dg < DG; ++dg) va[0][dg] = *(const bf16x8*)(stage + vfrag + dg * 32 * 32);
+        for (int dg = 0; dg < DG; ++dg) va[0][dg] = *(const bf16x8*)(stage + vfrag + dg * 32 * 32);
 #pragma unroll
-      for (int t = 0; t < KT / 16; ++t) {
-        if (t + 1 < KT / 16) {
+        for (int t = 0; t < KT / 16; ++t) {
+          if (t + 1 < KT / 16) {
 #pragma unroll
-          for (int dg = 0; dg < DG; ++dg)
-            va[(t + 1) & 1][dg] = *(const bf16x8*)(stage + vfrag + ((t + 1) * D + dg * 32) * 32);
+            for (int dg = 0; dg < DG; ++dg)
+              va[(t + 1) & 1][dg] = *(const bf16x8*)(stage + vfrag + ((t + 1) * D + dg * 32) * 32);
+          }
+#pragma unroll
+          for (int dg = 0; dg < DG; ++dg) {
+            bf16x8 vf = va[t & 1][dg];
+            if constexpr (TAIL) vf = v_keys_below(vf, key0 + t * 16 + 8 * hh, T);
+            o[dg] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[t], o[dg], 0, 0, 0);
+          }
         }
-#pragma unroll
-        for (int dg = 0; dg < DG; ++dg)
-          o[dg] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[t & 1][dg], pf[t], o[dg], 0, 0, 0);
-      }
+      };
+      if (key0 + KT > T) pv(IC<1>{});
+      else pv(IC<0>{});
     };
 
+    // ---- the window keys of the segment's tiles go to their pool slots
+    // first; then every tile streams through the direct-load ring
+    {
+      const int wa = max(L, j0 * KT), wb = min(T, j1 * KT);
+      if (wa < wb) {
+        append_window<D, NT>(tid, wa, wb, L, s, R, p.Hkv, kvh, pt, p.pool_pages, kpb, vpb, knb, vnb);
+        wait_vmcnt<0>();
+        __syncthreads();
+      }
+    }
     // ---- the segment's tiles, in sub-ranges whose page ids fit in LDS
+    const int n_valid = (T + 15) >> 4;    // pages the sequence holds
     for (int ja = j0; ja < j1; ja += SUB_TILES) {
       const int jb = min(j1, ja + SUB_TILES);
       const int pg_lo = ja * 4;
-      const int pg_hi = min(jb * 4, (T + 15) >> 4);
+      const int pg_hi = jb * 4;
       if (ja != j0) __syncthreads();
       if (tid == 0) s_flag[1] = 0;
       __syncthreads();
       for (int i = tid; i < pg_hi - pg_lo; i += NT) {
-        int pg = pt[pg_lo + i];
+        // pages past the last one of the sequence (in the tile that runs
+        // past T) repeat the last page: their keys are masked
+        int pg = pt[min(pg_lo + i, n_valid - 1)];
         if (pg < 0 || pg >= p.pool_pages) {
           pg = 0;
           s_flag[1] = 1;
@@ -667,9 +646,8 @@ __global__ void __launch_bounds__(NW * 64, 1) attn_bf16_kernel(AttnParams p) {
       __syncthreads();   // also completes the Q loads
       if (tid == 0 && s_flag[1]) set_err(p.err, DVS_ERR_BAD_PAGE);
 
-      // cache tiles (all 64 keys below L) through the direct-load ring
-      const int jm = min(jb, max(ja, L / KT));
-      const int n_main = jm - ja;
+      // every tile through the direct-load ring; tiles that reach L are masked
+      const int n_main = jb - ja;
       auto issue = [&](int i) {
         char* stage = smem + (i % NSTAGE) * STAGE_B;
         const int pbase = i * 4;          // first page of tile ja+i, relative to pg_lo
@@ -697,17 +675,7 @@ __global__ void __launch_bounds__(NW * 64, 1) attn_bf16_kernel(AttnParams p) {
         wait_tiles<NPL>(min(NSTAGE - 2, n_main - 1 - i));
         __builtin_amdgcn_s_barrier();     // tile i complete for every wave; tile i-1 consumed
         if (i + NSTAGE - 1 < n_main) issue(i + NSTAGE - 1);
-        compute_tile(smem + (i % NSTAGE) * STAGE_B, (ja + i) * KT, false);
-      }
-
-      // tiles that reach the window or run past T: staged through registers
-      for (int jt = jm; jt < jb; ++jt) {
-        const int t0 = jt * KT;
-        __syncthreads();
-        fill_window_tile<D, NT>(tid, t0, pg_lo, L, T, s, R, p.Hkv, kvh, rt == 0, s_pages, kpb, vpb, knb, vnb,
-                                smem, smem + KTILE_B);
-        __syncthreads();
-        compute_tile(smem, t0, true);
+        compute_tile(smem + (i % NSTAGE) * STAGE_B, (ja + i) * KT, ja + i >= L / KT);
       }
     }
 
@@ -838,11 +806,10 @@ __global__ void __launch_bounds__(NW * 64, 1) attn_bf16_kernel(AttnParams p) {
 // ---------------------------------------------------------------------------
 constexpr int PC_NSTAGE = 3;
 // Producer/consumer kernel, balanced split: cost units of a tile.  A tile
-// that reaches the window (staged through registers, unpipelined) costs about
-// 4.5 cache tiles (measured: 10.5 us against 2.3 us), so a workgroup's share
-// counts it that way instead of as one tile.
+// that reaches the window streams like a cache tile but adds the masking, and
+// the segment holding it first appends the window's K/V to the pool.
 constexpr int PC_WM = 4;    // units of a cache tile (keys below L)
-constexpr int PC_WW = 18;   // units of a window tile
+constexpr int PC_WW = 5;    // units of a window tile
 // units added to the last tile of an item: the end of a segment there (the
 // partial's publication, the next item's page staging and, for the last
 // workgroup to finish the item, the merge)
@@ -994,14 +961,17 @@ __global__ void __launch_bounds__(NP * 128, 1) attn_bf16_pc_kernel(AttnParams p)
         hi[g] = !rvalid[g] ? -1 : row_hi(p, L, rr[g]);
       }
 
+      const int n_valid = (T + 15) >> 4;    // pages the sequence holds
       auto stage_pages = [&](int ja, int jb) {
         const int pg_lo = ja * 4;
-        const int pg_hi = min(jb * 4, (T + 15) >> 4);
+        const int pg_hi = jb * 4;
         if (ja != j0) __syncthreads();
         if (tid == 0) s_flag[1] = 0;
         __syncthreads();
         for (int i = tidv; i < pg_hi - pg_lo; i += NP * 128) {
-          int pg = pt[pg_lo + i];
+          // pages past the last one of the sequence (in the tile that runs
+          // past T) repeat the last page: their keys are masked
+          int pg = pt[min(pg_lo + i, n_valid - 1)];
           if (pg < 0 || pg >= p.pool_pages) {
             pg = 0;
             s_flag[1] = 1;
@@ -1010,15 +980,6 @@ __global__ void __launch_bounds__(NP * 128, 1) attn_bf16_pc_kernel(AttnParams p)
         }
         __syncthreads();
         if (tid == 0 && s_flag[1]) set_err(p.err, DVS_ERR_BAD_PAGE);
-      };
-      // window tiles (reach [L, T) or past it): every thread stages them,
-      // keys < L from the pool, [L, T) from k_new / v_new (appended to the pool
-      // by row tile 0), >= T zero; K into K slot 0, V into V slot 0
-      auto fill_window = [&](int t0, int pg_lo) {
-        int tidw = tidv;   // opaque: nothing of the fill is hoisted out of it
-        asm volatile("" : "+v"(tidw));
-        fill_window_tile<D, NP * 128>(tidw, t0, pg_lo, L, T, s, R, p.Hkv, kvh, rt == 0, s_pages, kpb, vpb, knb,
-                                      vnb, kring, vring);
       };
       const int wg0 = owner(0);
       const size_t slot = part_slot(1, it, p.max_segs, wg0, kseg);
@@ -1106,6 +1067,19 @@ __global__ void __launch_bounds__(NP * 128, 1) attn_bf16_pc_kernel(AttnParams p)
           }
         }
       };
+
+      // the window keys of this segment's tiles go to their pool slots first;
+      // then every tile streams through the direct-load rings
+      {
+        const int wa = max(L, j0 * KT), wb = min(T, j1 * KT);
+        if (wa < wb) {
+          int tidw = tidv;   // opaque: nothing of the append is hoisted out of it
+          asm volatile("" : "+v"(tidw));
+          append_window<D, NP * 128>(tidw, wa, wb, L, s, R, p.Hkv, kvh, pt, p.pool_pages, kpb, vpb, knb, vnb);
+          wait_vmcnt<0>();
+          __syncthreads();
+        }
+      }
 
       if constexpr (PROD) {
         // =================== producer: QK and softmax ===================
@@ -1209,24 +1183,36 @@ __global__ void __launch_bounds__(NP * 128, 1) attn_bf16_pc_kernel(AttnParams p)
         for (int ja = j0; ja < j1; ja += SUB_TILES) {
           const int jb = min(j1, ja + SUB_TILES);
           stage_pages(ja, jb);
-          const int jm = min(jb, max(ja, L / KT));
-          const int n_main = jm - ja;
-          for (int i = 0; n_main > 0 && i <= n_main; ++i) {
-            pc_barrier();   // A: K(i) landed, P(i-1) taken
-            if (i < n_main) qk(kring + (i % NS) * KTILE_B);
-            pc_barrier();   // B: consumers hold P(i-1)
-            if (i < n_main) softmax_out(false, 0);
-          }
-          // LDS-only barriers: the fill's pool appends are read by no one in
-          // this launch, so they need not complete before the tile is used
-          for (int jt = jm; jt < jb; ++jt) {
-            pc_barrier();
-            fill_window(jt * KT, ja * 4);
-            pc_barrier();
-            qk(kring);
-            softmax_out(true, jt * KT);
-            pc_barrier();                                    // P of the window tile ready
-            pc_barrier();                                    // consumer done with it
+          const int n_main = jb - ja;
+          // tiles below L, then the tiles that reach L (masked) and the
+          // drain period: one period per tile plus one, as the consumer's
+          const int n_c = min(max(nm - ja, 0), n_main);
+          if (n_main > 0) {
+            for (int i = 0; i < n_c; ++i) {
+              pc_barrier();   // A: K(i) landed, P(i-1) taken
+              qk(kring + (i % NS) * KTILE_B);
+              pc_barrier();   // B: consumers hold P(i-1)
+              softmax_out(false, 0);
+            }
+            for (int i = n_c; i <= n_main; ++i) {
+              pc_barrier();
+              // tile i-1 runs past T: its V entries of keys >= T are zeroed
+              // in LDS before the consumer's products of this period read
+              // them (their weights are zero; a stale non-finite value would
+              // make the product NaN)
+              if (i >= 1 && (ja + i) * KT > T) {
+                char* vst = vring + ((i - 1) % NS) * VTILE_B;
+                const int nk = T - (ja + i - 1) * KT;
+                for (int e = tidv; e < (KT - nk) * D; e += NC) {
+                  const int kk = nk + e / D, d = e % D;
+                  const int tp = kk >> 4, kin = kk & 15;
+                  *(uint16_t*)(vst + (tp * D + d) * 32 + ((((kin >> 3) ^ vswz(d)) << 4) | ((kin & 7) * 2))) = 0;
+                }
+              }
+              if (i < n_main) qk(kring + (i % NS) * KTILE_B);
+              pc_barrier();
+              if (i < n_main) softmax_out(true, (ja + i) * KT);
+            }
           }
         }
         // segment-final m (l is the consumer's)
@@ -1319,8 +1305,7 @@ __global__ void __launch_bounds__(NP * 128, 1) attn_bf16_pc_kernel(AttnParams p)
         for (int ja = j0; ja < j1; ja += SUB_TILES) {
           const int jb = min(j1, ja + SUB_TILES);
           stage_pages(ja, jb);
-          const int jm = min(jb, max(ja, L / KT));
-          const int n_main = jm - ja;
+          const int n_main = jb - ja;
           // With 4 pairs, consumer wave k copies page k of every 4-page tile
           // (its K_INS / V_INS 1 KB segments are exactly that page).
           int kpg = 0, vpg = 0;
@@ -1439,17 +1424,6 @@ __global__ void __launch_bounds__(NP * 128, 1) attn_bf16_pc_kernel(AttnParams p)
             if (i >= 1) pv(hd, vring + ((i - 1) % NS) * VTILE_B);
             if (i <= n_main - 2) issue_v(i);
             if (nxt) take_pages();
-          }
-          for (int jt = jm; jt < jb; ++jt) {
-            pc_barrier();
-            fill_window(jt * KT, ja * 4);
-            pc_barrier();
-            pc_barrier();                                      // producer's P of the window tile
-            Hand hd;
-            take_p(hd);
-            add_l(hd);
-            pv(hd, vring);
-            pc_barrier();
           }
         }
         __syncthreads();                                       // F1

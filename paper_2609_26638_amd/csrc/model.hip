@@ -10,11 +10,13 @@
 // and the hot-path tail argmax_accept -> accept_commit.
 //
 // Every matrix product is C[m, n] = sum_k A[m, k] * W[n, k] with weights laid
-// out [out, in] so both MFMA operands are contiguous along k.  One wave owns
-// 32 output columns for ALL rows: it streams its weight rows exactly once, in
-// ascending k, and accumulates every 32-row group of A against them.  A row's
-// result therefore never depends on how many rows the call carries, so an AR
-// call (1 row) and a fused call (2B rows) produce bit-identical rows.
+// out [out, in] so both MFMA operands are contiguous along k.  K is cut into
+// a fixed number of logical splits that depends on K only; each output is the
+// in-order sum of the splits' in-order MFMA accumulations, whichever kernel
+// computes it (gemm_ws_kernel for calls of up to 256 rows, gemm_rt_kernel for
+// longer ones).  A row's result therefore never depends on how many rows the
+// call carries, so an AR call (1 row) and a fused call (2B rows) produce
+// bit-identical rows.
 #include <algorithm>
 #include <math.h>
 
@@ -252,10 +254,12 @@ __global__ void silu_mul_kernel(const T* __restrict__ gate, const T* __restrict_
 }
 
 // ---------------------------------------------------------------------------
-// GEMM: C[m, n] (=, or += into an fp32 residual) sum_k A[m, k] W[n, k]
-// One wave per 32 output columns; it walks k in ascending order, loading each
-// weight fragment once and applying it to every 32-row group of A (up to
-// MG_MAX groups, the rest in further passes).
+// Generic GEMM: C[m, n] (=, or += into an fp32 residual) sum_k A[m, k] W[n, k]
+// for the fp32 model and for bf16 shapes whose K is not a multiple of 64
+// (small test models).  One wave per 32 output columns; it walks k in
+// ascending order, loading each weight fragment once and applying it to every
+// 32-row group of A (up to MG_MAX groups, the rest in further passes), so a
+// row's result does not depend on the row count here either.
 // ---------------------------------------------------------------------------
 constexpr int MG_MAX = 8;   // 32-row groups per pass (256 rows)
 
