@@ -708,7 +708,10 @@ __global__ void __launch_bounds__(NW * 64, 1) attn_bf16_kernel(AttnParams p) {
     // item merges.
     const int wg0 = (int)blockIdx.x - k;
     const size_t slot = part_slot(p.balanced, it, p.max_segs, wg0, k);
-    {
+    // a wave whose 32 rows all lie past the item's rows has nothing to
+    // publish or merge (few-row calls run four waves for the copies)
+    const bool wave_rows = rt * RPW + w * 32 < p.rows_total;
+    if (wave_rows) {
       float* po = p.part_o + slot * (size_t)(NT * NREG) + (size_t)tid * NREG;
       float* pml = p.part_ml + slot * (size_t)(NT * 2) + (size_t)tid * 2;
       *(f32x2*)pml = f32x2{m, lsum};
@@ -730,6 +733,8 @@ __global__ void __launch_bounds__(NW * 64, 1) attn_bf16_kernel(AttnParams p) {
                                           __HIP_MEMORY_SCOPE_AGENT) == nseg - 1);
     __syncthreads();
     if (!s_flag[0]) continue;
+    if (tid == 0) __hip_atomic_store(&p.counters[it], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (!wave_rows) continue;
     // Partials are read in batches issued in full before any of it is used,
     // so the loads overlap instead of each one waiting for the previous.
     auto ml_of = [&](int c) {
@@ -776,7 +781,6 @@ __global__ void __launch_bounds__(NW * 64, 1) attn_bf16_kernel(AttnParams p) {
       }
     }
     write_out(acc, lt > 0.f ? 1.f / lt : 0.f);
-    if (tid == 0) __hip_atomic_store(&p.counters[it], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
 }
 
@@ -1642,6 +1646,10 @@ static AttnPlan plan_attn(int S, int R, int Hq, int Hkv, int D, int max_pages, i
     // (8 waves, one producer and one consumer per SIMD) over 256 rows
     pl.pc = (pl.balanced && pl.rows_total > 128) ? 1 : 0;
     if (pl.pc) pl.nw = 8;
+    // aligned chunks with few rows (decode steps): four waves all the same,
+    // so that a chunk's copies are spread over them (a row's arithmetic does
+    // not depend on the wave count)
+    if (!pl.balanced && pl.nw < 4) pl.nw = 4;
   } else {
     pl.nw = 4;
   }
