@@ -126,7 +126,11 @@ __global__ void fill_words_kernel(int32_t* __restrict__ p, int n, int32_t v) {
   if (i < n) p[i] = v;
 }
 
-// out[m, :] = x[m, :] / sqrt(mean(x^2) + eps) * g   (one workgroup per row)
+// out[m, :] = x[m, :] / sqrt(mean(x^2) + eps) * g   (one workgroup per row).
+// Thread t takes elements t, t + 256, ... (the sum of squares in that order,
+// then the waves' sums combined as (w0 + w1) + (w2 + w3)); a row of up to
+// 256 * RN_REG elements is loaded once, with its gains, before the reduction.
+constexpr int RN_REG = 8;
 template <typename T>
 __global__ void __launch_bounds__(256) rmsnorm_kernel(const float* __restrict__ x, const T* __restrict__ g,
                                                       int H, float eps, T* __restrict__ out) {
@@ -134,14 +138,36 @@ __global__ void __launch_bounds__(256) rmsnorm_kernel(const float* __restrict__ 
   const int mrow = blockIdx.x;
   const float* xr = x + (size_t)mrow * H;
   float ss = 0.f;
-  for (int i = threadIdx.x; i < H; i += 256) ss = fmaf(xr[i], xr[i], ss);
+  const bool held = H <= 256 * RN_REG;
+  float xv[RN_REG], gv[RN_REG];
+  if (held) {
+#pragma unroll
+    for (int j = 0; j < RN_REG; ++j) {
+      const int i = threadIdx.x + 256 * j;
+      xv[j] = i < H ? xr[i] : 0.f;
+      gv[j] = i < H ? to_f(g[i]) : 0.f;
+    }
+#pragma unroll
+    for (int j = 0; j < RN_REG; ++j)
+      if (threadIdx.x + 256 * j < H) ss = fmaf(xv[j], xv[j], ss);
+  } else {
+    for (int i = threadIdx.x; i < H; i += 256) ss = fmaf(xr[i], xr[i], ss);
+  }
   for (int off = 32; off > 0; off >>= 1) ss += __shfl_xor(ss, off);
   if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
   __syncthreads();
   const float tot = (red[0] + red[1]) + (red[2] + red[3]);
   const float inv = 1.0f / sqrtf(tot / (float)H + eps);
-  for (int i = threadIdx.x; i < H; i += 256)
-    out[(size_t)mrow * H + i] = from_f<T>(xr[i] * inv * to_f(g[i]));
+  if (held) {
+#pragma unroll
+    for (int j = 0; j < RN_REG; ++j) {
+      const int i = threadIdx.x + 256 * j;
+      if (i < H) out[(size_t)mrow * H + i] = from_f<T>(xv[j] * inv * gv[j]);
+    }
+  } else {
+    for (int i = threadIdx.x; i < H; i += 256)
+      out[(size_t)mrow * H + i] = from_f<T>(xr[i] * inv * to_f(g[i]));
+  }
 }
 
 // Position of window row r relative to kv_len: r, except for mask rows cut
