@@ -364,6 +364,7 @@ __global__ void __launch_bounds__(256) gemm_bf16_kernel(const __bf16* __restrict
 // ---------------------------------------------------------------------------
 constexpr int GK_SPLITS = 4;        // logical K splits when K % 256 == 0
 constexpr int WS_MAX_ROWS = 256;    // calls up to this many rows use gemm_ws_kernel
+constexpr int WS_NARROW_NB = 128;   // few-row calls below this many 32-column blocks take 16-column blocks
 
 static int gemm_ksplit(int K) { return K % (64 * GK_SPLITS) == 0 ? GK_SPLITS : 1; }
 
@@ -429,8 +430,15 @@ __device__ __forceinline__ void ws_wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
 }
 
-template <int MT>
+// NARROW: blocks of 16 output columns (few-row calls with few blocks, plain
+// epilogues): the products still span 32 columns, of which the second 16
+// read stale LDS rows and are discarded -- each kept column's arithmetic is
+// exactly the 32-column block's -- so the chip gets twice the workgroups
+// and each streams half the weights.
+template <int MT, bool NARROW>
 __global__ void __launch_bounds__(256, 2) gemm_ws_kernel(GemmArgs g) {
+  constexpr int CW = NARROW ? 16 : 32;     // output columns per block
+  constexpr int WI = NARROW ? 1 : 2;       // weight copies (16 rows each) per chunk
   constexpr int RG = MT / 32;              // 32-row groups per wave
   // ring stages per wave (deeper rings for the few-row calls measured no
   // faster: the few-row calls are bound by their few workgroups)
@@ -438,20 +446,21 @@ __global__ void __launch_bounds__(256, 2) gemm_ws_kernel(GemmArgs g) {
   constexpr int KC = 32;                   // k per chunk (64 bytes of a row)
   constexpr int WB = 32 * 64;              // W part of a chunk: 32 rows
   constexpr int CB = WB + MT * 64;         // chunk bytes (W rows, then A rows)
-  constexpr int NPL = (32 + MT) / 16;      // 1 KB copies per chunk and wave
+  constexpr int NPL = WI + MT / 16;        // 1 KB copies per chunk and wave
   static_assert(NPL * (NS - 1) < 64, "vmcnt range");
+  static_assert(!NARROW || MT == 32, "narrow blocks serve few-row calls");
   static_assert(4 * NS * CB >= GK_SPLITS * MT * 32 * 4, "the split sums reuse the rings");
   __shared__ __attribute__((aligned(1024))) char s_ring[4 * NS * CB];
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l32 = lane & 31, hh = lane >> 5;
-  const int NB = (g.ncols + 31) / 32;
+  const int NB = (g.ncols + CW - 1) / CW;
   // XCD-aware order: blocks b, b + 8, b + 16, ... share an XCD; the row
   // tiles of one column block are consecutive among them
   const int x = blockIdx.x & 7, j = blockIdx.x >> 3;
   const int cb = (j / g.n_rt) * 8 + x, rt = j % g.n_rt;
   if (cb >= NB) return;
-  const int c0 = cb * 32, m0 = rt * MT;
+  const int c0 = cb * CW, m0 = rt * MT;
   char* ring = s_ring + w * NS * CB;
 
   // Copies: instruction i of a chunk moves 1 KB, 16 rows of 64 bytes; lane L
@@ -460,9 +469,9 @@ __global__ void __launch_bounds__(256, 2) gemm_ws_kernel(GemmArgs g) {
   // rows an MFMA operand read serves at once hit distinct banks.
   const int crow = lane >> 2, cchk = lane & 3;
   int si = 0;
-  const __bf16* wsrc[2];   // this lane's weight rows (tile rows 16i + L/4)
+  const __bf16* wsrc[WI];  // this lane's weight rows (tile rows 16i + L/4)
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
+  for (int i = 0; i < WI; ++i) {
     const int r = 16 * i + crow;
     const __bf16* base;
     bool valid;
@@ -494,7 +503,7 @@ __global__ void __launch_bounds__(256, 2) gemm_ws_kernel(GemmArgs g) {
     char* dst = ring + (t % NS) * CB;
     const int k0 = kw + t * KC;
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < WI; ++i)
       __builtin_amdgcn_global_load_lds((const void*)(wsrc[i] + k0),
                                        (__attribute__((address_space(3))) void*)(dst + i * 1024), 16, 0, 0);
 #pragma unroll
@@ -541,7 +550,7 @@ __global__ void __launch_bounds__(256, 2) gemm_ws_kernel(GemmArgs g) {
   // rows of W past the segment end were read from row 0: zero their columns
   bool wvalid;
   if (g.epi == EPI_SWIGLU) wvalid = cb * 16 + (l32 & 15) < g.seg[0].n;
-  else wvalid = c0 - g.seg[si].n0 + l32 < g.seg[si].n;
+  else wvalid = l32 < CW && c0 - g.seg[si].n0 + l32 < g.seg[si].n;
 
   // splits in order through LDS (the rings are free once every wave is done)
   __syncthreads();
@@ -584,7 +593,7 @@ __global__ void __launch_bounds__(256, 2) gemm_ws_kernel(GemmArgs g) {
       }
     } else {
       const int col = c0 + c - g.seg[si].n0;
-      if (rv && col < g.seg[si].n) {
+      if (rv && c < CW && col < g.seg[si].n) {
         const size_t o = (size_t)row * g.seg[si].n + col;
         if (g.epi == EPI_BF16) ((__bf16*)g.seg[si].C)[o] = (__bf16)t;
         else if (g.epi == EPI_F32_ADD) ((float*)g.seg[si].C)[o] += t;
@@ -949,13 +958,18 @@ static StepLayout step_layout(const dvs_model* m, int S, int n_causal, int n_mas
 }
 
 static int launch_ws(GemmArgs& g, hipStream_t st) {
-  const int NB = (g.ncols + 31) / 32;
   const int MT = g.M <= 32 ? 32 : 64;
+  // few-row calls with few 32-column blocks and a plain epilogue: 16-column
+  // blocks (twice the workgroups)
+  const bool narrow = MT == 32 && (g.ncols + 31) / 32 < WS_NARROW_NB &&
+                      (g.epi == EPI_BF16 || g.epi == EPI_F32 || g.epi == EPI_F32_ADD);
+  const int NB = narrow ? (g.ncols + 15) / 16 : (g.ncols + 31) / 32;
   g.n_rt = (g.M + MT - 1) / MT;
   const long long grid = (long long)((NB + 7) / 8) * 8 * g.n_rt;
   DVS_CHECK_SUPPORTED(grid < (1LL << 31), "draft_verify_step: GEMM grid too large");
-  if (MT == 32) hipLaunchKernelGGL(gemm_ws_kernel<32>, dim3((unsigned)grid), dim3(256), 0, st, g);
-  else hipLaunchKernelGGL(gemm_ws_kernel<64>, dim3((unsigned)grid), dim3(256), 0, st, g);
+  if (narrow) hipLaunchKernelGGL((gemm_ws_kernel<32, true>), dim3((unsigned)grid), dim3(256), 0, st, g);
+  else if (MT == 32) hipLaunchKernelGGL((gemm_ws_kernel<32, false>), dim3((unsigned)grid), dim3(256), 0, st, g);
+  else hipLaunchKernelGGL((gemm_ws_kernel<64, false>), dim3((unsigned)grid), dim3(256), 0, st, g);
   return launch_status("draft_verify_step(gemm)");
 }
 
