@@ -440,9 +440,10 @@ __global__ void __launch_bounds__(256, 2) gemm_ws_kernel(GemmArgs g) {
   constexpr int CW = NARROW ? 16 : 32;     // output columns per block
   constexpr int WI = NARROW ? 1 : 2;       // weight copies (16 rows each) per chunk
   constexpr int RG = MT / 32;              // 32-row groups per wave
-  // ring stages per wave (deeper rings for the few-row calls measured no
-  // faster: the few-row calls are bound by their few workgroups)
-  constexpr int NS = 3;
+  // ring stages per wave: four for the few-row calls (64 KB of LDS, two
+  // workgroups per CU; six or eight stages, one workgroup per CU, measured
+  // slower), three for the wider tiles
+  constexpr int NS = MT == 32 ? 4 : 3;
   constexpr int KC = 32;                   // k per chunk (64 bytes of a row)
   constexpr int WB = 32 * 64;              // W part of a chunk: 32 rows
   constexpr int CB = WB + MT * 64;         // chunk bytes (W rows, then A rows)
