@@ -84,6 +84,15 @@ __device__ __forceinline__ int run_token(const CommitParams& p, int s, int A, in
   return j < A ? p.draft[(size_t)s * p.draft_width + j] : p.argmax[(size_t)s * p.R + A];
 }
 
+// FAST: acceptance here, no lead token, no draft groups, at most
+// COMMIT_FAST_W causal rows and draft slots.  A sequence's whole draft row,
+// its verify rows' top-1 and the next draft's rows are loaded at once, with
+// its state and the free-stack top, so the acceptance, the run and the next
+// draft come from registers (one memory round trip instead of one per chunk
+// and per dependent step); the results are the general path's.
+constexpr int COMMIT_FAST_W = 32;
+
+template <bool FAST>
 __global__ void __launch_bounds__(COMMIT_THREADS) kv_commit_kernel(CommitParams p) {
   __shared__ int sh[COMMIT_THREADS];
   __shared__ int s_err;
@@ -95,7 +104,55 @@ __global__ void __launch_bounds__(COMMIT_THREADS) kv_commit_kernel(CommitParams 
   int L = 0, n = 0, k = 0, need = 0, cnt = 0, A = 0;
   bool fin = false, stop = false;
   int last_tok = 0;
-  if (live_seq) {
+  constexpr int FW = FAST ? COMMIT_FAST_W : 1;
+  int dv[FW], av[FW], nx[FW];   // FAST: draft row, verify top-1, next draft
+  int top0 = 0;
+  if (FAST) top0 = *p.free_top;
+  if (FAST && live_seq) {
+    const int nd = p.n_causal - 1;
+    const int32_t* drow = p.draft + (size_t)s * p.draft_width;
+    const int32_t* arow = p.argmax + (size_t)s * p.R;
+    L = p.kv_len[s];
+    n = p.num_pages[s];
+    cnt = p.out_count[s];
+    fin = p.finished[s] != 0;
+#pragma unroll
+    for (int j = 0; j < FW; ++j) {
+      dv[j] = j < nd ? drow[j] : 0;
+      av[j] = j < p.n_causal ? arow[j] : 0;
+      nx[j] = (p.n_mask > 0 && j < p.draft_width) ? arow[p.n_causal + j] : 0;
+    }
+    if (!fin) {
+      bool go = true;
+#pragma unroll
+      for (int j = 0; j < FW; ++j) {
+        if (j < nd && go && dv[j] == av[j]) A = j + 1;
+        else go = false;
+      }
+    }
+    if (p.accept_out) p.accept_out[s] = fin ? 0 : A;
+    if (!fin) {
+      // run = d_1..d_A, a_{A+1}; keep up to the first stop token / budget
+      bool done = false;
+#pragma unroll
+      for (int j = 0; j < FW; ++j) {
+        if (done || j > A) continue;
+        const int tk = j < A ? dv[j] : av[j];
+        if (cnt + k >= p.max_new) {
+          stop = done = true;
+        } else {
+          if (tk < 0) atomicOr(&s_err, DVS_ERR_OPEN_BLOCK);
+          ++k;
+          last_tok = tk;
+          if (p.eos_id >= 0 && tk == p.eos_id) stop = done = true;
+        }
+      }
+      if (cnt + k >= p.max_new) stop = true;
+    }
+    need = (L + k + p.window + DVS_PAGE_SIZE - 1) / DVS_PAGE_SIZE;
+    if (need > p.max_pages || n < 0 || n > p.max_pages || L < 0)
+      atomicOr(&s_err, DVS_ERR_MAX_PAGES);
+  } else if (!FAST && live_seq) {
     L = p.kv_len[s];
     n = p.num_pages[s];
     cnt = p.out_count[s];
@@ -160,7 +217,7 @@ __global__ void __launch_bounds__(COMMIT_THREADS) kv_commit_kernel(CommitParams 
   int tot_push = 0, tot_pop = 0;
   const int push_off = block_exclusive_scan(push, sh, tot_push);
   const int pop_off = block_exclusive_scan(pop, sh, tot_pop);
-  const int top0 = *p.free_top;
+  if (!FAST) top0 = *p.free_top;
   if (s == 0) {
     if (tot_pop > top0 + tot_push) atomicOr(&s_err, DVS_ERR_POOL_EXHAUSTED);
     if (top0 + tot_push > p.pool_pages || top0 < 0) atomicOr(&s_err, DVS_ERR_POOL_EXHAUSTED);
@@ -186,7 +243,25 @@ __global__ void __launch_bounds__(COMMIT_THREADS) kv_commit_kernel(CommitParams 
   }
   if (s == 0) *p.free_top = top1 - tot_pop;
 
-  if (live_seq) {
+  if (FAST && live_seq) {
+    p.num_pages[s] = need;
+    if (!fin) {
+      int32_t* ot = p.out_tokens + (size_t)s * p.max_new + cnt;
+#pragma unroll
+      for (int j = 0; j < FW; ++j)
+        if (j < k) ot[j] = j < A ? dv[j] : av[j];
+      p.out_count[s] = cnt + k;
+      p.kv_len[s] = L + k;
+      if (k > 0) p.boundary[s] = last_tok;
+      if (p.n_mask > 0) {
+        int32_t* drow = p.draft + (size_t)s * p.draft_width;
+#pragma unroll
+        for (int j = 0; j < FW; ++j)
+          if (j < p.draft_width) drow[j] = nx[j];
+      }
+      p.finished[s] = stop ? 1 : 0;
+    }
+  } else if (!FAST && live_seq) {
     p.num_pages[s] = need;
     if (!fin) {
       int32_t* ot = p.out_tokens + (size_t)s * p.max_new;
@@ -260,7 +335,12 @@ static int launch_commit(const char* who, int32_t S, int32_t n_causal, int32_t n
   // one thread per sequence, in whole waves: the block scans and barriers
   // cost as many steps as the block has threads' log2
   const int threads = ((S + 63) / 64) * 64;
-  hipLaunchKernelGGL(kv_commit_kernel, dim3(1), dim3(threads), 0, (hipStream_t)stream, p);
+  const bool fast = accept_here && !lead && draft_group == 0 && n_causal <= COMMIT_FAST_W &&
+                    draft_width <= COMMIT_FAST_W;
+  if (fast)
+    hipLaunchKernelGGL(kv_commit_kernel<true>, dim3(1), dim3(threads), 0, (hipStream_t)stream, p);
+  else
+    hipLaunchKernelGGL(kv_commit_kernel<false>, dim3(1), dim3(threads), 0, (hipStream_t)stream, p);
   return launch_status(who);
 }
 
