@@ -1032,28 +1032,38 @@ __global__ void __launch_bounds__(NP * 128, 1) attn_bf16_pc_kernel(AttnParams p)
           for (int b = 0; b < QB; ++b)
 #pragma unroll
             for (int j = 0; j < 4; ++j) acc[b][j] = 0.f;
+          // SBM segments' words in flight at once, then added in segment order
+          constexpr int SBM = 2;
 #pragma unroll 1
-          for (int c = 0; c < nseg; ++c) {
-            // opaque offset: the addresses are formed here, not hoisted
-            int off = (int)part_slot(1, it, p.max_segs, wg0, c) * (NC * OREG / 2) + ct;
-            asm volatile("" : "+v"(off));
-            uint32_t v[QB][2];
+          for (int c0 = 0; c0 < nseg; c0 += SBM) {
+            uint32_t v[SBM][QB][2];
 #pragma unroll
-            for (int b = 0; b < QB; ++b) {
-              const int q = half + 2 * (q0 + b);     // run index: g, dg, i4
-              const int base_w = (q >> 2) * 8 + (q & 3) * 2;   // (g * DG + dg) * 8 + 2 * i4
+            for (int sb = 0; sb < SBM; ++sb) {
+              // opaque offset: the addresses are formed here, not hoisted
+              int off = (int)part_slot(1, it, p.max_segs, wg0, min(c0 + sb, nseg - 1)) * (NC * OREG / 2) + ct;
+              asm volatile("" : "+v"(off));
 #pragma unroll
-              for (int j = 0; j < 2; ++j)
-                v[b][j] = __hip_atomic_load(pob + off + (base_w + j) * NC, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+              for (int b = 0; b < QB; ++b) {
+                const int q = half + 2 * (q0 + b);     // run index: g, dg, i4
+                const int base_w = (q >> 2) * 8 + (q & 3) * 2;   // (g * DG + dg) * 8 + 2 * i4
+#pragma unroll
+                for (int j = 0; j < 2; ++j)
+                  v[sb][b][j] = __hip_atomic_load(pob + off + (base_w + j) * NC, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+              }
             }
 #pragma unroll
-            for (int b = 0; b < QB; ++b) {
-              const int q = half + 2 * (q0 + b);
-              const int g = q / (DG * 4);
-              const float wc = s_w[c * RPWG + mkp * 64 + g * 32 + ml32];
+            for (int sb = 0; sb < SBM; ++sb) {
+              const int c = c0 + sb;
+              if (c >= nseg) break;
 #pragma unroll
-              for (int j = 0; j < 4; ++j)
-                acc[b][j] += wc * __uint_as_float((j & 1) ? (v[b][j >> 1] & 0xffff0000u) : (v[b][j >> 1] << 16));
+              for (int b = 0; b < QB; ++b) {
+                const int q = half + 2 * (q0 + b);
+                const int g = q / (DG * 4);
+                const float wc = s_w[c * RPWG + mkp * 64 + g * 32 + ml32];
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                  acc[b][j] += wc * __uint_as_float((j & 1) ? (v[sb][b][j >> 1] & 0xffff0000u) : (v[sb][b][j >> 1] << 16));
+              }
             }
           }
 #pragma unroll
