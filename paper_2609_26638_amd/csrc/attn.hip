@@ -703,23 +703,24 @@ __global__ void __launch_bounds__(NW * 64, 1) attn_bf16_kernel(AttnParams p) {
       write_out(o, lsum > 0.f ? 1.f / lsum : 0.f);
       continue;
     }
-    // Publish the partial (each thread's O values and its (m, l) contiguous),
-    // wait for the stores, then count in; the workgroup that completes the
-    // item merges.
+    // Publish the partial (the O values as 16-byte words, word j of every
+    // thread side by side, so that each store and load of a wave covers 1 KB
+    // in one piece; (m, l) per thread), wait for the stores, then count in;
+    // the workgroup that completes the item merges.
     const int wg0 = (int)blockIdx.x - k;
     const size_t slot = part_slot(p.balanced, it, p.max_segs, wg0, k);
     // a wave whose 32 rows all lie past the item's rows has nothing to
     // publish or merge (few-row calls run four waves for the copies)
     const bool wave_rows = rt * RPW + w * 32 < p.rows_total;
     if (wave_rows) {
-      float* po = p.part_o + slot * (size_t)(NT * NREG) + (size_t)tid * NREG;
+      float* po = p.part_o + slot * (size_t)(NT * NREG) + (size_t)tid * 4;
       float* pml = p.part_ml + slot * (size_t)(NT * 2) + (size_t)tid * 2;
       *(f32x2*)pml = f32x2{m, lsum};
 #pragma unroll
       for (int dg = 0; dg < DG; ++dg)
 #pragma unroll
         for (int j = 0; j < 4; ++j)
-          *(f32x4*)(po + dg * 16 + 4 * j) =
+          *(f32x4*)(po + (dg * 4 + j) * (NT * 4)) =
               f32x4{o[dg][4 * j], o[dg][4 * j + 1], o[dg][4 * j + 2], o[dg][4 * j + 3]};
     }
     wait_vmcnt<0>();
@@ -754,9 +755,9 @@ __global__ void __launch_bounds__(NW * 64, 1) attn_bf16_kernel(AttnParams p) {
 #pragma unroll
     for (int dg = 0; dg < DG; ++dg) acc[dg] = f32x16{};
     float lt = 0.f;
-    // SB segments per batch (two where the registers allow), added in
+    // SB segments per batch (four where the registers allow), added in
     // segment order
-    constexpr int SB = NREG <= 48 ? 2 : 1;
+    constexpr int SB = NREG <= 48 ? 4 : 1;
     for (int c0 = 0; c0 < nseg; c0 += SB) {
       f32x4 pv[SB][NREG / 4];
       f32x2 mlc[SB];
@@ -764,9 +765,9 @@ __global__ void __launch_bounds__(NW * 64, 1) attn_bf16_kernel(AttnParams p) {
       for (int b = 0; b < SB; ++b) {
         const int c = min(c0 + b, nseg - 1);
         const float* src = p.part_o + part_slot(p.balanced, it, p.max_segs, wg0, c) * (NT * NREG) +
-                           (size_t)tid * NREG;
+                           (size_t)tid * 4;
 #pragma unroll
-        for (int j = 0; j < NREG / 4; ++j) pv[b][j] = *(const f32x4*)(src + 4 * j);
+        for (int j = 0; j < NREG / 4; ++j) pv[b][j] = *(const f32x4*)(src + j * (NT * 4));
         mlc[b] = ml_of(c);
       }
 #pragma unroll
