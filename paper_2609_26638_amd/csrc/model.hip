@@ -365,6 +365,7 @@ __global__ void __launch_bounds__(256) gemm_bf16_kernel(const __bf16* __restrict
 constexpr int GK_SPLITS = 4;        // logical K splits when K % 256 == 0
 constexpr int WS_MAX_ROWS = 256;    // calls up to this many rows use gemm_ws_kernel
 constexpr int WS_NARROW_NB = 128;   // few-row calls below this many 32-column blocks take 16-column blocks
+constexpr int WS_WIDE_MIN_WG = 256; // 64-row calls take 2 blocks per wave while the grid keeps this many
 
 static int gemm_ksplit(int K) { return K % (64 * GK_SPLITS) == 0 ? GK_SPLITS : 1; }
 
@@ -435,62 +436,75 @@ __device__ __forceinline__ void ws_wait_vmcnt() {
 // read stale LDS rows and are discarded -- each kept column's arithmetic is
 // exactly the 32-column block's -- so the chip gets twice the workgroups
 // and each streams half the weights.
-template <int MT, bool NARROW>
-__global__ void __launch_bounds__(256, 2) gemm_ws_kernel(GemmArgs g) {
+// CB: column blocks per wave (wider calls): each wave computes its split for
+// CB adjacent 32-column blocks, so one A chunk feeds CB blocks' products
+// (A is re-read once per CB blocks instead of once per block); per element
+// the arithmetic is the single block's.
+template <int MT, bool NARROW, int CB, int EPI>
+__global__ void __launch_bounds__(256, CB <= 2 ? 2 : 1) gemm_ws_kernel(GemmArgs g) {
   constexpr int CW = NARROW ? 16 : 32;     // output columns per block
-  constexpr int WI = NARROW ? 1 : 2;       // weight copies (16 rows each) per chunk
+  constexpr int WI = NARROW ? 1 : 2;       // weight copies (16 rows each) per block and chunk
   constexpr int RG = MT / 32;              // 32-row groups per wave
   // ring stages per wave: four for the few-row calls (64 KB of LDS, two
   // workgroups per CU; six or eight stages, one workgroup per CU, measured
-  // slower), three for the wider tiles
-  constexpr int NS = MT == 32 ? 4 : 3;
+  // slower), three for 64-row tiles of one block, two for tiles of two
+  // blocks (64 KB: two workgroups per CU, measured faster than three stages
+  // or four blocks per wave at one workgroup per CU)
+  constexpr int NS = MT == 32 ? 4 : (CB == 2 ? 2 : 3);
   constexpr int KC = 32;                   // k per chunk (64 bytes of a row)
-  constexpr int WB = 32 * 64;              // W part of a chunk: 32 rows
-  constexpr int CB = WB + MT * 64;         // chunk bytes (W rows, then A rows)
-  constexpr int NPL = WI + MT / 16;        // 1 KB copies per chunk and wave
+  constexpr int WB = 32 * 64;              // W part of a block's chunk: 32 rows
+  constexpr int CHB = CB * WB + MT * 64;   // chunk bytes (CB blocks' W rows, then A rows)
+  constexpr int NPL = CB * WI + MT / 16;   // 1 KB copies per chunk and wave
+  constexpr int TW = CB * 32;              // tile width in the split sums
   static_assert(NPL * (NS - 1) < 64, "vmcnt range");
-  static_assert(!NARROW || MT == 32, "narrow blocks serve few-row calls");
-  static_assert(4 * NS * CB >= GK_SPLITS * MT * 32 * 4, "the split sums reuse the rings");
-  __shared__ __attribute__((aligned(1024))) char s_ring[4 * NS * CB];
+  static_assert(!NARROW || (MT == 32 && CB == 1), "narrow blocks serve few-row calls");
+  static_assert(!NARROW || EPI == EPI_BF16 || EPI == EPI_F32 || EPI == EPI_F32_ADD,
+                "narrow blocks take plain epilogues");
+  static_assert(4 * NS * CHB >= GK_SPLITS * MT * TW * 4, "the split sums reuse the rings");
+  __shared__ __attribute__((aligned(1024))) char s_ring[4 * NS * CHB];
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l32 = lane & 31, hh = lane >> 5;
-  const int NB = (g.ncols + CW - 1) / CW;
-  // XCD-aware order: blocks b, b + 8, b + 16, ... share an XCD; the row
-  // tiles of one column block are consecutive among them
+  const int NB = (g.ncols + CW - 1) / CW;  // blocks
+  const int NG = (NB + CB - 1) / CB;       // groups of CB blocks
+  // XCD-aware order: groups b, b + 8, b + 16, ... share an XCD; the row
+  // tiles of one group are consecutive among them
   const int x = blockIdx.x & 7, j = blockIdx.x >> 3;
-  const int cb = (j / g.n_rt) * 8 + x, rt = j % g.n_rt;
-  if (cb >= NB) return;
-  const int c0 = cb * CW, m0 = rt * MT;
-  char* ring = s_ring + w * NS * CB;
+  const int cg = (j / g.n_rt) * 8 + x, rt = j % g.n_rt;
+  if (cg >= NG) return;
+  const int m0 = rt * MT;
+  char* ring = s_ring + w * NS * CHB;
 
-  // Copies: instruction i of a chunk moves 1 KB, 16 rows of 64 bytes; lane L
-  // takes row 16i + L/4 and 16-byte chunk (L & 3) ^ sw(row), sw(row) =
-  // (row / 4) & 3, so LDS slot c of a row holds its chunk c ^ sw(row): the 16
-  // rows an MFMA operand read serves at once hit distinct banks.
+  // Copies: instruction i of a block's chunk moves 1 KB, 16 rows of 64
+  // bytes; lane L takes row 16i + L/4 and 16-byte chunk (L & 3) ^ sw(row),
+  // sw(row) = (row / 4) & 3, so LDS slot c of a row holds its chunk
+  // c ^ sw(row): the 16 rows an MFMA operand read serves at once hit distinct
+  // banks.  The blocks of a group lie in one segment (the host checks it).
   const int crow = lane >> 2, cchk = lane & 3;
   int si = 0;
-  const __bf16* wsrc[WI];  // this lane's weight rows (tile rows 16i + L/4)
+  if (EPI != EPI_SWIGLU)
+    while (si + 1 < g.nseg && cg * CB * CW >= g.seg[si + 1].n0) ++si;
+  const __bf16* wsrc[CB][WI];  // this lane's weight rows (block b, tile rows 16i + L/4)
 #pragma unroll
-  for (int i = 0; i < WI; ++i) {
-    const int r = 16 * i + crow;
-    const __bf16* base;
-    bool valid;
-    int rowi;
-    if (g.epi == EPI_SWIGLU) {
-      rowi = cb * 16 + (r & 15);
-      valid = rowi < g.seg[0].n;
-      base = r < 16 ? g.seg[0].W : g.seg[1].W;
-    } else {
-      while (si + 1 < g.nseg && c0 >= g.seg[si + 1].n0) ++si;
-      rowi = c0 - g.seg[si].n0 + r;
-      valid = rowi < g.seg[si].n;
-      base = g.seg[si].W;
+  for (int b = 0; b < CB; ++b)
+#pragma unroll
+    for (int i = 0; i < WI; ++i) {
+      const int cb = cg * CB + b, c0 = cb * CW;
+      const int r = 16 * i + crow;
+      const __bf16* base;
+      bool valid;
+      int rowi;
+      if (EPI == EPI_SWIGLU) {
+        rowi = cb * 16 + (r & 15);
+        valid = rowi < g.seg[0].n;
+        base = r < 16 ? g.seg[0].W : g.seg[1].W;
+      } else {
+        rowi = c0 - g.seg[si].n0 + r;
+        valid = rowi < g.seg[si].n;
+        base = g.seg[si].W;
+      }
+      wsrc[b][i] = base + (size_t)(valid ? rowi : 0) * g.K + ((cchk ^ ((r >> 2) & 3)) << 3);
     }
-    wsrc[i] = base + (size_t)(valid ? rowi : 0) * g.K + ((cchk ^ ((r >> 2) & 3)) << 3);
-  }
-  if (g.epi != EPI_SWIGLU)
-    while (si + 1 < g.nseg && c0 >= g.seg[si + 1].n0) ++si;
   const __bf16* asrc[MT / 16];
 #pragma unroll
   for (int i = 0; i < MT / 16; ++i) {
@@ -501,21 +515,25 @@ __global__ void __launch_bounds__(256, 2) gemm_ws_kernel(GemmArgs g) {
   const int kw = w * kq;               // this wave's split
   const int nch = kq / KC;
   auto issue = [&](int t) {
-    char* dst = ring + (t % NS) * CB;
+    char* dst = ring + (t % NS) * CHB;
     const int k0 = kw + t * KC;
 #pragma unroll
-    for (int i = 0; i < WI; ++i)
-      __builtin_amdgcn_global_load_lds((const void*)(wsrc[i] + k0),
-                                       (__attribute__((address_space(3))) void*)(dst + i * 1024), 16, 0, 0);
+    for (int b = 0; b < CB; ++b)
+#pragma unroll
+      for (int i = 0; i < WI; ++i)
+        __builtin_amdgcn_global_load_lds((const void*)(wsrc[b][i] + k0),
+                                         (__attribute__((address_space(3))) void*)(dst + b * WB + i * 1024), 16, 0, 0);
 #pragma unroll
     for (int i = 0; i < MT / 16; ++i)
       __builtin_amdgcn_global_load_lds((const void*)(asrc[i] + k0),
-                                       (__attribute__((address_space(3))) void*)(dst + WB + i * 1024), 16, 0, 0);
+                                       (__attribute__((address_space(3))) void*)(dst + CB * WB + i * 1024), 16, 0, 0);
   };
 
-  f32x16 acc[RG];
+  f32x16 acc[RG][CB];
 #pragma unroll
-  for (int a = 0; a < RG; ++a) acc[a] = f32x16{};
+  for (int a = 0; a < RG; ++a)
+#pragma unroll
+    for (int b = 0; b < CB; ++b) acc[a][b] = f32x16{};
   static_for<0, NS - 1>([&](auto c) {
     if (decltype(c)::value < nch) issue(decltype(c)::value);
   });
@@ -529,80 +547,157 @@ __global__ void __launch_bounds__(256, 2) gemm_ws_kernel(GemmArgs g) {
   for (int t = 0; t < nch; ++t) {
     if (t + NS - 1 < nch) issue(t + NS - 1);
     wait_chunk(min(NS - 1, nch - 1 - t));
-    const char* src = ring + (t % NS) * CB;
+    const char* src = ring + (t % NS) * CHB;
     // every operand of the chunk from LDS first, then the products
-    bf16x8 bw[KC / 16], ba[KC / 16][RG];
+    bf16x8 bw[KC / 16][CB], ba[KC / 16][RG];
 #pragma unroll
     for (int ks = 0; ks < KC / 16; ++ks) {
       const int q = 2 * ks + hh;   // the lane's 16-byte chunk of the row
-      bw[ks] = *(const bf16x8*)(src + l32 * 64 + ((q ^ ((l32 >> 2) & 3)) << 4));
+#pragma unroll
+      for (int b = 0; b < CB; ++b)
+        bw[ks][b] = *(const bf16x8*)(src + b * WB + l32 * 64 + ((q ^ ((l32 >> 2) & 3)) << 4));
 #pragma unroll
       for (int a = 0; a < RG; ++a) {
         const int r = a * 32 + l32;
-        ba[ks][a] = *(const bf16x8*)(src + WB + r * 64 + ((q ^ ((r >> 2) & 3)) << 4));
+        ba[ks][a] = *(const bf16x8*)(src + CB * WB + r * 64 + ((q ^ ((r >> 2) & 3)) << 4));
       }
     }
 #pragma unroll
     for (int ks = 0; ks < KC / 16; ++ks)
 #pragma unroll
       for (int a = 0; a < RG; ++a)
-        acc[a] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ba[ks][a], bw[ks], acc[a], 0, 0, 0);
+#pragma unroll
+        for (int b = 0; b < CB; ++b)
+          acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ba[ks][a], bw[ks][b], acc[a][b], 0, 0, 0);
   }
-  // rows of W past the segment end were read from row 0: zero their columns
-  bool wvalid;
-  if (g.epi == EPI_SWIGLU) wvalid = cb * 16 + (l32 & 15) < g.seg[0].n;
-  else wvalid = l32 < CW && c0 - g.seg[si].n0 + l32 < g.seg[si].n;
 
-  // splits in order through LDS (the rings are free once every wave is done)
+  // splits in order through LDS (the rings are free once every wave is done);
+  // rows of W past the segment end were read from row 0: their columns are 0
   __syncthreads();
   float* s_red = (float*)s_ring;
 #pragma unroll
-  for (int a = 0; a < RG; ++a)
+  for (int b = 0; b < CB; ++b) {
+    const int cb = cg * CB + b, c0 = cb * CW;
+    bool wvalid;
+    if (EPI == EPI_SWIGLU) wvalid = cb * 16 + (l32 & 15) < g.seg[0].n;
+    else wvalid = l32 < CW && c0 - g.seg[si].n0 + l32 < g.seg[si].n;
 #pragma unroll
-    for (int i = 0; i < 16; ++i)
-      s_red[w * (MT * 32) + (a * 32 + 8 * (i >> 2) + 4 * hh + (i & 3)) * 32 + l32] =
-          wvalid ? acc[a][i] : 0.f;
+    for (int a = 0; a < RG; ++a)
+#pragma unroll
+      for (int i = 0; i < 16; ++i)
+        s_red[w * (MT * TW) + (a * 32 + 8 * (i >> 2) + 4 * hh + (i & 3)) * TW + b * 32 + l32] =
+            wvalid ? acc[a][b][i] : 0.f;
+  }
   __syncthreads();
-  bool nonfinite = false;
+  // the tile's sums, 4 adjacent columns at a time: ((0 + p0) + p1) + p2) + p3
+  // per element, the splits in order
+  auto sum4 = [&](int r, int cc) {
+    f32x4 t = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-  for (int e0 = 0; e0 < MT * 32; e0 += 256) {
-    const int e = e0 + tid;
-    const int r = e >> 5, c = e & 31;
-    float t = 0.f;
+    for (int sp = 0; sp < GK_SPLITS; ++sp) t += *(const f32x4*)(s_red + sp * (MT * TW) + r * TW + cc);
+    return t;
+  };
+  if constexpr (EPI == EPI_BF16 || EPI == EPI_F32 || EPI == EPI_F32_ADD) {
+    const GemmSeg sg = g.seg[si];
+    const bool vec = (sg.n & 3) == 0;    // whole 4-column runs are aligned
+    constexpr int UNITS = MT * TW / 4;
 #pragma unroll
-    for (int sp = 0; sp < GK_SPLITS; ++sp) t += s_red[sp * (MT * 32) + e];
-    const int row = m0 + r;
-    const bool rv = row < g.M;
-    if (g.epi == EPI_ARGMAX) {
-      const int col = c0 + c;
-      uint64_t kv = (rv && col < g.ncols) ? pack_logit(t, col, nonfinite) : 0;
+    for (int u0 = 0; u0 < UNITS; u0 += 256) {
+      const int u = u0 + tid;
+      const int r = u / (TW / 4), cc = (u % (TW / 4)) * 4;
+      const int c = cc & 31;
+      const int row = m0 + r;
+      const int col = (cg * CB + (cc >> 5)) * CW + c - sg.n0;   // column in the segment
+      if (u >= UNITS || row >= g.M || c >= CW || col >= sg.n) continue;
+      const f32x4 t = sum4(r, cc);
+      const size_t o = (size_t)row * sg.n + col;
+      if (vec && col + 4 <= sg.n) {
+        if constexpr (EPI == EPI_BF16) {
+          const bf16x2 lo = __builtin_convertvector(f32x2{t[0], t[1]}, bf16x2);
+          const bf16x2 hi = __builtin_convertvector(f32x2{t[2], t[3]}, bf16x2);
+          *(u32x2*)((__bf16*)sg.C + o) =
+              u32x2{__builtin_bit_cast(uint32_t, lo), __builtin_bit_cast(uint32_t, hi)};
+        } else if constexpr (EPI == EPI_F32_ADD) {
+          f32x4 v = *(const f32x4*)((float*)sg.C + o);
+          v += t;
+          *(f32x4*)((float*)sg.C + o) = v;
+        } else {
+          *(f32x4*)((float*)sg.C + o) = t;
+        }
+      } else {
 #pragma unroll
-      for (int off = 16; off > 0; off >>= 1) {
+        for (int i = 0; i < 4; ++i) {
+          if (col + i >= sg.n) break;
+          if constexpr (EPI == EPI_BF16) ((__bf16*)sg.C)[o + i] = (__bf16)t[i];
+          else if constexpr (EPI == EPI_F32_ADD) ((float*)sg.C)[o + i] += t[i];
+          else ((float*)sg.C)[o + i] = t[i];
+        }
+      }
+    }
+  } else if constexpr (EPI == EPI_SWIGLU) {
+    // a unit: 4 gate columns of a block and the 4 up columns 16 further on
+    const GemmSeg sg = g.seg[0];
+    constexpr int UNITS = MT * CB * 4;
+#pragma unroll
+    for (int u0 = 0; u0 < UNITS; u0 += 256) {
+      const int u = u0 + tid;
+      const int r = u / (CB * 4), b = (u / 4) % CB, c = (u % 4) * 4;
+      const int row = m0 + r;
+      const int f = (cg * CB + b) * 16 + c;
+      if (u >= UNITS || row >= g.M || f >= sg.n) continue;
+      const f32x4 gt = sum4(r, b * 32 + c), upv = sum4(r, b * 32 + 16 + c);
+      __bf16 act[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float v = (float)(__bf16)gt[i];        // gate and up, rounded as their own outputs
+        const float o = (float)(__bf16)upv[i];
+        act[i] = (__bf16)(v / (1.0f + expf(-v)) * o);
+      }
+      __bf16* dst = (__bf16*)sg.C + (size_t)row * sg.n + f;
+      if ((sg.n & 3) == 0 && f + 4 <= sg.n) {
+        *(u32x2*)dst = __builtin_bit_cast(u32x2, act);
+      } else {
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          if (f + i < sg.n) dst[i] = act[i];
+      }
+    }
+  } else {
+    // EPI_ARGMAX: a unit is 8 columns of a block's row; the 4 units of a
+    // block row are adjacent lanes (the key max is exact and the keys are
+    // distinct, so the order of the max does not matter)
+    bool nonfinite = false;
+    constexpr int UNITS = MT * CB * 4;
+    static_assert(UNITS % 256 == 0 || UNITS < 256, "whole lane quads");
+#pragma unroll
+    for (int u0 = 0; u0 < UNITS; u0 += 256) {
+      const int u = u0 + tid;
+      const int r = u / (CB * 4), b = (u / 4) % CB, q = u % 4;
+      const int row = m0 + r;
+      const int cb = cg * CB + b;
+      const bool live = u < UNITS && row < g.M && cb < NB;
+      uint64_t kv = 0;
+      if (live) {
+        const f32x4 t0 = sum4(r, b * 32 + q * 8), t1 = sum4(r, b * 32 + q * 8 + 4);
+        const int col0 = cb * CW + q * 8;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          const int col = col0 + i;
+          const uint64_t k = col < g.ncols ? pack_logit(i < 4 ? t0[i] : t1[i - 4], col, nonfinite) : 0;
+          kv = k > kv ? k : kv;
+        }
+      }
+#pragma unroll
+      for (int off = 1; off < 4; off <<= 1) {
         const uint32_t lo = __shfl_xor((uint32_t)kv, off);
         const uint32_t hi = __shfl_xor((uint32_t)(kv >> 32), off);
         const uint64_t o = ((uint64_t)hi << 32) | lo;
         kv = o > kv ? o : kv;
       }
-      if (c == 0 && rv) g.part[(size_t)row * NB + cb] = kv;
-    } else if (g.epi == EPI_SWIGLU) {
-      const float v = (float)(__bf16)t;             // gate or up, rounded as its own output
-      const float o = __shfl_xor(v, 16);
-      const int f = cb * 16 + c;
-      if (c < 16 && rv && f < g.seg[0].n) {
-        const float act = v / (1.0f + expf(-v)) * o;
-        ((__bf16*)g.seg[0].C)[(size_t)row * g.seg[0].n + f] = (__bf16)act;
-      }
-    } else {
-      const int col = c0 + c - g.seg[si].n0;
-      if (rv && c < CW && col < g.seg[si].n) {
-        const size_t o = (size_t)row * g.seg[si].n + col;
-        if (g.epi == EPI_BF16) ((__bf16*)g.seg[si].C)[o] = (__bf16)t;
-        else if (g.epi == EPI_F32_ADD) ((float*)g.seg[si].C)[o] += t;
-        else ((float*)g.seg[si].C)[o] = t;
-      }
+      if (live && q == 0) g.part[(size_t)row * NB + cb] = kv;
     }
+    if (__any(nonfinite) && lane == 0) set_err(g.err, DVS_ERR_NONFINITE);
   }
-  if (g.epi == EPI_ARGMAX && __any(nonfinite) && lane == 0) set_err(g.err, DVS_ERR_NONFINITE);
 }
 
 // Top-1 of each row from its column blocks' packed (key, index) maxima: one
@@ -958,6 +1053,18 @@ static StepLayout step_layout(const dvs_model* m, int S, int n_causal, int n_mas
   return L;
 }
 
+template <int MT, int CB>
+static void launch_ws_epi(const GemmArgs& g, dim3 gr, hipStream_t st) {
+  const dim3 blk(256);
+  switch (g.epi) {
+    case EPI_BF16: hipLaunchKernelGGL((gemm_ws_kernel<MT, false, CB, EPI_BF16>), gr, blk, 0, st, g); break;
+    case EPI_F32: hipLaunchKernelGGL((gemm_ws_kernel<MT, false, CB, EPI_F32>), gr, blk, 0, st, g); break;
+    case EPI_F32_ADD: hipLaunchKernelGGL((gemm_ws_kernel<MT, false, CB, EPI_F32_ADD>), gr, blk, 0, st, g); break;
+    case EPI_SWIGLU: hipLaunchKernelGGL((gemm_ws_kernel<MT, false, CB, EPI_SWIGLU>), gr, blk, 0, st, g); break;
+    default: hipLaunchKernelGGL((gemm_ws_kernel<MT, false, CB, EPI_ARGMAX>), gr, blk, 0, st, g); break;
+  }
+}
+
 static int launch_ws(GemmArgs& g, hipStream_t st) {
   const int MT = g.M <= 32 ? 32 : 64;
   // few-row calls with few 32-column blocks and a plain epilogue: 16-column
@@ -966,11 +1073,32 @@ static int launch_ws(GemmArgs& g, hipStream_t st) {
                       (g.epi == EPI_BF16 || g.epi == EPI_F32 || g.epi == EPI_F32_ADD);
   const int NB = narrow ? (g.ncols + 15) / 16 : (g.ncols + 31) / 32;
   g.n_rt = (g.M + MT - 1) / MT;
-  const long long grid = (long long)((NB + 7) / 8) * 8 * g.n_rt;
+  // wider calls: CB blocks per wave while that still gives the chip enough
+  // workgroups, and every segment starts on a group boundary
+  int CB = 1;
+  if (MT == 64) {
+    auto groups_ok = [&](int cb) {
+      for (int i = 0; i < g.nseg; ++i)
+        if (g.seg[i].n0 % (32 * cb)) return false;
+      return true;
+    };
+    if ((NB / 2) * g.n_rt >= WS_WIDE_MIN_WG && groups_ok(2)) CB = 2;
+  }
+  const int NG = (NB + CB - 1) / CB;
+  const long long grid = (long long)((NG + 7) / 8) * 8 * g.n_rt;
   DVS_CHECK_SUPPORTED(grid < (1LL << 31), "draft_verify_step: GEMM grid too large");
-  if (narrow) hipLaunchKernelGGL((gemm_ws_kernel<32, true>), dim3((unsigned)grid), dim3(256), 0, st, g);
-  else if (MT == 32) hipLaunchKernelGGL((gemm_ws_kernel<32, false>), dim3((unsigned)grid), dim3(256), 0, st, g);
-  else hipLaunchKernelGGL((gemm_ws_kernel<64, false>), dim3((unsigned)grid), dim3(256), 0, st, g);
+  const dim3 gr((unsigned)grid), blk(256);
+  if (narrow) {
+    if (g.epi == EPI_BF16) hipLaunchKernelGGL((gemm_ws_kernel<32, true, 1, EPI_BF16>), gr, blk, 0, st, g);
+    else if (g.epi == EPI_F32) hipLaunchKernelGGL((gemm_ws_kernel<32, true, 1, EPI_F32>), gr, blk, 0, st, g);
+    else hipLaunchKernelGGL((gemm_ws_kernel<32, true, 1, EPI_F32_ADD>), gr, blk, 0, st, g);
+  } else if (MT == 32) {
+    launch_ws_epi<32, 1>(g, gr, st);
+  } else if (CB == 2) {
+    launch_ws_epi<64, 2>(g, gr, st);
+  } else {
+    launch_ws_epi<64, 1>(g, gr, st);
+  }
   return launch_status("draft_verify_step(gemm)");
 }
 
@@ -1031,27 +1159,9 @@ static int lm_head_top1(const dvs_model* m, const StepLayout& L, char* ws, const
   g.epi = EPI_ARGMAX;
   g.part = (uint64_t*)(ws + L.part);
   g.err = err;
-  int rc;
-  if (M <= 32) {
-    rc = launch_ws(g, st);
-  } else {
-    // wide tiles: the rows of A are shared by 128 columns, the weights by
-    // up to 128 rows (32-column tiles would re-read A once per 32 columns)
-    const int N = m->vocab, K = m->hidden, ksp = gemm_ksplit(K);
-    int mt = gemm_rows_per_tile(M, N);
-    if (mt == 256 && ksp > 1) mt = 128;
-    const long long grid = (long long)((N + RT_NT - 1) / RT_NT) * ((M + mt - 1) / mt);
-    DVS_CHECK_SUPPORTED(grid < (1LL << 31), "draft_verify_step: GEMM grid too large");
-    const dim3 gr((unsigned)grid), blk(256);
-    const __bf16* a = (const __bf16*)h;
-    const __bf16* wt = (const __bf16*)m->lm_head;
-    switch (mt) {
-      case 256: hipLaunchKernelGGL((gemm_rt_kernel<256, false>), gr, blk, 0, st, a, wt, M, N, K, nullptr, 1, 0, ksp, g.part, err); break;
-      case 128: hipLaunchKernelGGL((gemm_rt_kernel<128, true>), gr, blk, 0, st, a, wt, M, N, K, nullptr, 1, 0, ksp, g.part, err); break;
-      default: hipLaunchKernelGGL((gemm_rt_kernel<64, true>), gr, blk, 0, st, a, wt, M, N, K, nullptr, 1, 0, ksp, g.part, err); break;
-    }
-    rc = launch_status("draft_verify_step(lm head)");
-  }
+  // (calls of more than 32 rows take two 32-column blocks per wave, so each
+  // A chunk serves 64 columns)
+  int rc = launch_ws(g, st);
   if (rc) return rc;
   const int NB = (m->vocab + 31) / 32;
   hipLaunchKernelGGL(argmax_rows_kernel, dim3((unsigned)((M + 3) / 4)), dim3(256), 0, st, g.part,
