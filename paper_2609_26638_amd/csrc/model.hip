@@ -181,9 +181,40 @@ __device__ __forceinline__ int window_offset(int r, int n_causal, int n_mask, in
   return n_causal - n_groups + g + 1 + i;
 }
 
+// Rotate-half rotary embedding: pair (x1 = element i, x2 = element i + D/2
+// of a head) at position pos turns by the angle pos * theta^(-2i/D),
+// computed in double precision (positions reach thousands of radians).  One
+// definition for the standalone kernel and the per-step table the Q|K|V
+// GEMM epilogue reads, so both round alike.
+__device__ __forceinline__ void rope_cs_sn(int i, int D, double log2_theta, double pos, double& cs,
+                                           double& sn) {
+  const double inv = exp2(-2.0 * i / D * log2_theta);
+  sincos(pos * inv, &sn, &cs);
+}
+__device__ __forceinline__ void rope_rotate(float x1, float x2, double cs, double sn, float& o1,
+                                            float& o2) {
+  o1 = (float)(x1 * cs - x2 * sn);
+  o2 = (float)(x1 * sn + x2 * cs);
+}
+
+// (cos, sin) of every (row, i < D/2) of a step: row s * R + r at position
+// kv_len[s] + window_offset(r); the same for every layer of the step.
+__global__ void rope_table_kernel(double2* __restrict__ tab, int M, int R, int D, double log2_theta,
+                                  const int32_t* __restrict__ kv_len, int n_causal, int n_mask,
+                                  int group) {
+  const int half = D / 2;
+  const int idx = blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= M * half) return;
+  const int mrow = idx / half, i = idx - mrow * half;
+  const int s = mrow / R, r = mrow - s * R;
+  const double pos = (double)(kv_len[s] + window_offset(r, n_causal, n_mask, group));
+  double cs, sn;
+  rope_cs_sn(i, D, log2_theta, pos, cs, sn);
+  tab[idx] = double2{cs, sn};
+}
+
 // rotate-half rotary embedding, in place, at position kv_len[s] +
-// window_offset(r); angles in double precision (positions reach thousands
-// of radians).
+// window_offset(r)
 template <typename T>
 __global__ void rope_kernel(T* __restrict__ xq, int nhq, T* __restrict__ xk, int nhk, int M, int R,
                             int D, double log2_theta, const int32_t* __restrict__ kv_len,
@@ -206,13 +237,13 @@ __global__ void rope_kernel(T* __restrict__ xq, int nhq, T* __restrict__ xk, int
   const int mrow = (int)(mh / nh);
   const int s = mrow / R, r = mrow - s * R;
   const double pos = (double)(kv_len[s] + window_offset(r, n_causal, n_mask, group));
-  const double inv = exp2(-2.0 * i / D * log2_theta);
-  double sn, cs;
-  sincos(pos * inv, &sn, &cs);
   T* v = x + mh * D;
-  const float x1 = to_f(v[i]), x2 = to_f(v[i + half]);
-  v[i] = from_f<T>((float)(x1 * cs - x2 * sn));
-  v[i + half] = from_f<T>((float)(x1 * sn + x2 * cs));
+  double cs, sn;
+  rope_cs_sn(i, D, log2_theta, pos, cs, sn);
+  float o1, o2;
+  rope_rotate(to_f(v[i]), to_f(v[i + half]), cs, sn, o1, o2);
+  v[i] = from_f<T>(o1);
+  v[i + half] = from_f<T>(o2);
 }
 
 // Prefill rows: row r < P of sequence s takes embed[tokens[s, r]] when that
@@ -413,6 +444,11 @@ struct GemmArgs {
   int nseg, epi, n_rt;
   uint64_t* part;    // EPI_ARGMAX: [M, ncols / 32]
   int32_t* err;
+  // EPI_BF16 with rope_tab set: segments 0 and 1 (Q and K, heads of rope_D)
+  // leave rotated by the rotary embedding, (cos, sin) of (row, i) at
+  // rope_tab[row * rope_D / 2 + i] (rope_table_kernel)
+  const double2* rope_tab;
+  int rope_D;
 };
 
 __device__ __forceinline__ uint64_t pack_logit(float v, int idx, bool& nonfinite) {
@@ -484,6 +520,7 @@ __global__ void __launch_bounds__(256, CB <= 2 ? 2 : 1) gemm_ws_kernel(GemmArgs 
   int si = 0;
   if (EPI != EPI_SWIGLU)
     while (si + 1 < g.nseg && cg * CB * CW >= g.seg[si + 1].n0) ++si;
+  const bool rope = EPI == EPI_BF16 && g.rope_tab != nullptr && si < 2;
   const __bf16* wsrc[CB][WI];  // this lane's weight rows (block b, tile rows 16i + L/4)
 #pragma unroll
   for (int b = 0; b < CB; ++b)
@@ -500,6 +537,13 @@ __global__ void __launch_bounds__(256, CB <= 2 ? 2 : 1) gemm_ws_kernel(GemmArgs 
         base = r < 16 ? g.seg[0].W : g.seg[1].W;
       } else {
         rowi = c0 - g.seg[si].n0 + r;
+        if (rope) {
+          // block bh of a head holds dims bh*P .. bh*P+P-1 and their
+          // rotate-half partners D/2 + bh*P ..
+          const int hd = rowi / g.rope_D, cp = rowi - hd * g.rope_D;
+          const int bh = cp / CW, c = cp - bh * CW;
+          rowi = hd * g.rope_D + (c < CW / 2 ? bh * (CW / 2) + c : g.rope_D / 2 + bh * (CW / 2) + c - CW / 2);
+        }
         valid = rowi < g.seg[si].n;
         base = g.seg[si].W;
       }
@@ -597,7 +641,36 @@ __global__ void __launch_bounds__(256, CB <= 2 ? 2 : 1) gemm_ws_kernel(GemmArgs 
     for (int sp = 0; sp < GK_SPLITS; ++sp) t += *(const f32x4*)(s_red + sp * (MT * TW) + r * TW + cc);
     return t;
   };
-  if constexpr (EPI == EPI_BF16 || EPI == EPI_F32 || EPI == EPI_F32_ADD) {
+  if (EPI == EPI_BF16 && rope) {
+    // a unit: column j < P of a block (dim i of a head) and its partner
+    // column P + j (dim i + D/2), each rounded to bf16 as the projection
+    // writes it, then rotated
+    const GemmSeg sg = g.seg[si];
+    constexpr int P = CW / 2;
+    constexpr int UNITS = MT * CB * P;
+    const int D = g.rope_D, half = D / 2;
+#pragma unroll
+    for (int u0 = 0; u0 < UNITS; u0 += 256) {
+      const int u = u0 + tid;
+      const int r = u / (CB * P), b = (u / P) % CB, j = u % P;
+      const int row = m0 + r;
+      const int cs = (cg * CB + b) * CW - sg.n0;   // the block's first column in the segment
+      if (u >= UNITS || row >= g.M || cs >= sg.n) continue;
+      const int hd = cs / D, i = (cs - hd * D) / CW * P + j;
+      float t1 = 0.f, t2 = 0.f;
+#pragma unroll
+      for (int sp = 0; sp < GK_SPLITS; ++sp) {
+        t1 += s_red[sp * (MT * TW) + r * TW + b * 32 + j];
+        t2 += s_red[sp * (MT * TW) + r * TW + b * 32 + P + j];
+      }
+      const double2 cssn = g.rope_tab[(size_t)row * half + i];
+      float o1, o2;
+      rope_rotate((float)(__bf16)t1, (float)(__bf16)t2, cssn.x, cssn.y, o1, o2);
+      __bf16* dst = (__bf16*)sg.C + (size_t)row * sg.n + hd * D + i;
+      dst[0] = (__bf16)o1;
+      dst[half] = (__bf16)o2;
+    }
+  } else if constexpr (EPI == EPI_BF16 || EPI == EPI_F32 || EPI == EPI_F32_ADD) {
     const GemmSeg sg = g.seg[si];
     const bool vec = (sg.n & 3) == 0;    // whole 4-column runs are aligned
     constexpr int UNITS = MT * TW / 4;
@@ -990,7 +1063,7 @@ __global__ void __launch_bounds__(256) gemm_f32_kernel(const float* __restrict__
 // ---------------------------------------------------------------------------
 struct StepLayout {
   size_t x, h, hsel, q, k, v, att, gate, up, act, logits, am, conf, nopen, blk, acc, lead, part,
-      attn_ws, total, attn_bytes, attn_counters;
+      attn_ws, rope, total, attn_bytes, attn_counters;
 };
 
 // Rows per tile when all splits run in one workgroup (more than 32 rows):
@@ -1049,6 +1122,9 @@ static StepLayout step_layout(const dvs_model* m, int S, int n_causal, int n_mas
   L.attn_counters = attn_counter_bytes(S, n_causal + n_mask, m->n_heads, m->n_kv_heads,
                                        m->head_dim, max_pages, chunk_keys, m->dtype);
   L.attn_ws = off; off += al(L.attn_bytes);
+  // the step's rotary (cos, sin) table, for calls whose Q|K|V projection
+  // takes the rotation in its epilogue (up to WS_MAX_ROWS rows)
+  L.rope = off; off += al(M <= (size_t)WS_MAX_ROWS ? M * (m->head_dim / 2) * 16 : 0);
   L.total = off;
   return L;
 }
@@ -1197,6 +1273,13 @@ static int forward_layers(const dvs_model* m, const dvs_state* st, int n_causal,
                        (int32_t*)(ws + L.attn_ws), nw);
   }
   const double log2_theta = log2((double)m->rope_theta);
+  const bool rope_fused = use_ws(dt, M, H) && D % 32 == 0;
+  if (rope_fused) {
+    hipLaunchKernelGGL(rope_table_kernel, dim3((M * (D / 2) + 255) / 256), dim3(256), 0, stream,
+                       (double2*)(ws + L.rope), M, R, D, log2_theta, st->kv_len, n_causal, n_mask,
+                       group);
+    if ((rc = launch_status("draft_verify_step(rope table)"))) return rc;
+  }
   for (int l = 0; l < m->n_layers; ++l) {
     const dvs_layer& ly = m->layers[l];
     hipLaunchKernelGGL(rmsnorm_kernel<T>, dim3(M), dim3(256), 0, stream, x, (const T*)ly.g_attn, H,
@@ -1210,16 +1293,24 @@ static int forward_layers(const dvs_model* m, const dvs_state* st, int n_causal,
       g.seg[2] = GemmSeg{(const __bf16*)ly.wv, v, (Hq + Hkv) * D, Hkv * D};
       g.nseg = 3;
       g.epi = EPI_BF16;
+      // the rotary embedding in the epilogue (heads split evenly into
+      // 16- or 32-column blocks)
+      if (rope_fused) {
+        g.rope_tab = (const double2*)(ws + L.rope);
+        g.rope_D = D;
+      }
       if ((rc = launch_ws(g, stream))) return rc;
     } else {
       if ((rc = gemm(L, ws, dt, h, ly.wq, M, Hq * D, H, q, 0, 0, stream))) return rc;
       if ((rc = gemm(L, ws, dt, h, ly.wk, M, Hkv * D, H, k, 0, 0, stream))) return rc;
       if ((rc = gemm(L, ws, dt, h, ly.wv, M, Hkv * D, H, v, 0, 0, stream))) return rc;
     }
-    const long long nqk = (long long)M * (Hq + Hkv) * (D / 2);
-    hipLaunchKernelGGL(rope_kernel<T>, dim3((unsigned)((nqk + 255) / 256)), dim3(256), 0, stream, q,
-                       Hq, k, Hkv, M, R, D, log2_theta, st->kv_len, n_causal, n_mask, group);
-    if ((rc = launch_status("draft_verify_step(rope)"))) return rc;
+    if (!rope_fused) {
+      const long long nqk = (long long)M * (Hq + Hkv) * (D / 2);
+      hipLaunchKernelGGL(rope_kernel<T>, dim3((unsigned)((nqk + 255) / 256)), dim3(256), 0, stream,
+                         q, Hq, k, Hkv, M, R, D, log2_theta, st->kv_len, n_causal, n_mask, group);
+      if ((rc = launch_status("draft_verify_step(rope)"))) return rc;
+    }
     rc = attn_hybrid_block_grouped(q, k, v, ly.k_pool, ly.v_pool, st->page_table, st->kv_len, S,
                                    n_causal, n_mask, group, Hq, Hkv, D, st->max_pages,
                                    st->num_pool_pages, (float)(1.0 / sqrt((double)D)), dt,
