@@ -1630,18 +1630,6 @@ struct AttnPlan {
 
 static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-static int device_cus() {
-  static int cus = 0;
-  if (cus == 0) {
-    int dev = 0, v = 0;
-    if (hipGetDevice(&dev) == hipSuccess &&
-        hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && v > 0)
-      cus = v;
-    else
-      cus = 256;
-  }
-  return cus;
-}
 
 static AttnPlan plan_attn(int S, int R, int Hq, int Hkv, int D, int max_pages, int chunk_keys,
                           int dtype) {

@@ -89,4 +89,18 @@ __device__ __forceinline__ void static_for(F&& f) {
   }
 }
 
+// Compute units of the current device (queried once; 256 if the query fails).
+inline int device_cus() {
+  static int cus = 0;
+  if (cus == 0) {
+    int dev = 0, v = 0;
+    if (hipGetDevice(&dev) == hipSuccess &&
+        hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && v > 0)
+      cus = v;
+    else
+      cus = 256;
+  }
+  return cus;
+}
+
 }  // namespace dvs

@@ -476,21 +476,26 @@ __device__ __forceinline__ void ws_wait_vmcnt() {
 // CB adjacent 32-column blocks, so one A chunk feeds CB blocks' products
 // (A is re-read once per CB blocks instead of once per block); per element
 // the arithmetic is the single block's.
-template <int MT, bool NARROW, int CB, int EPI>
-__global__ void __launch_bounds__(256, CB <= 2 ? 2 : 1) gemm_ws_kernel(GemmArgs g) {
+template <int MT, bool NARROW, int CB, int EPI, bool WK>
+__global__ void __launch_bounds__(256, WK ? 1 : 2) gemm_ws_kernel(GemmArgs g) {
   constexpr int CW = NARROW ? 16 : 32;     // output columns per block
-  constexpr int WI = NARROW ? 1 : 2;       // weight copies (16 rows each) per block and chunk
+  // k per chunk.  WK (calls of at most one workgroup per CU): 64, so that a
+  // copy takes whole 128-byte lines of a row (copies of half lines, the
+  // other half taken by the next chunk, moved 1.6x fewer useful bytes per
+  // CU in a measurement), in rings of up to 144 KB.  Otherwise 32, in
+  // rings that leave room for two workgroups per CU.
+  constexpr int KC = WK ? 64 : 32;
+  constexpr int RB = KC * 2;               // bytes of a row in a chunk
+  constexpr int RPI = 1024 / RB;           // rows per 1 KB copy
+  constexpr int WI = (NARROW ? 16 : 32) / RPI;   // weight copies per block and chunk
   constexpr int RG = MT / 32;              // 32-row groups per wave
-  // ring stages per wave: four for the few-row calls (64 KB of LDS, two
-  // workgroups per CU; six or eight stages, one workgroup per CU, measured
-  // slower), three for 64-row tiles of one block, two for tiles of two
-  // blocks (64 KB: two workgroups per CU, measured faster than three stages
-  // or four blocks per wave at one workgroup per CU)
-  constexpr int NS = MT == 32 ? 4 : (CB == 2 ? 2 : 3);
-  constexpr int KC = 32;                   // k per chunk (64 bytes of a row)
-  constexpr int WB = 32 * 64;              // W part of a block's chunk: 32 rows
-  constexpr int CHB = CB * WB + MT * 64;   // chunk bytes (CB blocks' W rows, then A rows)
-  constexpr int NPL = CB * WI + MT / 16;   // 1 KB copies per chunk and wave
+  // ring stages per wave: WK three (two for tiles of two blocks); otherwise
+  // four for the few-row calls (64 KB), three for 64-row tiles of one block
+  // (72 KB), two for tiles of two blocks (64 KB)
+  constexpr int NS = WK ? (CB == 2 ? 2 : 3) : (MT == 32 ? 4 : (CB == 2 ? 2 : 3));
+  constexpr int WB = 32 * RB;              // W part of a block's chunk: 32 rows
+  constexpr int CHB = CB * WB + MT * RB;   // chunk bytes (CB blocks' W rows, then A rows)
+  constexpr int NPL = CB * WI + MT / RPI;  // 1 KB copies per chunk and wave
   constexpr int TW = CB * 32;              // tile width in the split sums
   static_assert(NPL * (NS - 1) < 64, "vmcnt range");
   static_assert(!NARROW || (MT == 32 && CB == 1), "narrow blocks serve few-row calls");
@@ -511,23 +516,26 @@ __global__ void __launch_bounds__(256, CB <= 2 ? 2 : 1) gemm_ws_kernel(GemmArgs 
   const int m0 = rt * MT;
   char* ring = s_ring + w * NS * CHB;
 
-  // Copies: instruction i of a block's chunk moves 1 KB, 16 rows of 64
-  // bytes; lane L takes row 16i + L/4 and 16-byte chunk (L & 3) ^ sw(row),
-  // sw(row) = (row / 4) & 3, so LDS slot c of a row holds its chunk
-  // c ^ sw(row): the 16 rows an MFMA operand read serves at once hit distinct
-  // banks.  The blocks of a group lie in one segment (the host checks it).
-  const int crow = lane >> 2, cchk = lane & 3;
+  // Copies: instruction i of a block's chunk moves 1 KB, RPI rows of RB
+  // bytes; lane L takes row RPI*i + L/(RB/16) and 16-byte chunk
+  // (L mod RB/16) ^ sw(row), sw(row) = (row / 2) & 7 for 128-byte rows and
+  // (row / 4) & 3 for 64-byte rows, so LDS slot c of a row holds its chunk
+  // c ^ sw(row): the 16 rows an MFMA operand read serves at once hit
+  // distinct banks.  The blocks of a group lie in one segment (the host
+  // checks it).
+  const int crow = lane / (RB / 16), cchk = lane % (RB / 16);
+  auto sw = [](int row) { return KC == 64 ? (row >> 1) & 7 : (row >> 2) & 3; };
   int si = 0;
   if (EPI != EPI_SWIGLU)
     while (si + 1 < g.nseg && cg * CB * CW >= g.seg[si + 1].n0) ++si;
   const bool rope = EPI == EPI_BF16 && g.rope_tab != nullptr && si < 2;
-  const __bf16* wsrc[CB][WI];  // this lane's weight rows (block b, tile rows 16i + L/4)
+  const __bf16* wsrc[CB][WI];  // this lane's weight rows (block b, tile rows 8i + L/8)
 #pragma unroll
   for (int b = 0; b < CB; ++b)
 #pragma unroll
     for (int i = 0; i < WI; ++i) {
       const int cb = cg * CB + b, c0 = cb * CW;
-      const int r = 16 * i + crow;
+      const int r = RPI * i + crow;
       const __bf16* base;
       bool valid;
       int rowi;
@@ -547,13 +555,13 @@ __global__ void __launch_bounds__(256, CB <= 2 ? 2 : 1) gemm_ws_kernel(GemmArgs 
         valid = rowi < g.seg[si].n;
         base = g.seg[si].W;
       }
-      wsrc[b][i] = base + (size_t)(valid ? rowi : 0) * g.K + ((cchk ^ ((r >> 2) & 3)) << 3);
+      wsrc[b][i] = base + (size_t)(valid ? rowi : 0) * g.K + ((cchk ^ sw(r)) << 3);
     }
-  const __bf16* asrc[MT / 16];
+  const __bf16* asrc[MT / RPI];
 #pragma unroll
-  for (int i = 0; i < MT / 16; ++i) {
-    const int r = 16 * i + crow;
-    asrc[i] = g.A + (size_t)min(m0 + r, g.M - 1) * g.K + ((cchk ^ ((r >> 2) & 3)) << 3);
+  for (int i = 0; i < MT / RPI; ++i) {
+    const int r = RPI * i + crow;
+    asrc[i] = g.A + (size_t)min(m0 + r, g.M - 1) * g.K + ((cchk ^ sw(r)) << 3);
   }
   const int kq = g.K / GK_SPLITS;
   const int kw = w * kq;               // this wave's split
@@ -568,7 +576,7 @@ __global__ void __launch_bounds__(256, CB <= 2 ? 2 : 1) gemm_ws_kernel(GemmArgs 
         __builtin_amdgcn_global_load_lds((const void*)(wsrc[b][i] + k0),
                                          (__attribute__((address_space(3))) void*)(dst + b * WB + i * 1024), 16, 0, 0);
 #pragma unroll
-    for (int i = 0; i < MT / 16; ++i)
+    for (int i = 0; i < MT / RPI; ++i)
       __builtin_amdgcn_global_load_lds((const void*)(asrc[i] + k0),
                                        (__attribute__((address_space(3))) void*)(dst + CB * WB + i * 1024), 16, 0, 0);
   };
@@ -599,12 +607,22 @@ __global__ void __launch_bounds__(256, CB <= 2 ? 2 : 1) gemm_ws_kernel(GemmArgs 
       const int q = 2 * ks + hh;   // the lane's 16-byte chunk of the row
 #pragma unroll
       for (int b = 0; b < CB; ++b)
-        bw[ks][b] = *(const bf16x8*)(src + b * WB + l32 * 64 + ((q ^ ((l32 >> 2) & 3)) << 4));
+        bw[ks][b] = *(const bf16x8*)(src + b * WB + l32 * RB + ((q ^ sw(l32)) << 4));
 #pragma unroll
       for (int a = 0; a < RG; ++a) {
         const int r = a * 32 + l32;
-        ba[ks][a] = *(const bf16x8*)(src + CB * WB + r * 64 + ((q ^ ((r >> 2) & 3)) << 4));
+        ba[ks][a] = *(const bf16x8*)(src + CB * WB + r * RB + ((q ^ sw(r)) << 4));
       }
+    }
+    // every read issued before the first product: the fragments pass
+    // through an empty asm that the products depend on (left to itself the
+    // scheduler interleaves reads and products and waits for each in turn)
+#pragma unroll
+    for (int ks = 0; ks < KC / 16; ++ks) {
+#pragma unroll
+      for (int b = 0; b < CB; ++b) asm volatile("" : "+v"(bw[ks][b]));
+#pragma unroll
+      for (int a = 0; a < RG; ++a) asm volatile("" : "+v"(ba[ks][a]));
     }
 #pragma unroll
     for (int ks = 0; ks < KC / 16; ++ks)
@@ -1129,16 +1147,26 @@ static StepLayout step_layout(const dvs_model* m, int S, int n_causal, int n_mas
   return L;
 }
 
-template <int MT, int CB>
+template <int MT, bool NARROW, int CB, bool WK>
 static void launch_ws_epi(const GemmArgs& g, dim3 gr, hipStream_t st) {
   const dim3 blk(256);
   switch (g.epi) {
-    case EPI_BF16: hipLaunchKernelGGL((gemm_ws_kernel<MT, false, CB, EPI_BF16>), gr, blk, 0, st, g); break;
-    case EPI_F32: hipLaunchKernelGGL((gemm_ws_kernel<MT, false, CB, EPI_F32>), gr, blk, 0, st, g); break;
-    case EPI_F32_ADD: hipLaunchKernelGGL((gemm_ws_kernel<MT, false, CB, EPI_F32_ADD>), gr, blk, 0, st, g); break;
-    case EPI_SWIGLU: hipLaunchKernelGGL((gemm_ws_kernel<MT, false, CB, EPI_SWIGLU>), gr, blk, 0, st, g); break;
-    default: hipLaunchKernelGGL((gemm_ws_kernel<MT, false, CB, EPI_ARGMAX>), gr, blk, 0, st, g); break;
+    case EPI_BF16: hipLaunchKernelGGL((gemm_ws_kernel<MT, NARROW, CB, EPI_BF16, WK>), gr, blk, 0, st, g); break;
+    case EPI_F32: hipLaunchKernelGGL((gemm_ws_kernel<MT, NARROW, CB, EPI_F32, WK>), gr, blk, 0, st, g); break;
+    case EPI_F32_ADD: hipLaunchKernelGGL((gemm_ws_kernel<MT, NARROW, CB, EPI_F32_ADD, WK>), gr, blk, 0, st, g); break;
+    default:
+      if constexpr (!NARROW) {
+        if (g.epi == EPI_SWIGLU) hipLaunchKernelGGL((gemm_ws_kernel<MT, false, CB, EPI_SWIGLU, WK>), gr, blk, 0, st, g);
+        else hipLaunchKernelGGL((gemm_ws_kernel<MT, false, CB, EPI_ARGMAX, WK>), gr, blk, 0, st, g);
+      }
+      break;
   }
+}
+
+template <int MT, bool NARROW, int CB>
+static void launch_ws_k(const GemmArgs& g, dim3 gr, bool wk, hipStream_t st) {
+  if (wk) launch_ws_epi<MT, NARROW, CB, true>(g, gr, st);
+  else launch_ws_epi<MT, NARROW, CB, false>(g, gr, st);
 }
 
 static int launch_ws(GemmArgs& g, hipStream_t st) {
@@ -1163,18 +1191,13 @@ static int launch_ws(GemmArgs& g, hipStream_t st) {
   const int NG = (NB + CB - 1) / CB;
   const long long grid = (long long)((NG + 7) / 8) * 8 * g.n_rt;
   DVS_CHECK_SUPPORTED(grid < (1LL << 31), "draft_verify_step: GEMM grid too large");
-  const dim3 gr((unsigned)grid), blk(256);
-  if (narrow) {
-    if (g.epi == EPI_BF16) hipLaunchKernelGGL((gemm_ws_kernel<32, true, 1, EPI_BF16>), gr, blk, 0, st, g);
-    else if (g.epi == EPI_F32) hipLaunchKernelGGL((gemm_ws_kernel<32, true, 1, EPI_F32>), gr, blk, 0, st, g);
-    else hipLaunchKernelGGL((gemm_ws_kernel<32, true, 1, EPI_F32_ADD>), gr, blk, 0, st, g);
-  } else if (MT == 32) {
-    launch_ws_epi<32, 1>(g, gr, st);
-  } else if (CB == 2) {
-    launch_ws_epi<64, 2>(g, gr, st);
-  } else {
-    launch_ws_epi<64, 1>(g, gr, st);
-  }
+  const dim3 gr((unsigned)grid);
+  // calls of at most one workgroup per CU: whole-line chunks, deeper rings
+  const bool wk = (long long)NG * g.n_rt <= device_cus();
+  if (narrow) launch_ws_k<32, true, 1>(g, gr, wk, st);
+  else if (MT == 32) launch_ws_k<32, false, 1>(g, gr, wk, st);
+  else if (CB == 2) launch_ws_k<64, false, 2>(g, gr, wk, st);
+  else launch_ws_k<64, false, 1>(g, gr, wk, st);
   return launch_status("draft_verify_step(gemm)");
 }
 
