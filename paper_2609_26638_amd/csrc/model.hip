@@ -401,22 +401,23 @@ constexpr int WS_WIDE_MIN_WG = 256; // 64-row calls take 2 blocks per wave while
 static int gemm_ksplit(int K) { return K % (64 * GK_SPLITS) == 0 ? GK_SPLITS : 1; }
 
 // ---------------------------------------------------------------------------
-// gemm_ws_kernel<MT>: weight-streaming GEMM for decode-step row counts.
+// gemm_ws_kernel<MT, NARROW, CB, EPI, WK>: weight-streaming GEMM for
+// decode-step row counts.
 //
-// Workgroup = 4 waves = one (row tile of MT rows, 32-column block); wave s
-// computes split s (K/4 consecutive k) for the whole tile.  Each wave copies
-// its 32-wide K chunks (32 weight rows and MT rows of A, 64 bytes each)
+// Workgroup = 4 waves = one (row tile of MT rows, group of CB 32-column
+// blocks); wave s computes split s (K/4 consecutive k) for the whole tile.
+// Each wave copies its K chunks (the blocks' weight rows and MT rows of A)
 // with direct global -> LDS 16-byte loads, fully coalesced, into a private
-// 3-stage ring two chunks ahead of its products, and feeds the MFMAs from
-// there (no barriers between the waves until the split sums).  Each weight
-// element is read once per row tile; the row tiles of
-// a column block are dispatched back to back on one XCD (blockIdx mod 8), so
-// the second and later ones find the block's weights in that XCD's L2.
-// The splits meet in LDS and are added in order, then an epilogue writes the
-// tile:
+// ring ahead of its products, and feeds the MFMAs from there (no barriers
+// between the waves until the split sums).  Each weight element is read
+// once per row tile; the row tiles of a column group are dispatched back to
+// back on one XCD (blockIdx mod 8), so the second and later ones find the
+// group's weights in that XCD's L2.  The splits meet in LDS and are added in
+// order, then the epilogue EPI writes the tile:
 //   EPI_BF16       C (bf16) of the column block's segment (fused projections:
 //                  up to three weight matrices side by side, e.g. Wq|Wk|Wv,
-//                  each output into its own array);
+//                  each output into its own array; with a rotary table the
+//                  first two leave rotated);
 //   EPI_F32_ADD    C (fp32) += tile (the residual stream);
 //   EPI_F32        C (fp32) = tile (logits);
 //   EPI_SWIGLU     columns 0..15 of a block are gate rows, 16..31 the same up
