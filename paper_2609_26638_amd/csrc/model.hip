@@ -468,6 +468,155 @@ __device__ __forceinline__ void ws_wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
 }
 
+// The epilogue of a weight-streaming GEMM tile (MT rows x CB 32-column
+// blocks of CW kept columns): s_red holds NSP planes [NSP][MT][CB * 32] of
+// fp32 partial sums (the splits, or one plane already summed in order),
+// added in plane order as ((0 + p0) + p1) + ...; then EPI writes the tile.
+template <int MT, int CB, int CW, int EPI, int NSP>
+__device__ __forceinline__ void ws_epilogue(const GemmArgs& g, const float* __restrict__ s_red,
+                                            int tid, int lane, int m0, int cg, int si, int NB,
+                                            bool rope) {
+  constexpr int TW = CB * 32;
+  // the tile's sums, 4 adjacent columns at a time: ((0 + p0) + p1) + ...
+  // per element, the split planes in order
+  auto sum4 = [&](int r, int cc) {
+    f32x4 t = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int sp = 0; sp < NSP; ++sp) t += *(const f32x4*)(s_red + sp * (MT * TW) + r * TW + cc);
+    return t;
+  };
+  if (EPI == EPI_BF16 && rope) {
+    // a unit: column j < P of a block (dim i of a head) and its partner
+    // column P + j (dim i + D/2), each rounded to bf16 as the projection
+    // writes it, then rotated
+    const GemmSeg sg = g.seg[si];
+    constexpr int P = CW / 2;
+    constexpr int UNITS = MT * CB * P;
+    const int D = g.rope_D, half = D / 2;
+#pragma unroll
+    for (int u0 = 0; u0 < UNITS; u0 += 256) {
+      const int u = u0 + tid;
+      const int r = u / (CB * P), b = (u / P) % CB, j = u % P;
+      const int row = m0 + r;
+      const int cs = (cg * CB + b) * CW - sg.n0;   // the block's first column in the segment
+      if (u >= UNITS || row >= g.M || cs >= sg.n) continue;
+      const int hd = cs / D, i = (cs - hd * D) / CW * P + j;
+      float t1 = 0.f, t2 = 0.f;
+#pragma unroll
+      for (int sp = 0; sp < NSP; ++sp) {
+        t1 += s_red[sp * (MT * TW) + r * TW + b * 32 + j];
+        t2 += s_red[sp * (MT * TW) + r * TW + b * 32 + P + j];
+      }
+      const double2 cssn = g.rope_tab[(size_t)row * half + i];
+      float o1, o2;
+      rope_rotate((float)(__bf16)t1, (float)(__bf16)t2, cssn.x, cssn.y, o1, o2);
+      __bf16* dst = (__bf16*)sg.C + (size_t)row * sg.n + hd * D + i;
+      dst[0] = (__bf16)o1;
+      dst[half] = (__bf16)o2;
+    }
+  } else if constexpr (EPI == EPI_BF16 || EPI == EPI_F32 || EPI == EPI_F32_ADD) {
+    const GemmSeg sg = g.seg[si];
+    const bool vec = (sg.n & 3) == 0;    // whole 4-column runs are aligned
+    constexpr int UNITS = MT * TW / 4;
+#pragma unroll
+    for (int u0 = 0; u0 < UNITS; u0 += 256) {
+      const int u = u0 + tid;
+      const int r = u / (TW / 4), cc = (u % (TW / 4)) * 4;
+      const int c = cc & 31;
+      const int row = m0 + r;
+      const int col = (cg * CB + (cc >> 5)) * CW + c - sg.n0;   // column in the segment
+      if (u >= UNITS || row >= g.M || c >= CW || col >= sg.n) continue;
+      const f32x4 t = sum4(r, cc);
+      const size_t o = (size_t)row * sg.n + col;
+      if (vec && col + 4 <= sg.n) {
+        if constexpr (EPI == EPI_BF16) {
+          const bf16x2 lo = __builtin_convertvector(f32x2{t[0], t[1]}, bf16x2);
+          const bf16x2 hi = __builtin_convertvector(f32x2{t[2], t[3]}, bf16x2);
+          *(u32x2*)((__bf16*)sg.C + o) =
+              u32x2{__builtin_bit_cast(uint32_t, lo), __builtin_bit_cast(uint32_t, hi)};
+        } else if constexpr (EPI == EPI_F32_ADD) {
+          f32x4 v = *(const f32x4*)((float*)sg.C + o);
+          v += t;
+          *(f32x4*)((float*)sg.C + o) = v;
+        } else {
+          *(f32x4*)((float*)sg.C + o) = t;
+        }
+      } else {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          if (col + i >= sg.n) break;
+          if constexpr (EPI == EPI_BF16) ((__bf16*)sg.C)[o + i] = (__bf16)t[i];
+          else if constexpr (EPI == EPI_F32_ADD) ((float*)sg.C)[o + i] += t[i];
+          else ((float*)sg.C)[o + i] = t[i];
+        }
+      }
+    }
+  } else if constexpr (EPI == EPI_SWIGLU) {
+    // a unit: 4 gate columns of a block and the 4 up columns 16 further on
+    const GemmSeg sg = g.seg[0];
+    constexpr int UNITS = MT * CB * 4;
+#pragma unroll
+    for (int u0 = 0; u0 < UNITS; u0 += 256) {
+      const int u = u0 + tid;
+      const int r = u / (CB * 4), b = (u / 4) % CB, c = (u % 4) * 4;
+      const int row = m0 + r;
+      const int f = (cg * CB + b) * 16 + c;
+      if (u >= UNITS || row >= g.M || f >= sg.n) continue;
+      const f32x4 gt = sum4(r, b * 32 + c), upv = sum4(r, b * 32 + 16 + c);
+      __bf16 act[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float v = (float)(__bf16)gt[i];        // gate and up, rounded as their own outputs
+        const float o = (float)(__bf16)upv[i];
+        act[i] = (__bf16)(v / (1.0f + expf(-v)) * o);
+      }
+      __bf16* dst = (__bf16*)sg.C + (size_t)row * sg.n + f;
+      if ((sg.n & 3) == 0 && f + 4 <= sg.n) {
+        *(u32x2*)dst = __builtin_bit_cast(u32x2, act);
+      } else {
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          if (f + i < sg.n) dst[i] = act[i];
+      }
+    }
+  } else {
+    // EPI_ARGMAX: a unit is 8 columns of a block's row; the 4 units of a
+    // block row are adjacent lanes (the key max is exact and the keys are
+    // distinct, so the order of the max does not matter)
+    bool nonfinite = false;
+    constexpr int UNITS = MT * CB * 4;
+    static_assert(UNITS % 256 == 0 || UNITS < 256, "whole lane quads");
+#pragma unroll
+    for (int u0 = 0; u0 < UNITS; u0 += 256) {
+      const int u = u0 + tid;
+      const int r = u / (CB * 4), b = (u / 4) % CB, q = u % 4;
+      const int row = m0 + r;
+      const int cb = cg * CB + b;
+      const bool live = u < UNITS && row < g.M && cb < NB;
+      uint64_t kv = 0;
+      if (live) {
+        const f32x4 t0 = sum4(r, b * 32 + q * 8), t1 = sum4(r, b * 32 + q * 8 + 4);
+        const int col0 = cb * CW + q * 8;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          const int col = col0 + i;
+          const uint64_t k = col < g.ncols ? pack_logit(i < 4 ? t0[i] : t1[i - 4], col, nonfinite) : 0;
+          kv = k > kv ? k : kv;
+        }
+      }
+#pragma unroll
+      for (int off = 1; off < 4; off <<= 1) {
+        const uint32_t lo = __shfl_xor((uint32_t)kv, off);
+        const uint32_t hi = __shfl_xor((uint32_t)(kv >> 32), off);
+        const uint64_t o = ((uint64_t)hi << 32) | lo;
+        kv = o > kv ? o : kv;
+      }
+      if (live && q == 0) g.part[(size_t)row * NB + cb] = kv;
+    }
+    if (__any(nonfinite) && lane == 0) set_err(g.err, DVS_ERR_NONFINITE);
+  }
+}
+
 // NARROW: blocks of 16 output columns (few-row calls with few blocks, plain
 // epilogues): the products still span 32 columns, of which the second 16
 // read stale LDS rows and are discarded -- each kept column's arithmetic is
@@ -652,144 +801,162 @@ __global__ void __launch_bounds__(256, WK ? 1 : 2) gemm_ws_kernel(GemmArgs g) {
             wvalid ? acc[a][b][i] : 0.f;
   }
   __syncthreads();
-  // the tile's sums, 4 adjacent columns at a time: ((0 + p0) + p1) + p2) + p3
-  // per element, the splits in order
-  auto sum4 = [&](int r, int cc) {
-    f32x4 t = f32x4{0.f, 0.f, 0.f, 0.f};
+  ws_epilogue<MT, CB, CW, EPI, GK_SPLITS>(g, s_red, tid, lane, m0, cg, si, NB, rope);
+}
+
+// gemm_ns_kernel<EPI, MT, NS>: the weight-streaming GEMM with the waves
+// split over columns instead of K.  Workgroup = 4 waves = one (row tile of
+// MT rows, group of 4 32-column blocks); wave w computes block w for all of
+// K, keeping the four splits' sums apart (acc[s] is the in-order MFMA
+// accumulation over split s's K range, exactly gemm_ws_kernel's p_s), and
+// adds them in order at the end, so every output element is bit-identical
+// to gemm_ws_kernel's.  The A chunk (MT rows x 64 k, whole 128-byte lines)
+// is copied once per workgroup and read by all four waves, so A is re-read
+// once per 128 output columns; each wave copies its block's weight rows.
+// MT = 64 with a 3-stage ring of 24 KB stages (72 KB) leaves room for two
+// workgroups per CU.  Used for the 64-row LM head (top-1 or fp32 logits):
+// 14% faster there; for gate|up (256 workgroups, one per CU, each walking
+// all of K with a barrier per chunk) it was slower than gemm_ws_kernel at
+// 64 or 32 rows and three or four stages.
+constexpr int NS_BLOCKS = 4;   // 32-column blocks per workgroup
+template <int EPI, int MT, int NS>
+__global__ void __launch_bounds__(256, NS * (MT * 128 + NS_BLOCKS * 4096) <= 81920 ? 2 : 1)
+gemm_ns_kernel(GemmArgs g) {
+  constexpr int RG = MT / 32, CW = 32, KC = 64, RB = KC * 2;
+  constexpr int AB = MT * RB;                   // A part of a stage: 4 or 8 KB
+  constexpr int WB = 32 * RB;                   // one block's weight rows: 4 KB
+  constexpr int STB = AB + NS_BLOCKS * WB;
+  constexpr int TW = NS_BLOCKS * 32;
+  constexpr int AI = MT / 32;                   // A copies per wave and chunk (MT/8 rows-copies over 4 waves)
+  constexpr int NPL = AI + 4;                   // 1 KB copies per wave and chunk (A rows, own W)
+  static_assert(NS * STB >= MT * TW * 4, "the summed tile reuses the ring");
+  __shared__ __attribute__((aligned(1024))) char s_ring[NS * STB];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int l32 = lane & 31, hh = lane >> 5;
+  const int NB = (g.ncols + CW - 1) / CW;
+  const int NG = (NB + NS_BLOCKS - 1) / NS_BLOCKS;
+  // XCD-aware order, as in gemm_ws_kernel
+  const int x = blockIdx.x & 7, j = blockIdx.x >> 3;
+  const int cg = (j / g.n_rt) * 8 + x, rt = j % g.n_rt;
+  if (cg >= NG) return;
+  const int m0 = rt * MT;
+
+  // copies (whole lines): 8 rows of 128 bytes per 1 KB instruction, lane L
+  // takes row 8i + L/8 and 16-byte chunk (L & 7) ^ sw(row)
+  const int crow = lane >> 3, cchk = lane & 7;
+  auto sw = [](int row) { return (row >> 1) & 7; };
+  int si = 0;
+  if (EPI != EPI_SWIGLU)
+    while (si + 1 < g.nseg && cg * NS_BLOCKS * CW >= g.seg[si + 1].n0) ++si;
+  const int cb = cg * NS_BLOCKS + w;            // this wave's block
+  const __bf16* wsrc[4];
 #pragma unroll
-    for (int sp = 0; sp < GK_SPLITS; ++sp) t += *(const f32x4*)(s_red + sp * (MT * TW) + r * TW + cc);
-    return t;
-  };
-  if (EPI == EPI_BF16 && rope) {
-    // a unit: column j < P of a block (dim i of a head) and its partner
-    // column P + j (dim i + D/2), each rounded to bf16 as the projection
-    // writes it, then rotated
-    const GemmSeg sg = g.seg[si];
-    constexpr int P = CW / 2;
-    constexpr int UNITS = MT * CB * P;
-    const int D = g.rope_D, half = D / 2;
-#pragma unroll
-    for (int u0 = 0; u0 < UNITS; u0 += 256) {
-      const int u = u0 + tid;
-      const int r = u / (CB * P), b = (u / P) % CB, j = u % P;
-      const int row = m0 + r;
-      const int cs = (cg * CB + b) * CW - sg.n0;   // the block's first column in the segment
-      if (u >= UNITS || row >= g.M || cs >= sg.n) continue;
-      const int hd = cs / D, i = (cs - hd * D) / CW * P + j;
-      float t1 = 0.f, t2 = 0.f;
-#pragma unroll
-      for (int sp = 0; sp < GK_SPLITS; ++sp) {
-        t1 += s_red[sp * (MT * TW) + r * TW + b * 32 + j];
-        t2 += s_red[sp * (MT * TW) + r * TW + b * 32 + P + j];
-      }
-      const double2 cssn = g.rope_tab[(size_t)row * half + i];
-      float o1, o2;
-      rope_rotate((float)(__bf16)t1, (float)(__bf16)t2, cssn.x, cssn.y, o1, o2);
-      __bf16* dst = (__bf16*)sg.C + (size_t)row * sg.n + hd * D + i;
-      dst[0] = (__bf16)o1;
-      dst[half] = (__bf16)o2;
+  for (int i = 0; i < 4; ++i) {
+    const int r = 8 * i + crow;
+    const __bf16* base;
+    bool valid;
+    int rowi;
+    if (EPI == EPI_SWIGLU) {
+      rowi = cb * 16 + (r & 15);
+      valid = rowi < g.seg[0].n;
+      base = r < 16 ? g.seg[0].W : g.seg[1].W;
+    } else {
+      rowi = cb * CW - g.seg[si].n0 + r;
+      valid = rowi < g.seg[si].n;
+      base = g.seg[si].W;
     }
-  } else if constexpr (EPI == EPI_BF16 || EPI == EPI_F32 || EPI == EPI_F32_ADD) {
-    const GemmSeg sg = g.seg[si];
-    const bool vec = (sg.n & 3) == 0;    // whole 4-column runs are aligned
-    constexpr int UNITS = MT * TW / 4;
-#pragma unroll
-    for (int u0 = 0; u0 < UNITS; u0 += 256) {
-      const int u = u0 + tid;
-      const int r = u / (TW / 4), cc = (u % (TW / 4)) * 4;
-      const int c = cc & 31;
-      const int row = m0 + r;
-      const int col = (cg * CB + (cc >> 5)) * CW + c - sg.n0;   // column in the segment
-      if (u >= UNITS || row >= g.M || c >= CW || col >= sg.n) continue;
-      const f32x4 t = sum4(r, cc);
-      const size_t o = (size_t)row * sg.n + col;
-      if (vec && col + 4 <= sg.n) {
-        if constexpr (EPI == EPI_BF16) {
-          const bf16x2 lo = __builtin_convertvector(f32x2{t[0], t[1]}, bf16x2);
-          const bf16x2 hi = __builtin_convertvector(f32x2{t[2], t[3]}, bf16x2);
-          *(u32x2*)((__bf16*)sg.C + o) =
-              u32x2{__builtin_bit_cast(uint32_t, lo), __builtin_bit_cast(uint32_t, hi)};
-        } else if constexpr (EPI == EPI_F32_ADD) {
-          f32x4 v = *(const f32x4*)((float*)sg.C + o);
-          v += t;
-          *(f32x4*)((float*)sg.C + o) = v;
-        } else {
-          *(f32x4*)((float*)sg.C + o) = t;
-        }
-      } else {
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          if (col + i >= sg.n) break;
-          if constexpr (EPI == EPI_BF16) ((__bf16*)sg.C)[o + i] = (__bf16)t[i];
-          else if constexpr (EPI == EPI_F32_ADD) ((float*)sg.C)[o + i] += t[i];
-          else ((float*)sg.C)[o + i] = t[i];
-        }
-      }
-    }
-  } else if constexpr (EPI == EPI_SWIGLU) {
-    // a unit: 4 gate columns of a block and the 4 up columns 16 further on
-    const GemmSeg sg = g.seg[0];
-    constexpr int UNITS = MT * CB * 4;
-#pragma unroll
-    for (int u0 = 0; u0 < UNITS; u0 += 256) {
-      const int u = u0 + tid;
-      const int r = u / (CB * 4), b = (u / 4) % CB, c = (u % 4) * 4;
-      const int row = m0 + r;
-      const int f = (cg * CB + b) * 16 + c;
-      if (u >= UNITS || row >= g.M || f >= sg.n) continue;
-      const f32x4 gt = sum4(r, b * 32 + c), upv = sum4(r, b * 32 + 16 + c);
-      __bf16 act[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const float v = (float)(__bf16)gt[i];        // gate and up, rounded as their own outputs
-        const float o = (float)(__bf16)upv[i];
-        act[i] = (__bf16)(v / (1.0f + expf(-v)) * o);
-      }
-      __bf16* dst = (__bf16*)sg.C + (size_t)row * sg.n + f;
-      if ((sg.n & 3) == 0 && f + 4 <= sg.n) {
-        *(u32x2*)dst = __builtin_bit_cast(u32x2, act);
-      } else {
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-          if (f + i < sg.n) dst[i] = act[i];
-      }
-    }
-  } else {
-    // EPI_ARGMAX: a unit is 8 columns of a block's row; the 4 units of a
-    // block row are adjacent lanes (the key max is exact and the keys are
-    // distinct, so the order of the max does not matter)
-    bool nonfinite = false;
-    constexpr int UNITS = MT * CB * 4;
-    static_assert(UNITS % 256 == 0 || UNITS < 256, "whole lane quads");
-#pragma unroll
-    for (int u0 = 0; u0 < UNITS; u0 += 256) {
-      const int u = u0 + tid;
-      const int r = u / (CB * 4), b = (u / 4) % CB, q = u % 4;
-      const int row = m0 + r;
-      const int cb = cg * CB + b;
-      const bool live = u < UNITS && row < g.M && cb < NB;
-      uint64_t kv = 0;
-      if (live) {
-        const f32x4 t0 = sum4(r, b * 32 + q * 8), t1 = sum4(r, b * 32 + q * 8 + 4);
-        const int col0 = cb * CW + q * 8;
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          const int col = col0 + i;
-          const uint64_t k = col < g.ncols ? pack_logit(i < 4 ? t0[i] : t1[i - 4], col, nonfinite) : 0;
-          kv = k > kv ? k : kv;
-        }
-      }
-#pragma unroll
-      for (int off = 1; off < 4; off <<= 1) {
-        const uint32_t lo = __shfl_xor((uint32_t)kv, off);
-        const uint32_t hi = __shfl_xor((uint32_t)(kv >> 32), off);
-        const uint64_t o = ((uint64_t)hi << 32) | lo;
-        kv = o > kv ? o : kv;
-      }
-      if (live && q == 0) g.part[(size_t)row * NB + cb] = kv;
-    }
-    if (__any(nonfinite) && lane == 0) set_err(g.err, DVS_ERR_NONFINITE);
+    wsrc[i] = base + (size_t)(valid ? rowi : 0) * g.K + ((cchk ^ sw(r)) << 3);
   }
+  const __bf16* asrc[AI];                       // A rows 8(AI w + i) + L/8
+#pragma unroll
+  for (int i = 0; i < AI; ++i) {
+    const int r = 8 * (AI * w + i) + crow;
+    asrc[i] = g.A + (size_t)min(m0 + r, g.M - 1) * g.K + ((cchk ^ sw(r)) << 3);
+  }
+  const int nch = g.K / KC;                     // a multiple of 4 (K % 256 == 0)
+  const int cps = nch / GK_SPLITS;              // chunks per split
+  auto issue = [&](int t) {
+    char* stage = s_ring + (t % NS) * STB;
+    const int k0 = t * KC;
+#pragma unroll
+    for (int i = 0; i < AI; ++i)
+      __builtin_amdgcn_global_load_lds((const void*)(asrc[i] + k0),
+                                       (__attribute__((address_space(3))) void*)(stage + (AI * w + i) * 1024), 16, 0, 0);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      __builtin_amdgcn_global_load_lds((const void*)(wsrc[i] + k0),
+                                       (__attribute__((address_space(3))) void*)(stage + AB + w * WB + i * 1024), 16, 0, 0);
+  };
+  auto wait_chunk = [&](int later) {
+    static_for<0, NS>([&](auto c) {
+      constexpr int n = NS - 1 - decltype(c)::value;
+      if (later == n) ws_wait_vmcnt<n * NPL>();
+    });
+  };
+
+  f32x16 acc[GK_SPLITS][RG];
+#pragma unroll
+  for (int sp = 0; sp < GK_SPLITS; ++sp)
+#pragma unroll
+    for (int a = 0; a < RG; ++a) acc[sp][a] = f32x16{};
+  static_for<0, NS - 1>([&](auto c) {
+    if (decltype(c)::value < nch) issue(decltype(c)::value);
+  });
+  static_for<0, GK_SPLITS>([&](auto spc) {
+    constexpr int sp = decltype(spc)::value;
+    for (int tt = 0; tt < cps; ++tt) {
+      const int t = sp * cps + tt;
+      // this wave's copies of chunk t are in; the barrier makes everyone's
+      // (the A rows are shared) and frees the slot chunk t-1 used
+      wait_chunk(min(NS - 2, nch - 1 - t));
+      __syncthreads();
+      if (t + NS - 1 < nch) issue(t + NS - 1);
+      const char* stage = s_ring + (t % NS) * STB;
+      bf16x8 bw[KC / 16], ba[KC / 16][RG];
+#pragma unroll
+      for (int ks = 0; ks < KC / 16; ++ks) {
+        const int q = 2 * ks + hh;
+        bw[ks] = *(const bf16x8*)(stage + AB + w * WB + l32 * RB + ((q ^ sw(l32)) << 4));
+#pragma unroll
+        for (int a = 0; a < RG; ++a) {
+          const int r = a * 32 + l32;
+          ba[ks][a] = *(const bf16x8*)(stage + r * RB + ((q ^ sw(r)) << 4));
+        }
+      }
+#pragma unroll
+      for (int ks = 0; ks < KC / 16; ++ks) {
+        asm volatile("" : "+v"(bw[ks]));
+#pragma unroll
+        for (int a = 0; a < RG; ++a) asm volatile("" : "+v"(ba[ks][a]));
+      }
+#pragma unroll
+      for (int ks = 0; ks < KC / 16; ++ks)
+#pragma unroll
+        for (int a = 0; a < RG; ++a)
+          acc[sp][a] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ba[ks][a], bw[ks], acc[sp][a], 0, 0, 0);
+    }
+  });
+
+  // the splits in order, in registers; rows of W past the segment end were
+  // read from row 0: their columns are 0.  The summed tile goes to LDS (the
+  // ring is free once every wave is done) for the shared epilogue.
+  bool wvalid;
+  if (EPI == EPI_SWIGLU) wvalid = cb * 16 + (l32 & 15) < g.seg[0].n;
+  else wvalid = cb * CW - g.seg[si].n0 + l32 < g.seg[si].n;
+  __syncthreads();
+  float* s_sum = (float*)s_ring;
+#pragma unroll
+  for (int a = 0; a < RG; ++a)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      float t = 0.f;
+#pragma unroll
+      for (int sp = 0; sp < GK_SPLITS; ++sp) t += wvalid ? acc[sp][a][i] : 0.f;
+      s_sum[(a * 32 + 8 * (i >> 2) + 4 * hh + (i & 3)) * TW + w * 32 + l32] = t;
+    }
+  __syncthreads();
+  ws_epilogue<MT, NS_BLOCKS, CW, EPI, 1>(g, s_sum, tid, lane, m0, cg, si, NB, false);
 }
 
 // Top-1 of each row from its column blocks' packed (key, index) maxima: one
@@ -1188,6 +1355,22 @@ static int launch_ws(GemmArgs& g, hipStream_t st) {
       return true;
     };
     if ((NB / 2) * g.n_rt >= WS_WIDE_MIN_WG && groups_ok(2)) CB = 2;
+  }
+  // 64-row calls with many 128-column groups and a top-1 or fp32 epilogue
+  // (the LM head): the column-split kernel (one A chunk per four blocks)
+  if (MT == 64 && !narrow && (g.epi == EPI_ARGMAX || g.epi == EPI_F32)) {
+    const int NGn = (NB + NS_BLOCKS - 1) / NS_BLOCKS;
+    bool ok = (long long)NGn * g.n_rt >= WS_WIDE_MIN_WG;
+    for (int i = 0; i < g.nseg; ++i)
+      if (g.seg[i].n0 % (32 * NS_BLOCKS)) ok = false;
+    if (ok) {
+      const long long gridn = (long long)((NGn + 7) / 8) * 8 * g.n_rt;
+      DVS_CHECK_SUPPORTED(gridn < (1LL << 31), "draft_verify_step: GEMM grid too large");
+      const dim3 grn((unsigned)gridn), blk(256);
+      if (g.epi == EPI_ARGMAX) hipLaunchKernelGGL((gemm_ns_kernel<EPI_ARGMAX, 64, 3>), grn, blk, 0, st, g);
+      else hipLaunchKernelGGL((gemm_ns_kernel<EPI_F32, 64, 3>), grn, blk, 0, st, g);
+      return launch_status("draft_verify_step(gemm)");
+    }
   }
   const int NG = (NB + CB - 1) / CB;
   const long long grid = (long long)((NG + 7) / 8) * 8 * g.n_rt;
