@@ -198,12 +198,20 @@ __device__ __forceinline__ void rope_rotate(float x1, float x2, double cs, doubl
 }
 
 // (cos, sin) of every (row, i < D/2) of a step: row s * R + r at position
-// kv_len[s] + window_offset(r); the same for every layer of the step.
+// kv_len[s] + window_offset(r); the same for every layer of the step.  The
+// first zero_blocks workgroups clear zero[0 .. n_zero) instead (the
+// attention's split counters), so that both take one launch.
 __global__ void rope_table_kernel(double2* __restrict__ tab, int M, int R, int D, double log2_theta,
                                   const int32_t* __restrict__ kv_len, int n_causal, int n_mask,
-                                  int group) {
+                                  int group, int32_t* __restrict__ zero, int n_zero,
+                                  int zero_blocks) {
+  if ((int)blockIdx.x < zero_blocks) {
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n_zero) zero[i] = 0;
+    return;
+  }
   const int half = D / 2;
-  const int idx = blockIdx.x * blockDim.x + threadIdx.x;
+  const int idx = (blockIdx.x - zero_blocks) * blockDim.x + threadIdx.x;
   if (idx >= M * half) return;
   const int mrow = idx / half, i = idx - mrow * half;
   const int s = mrow / R, r = mrow - s * R;
@@ -960,15 +968,24 @@ gemm_ns_kernel(GemmArgs g) {
 }
 
 // Top-1 of each row from its column blocks' packed (key, index) maxima: one
-// wave per row, a 64-bit max, the lowest index among equal maxima; a row
-// whose values were all NaN gives 0.
+// workgroup per row, every load of a thread in flight at once (a clamped
+// index repeats the last block, which leaves the maximum unchanged), a
+// 64-bit max over the lanes and then the waves; the lowest index wins among
+// equal maxima; a row whose values were all NaN gives 0.
 __global__ void __launch_bounds__(256) argmax_rows_kernel(const uint64_t* __restrict__ part, int M,
                                                           int NB, int32_t* __restrict__ out) {
-  const int row = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  __shared__ uint64_t s_b[4];
+  const int row = blockIdx.x, tid = threadIdx.x, lane = tid & 63;
   if (row >= M) return;
   const uint64_t* p = part + (size_t)row * NB;
   uint64_t b = 0;
-  for (int i = lane; i < NB; i += 64) b = p[i] > b ? p[i] : b;
+  for (int i0 = 0; i0 < NB; i0 += 256 * 8) {
+    uint64_t v[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) v[j] = p[min(i0 + tid + 256 * j, NB - 1)];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) b = v[j] > b ? v[j] : b;
+  }
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) {
     const uint32_t lo = __shfl_xor((uint32_t)b, off);
@@ -976,7 +993,14 @@ __global__ void __launch_bounds__(256) argmax_rows_kernel(const uint64_t* __rest
     const uint64_t o = ((uint64_t)hi << 32) | lo;
     b = o > b ? o : b;
   }
-  if (lane == 0) out[row] = b == 0 ? 0 : 0x7fffffff - (int)(uint32_t)(b & 0xffffffffu);
+  if (lane == 0) s_b[tid >> 6] = b;
+  __syncthreads();
+  if (tid == 0) {
+    b = s_b[0];
+#pragma unroll
+    for (int i = 1; i < 4; ++i) b = s_b[i] > b ? s_b[i] : b;
+    out[row] = b == 0 ? 0 : 0x7fffffff - (int)(uint32_t)(b & 0xffffffffu);
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -1447,7 +1471,7 @@ static int lm_head_top1(const dvs_model* m, const StepLayout& L, char* ws, const
   int rc = launch_ws(g, st);
   if (rc) return rc;
   const int NB = (m->vocab + 31) / 32;
-  hipLaunchKernelGGL(argmax_rows_kernel, dim3((unsigned)((M + 3) / 4)), dim3(256), 0, st, g.part,
+  hipLaunchKernelGGL(argmax_rows_kernel, dim3((unsigned)M), dim3(256), 0, st, g.part,
                      M, NB, am);
   return launch_status("draft_verify_step(lm head top-1)");
 }
@@ -1474,18 +1498,19 @@ static int forward_layers(const dvs_model* m, const dvs_state* st, int n_causal,
   // The workspace may carry another call shape's data where this shape keeps
   // the attention's split counters: clear them once; every attention call
   // leaves them zero for the next layer.
-  if (L.attn_counters) {
-    const int nw = (int)(L.attn_counters / 4);
-    hipLaunchKernelGGL(zero_words_kernel, dim3((nw + 255) / 256), dim3(256), 0, stream,
-                       (int32_t*)(ws + L.attn_ws), nw);
-  }
   const double log2_theta = log2((double)m->rope_theta);
   const bool rope_fused = use_ws(dt, M, H) && D % 32 == 0;
+  const int nw = (int)(L.attn_counters / 4);
   if (rope_fused) {
-    hipLaunchKernelGGL(rope_table_kernel, dim3((M * (D / 2) + 255) / 256), dim3(256), 0, stream,
+    // the rotary table, with the counters' clearing in the same launch
+    const int zb = (nw + 255) / 256;
+    hipLaunchKernelGGL(rope_table_kernel, dim3(zb + (M * (D / 2) + 255) / 256), dim3(256), 0, stream,
                        (double2*)(ws + L.rope), M, R, D, log2_theta, st->kv_len, n_causal, n_mask,
-                       group);
+                       group, (int32_t*)(ws + L.attn_ws), nw, zb);
     if ((rc = launch_status("draft_verify_step(rope table)"))) return rc;
+  } else if (nw) {
+    hipLaunchKernelGGL(zero_words_kernel, dim3((nw + 255) / 256), dim3(256), 0, stream,
+                       (int32_t*)(ws + L.attn_ws), nw);
   }
   for (int l = 0; l < m->n_layers; ++l) {
     const dvs_layer& ly = m->layers[l];
