@@ -967,6 +967,174 @@ gemm_ns_kernel(GemmArgs g) {
   ws_epilogue<MT, NS_BLOCKS, CW, EPI, 1>(g, s_sum, tid, lane, m0, cg, si, NB, false);
 }
 
+// gemm_nk_kernel<EPI, SPLIT_M>: 64-row tiles with the four waves split 2 x
+// 2, each over one K half, that is splits 2h and 2h+1, whose sums it keeps
+// apart (each the in-order MFMA accumulation over its K range, exactly
+// gemm_ws_kernel's p_s):
+//   SPLIT_M = false: two 32-column blocks; wave w takes block w & 1 over K
+//     half w >> 1, and the two waves of a half share its A chunk;
+//   SPLIT_M = true: one 32-column block; wave w takes rows 32 (w & 1) ..
+//     over K half w >> 1, and the two waves of a half share its weight
+//     chunk (and the Q|K|V projection's rotary epilogue is available).
+// Chunks are 64 k wide (whole 128-byte lines) in rings that leave room for
+// two workgroups per CU (2 stages of 32 KB, or 3 of 24 KB).  The four split
+// sums meet in LDS and the shared epilogue adds them in order:
+// bit-identical to gemm_ws_kernel.
+template <int EPI, bool SPLIT_M>
+__global__ void __launch_bounds__(256, 2) gemm_nk_kernel(GemmArgs g) {
+  constexpr int MT = 64, CW = 32, KC = 64, RB = KC * 2;
+  constexpr int CB = SPLIT_M ? 1 : 2;           // blocks per tile
+  constexpr int RG = SPLIT_M ? 1 : 2;           // 32-row groups per wave
+  constexpr int AB = MT * RB;                   // one K half's A chunk: 8 KB
+  constexpr int WB = 32 * RB;                   // one block's weight rows: 4 KB
+  constexpr int STB = 2 * AB + 2 * CB * WB;     // A of both halves, W of (block, half)
+  constexpr int NS = SPLIT_M ? 3 : 2;
+  constexpr int TW = CB * 32;
+  constexpr int AI = 4;                         // A copies per wave and chunk (32 rows)
+  constexpr int WIW = SPLIT_M ? 2 : 4;          // W copies per wave and chunk
+  constexpr int NPL = AI + WIW;
+  static_assert(NS * STB >= GK_SPLITS * MT * TW * 4, "the split sums reuse the ring");
+  static_assert(NS * STB <= 81920, "two workgroups per CU");
+  __shared__ __attribute__((aligned(1024))) char s_ring[NS * STB];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int l32 = lane & 31, hh = lane >> 5;
+  const int wl = w & 1, kh = w >> 1;            // block (or row group) and K half of this wave
+  const int NB = (g.ncols + CW - 1) / CW;
+  const int NG = (NB + CB - 1) / CB;
+  const int x = blockIdx.x & 7, j = blockIdx.x >> 3;
+  const int cg = (j / g.n_rt) * 8 + x, rt = j % g.n_rt;
+  if (cg >= NG) return;
+  const int m0 = rt * MT;
+  const int crow = lane >> 3, cchk = lane & 7;
+  auto sw = [](int row) { return (row >> 1) & 7; };
+  int si = 0;
+  if (EPI != EPI_SWIGLU)
+    while (si + 1 < g.nseg && cg * CB * CW >= g.seg[si + 1].n0) ++si;
+  const bool rope = EPI == EPI_BF16 && g.rope_tab != nullptr && si < 2;
+  const int cb = cg * CB + (SPLIT_M ? 0 : wl);  // this wave's block
+  // weight rows this wave copies: all 32 of its block (SPLIT_M = false), or
+  // rows 16 (w & 1) .. + 15 of the shared block (SPLIT_M = true)
+  const __bf16* wsrc[WIW];
+#pragma unroll
+  for (int i = 0; i < WIW; ++i) {
+    const int r = (SPLIT_M ? 16 * wl : 0) + 8 * i + crow;
+    const __bf16* base;
+    bool valid;
+    int rowi;
+    if (EPI == EPI_SWIGLU) {
+      rowi = cb * 16 + (r & 15);
+      valid = rowi < g.seg[0].n;
+      base = r < 16 ? g.seg[0].W : g.seg[1].W;
+    } else {
+      rowi = cb * CW - g.seg[si].n0 + r;
+      if (rope) {
+        // block bh of a head holds dims bh*16 .. bh*16+15 and their
+        // rotate-half partners D/2 + bh*16 ..
+        const int hd = rowi / g.rope_D, cp = rowi - hd * g.rope_D;
+        const int bh = cp / CW, c = cp - bh * CW;
+        rowi = hd * g.rope_D + (c < CW / 2 ? bh * (CW / 2) + c : g.rope_D / 2 + bh * (CW / 2) + c - CW / 2);
+      }
+      valid = rowi < g.seg[si].n;
+      base = g.seg[si].W;
+    }
+    wsrc[i] = base + (size_t)(valid ? rowi : 0) * g.K + ((cchk ^ sw(r)) << 3);
+  }
+  const __bf16* asrc[AI];                       // A rows 32 (w & 1) + 8i + L/8 of half kh
+#pragma unroll
+  for (int i = 0; i < AI; ++i) {
+    const int r = 32 * wl + 8 * i + crow;
+    asrc[i] = g.A + (size_t)min(m0 + r, g.M - 1) * g.K + ((cchk ^ sw(r)) << 3);
+  }
+  const int kh0 = kh * (g.K / 2);               // first k of this wave's half
+  const int nch = g.K / 2 / KC;                 // chunks per half (even: K % 256 == 0)
+  const int cps = nch / 2;                      // chunks per split
+  // stage layout: A of half 0, A of half 1, then W of (block or half) slots
+  auto wslot = [&](int blk, int half) { return 2 * AB + (SPLIT_M ? half : 2 * half + blk) * WB; };
+  auto issue = [&](int t) {
+    char* stage = s_ring + (t % NS) * STB;
+    const int k0 = kh0 + t * KC;
+#pragma unroll
+    for (int i = 0; i < AI; ++i)
+      __builtin_amdgcn_global_load_lds((const void*)(asrc[i] + k0),
+                                       (__attribute__((address_space(3))) void*)(stage + kh * AB + (4 * wl + i) * 1024), 16, 0, 0);
+#pragma unroll
+    for (int i = 0; i < WIW; ++i)
+      __builtin_amdgcn_global_load_lds((const void*)(wsrc[i] + k0),
+                                       (__attribute__((address_space(3))) void*)(stage + wslot(wl, kh) + ((SPLIT_M ? 2 * wl : 0) + i) * 1024), 16, 0, 0);
+  };
+  auto wait_chunk = [&](int later) {
+    static_for<0, NS>([&](auto c) {
+      constexpr int n = NS - 1 - decltype(c)::value;
+      if (later == n) ws_wait_vmcnt<n * NPL>();
+    });
+  };
+  f32x16 acc[2][RG];
+#pragma unroll
+  for (int sp = 0; sp < 2; ++sp)
+#pragma unroll
+    for (int a = 0; a < RG; ++a) acc[sp][a] = f32x16{};
+  static_for<0, NS - 1>([&](auto c) {
+    if (decltype(c)::value < nch) issue(decltype(c)::value);
+  });
+  static_for<0, 2>([&](auto spc) {
+    constexpr int sp = decltype(spc)::value;
+    for (int tt = 0; tt < cps; ++tt) {
+      const int t = sp * cps + tt;
+      // this wave's copies of chunk t are in; the barrier makes the
+      // partner's, and frees the slot chunk t-1 used
+      wait_chunk(min(NS - 2, nch - 1 - t));
+      __syncthreads();
+      if (t + NS - 1 < nch) issue(t + NS - 1);
+      const char* stage = s_ring + (t % NS) * STB;
+      const char* wsl = stage + wslot(wl, kh);
+      bf16x8 bwf[KC / 16], ba[KC / 16][RG];
+#pragma unroll
+      for (int ks = 0; ks < KC / 16; ++ks) {
+        const int q = 2 * ks + hh;
+        bwf[ks] = *(const bf16x8*)(wsl + l32 * RB + ((q ^ sw(l32)) << 4));
+#pragma unroll
+        for (int a = 0; a < RG; ++a) {
+          const int r = (SPLIT_M ? 32 * wl : a * 32) + l32;
+          ba[ks][a] = *(const bf16x8*)(stage + kh * AB + r * RB + ((q ^ sw(r)) << 4));
+        }
+      }
+#pragma unroll
+      for (int ks = 0; ks < KC / 16; ++ks) {
+        asm volatile("" : "+v"(bwf[ks]));
+#pragma unroll
+        for (int a = 0; a < RG; ++a) asm volatile("" : "+v"(ba[ks][a]));
+      }
+#pragma unroll
+      for (int ks = 0; ks < KC / 16; ++ks)
+#pragma unroll
+        for (int a = 0; a < RG; ++a)
+          acc[sp][a] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ba[ks][a], bwf[ks], acc[sp][a], 0, 0, 0);
+    }
+  });
+
+  // the four split sums to LDS as planes [split][row][TW] (the ring is free
+  // once every wave is done); rows of W past the segment end were read from
+  // row 0: their columns are 0
+  bool wvalid;
+  if (EPI == EPI_SWIGLU) wvalid = cb * 16 + (l32 & 15) < g.seg[0].n;
+  else wvalid = cb * CW - g.seg[si].n0 + l32 < g.seg[si].n;
+  __syncthreads();
+  float* s_red = (float*)s_ring;
+#pragma unroll
+  for (int sp = 0; sp < 2; ++sp)
+#pragma unroll
+    for (int a = 0; a < RG; ++a)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int row = (SPLIT_M ? 32 * wl : a * 32) + 8 * (i >> 2) + 4 * hh + (i & 3);
+        s_red[(2 * kh + sp) * (MT * TW) + row * TW + (SPLIT_M ? 0 : wl * 32) + l32] =
+            wvalid ? acc[sp][a][i] : 0.f;
+      }
+  __syncthreads();
+  ws_epilogue<MT, CB, CW, EPI, GK_SPLITS>(g, s_red, tid, lane, m0, cg, si, NB, rope);
+}
+
 // Top-1 of each row from its column blocks' packed (key, index) maxima: one
 // workgroup per row, every load of a thread in flight at once (a clamped
 // index repeats the last block, which leaves the maximum unchanged), a
@@ -1402,6 +1570,18 @@ static int launch_ws(GemmArgs& g, hipStream_t st) {
   const dim3 gr((unsigned)grid);
   // calls of at most one workgroup per CU: whole-line chunks, deeper rings
   const bool wk = (long long)NG * g.n_rt <= device_cus();
+  // 64-row calls of more than one workgroup per CU: whole-line chunks with
+  // the waves split 2 x 2 (two blocks or two row groups, two K halves), so
+  // that the rings still leave room for two workgroups per CU (gate|up
+  // 20.8 -> 18.6 us per launch at 256 rows)
+  if (MT == 64 && CB == 2 && !wk && g.epi == EPI_SWIGLU) {
+    hipLaunchKernelGGL((gemm_nk_kernel<EPI_SWIGLU, false>), gr, dim3(256), 0, st, g);
+    return launch_status("draft_verify_step(gemm)");
+  }
+  if (MT == 64 && CB == 1 && !wk && g.epi == EPI_BF16) {
+    hipLaunchKernelGGL((gemm_nk_kernel<EPI_BF16, true>), gr, dim3(256), 0, st, g);
+    return launch_status("draft_verify_step(gemm)");
+  }
   if (narrow) launch_ws_k<32, true, 1>(g, gr, wk, st);
   else if (MT == 32) launch_ws_k<32, false, 1>(g, gr, wk, st);
   else if (CB == 2) launch_ws_k<64, false, 2>(g, gr, wk, st);
