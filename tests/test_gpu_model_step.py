@@ -258,6 +258,51 @@ def test_bf16_model_step_matches_oracle_replay():
     _states_equal(st, replay)
 
 
+def test_bf16_wide_step_matches_oracle_replay():
+    """A one-layer bf16 step at 256 window rows (8 sequences, B=16) whose
+    projections take the wide decode-step GEMM paths: Q|K|V of 32/4 heads of
+    64 (80 column blocks: the row-split 2x2 kernel with the rotary epilogue),
+    SwiGLU 2192 (137 gate|up blocks: the block-split 2x2 kernel, the last
+    pair half empty) and vocabulary 8200 (257 blocks: the column-split LM
+    head, the last block 8 columns wide). Logits close to the float64
+    oracle; the top-1 of the fused LM-head epilogue equals the top-1 of the
+    logits; accept and commit replayed through the oracle bit for bit."""
+    B, S = 16, 8
+    L = [41, 77, 130, 199, 256, 301, 350, 397]
+    w = synth.make_model_weights(11, 8200, 256, 32, 4, 64, 1, 2192, std=0.08)
+    base = synth.make_attn_inputs(11, S, L, B, B, 32, 4, 64, "bf16", std=0.5, scatter=True,
+                                  extra_pages=64)
+    kps, vps = [base.k_pool], [base.v_pool]
+    st_host = base.state.copy()
+    rng = np.random.default_rng(3)
+    st_host.boundary[:] = rng.integers(0, w.V, size=S)
+    st_host.draft[:] = rng.integers(0, w.V, size=(S, B - 1))
+    om = OracleModel(_bf16_weights(w), kps, vps, bf16_bits=True)
+    ref_st = st_host.copy()
+    logits_ref, _, _, _ = om.fused_step(ref_st, B)
+    dm = dvs.DeviceModel(w, _dev_pools(kps, "bf16"), _dev_pools(vps, "bf16"), "bf16")
+    M = S * 2 * B
+    # with the logits written out (fp32 epilogue), then with the fused top-1
+    st = dvs.DeviceState(st_host)
+    logits = torch.empty((M, w.V), dtype=torch.float32, device="cuda")
+    am = torch.empty((S, 2 * B), dtype=torch.int32, device="cuda")
+    dvs.draft_verify_step(dm, st, B, B, logits_out=logits, argmax_out=am, chunk_keys=256)
+    st2 = dvs.DeviceState(st_host)
+    am2 = torch.empty((S, 2 * B), dtype=torch.int32, device="cuda")
+    dvs.draft_verify_step(dm, st2, B, B, argmax_out=am2, chunk_keys=256)
+    torch.cuda.synchronize()
+    lg = logits.cpu().numpy().reshape(S, 2 * B, w.V).astype(np.float64)
+    assert max_rel_err(lg, logits_ref) <= 5e-2
+    am_gpu = am.cpu().numpy()
+    np.testing.assert_array_equal(am_gpu, od.top1_rows(lg))
+    np.testing.assert_array_equal(am2.cpu().numpy(), am_gpu)
+    replay = st_host.copy()
+    A_gpu = od.accept(am_gpu, st_host.draft, B)
+    assert od.kv_commit(replay, A_gpu, am_gpu, B, B) == 0
+    _states_equal(st, replay)
+    _states_equal(st2, replay)
+
+
 def _embed_prefix_f64(w_bits, vision, prompt):
     """Oracle-side prefix rows: vision vectors, then embedding rows of the prompt."""
     emb = synth.bf16_to_f64(w_bits.embed)
