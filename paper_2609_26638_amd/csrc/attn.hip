@@ -703,25 +703,32 @@ __global__ void __launch_bounds__(NW * 64, 1) attn_bf16_kernel(AttnParams p) {
       write_out(o, lsum > 0.f ? 1.f / lsum : 0.f);
       continue;
     }
-    // Publish the partial (the O values as 16-byte words, word j of every
-    // thread side by side, so that each store and load of a wave covers 1 KB
-    // in one piece; (m, l) per thread), wait for the stores, then count in;
-    // the workgroup that completes the item merges.
+    // Publish the partial: O / l in bf16 (16-byte words of 8 values, word j
+    // of every thread side by side, so that each store and load of a wave
+    // covers 1 KB in one piece) and (m, l) in fp32 per thread; wait for the
+    // stores, then count in; the workgroup that completes the item merges.
     const int wg0 = (int)blockIdx.x - k;
     const size_t slot = part_slot(p.balanced, it, p.max_segs, wg0, k);
     // a wave whose 32 rows all lie past the item's rows has nothing to
     // publish or merge (few-row calls run four waves for the copies)
     const bool wave_rows = rt * RPW + w * 32 < p.rows_total;
+    constexpr int NWD = NREG / 8;   // 16-byte words of a thread's partial
     if (wave_rows) {
-      float* po = p.part_o + slot * (size_t)(NT * NREG) + (size_t)tid * 4;
+      uint32_t* po = (uint32_t*)p.part_o + slot * (size_t)(NT * NREG / 2) + (size_t)tid * 4;
       float* pml = p.part_ml + slot * (size_t)(NT * 2) + (size_t)tid * 2;
       *(f32x2*)pml = f32x2{m, lsum};
+      const float inv = lsum > 0.f ? 1.f / lsum : 0.f;
 #pragma unroll
-      for (int dg = 0; dg < DG; ++dg)
+      for (int jw = 0; jw < NWD; ++jw) {
+        u32x4 v;
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
-          *(f32x4*)(po + (dg * 4 + j) * (NT * 4)) =
-              f32x4{o[dg][4 * j], o[dg][4 * j + 1], o[dg][4 * j + 2], o[dg][4 * j + 3]};
+        for (int e = 0; e < 4; ++e) {
+          const int f0 = 8 * jw + 2 * e;   // element f of the thread: o[f / 16][f % 16]
+          const f32x2 pr = f32x2{o[f0 / 16][f0 % 16] * inv, o[(f0 + 1) / 16][(f0 + 1) % 16] * inv};
+          v[e] = __builtin_bit_cast(uint32_t, __builtin_convertvector(pr, bf16x2));
+        }
+        *(u32x4*)(po + jw * (NT * 4)) = v;
+      }
     }
     wait_vmcnt<0>();
     __syncthreads();
@@ -755,30 +762,36 @@ __global__ void __launch_bounds__(NW * 64, 1) attn_bf16_kernel(AttnParams p) {
 #pragma unroll
     for (int dg = 0; dg < DG; ++dg) acc[dg] = f32x16{};
     float lt = 0.f;
-    // SB segments per batch (four where the registers allow), added in
-    // segment order
-    constexpr int SB = NREG <= 48 ? 4 : 1;
+    // SB segments per batch (eight where the registers allow), added in
+    // segment order: O += exp2(m_c - M) l_c (O_c / l_c), l += exp2(m_c - M) l_c
+    constexpr int SB = NREG <= 48 ? 8 : 4;
     for (int c0 = 0; c0 < nseg; c0 += SB) {
-      f32x4 pv[SB][NREG / 4];
+      u32x4 pv[SB][NWD];
       f32x2 mlc[SB];
 #pragma unroll
       for (int b = 0; b < SB; ++b) {
         const int c = min(c0 + b, nseg - 1);
-        const float* src = p.part_o + part_slot(p.balanced, it, p.max_segs, wg0, c) * (NT * NREG) +
-                           (size_t)tid * 4;
+        const uint32_t* src = (const uint32_t*)p.part_o +
+                              part_slot(p.balanced, it, p.max_segs, wg0, c) * (NT * NREG / 2) +
+                              (size_t)tid * 4;
 #pragma unroll
-        for (int j = 0; j < NREG / 4; ++j) pv[b][j] = *(const f32x4*)(src + j * (NT * 4));
+        for (int jw = 0; jw < NWD; ++jw) pv[b][jw] = *(const u32x4*)(src + jw * (NT * 4));
         mlc[b] = ml_of(c);
       }
 #pragma unroll
       for (int b = 0; b < SB; ++b) {
         if (c0 + b >= nseg) break;
-        const float wgt = __builtin_amdgcn_exp2f(mlc[b][0] - Ms);
-        lt += wgt * mlc[b][1];
+        const float wgt = __builtin_amdgcn_exp2f(mlc[b][0] - Ms) * mlc[b][1];
+        lt += wgt;
 #pragma unroll
-        for (int dg = 0; dg < DG; ++dg)
+        for (int jw = 0; jw < NWD; ++jw)
 #pragma unroll
-          for (int i = 0; i < 16; ++i) acc[dg][i] += wgt * pv[b][(dg * 16 + i) / 4][i % 4];
+          for (int e = 0; e < 4; ++e) {
+            const int f0 = 8 * jw + 2 * e;
+            const uint32_t wd = pv[b][jw][e];
+            acc[f0 / 16][f0 % 16] += wgt * __uint_as_float(wd << 16);
+            acc[(f0 + 1) / 16][(f0 + 1) % 16] += wgt * __uint_as_float(wd & 0xffff0000u);
+          }
       }
     }
     write_out(acc, lt > 0.f ? 1.f / lt : 0.f);
@@ -1681,12 +1694,12 @@ static AttnPlan plan_attn(int S, int R, int Hq, int Hkv, int D, int max_pages, i
   // chunk) in the aligned one (part_slot)
   const size_t slots = pl.balanced ? (size_t)2 * pl.grid : (size_t)pl.n_items * pl.max_segs;
   if (dtype == DVS_BF16) {
-    // per slot: m and l of every query row (fp32), and O -- fp32 per thread
-    // and register in attn_bf16_kernel, O / l as bf16 pairs per consumer
-    // thread in the producer/consumer kernel (4 pairs, 256 rows)
+    // per slot: m and l of every query row (fp32), and O / l in bf16 -- per
+    // thread and register in attn_bf16_kernel, as pairs per consumer thread
+    // in the producer/consumer kernel (4 pairs, 256 rows)
     const size_t ml_b = pl.pc ? (size_t)2 * 256 * sizeof(float) : (size_t)NT * 2 * sizeof(float);
     const size_t o_b = pl.pc ? (size_t)256 * (2 * (D / 32) * 16) * 2
-                             : (size_t)NT * (D / 32) * 16 * sizeof(float);
+                             : (size_t)NT * (D / 32) * 16 * 2;
     pl.off_counters = 0;
     pl.off_ml = align256((size_t)pl.n_items * sizeof(int32_t));
     pl.off_o = pl.off_ml + align256(slots * ml_b);
