@@ -634,7 +634,7 @@ __device__ __forceinline__ void ws_epilogue(const GemmArgs& g, const float* __re
 // CB adjacent 32-column blocks, so one A chunk feeds CB blocks' products
 // (A is re-read once per CB blocks instead of once per block); per element
 // the arithmetic is the single block's.
-template <int MT, bool NARROW, int CB, int EPI, bool WK>
+template <int MT, bool NARROW, int CB, int EPI, bool WK, bool FEW = false>
 __global__ void __launch_bounds__(256, WK ? 1 : 2) gemm_ws_kernel(GemmArgs g) {
   constexpr int CW = NARROW ? 16 : 32;     // output columns per block
   // k per chunk.  WK (calls of at most one workgroup per CU): 64, so that a
@@ -653,7 +653,11 @@ __global__ void __launch_bounds__(256, WK ? 1 : 2) gemm_ws_kernel(GemmArgs g) {
   constexpr int NS = WK ? (CB == 2 ? 2 : 3) : (MT == 32 ? 4 : (CB == 2 ? 2 : 3));
   constexpr int WB = 32 * RB;              // W part of a block's chunk: 32 rows
   constexpr int CHB = CB * WB + MT * RB;   // chunk bytes (CB blocks' W rows, then A rows)
-  constexpr int NPL = CB * WI + MT / RPI;  // 1 KB copies per chunk and wave
+  // FEW: calls of at most RPI rows copy only the first RPI rows of A (one
+  // copy per chunk); the tile's other rows read stale LDS and their outputs
+  // are discarded
+  constexpr int AI = FEW ? 1 : MT / RPI;   // A copies per chunk and wave
+  constexpr int NPL = CB * WI + AI;        // 1 KB copies per chunk and wave
   constexpr int TW = CB * 32;              // tile width in the split sums
   static_assert(NPL * (NS - 1) < 64, "vmcnt range");
   static_assert(!NARROW || (MT == 32 && CB == 1), "narrow blocks serve few-row calls");
@@ -715,9 +719,9 @@ __global__ void __launch_bounds__(256, WK ? 1 : 2) gemm_ws_kernel(GemmArgs g) {
       }
       wsrc[b][i] = base + (size_t)(valid ? rowi : 0) * g.K + ((cchk ^ sw(r)) << 3);
     }
-  const __bf16* asrc[MT / RPI];
+  const __bf16* asrc[AI];
 #pragma unroll
-  for (int i = 0; i < MT / RPI; ++i) {
+  for (int i = 0; i < AI; ++i) {
     const int r = RPI * i + crow;
     asrc[i] = g.A + (size_t)min(m0 + r, g.M - 1) * g.K + ((cchk ^ sw(r)) << 3);
   }
@@ -734,7 +738,7 @@ __global__ void __launch_bounds__(256, WK ? 1 : 2) gemm_ws_kernel(GemmArgs g) {
         __builtin_amdgcn_global_load_lds((const void*)(wsrc[b][i] + k0),
                                          (__attribute__((address_space(3))) void*)(dst + b * WB + i * 1024), 16, 0, 0);
 #pragma unroll
-    for (int i = 0; i < MT / RPI; ++i)
+    for (int i = 0; i < AI; ++i)
       __builtin_amdgcn_global_load_lds((const void*)(asrc[i] + k0),
                                        (__attribute__((address_space(3))) void*)(dst + CB * WB + i * 1024), 16, 0, 0);
   };
@@ -1507,17 +1511,17 @@ static StepLayout step_layout(const dvs_model* m, int S, int n_causal, int n_mas
   return L;
 }
 
-template <int MT, bool NARROW, int CB, bool WK>
+template <int MT, bool NARROW, int CB, bool WK, bool FEW>
 static void launch_ws_epi(const GemmArgs& g, dim3 gr, hipStream_t st) {
   const dim3 blk(256);
   switch (g.epi) {
-    case EPI_BF16: hipLaunchKernelGGL((gemm_ws_kernel<MT, NARROW, CB, EPI_BF16, WK>), gr, blk, 0, st, g); break;
-    case EPI_F32: hipLaunchKernelGGL((gemm_ws_kernel<MT, NARROW, CB, EPI_F32, WK>), gr, blk, 0, st, g); break;
-    case EPI_F32_ADD: hipLaunchKernelGGL((gemm_ws_kernel<MT, NARROW, CB, EPI_F32_ADD, WK>), gr, blk, 0, st, g); break;
+    case EPI_BF16: hipLaunchKernelGGL((gemm_ws_kernel<MT, NARROW, CB, EPI_BF16, WK, FEW>), gr, blk, 0, st, g); break;
+    case EPI_F32: hipLaunchKernelGGL((gemm_ws_kernel<MT, NARROW, CB, EPI_F32, WK, FEW>), gr, blk, 0, st, g); break;
+    case EPI_F32_ADD: hipLaunchKernelGGL((gemm_ws_kernel<MT, NARROW, CB, EPI_F32_ADD, WK, FEW>), gr, blk, 0, st, g); break;
     default:
       if constexpr (!NARROW) {
-        if (g.epi == EPI_SWIGLU) hipLaunchKernelGGL((gemm_ws_kernel<MT, false, CB, EPI_SWIGLU, WK>), gr, blk, 0, st, g);
-        else hipLaunchKernelGGL((gemm_ws_kernel<MT, false, CB, EPI_ARGMAX, WK>), gr, blk, 0, st, g);
+        if (g.epi == EPI_SWIGLU) hipLaunchKernelGGL((gemm_ws_kernel<MT, false, CB, EPI_SWIGLU, WK, FEW>), gr, blk, 0, st, g);
+        else hipLaunchKernelGGL((gemm_ws_kernel<MT, false, CB, EPI_ARGMAX, WK, FEW>), gr, blk, 0, st, g);
       }
       break;
   }
@@ -1525,8 +1529,17 @@ static void launch_ws_epi(const GemmArgs& g, dim3 gr, hipStream_t st) {
 
 template <int MT, bool NARROW, int CB>
 static void launch_ws_k(const GemmArgs& g, dim3 gr, bool wk, hipStream_t st) {
-  if (wk) launch_ws_epi<MT, NARROW, CB, true>(g, gr, st);
-  else launch_ws_epi<MT, NARROW, CB, false>(g, gr, st);
+  if constexpr (MT == 32) {
+    // calls whose rows fit one copy of A rows (8 rows in 64-k chunks, 16 in
+    // 32-k chunks)
+    if (g.M <= (wk ? 8 : 16)) {
+      if (wk) launch_ws_epi<MT, NARROW, CB, true, true>(g, gr, st);
+      else launch_ws_epi<MT, NARROW, CB, false, true>(g, gr, st);
+      return;
+    }
+  }
+  if (wk) launch_ws_epi<MT, NARROW, CB, true, false>(g, gr, st);
+  else launch_ws_epi<MT, NARROW, CB, false, false>(g, gr, st);
 }
 
 static int launch_ws(GemmArgs& g, hipStream_t st) {
