@@ -127,46 +127,56 @@ __global__ void fill_words_kernel(int32_t* __restrict__ p, int n, int32_t v) {
 }
 
 // out[m, :] = x[m, :] / sqrt(mean(x^2) + eps) * g   (one workgroup per row).
-// Thread t takes elements t, t + 256, ... (the sum of squares in that order,
-// then the waves' sums combined as (w0 + w1) + (w2 + w3)); a row of up to
-// 256 * RN_REG elements is loaded once, with its gains, before the reduction.
-constexpr int RN_REG = 8;
+// Thread t takes the runs of 8 elements 8(t + 256c) .. 8(t + 256c) + 7,
+// c = 0, 1, ... (16-byte loads; the sum of squares in that order), then a
+// butterfly over its wave, then (w0 + w1) + (w2 + w3).  H is a multiple of
+// 8; a row of up to 2048 elements is loaded once before the reduction, with
+// no per-element branch around the loads (the per-element form waited for
+// each load in turn: 4.5 -> about 2.5 us per launch).
 template <typename T>
 __global__ void __launch_bounds__(256) rmsnorm_kernel(const float* __restrict__ x, const T* __restrict__ g,
                                                       int H, float eps, T* __restrict__ out) {
   __shared__ float red[4];
-  const int mrow = blockIdx.x;
+  const int mrow = blockIdx.x, t = threadIdx.x;
   const float* xr = x + (size_t)mrow * H;
+  T* orow = out + (size_t)mrow * H;
+  const int nrun = H / 8;
   float ss = 0.f;
-  const bool held = H <= 256 * RN_REG;
-  float xv[RN_REG], gv[RN_REG];
+  const bool held = nrun <= 256;
+  const bool live = t < nrun;
+  f32x4 xa = f32x4{0.f, 0.f, 0.f, 0.f}, xb = xa;
   if (held) {
-#pragma unroll
-    for (int j = 0; j < RN_REG; ++j) {
-      const int i = threadIdx.x + 256 * j;
-      xv[j] = i < H ? xr[i] : 0.f;
-      gv[j] = i < H ? to_f(g[i]) : 0.f;
+    if (live) {
+      xa = *(const f32x4*)(xr + 8 * t);
+      xb = *(const f32x4*)(xr + 8 * t + 4);
     }
 #pragma unroll
-    for (int j = 0; j < RN_REG; ++j)
-      if (threadIdx.x + 256 * j < H) ss = fmaf(xv[j], xv[j], ss);
+    for (int e = 0; e < 4; ++e) ss = fmaf(xa[e], xa[e], ss);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) ss = fmaf(xb[e], xb[e], ss);
   } else {
-    for (int i = threadIdx.x; i < H; i += 256) ss = fmaf(xr[i], xr[i], ss);
+    for (int c = t; c < nrun; c += 256) {
+      const f32x4 a = *(const f32x4*)(xr + 8 * c), b = *(const f32x4*)(xr + 8 * c + 4);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) ss = fmaf(a[e], a[e], ss);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) ss = fmaf(b[e], b[e], ss);
+    }
   }
   for (int off = 32; off > 0; off >>= 1) ss += __shfl_xor(ss, off);
-  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
+  if ((t & 63) == 0) red[t >> 6] = ss;
   __syncthreads();
   const float tot = (red[0] + red[1]) + (red[2] + red[3]);
   const float inv = 1.0f / sqrtf(tot / (float)H + eps);
-  if (held) {
-#pragma unroll
-    for (int j = 0; j < RN_REG; ++j) {
-      const int i = threadIdx.x + 256 * j;
-      if (i < H) out[(size_t)mrow * H + i] = from_f<T>(xv[j] * inv * gv[j]);
+  for (int c = t; c < nrun; c += 256) {
+    f32x4 a = xa, b = xb;
+    if (!held) {
+      a = *(const f32x4*)(xr + 8 * c);
+      b = *(const f32x4*)(xr + 8 * c + 4);
     }
-  } else {
-    for (int i = threadIdx.x; i < H; i += 256)
-      out[(size_t)mrow * H + i] = from_f<T>(xr[i] * inv * to_f(g[i]));
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+      orow[8 * c + e] = from_f<T>((e < 4 ? a[e] : b[e - 4]) * inv * to_f(g[8 * c + e]));
   }
 }
 
