@@ -490,10 +490,34 @@ __device__ __forceinline__ void ws_wait_vmcnt() {
 // blocks of CW kept columns): s_red holds NSP planes [NSP][MT][CB * 32] of
 // fp32 partial sums (the splits, or one plane already summed in order),
 // added in plane order as ((0 + p0) + p1) + ...; then EPI writes the tile.
+// EPI_F32_ADD: the residual values of the tile's whole 4-column runs, loaded
+// when the kernel starts (the tile is written only by its own epilogue), so
+// that the epilogue does not wait for them; unit u0 + tid of the epilogue's
+// loop is cpre[u0 / 256].
+template <int MT, int CB, int CW>
+__device__ __forceinline__ void ws_residual_prefetch(const GemmArgs& g, int tid, int m0, int cg, int si,
+                                                     f32x4* cpre) {
+  constexpr int TW = CB * 32;
+  constexpr int UNITS = MT * TW / 4;
+  const GemmSeg sg = g.seg[si];
+  const bool vec = (sg.n & 3) == 0;
+#pragma unroll
+  for (int u0 = 0; u0 < UNITS; u0 += 256) {
+    const int u = u0 + tid;
+    const int r = u / (TW / 4), cc = (u % (TW / 4)) * 4;
+    const int c = cc & 31;
+    const int row = m0 + r;
+    const int col = (cg * CB + (cc >> 5)) * CW + c - sg.n0;
+    cpre[u0 / 256] = f32x4{0.f, 0.f, 0.f, 0.f};
+    if (u < UNITS && row < g.M && c < CW && vec && col + 4 <= sg.n)
+      cpre[u0 / 256] = *(const f32x4*)((const float*)sg.C + (size_t)row * sg.n + col);
+  }
+}
+
 template <int MT, int CB, int CW, int EPI, int NSP>
 __device__ __forceinline__ void ws_epilogue(const GemmArgs& g, const float* __restrict__ s_red,
                                             int tid, int lane, int m0, int cg, int si, int NB,
-                                            bool rope) {
+                                            bool rope, const f32x4* cpre = nullptr) {
   constexpr int TW = CB * 32;
   // the tile's sums, 4 adjacent columns at a time: ((0 + p0) + p1) + ...
   // per element, the split planes in order
@@ -553,7 +577,7 @@ __device__ __forceinline__ void ws_epilogue(const GemmArgs& g, const float* __re
           *(u32x2*)((__bf16*)sg.C + o) =
               u32x2{__builtin_bit_cast(uint32_t, lo), __builtin_bit_cast(uint32_t, hi)};
         } else if constexpr (EPI == EPI_F32_ADD) {
-          f32x4 v = *(const f32x4*)((float*)sg.C + o);
+          f32x4 v = cpre ? cpre[u0 / 256] : *(const f32x4*)((float*)sg.C + o);
           v += t;
           *(f32x4*)((float*)sg.C + o) = v;
         } else {
@@ -701,6 +725,8 @@ __global__ void __launch_bounds__(256, WK ? 1 : 2) gemm_ws_kernel(GemmArgs g) {
   if (EPI != EPI_SWIGLU)
     while (si + 1 < g.nseg && cg * CB * CW >= g.seg[si + 1].n0) ++si;
   const bool rope = EPI == EPI_BF16 && g.rope_tab != nullptr && si < 2;
+  f32x4 cpre[(MT * CB * 32 / 4 + 255) / 256];
+  if constexpr (EPI == EPI_F32_ADD) ws_residual_prefetch<MT, CB, CW>(g, tid, m0, cg, si, cpre);
   const __bf16* wsrc[CB][WI];  // this lane's weight rows (block b, tile rows 8i + L/8)
 #pragma unroll
   for (int b = 0; b < CB; ++b)
@@ -823,7 +849,8 @@ __global__ void __launch_bounds__(256, WK ? 1 : 2) gemm_ws_kernel(GemmArgs g) {
             wvalid ? acc[a][b][i] : 0.f;
   }
   __syncthreads();
-  ws_epilogue<MT, CB, CW, EPI, GK_SPLITS>(g, s_red, tid, lane, m0, cg, si, NB, rope);
+  ws_epilogue<MT, CB, CW, EPI, GK_SPLITS>(g, s_red, tid, lane, m0, cg, si, NB, rope,
+                                         EPI == EPI_F32_ADD ? cpre : nullptr);
 }
 
 // gemm_ns_kernel<EPI, MT, NS>: the weight-streaming GEMM with the waves
