@@ -48,7 +48,17 @@ __global__ void embed_rows_kernel(const T* __restrict__ embed, int H, int vocab,
   else if (block) tok = block[(size_t)s * block_stride + (r - n_causal)];  // -1: [M]
   if (tok < 0 || tok > vocab) tok = vocab;
   const T* e = embed + (size_t)tok * H;
-  for (int i = threadIdx.x; i < H; i += blockDim.x) x[(size_t)mrow * H + i] = to_f(e[i]);
+  float* xr = x + (size_t)mrow * H;
+  if constexpr (sizeof(T) == 2) {
+    // runs of 8 (H is a multiple of 16): one 16-byte read, two 16-byte writes
+    for (int c = threadIdx.x; c < H / 8; c += blockDim.x) {
+      const bf16x8 v = *(const bf16x8*)(e + 8 * c);
+      *(f32x4*)(xr + 8 * c) = f32x4{(float)v[0], (float)v[1], (float)v[2], (float)v[3]};
+      *(f32x4*)(xr + 8 * c + 4) = f32x4{(float)v[4], (float)v[5], (float)v[6], (float)v[7]};
+    }
+  } else {
+    for (int i = threadIdx.x; i < H; i += blockDim.x) xr[i] = to_f(e[i]);
+  }
 }
 
 // Two-forward round, between the forwards (appendix "Self-Speculative
