@@ -669,7 +669,7 @@ __device__ __forceinline__ void ws_epilogue(const GemmArgs& g, const float* __re
   }
 }
 
-// NARROW: blocks of 16 output columns (few-row calls with few blocks, plain
+// NARROW (CWT 16 or 8): blocks of 16 or 8 output columns (few-row calls with few blocks, plain
 // epilogues): the products still span 32 columns, of which the second 16
 // read stale LDS rows and are discarded -- each kept column's arithmetic is
 // exactly the 32-column block's -- so the chip gets twice the workgroups
@@ -678,9 +678,10 @@ __device__ __forceinline__ void ws_epilogue(const GemmArgs& g, const float* __re
 // CB adjacent 32-column blocks, so one A chunk feeds CB blocks' products
 // (A is re-read once per CB blocks instead of once per block); per element
 // the arithmetic is the single block's.
-template <int MT, bool NARROW, int CB, int EPI, bool WK, bool FEW = false>
+template <int MT, int CWT, int CB, int EPI, bool WK, bool FEW = false>
 __global__ void __launch_bounds__(256, WK ? 1 : 2) gemm_ws_kernel(GemmArgs g) {
-  constexpr int CW = NARROW ? 16 : 32;     // output columns per block
+  constexpr int CW = CWT;                  // output columns per block (32, or 16 or 8: narrow)
+  constexpr bool NARROW = CWT < 32;
   // k per chunk.  WK (calls of at most one workgroup per CU): 64, so that a
   // copy takes whole 128-byte lines of a row (copies of half lines, the
   // other half taken by the next chunk, moved 1.6x fewer useful bytes per
@@ -689,7 +690,8 @@ __global__ void __launch_bounds__(256, WK ? 1 : 2) gemm_ws_kernel(GemmArgs g) {
   constexpr int KC = WK ? 64 : 32;
   constexpr int RB = KC * 2;               // bytes of a row in a chunk
   constexpr int RPI = 1024 / RB;           // rows per 1 KB copy
-  constexpr int WI = (NARROW ? 16 : 32) / RPI;   // weight copies per block and chunk
+  constexpr int WI = CW / RPI;             // weight copies per block and chunk
+  static_assert(CW % RPI == 0, "a block's weight rows fill whole copies");
   constexpr int RG = MT / 32;              // 32-row groups per wave
   // ring stages per wave: WK three (two for tiles of two blocks); otherwise
   // four for the few-row calls (64 KB), three for 64-row tiles of one block
@@ -1558,35 +1560,44 @@ static StepLayout step_layout(const dvs_model* m, int S, int n_causal, int n_mas
   return L;
 }
 
-template <int MT, bool NARROW, int CB, bool WK, bool FEW>
+template <int MT, int CWT, int CB, bool WK, bool FEW>
 static void launch_ws_epi(const GemmArgs& g, dim3 gr, hipStream_t st) {
   const dim3 blk(256);
   switch (g.epi) {
-    case EPI_BF16: hipLaunchKernelGGL((gemm_ws_kernel<MT, NARROW, CB, EPI_BF16, WK, FEW>), gr, blk, 0, st, g); break;
-    case EPI_F32: hipLaunchKernelGGL((gemm_ws_kernel<MT, NARROW, CB, EPI_F32, WK, FEW>), gr, blk, 0, st, g); break;
-    case EPI_F32_ADD: hipLaunchKernelGGL((gemm_ws_kernel<MT, NARROW, CB, EPI_F32_ADD, WK, FEW>), gr, blk, 0, st, g); break;
+    case EPI_BF16: hipLaunchKernelGGL((gemm_ws_kernel<MT, CWT, CB, EPI_BF16, WK, FEW>), gr, blk, 0, st, g); break;
+    case EPI_F32: hipLaunchKernelGGL((gemm_ws_kernel<MT, CWT, CB, EPI_F32, WK, FEW>), gr, blk, 0, st, g); break;
+    case EPI_F32_ADD: hipLaunchKernelGGL((gemm_ws_kernel<MT, CWT, CB, EPI_F32_ADD, WK, FEW>), gr, blk, 0, st, g); break;
     default:
-      if constexpr (!NARROW) {
-        if (g.epi == EPI_SWIGLU) hipLaunchKernelGGL((gemm_ws_kernel<MT, false, CB, EPI_SWIGLU, WK, FEW>), gr, blk, 0, st, g);
-        else hipLaunchKernelGGL((gemm_ws_kernel<MT, false, CB, EPI_ARGMAX, WK, FEW>), gr, blk, 0, st, g);
+      if constexpr (CWT == 32) {
+        if (g.epi == EPI_SWIGLU) hipLaunchKernelGGL((gemm_ws_kernel<MT, 32, CB, EPI_SWIGLU, WK, FEW>), gr, blk, 0, st, g);
+        else hipLaunchKernelGGL((gemm_ws_kernel<MT, 32, CB, EPI_ARGMAX, WK, FEW>), gr, blk, 0, st, g);
       }
       break;
   }
 }
 
-template <int MT, bool NARROW, int CB>
+template <int MT, int CWT, int CB>
 static void launch_ws_k(const GemmArgs& g, dim3 gr, bool wk, hipStream_t st) {
-  if constexpr (MT == 32) {
-    // calls whose rows fit one copy of A rows (8 rows in 64-k chunks, 16 in
-    // 32-k chunks)
-    if (g.M <= (wk ? 8 : 16)) {
-      if (wk) launch_ws_epi<MT, NARROW, CB, true, true>(g, gr, st);
-      else launch_ws_epi<MT, NARROW, CB, false, true>(g, gr, st);
-      return;
+  if constexpr (CWT == 8) {
+    // 8-column blocks: whole-line chunks only (one copy of 8 weight rows)
+    if constexpr (MT == 32) {
+      if (g.M <= 8) launch_ws_epi<MT, 8, CB, true, true>(g, gr, st);
+      else launch_ws_epi<MT, 8, CB, true, false>(g, gr, st);
     }
+    return;
+  } else {
+    if constexpr (MT == 32) {
+      // calls whose rows fit one copy of A rows (8 rows in 64-k chunks, 16
+      // in 32-k chunks)
+      if (g.M <= (wk ? 8 : 16)) {
+        if (wk) launch_ws_epi<MT, CWT, CB, true, true>(g, gr, st);
+        else launch_ws_epi<MT, CWT, CB, false, true>(g, gr, st);
+        return;
+      }
+    }
+    if (wk) launch_ws_epi<MT, CWT, CB, true, false>(g, gr, st);
+    else launch_ws_epi<MT, CWT, CB, false, false>(g, gr, st);
   }
-  if (wk) launch_ws_epi<MT, NARROW, CB, true, false>(g, gr, st);
-  else launch_ws_epi<MT, NARROW, CB, false, false>(g, gr, st);
 }
 
 static int launch_ws(GemmArgs& g, hipStream_t st) {
@@ -1595,8 +1606,16 @@ static int launch_ws(GemmArgs& g, hipStream_t st) {
   // blocks (twice the workgroups)
   const bool narrow = MT == 32 && (g.ncols + 31) / 32 < WS_NARROW_NB &&
                       (g.epi == EPI_BF16 || g.epi == EPI_F32 || g.epi == EPI_F32_ADD);
-  const int NB = narrow ? (g.ncols + 15) / 16 : (g.ncols + 31) / 32;
   g.n_rt = (g.M + MT - 1) / MT;
+  // narrow calls whose 8-column blocks still fit one workgroup per CU take
+  // 8-column blocks (whole-line chunks), else 16-column ones
+  int cw = 32;
+  if (narrow) cw = (long long)((g.ncols + 7) / 8) * g.n_rt <= device_cus() ? 8 : 16;
+  if (narrow) {
+    for (int i = 0; i < g.nseg; ++i)
+      if (g.seg[i].n0 % cw) cw = 16;
+  }
+  const int NB = (g.ncols + cw - 1) / cw;
   // wider calls: CB blocks per wave while that still gives the chip enough
   // workgroups, and every segment starts on a group boundary
   int CB = 1;
@@ -1642,10 +1661,11 @@ static int launch_ws(GemmArgs& g, hipStream_t st) {
     hipLaunchKernelGGL((gemm_nk_kernel<EPI_BF16, true>), gr, dim3(256), 0, st, g);
     return launch_status("draft_verify_step(gemm)");
   }
-  if (narrow) launch_ws_k<32, true, 1>(g, gr, wk, st);
-  else if (MT == 32) launch_ws_k<32, false, 1>(g, gr, wk, st);
-  else if (CB == 2) launch_ws_k<64, false, 2>(g, gr, wk, st);
-  else launch_ws_k<64, false, 1>(g, gr, wk, st);
+  if (cw == 8) launch_ws_k<32, 8, 1>(g, gr, wk, st);
+  else if (narrow) launch_ws_k<32, 16, 1>(g, gr, wk, st);
+  else if (MT == 32) launch_ws_k<32, 32, 1>(g, gr, wk, st);
+  else if (CB == 2) launch_ws_k<64, 32, 2>(g, gr, wk, st);
+  else launch_ws_k<64, 32, 1>(g, gr, wk, st);
   return launch_status("draft_verify_step(gemm)");
 }
 
