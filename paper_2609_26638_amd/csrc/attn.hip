@@ -486,6 +486,11 @@ __global__ void __launch_bounds__(NW * 64, 1) attn_bf16_kernel(AttnParams p) {
     first_segment = false;
     const int T = L + R;
     const int32_t* __restrict__ pt = p.page_table + (size_t)s * p.max_pages;
+    const int n_valid = (T + 15) >> 4;    // pages the sequence holds
+    // the page ids of the segment's first sub-range, loaded together with Q
+    // (one wait for both)
+    int pg_pre = 0;
+    if (tid < min(j1, j0 + SUB_TILES) * 4 - j0 * 4) pg_pre = pt[min(j0 * 4 + tid, n_valid - 1)];
 
     // ---- rows of this lane: Q fragments (B operand), visibility limit
     const int n = rt * RPW + w * 32 + l32;
@@ -625,7 +630,6 @@ __global__ void __launch_bounds__(NW * 64, 1) attn_bf16_kernel(AttnParams p) {
       }
     }
     // ---- the segment's tiles, in sub-ranges whose page ids fit in LDS
-    const int n_valid = (T + 15) >> 4;    // pages the sequence holds
     for (int ja = j0; ja < j1; ja += SUB_TILES) {
       const int jb = min(j1, ja + SUB_TILES);
       const int pg_lo = ja * 4;
@@ -636,7 +640,7 @@ __global__ void __launch_bounds__(NW * 64, 1) attn_bf16_kernel(AttnParams p) {
       for (int i = tid; i < pg_hi - pg_lo; i += NT) {
         // pages past the last one of the sequence (in the tile that runs
         // past T) repeat the last page: their keys are masked
-        int pg = pt[min(pg_lo + i, n_valid - 1)];
+        int pg = (ja == j0 && i == tid) ? pg_pre : pt[min(pg_lo + i, n_valid - 1)];
         if (pg < 0 || pg >= p.pool_pages) {
           pg = 0;
           s_flag[1] = 1;
@@ -749,22 +753,27 @@ __global__ void __launch_bounds__(NW * 64, 1) attn_bf16_kernel(AttnParams p) {
       return *(const f32x2*)(p.part_ml + part_slot(p.balanced, it, p.max_segs, wg0, c) * (NT * 2) +
                              (size_t)tid * 2);
     };
+    // SB segments per batch (eight where the registers allow), added in
+    // segment order: O += exp2(m_c - M) l_c (O_c / l_c), l += exp2(m_c - M) l_c.
+    // M, the largest m_c, is found in a first pass over the (m, l) pairs,
+    // or from the batch itself when one batch holds every segment (one
+    // round of loads instead of two).
+    constexpr int SB = NREG <= 48 ? 8 : 4;
     float M = -INFINITY;
-    for (int c0 = 0; c0 < nseg; c0 += 8) {
-      f32x2 mv[8];
+    if (nseg > SB) {
+      for (int c0 = 0; c0 < nseg; c0 += 8) {
+        f32x2 mv[8];
 #pragma unroll
-      for (int j = 0; j < 8; ++j) mv[j] = ml_of(min(c0 + j, nseg - 1));
+        for (int j = 0; j < 8; ++j) mv[j] = ml_of(min(c0 + j, nseg - 1));
 #pragma unroll
-      for (int j = 0; j < 8; ++j) M = fmaxf(M, mv[j][0]);   // repeats of the last segment are harmless
+        for (int j = 0; j < 8; ++j) M = fmaxf(M, mv[j][0]);   // repeats of the last segment are harmless
+      }
     }
-    const float Ms = (M == -INFINITY) ? 0.f : M;
+    float Ms = (M == -INFINITY) ? 0.f : M;
     f32x16 acc[DG];
 #pragma unroll
     for (int dg = 0; dg < DG; ++dg) acc[dg] = f32x16{};
     float lt = 0.f;
-    // SB segments per batch (eight where the registers allow), added in
-    // segment order: O += exp2(m_c - M) l_c (O_c / l_c), l += exp2(m_c - M) l_c
-    constexpr int SB = NREG <= 48 ? 8 : 4;
     for (int c0 = 0; c0 < nseg; c0 += SB) {
       u32x4 pv[SB][NWD];
       f32x2 mlc[SB];
@@ -777,6 +786,11 @@ __global__ void __launch_bounds__(NW * 64, 1) attn_bf16_kernel(AttnParams p) {
 #pragma unroll
         for (int jw = 0; jw < NWD; ++jw) pv[b][jw] = *(const u32x4*)(src + jw * (NT * 4));
         mlc[b] = ml_of(c);
+      }
+      if (nseg <= SB) {
+#pragma unroll
+        for (int b = 0; b < SB; ++b) M = fmaxf(M, mlc[b][0]);   // repeats of the last segment are harmless
+        Ms = (M == -INFINITY) ? 0.f : M;
       }
 #pragma unroll
       for (int b = 0; b < SB; ++b) {
