@@ -303,6 +303,53 @@ def test_bf16_wide_step_matches_oracle_replay():
     _states_equal(st2, replay)
 
 
+@pytest.mark.parametrize("S", [8, 5])
+def test_bf16_ar_steps_match_oracle_replay(S):
+    """Greedy AR steps of a two-layer bf16 model (one row per sequence)
+    through the few-row decode GEMM paths: Q|K|V of 32/4 heads of 64 in
+    16-column blocks with the rotary epilogue, the O and down projections in
+    8-column blocks, only the first rows of A copied per chunk, gate|up with
+    SwiGLU, and the LM head (vocabulary 8200, 257 blocks, the last 8 columns
+    wide) with its fused top-1. Three steps in a row: logits close to the
+    float64 oracle on the same state; the top-1 of the fused LM-head
+    epilogue equals the top-1 of the logits; the commit replayed through the
+    oracle bit for bit, which also keeps both sides on the same state."""
+    L = [41, 77, 130, 199, 256, 301, 350, 397][:S]
+    w = synth.make_model_weights(13, 8200, 256, 32, 4, 64, 2, 2304, std=0.08)
+    pools = [synth.make_attn_inputs(13 + 100 * l, S, L, 16, 16, 32, 4, 64, "bf16", std=0.5,
+                                    scatter=True, extra_pages=64) for l in range(2)]
+    kps, vps = [p.k_pool for p in pools], [p.v_pool for p in pools]
+    st_host = pools[0].state.copy()
+    st_host.boundary[:] = np.random.default_rng(4).integers(0, w.V, size=S)
+    om = OracleModel(_bf16_weights(w), kps, vps, bf16_bits=True)
+    dm = dvs.DeviceModel(w, _dev_pools(kps, "bf16"), _dev_pools(vps, "bf16"), "bf16")
+    st = dvs.DeviceState(st_host)
+    st2 = dvs.DeviceState(st_host)
+    ref = st_host.copy()
+    for step in range(3):
+        logits_ref, _, err = om.ar_step(ref)
+        assert err == 0
+        logits = torch.empty((S, w.V), dtype=torch.float32, device="cuda")
+        am = torch.empty((S, 1), dtype=torch.int32, device="cuda")
+        am2 = torch.empty((S, 1), dtype=torch.int32, device="cuda")
+        before = st.to_host(st_host)
+        dvs.draft_verify_step(dm, st, 1, 0, logits_out=logits, argmax_out=am, chunk_keys=256)
+        dvs.draft_verify_step(dm, st2, 1, 0, argmax_out=am2, chunk_keys=256)
+        torch.cuda.synchronize()
+        lg = logits.cpu().numpy().reshape(S, 1, w.V).astype(np.float64)
+        assert max_rel_err(lg, logits_ref) <= 5e-2, step
+        am_gpu = am.cpu().numpy()
+        np.testing.assert_array_equal(am_gpu, od.top1_rows(lg))
+        np.testing.assert_array_equal(am2.cpu().numpy(), am_gpu)
+        # the oracle's own commit used its top-1; replay the GPU's on the
+        # state before the step, and carry the oracle on with that state
+        replay = before.copy()
+        assert od.kv_commit(replay, np.zeros(S, dtype=np.int32), am_gpu, 1, 0) == 0
+        _states_equal(st, replay)
+        _states_equal(st2, replay)
+        ref = replay
+
+
 def _embed_prefix_f64(w_bits, vision, prompt):
     """Oracle-side prefix rows: vision vectors, then embedding rows of the prompt."""
     emb = synth.bf16_to_f64(w_bits.embed)
