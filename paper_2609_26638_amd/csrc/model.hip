@@ -423,7 +423,7 @@ __global__ void __launch_bounds__(256) gemm_bf16_kernel(const __bf16* __restrict
 // ---------------------------------------------------------------------------
 constexpr int GK_SPLITS = 4;        // logical K splits when K % 256 == 0
 constexpr int WS_MAX_ROWS = 256;    // calls up to this many rows use gemm_ws_kernel
-constexpr int WS_NARROW_NB = 128;   // few-row calls below this many 32-column blocks take 16-column blocks
+constexpr int WS_NARROW_NB = 128;   // few-row calls below this many 32-column blocks take narrow blocks
 constexpr int WS_WIDE_MIN_WG = 256; // 64-row calls take 2 blocks per wave while the grid keeps this many
 
 static int gemm_ksplit(int K) { return K % (64 * GK_SPLITS) == 0 ? GK_SPLITS : 1; }
@@ -669,11 +669,12 @@ __device__ __forceinline__ void ws_epilogue(const GemmArgs& g, const float* __re
   }
 }
 
-// NARROW (CWT 16 or 8): blocks of 16 or 8 output columns (few-row calls with few blocks, plain
-// epilogues): the products still span 32 columns, of which the second 16
-// read stale LDS rows and are discarded -- each kept column's arithmetic is
-// exactly the 32-column block's -- so the chip gets twice the workgroups
-// and each streams half the weights.
+// Narrow blocks (CWT 16 or 8; few-row calls with few blocks, plain
+// epilogues): only CWT weight rows are copied per chunk; the products still
+// span 32 columns, of which the columns past CWT read stale LDS rows and are
+// discarded -- each kept column's arithmetic is exactly the 32-column
+// block's -- so the chip gets two or four times the workgroups and each
+// streams a half or a quarter of the weights.
 // CB: column blocks per wave (wider calls): each wave computes its split for
 // CB adjacent 32-column blocks, so one A chunk feeds CB blocks' products
 // (A is re-read once per CB blocks instead of once per block); per element
@@ -1602,8 +1603,8 @@ static void launch_ws_k(const GemmArgs& g, dim3 gr, bool wk, hipStream_t st) {
 
 static int launch_ws(GemmArgs& g, hipStream_t st) {
   const int MT = g.M <= 32 ? 32 : 64;
-  // few-row calls with few 32-column blocks and a plain epilogue: 16-column
-  // blocks (twice the workgroups)
+  // few-row calls with few 32-column blocks and a plain epilogue: narrow
+  // blocks of 16 or 8 columns (more workgroups)
   const bool narrow = MT == 32 && (g.ncols + 31) / 32 < WS_NARROW_NB &&
                       (g.epi == EPI_BF16 || g.epi == EPI_F32 || g.epi == EPI_F32_ADD);
   g.n_rt = (g.M + MT - 1) / MT;
