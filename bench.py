@@ -37,6 +37,7 @@ MFMA_PEAK_TFLOPS = 2500.0   # dense bf16 matrix cores (no sparsity)
 COUNTERS = os.path.join(ROOT, "profiles", "attn_long_document_counters.json")
 ATTN_SOURCES = [os.path.join(ROOT, "paper_2609_26638_amd", "csrc", f)
                 for f in ("attn.hip", "dvs_common.h")]
+STACK_COUNTERS = os.path.join(ROOT, "profiles", "decoder_stack_fused_counters.json")
 
 
 def _code_only(text: str) -> str:
@@ -51,6 +52,17 @@ def attn_source_hash() -> str:
     h = hashlib.sha256()
     for f in ATTN_SOURCES:
         h.update(_code_only(open(f).read()).encode())
+    return h.hexdigest()[:16]
+
+
+def stack_source_hash() -> str:
+    """Hash of every kernel source (code only): the decoder stack's counters
+    stay valid while none of them changes."""
+    d = os.path.join(ROOT, "paper_2609_26638_amd", "csrc")
+    h = hashlib.sha256()
+    for f in sorted(os.listdir(d)):
+        if f.endswith((".hip", ".h")):
+            h.update(_code_only(open(os.path.join(d, f)).read()).encode())
     return h.hexdigest()[:16]
 
 
@@ -287,6 +299,7 @@ def run_decoder_stack(args):
     # the two-forward round keeps d_1..d_B in the draft array
     wide = si.state.copy()
     wide.draft = np.zeros((wide.draft.shape[0], si.B), np.int32)
+    kv_step_bytes = w.n_layers * w.Hkv * w.D * 2 * 2      # KV bytes per cached token and forward
 
     def step(st, mode, nc, nm):
         """One step of the mode; returns the forwards it ran."""
@@ -308,6 +321,33 @@ def run_decoder_stack(args):
         dvs.draft_verify_step(dm, st, nc, nm, chunk_keys=chunk)
         return 1
 
+    if args.profile_stack:
+        # counter collection: prefill, warmup, then `steps` steps of one mode
+        # (each step's first launch is embed_rows_kernel), then a 1 GiB
+        # device-to-device copy that calibrates FETCH_SIZE / WRITE_SIZE
+        # (the copy's buffers are filled before the steps, and nothing runs
+        # between the last step and the copy)
+        mode = args.profile_stack
+        nc, nm = {"ar": (1, 0), "fused": (si.B, si.B)}[mode]
+        src = torch.ones(1 << 30, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        st = dvs.DeviceState(si.state)
+        dvs.prefill(dm, st, si.P, si.B, prefix_tokens=torch.from_numpy(si.prefix_tokens()).cuda(),
+                    x_prefix=torch.from_numpy(si.x_prefix()).cuda(), chunk_keys=chunk)
+        for _ in range(args.warmup):
+            step(st, mode, nc, nm)
+        kv0 = int(st.kv_len.sum().item())
+        torch.cuda.synchronize()
+        for _ in range(args.steps):
+            step(st, mode, nc, nm)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        kv_mean = (kv0 + int(st.kv_len.sum().item())) / 2
+        print(json.dumps({"profile_stack": mode, "steps": args.steps, "marker": "embed_rows_kernel",
+                          "step_algorithmic_bytes": int(weight_bytes + kv_mean * kv_step_bytes),
+                          "weight_bytes": weight_bytes, "copy_bytes": 1 << 30,
+                          "src_hash": stack_source_hash(), "err": int(st.err.item())}), flush=True)
+        return
     # the multi-draft step's window is B + B*B rows: a state whose pages cover it
     md_state = synth.stack_state(3, si.state.kv_len.shape[0], si.P, si.B, si.max_new,
                                  si.B + si.B * si.B)
@@ -366,7 +406,7 @@ def run_decoder_stack(args):
             graph = {"ms_per_step": round(gms, 4),
                      "tokens_per_s": round(gtoks / (gms * args.steps / 1e3), 1)}
             del g
-        step_bytes = fwd * (weight_bytes + kv_mean * w.n_layers * w.Hkv * w.D * 2 * 2)
+        step_bytes = fwd * (weight_bytes + kv_mean * kv_step_bytes)
         res[mode] = {"ms_per_step": round(ms, 4), "tokens_per_step": round(toks / args.steps, 3),
                      "tokens_per_s": round(toks / (ms * args.steps / 1e3), 1),
                      "forwards_per_step": round(fwd, 3),
@@ -380,6 +420,13 @@ def run_decoder_stack(args):
             res[mode]["tokens_per_denoising_forward"] = round(
                 toks / st.kv_len.shape[0] / (n_fwd - args.steps), 3)
     f = res["fused"]
+    # HBM bytes per fused step from the counters (profiles/), while every
+    # kernel source is the one they were taken on
+    traffic = None
+    if os.path.exists(STACK_COUNTERS):
+        c = json.load(open(STACK_COUNTERS))
+        if c.get("src_hash") == stack_source_hash():
+            traffic = int(c["bytes_per_step"])
     line = {
         "metric": "committed tokens/sec per GPU, 16-layer decoder stack (self-speculative fused step)",
         "value": f["tokens_per_s"], "unit": "committed tokens/s", "n_gpus": 1,
@@ -390,7 +437,7 @@ def run_decoder_stack(args):
                                "SwiGLU 4096, vocab 65536, 8 sequences, 1024 vision + 64 prompt "
                                "tokens, B=16", "chunk_keys": chunk},
         "roofline": {"bound": "hbm", "achieved": f["hbm_gbs"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(f["hbm_gbs"] / HBM_PEAK_GBS, 4), "traffic": None,
+                     "frac": round(f["hbm_gbs"] / HBM_PEAK_GBS, 4), "traffic": traffic,
                      "kernel": "whole fused step (weights once + KV per layer)",
                      "algorithmic_bytes": f["hbm_bytes_per_step"]},
         "fused_hip_graph": res["fused"].get("hip_graph"),
@@ -431,6 +478,10 @@ def main():
                     help="counter-collection mode: N attention launches on the workload, "
                          "then one 1 GiB device-to-device copy (calibrates FETCH_SIZE / "
                          "WRITE_SIZE against known bytes); prints no bench line")
+    ap.add_argument("--profile-stack", choices=["ar", "fused"], default=None,
+                    help="counter-collection mode for --workload decoder-stack: prefill, "
+                         "--warmup then --steps steps of one mode, then one 1 GiB "
+                         "device-to-device copy; prints no bench line")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))

@@ -15,6 +15,12 @@
   dispatches.  The result is written as JSON next to the source hash the
   bench compares against, so that a changed kernel does not report stale
   traffic.
+* ``steps``: HBM bytes per step of the decoder stack, per kernel, from a
+  ``--pmc FETCH_SIZE`` run and a ``--pmc WRITE_SIZE`` run of ``bench.py
+  --workload decoder-stack --profile-stack MODE``: the dispatches of the last
+  ``steps`` steps (each starts with the marker kernel; the steps end at the
+  run's final 1 GiB copy), calibrated against that copy as in ``traffic``; written as JSON (with the
+  kernel-source hash the bench compares against) and as a markdown table.
 * ``matrix``: matrix-core and vector-ALU use of one kernel from a ``--pmc``
   run with GRBM_GUI_ACTIVE, SQ_VALU_MFMA_BUSY_CYCLES, SQ_VALU_MFMA_COEXEC_CYCLES,
   SQ_ACTIVE_INST_VALU and SQ_INSTS_VALU_MFMA_MOPS_BF16: the clock (GPU busy
@@ -100,14 +106,14 @@ def per_dispatch(counter_dir, counter):
     return acc
 
 
-def _meta(path):
+def _meta(path, key="profile_attn"):
     meta = None
     for line in open(path):
         line = line.strip()
-        if line.startswith("{") and "profile_attn" in line:
+        if line.startswith("{") and key in line:
             meta = json.loads(line)
     if meta is None:
-        raise SystemExit("no profile_attn line in " + path)
+        raise SystemExit(f"no {key} line in " + path)
     return meta
 
 
@@ -134,6 +140,30 @@ def traffic(fetch_dir, write_dir, kernel, copy_bytes):
         scale = copy_bytes / (copy_kib * 1024.0)
         out[counter] = {"kib_per_dispatch": vals, "copy_kib": copy_kib, "scale": scale,
                         "bytes_per_dispatch": sum(vals) / len(vals) * 1024.0 * scale}
+    return out
+
+
+def steps(fetch_dir, write_dir, marker, n_steps, copy_bytes):
+    """Per-kernel calibrated bytes of the last n_steps steps (a step starts
+    with the marker kernel): {counter: (scale, {kernel: [calls, bytes]})}."""
+    out = {}
+    for counter, d in (("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)):
+        disp = list(per_dispatch(d, counter).values())
+        copies = [v for n, v in disp if "copyBuffer" in n]
+        if not copies:
+            raise ValueError(f"{counter}: no calibration copy")
+        scale = copy_bytes / (max(copies) * 1024.0)
+        marks = [i for i, (n, _) in enumerate(disp) if marker in n]
+        if len(marks) < n_steps:
+            raise ValueError(f"{counter}: {len(marks)} steps found, {n_steps} asked")
+        agg = collections.OrderedDict()
+        for n, v in disp[marks[-n_steps]:]:
+            if "copyBuffer" in n:
+                break                      # the steps end at the calibration copy
+            e = agg.setdefault(n, [0, 0.0])
+            e[0] += 1
+            e[1] += v * 1024.0 * scale
+        out[counter] = (scale, agg)
     return out
 
 
@@ -198,6 +228,14 @@ def main():
     t.add_argument("--kernel", default="attn_bf16")
     t.add_argument("--command", required=True)
     t.add_argument("--out", required=True)
+    st = sub.add_parser("steps")
+    st.add_argument("--fetch", required=True, help="output directory of the FETCH_SIZE run")
+    st.add_argument("--write", required=True, help="output directory of the WRITE_SIZE run")
+    st.add_argument("--meta", required=True, help="the JSON line bench.py --profile-stack printed")
+    st.add_argument("--title", required=True)
+    st.add_argument("--command", required=True)
+    st.add_argument("--out-json", required=True)
+    st.add_argument("--out-md", required=True)
     m = sub.add_parser("matrix")
     m.add_argument("--pmc", required=True, help="output directory of the --pmc run")
     m.add_argument("--meta", required=True, help="the JSON line bench.py --profile-attn printed")
@@ -205,6 +243,46 @@ def main():
     m.add_argument("--command", required=True)
     m.add_argument("--out", required=True)
     a = ap.parse_args()
+    if a.cmd == "steps":
+        meta = _meta(a.meta, "profile_stack")
+        n = meta["steps"]
+        tr = steps(a.fetch, a.write, meta["marker"], n, meta["copy_bytes"])
+        fs, fa = tr["FETCH_SIZE"]
+        ws, wa = tr["WRITE_SIZE"]
+        kernels = []
+        for name, (calls, fb) in fa.items():
+            wb = wa.get(name, [calls, 0.0])[1]
+            kernels.append({"kernel": name, "calls_per_step": calls / n,
+                            "fetch_bytes_per_call": fb / calls, "write_bytes_per_call": wb / calls,
+                            "bytes_per_step": (fb + wb) / n})
+        kernels.sort(key=lambda k: -k["bytes_per_step"])
+        total = sum(k["bytes_per_step"] for k in kernels)
+        res = {"mode": meta["profile_stack"], "src_hash": meta["src_hash"], "command": a.command,
+               "steps": n, "step_algorithmic_bytes": meta["step_algorithmic_bytes"],
+               "bytes_per_step": total,
+               "traffic_over_algorithmic": total / meta["step_algorithmic_bytes"],
+               "fetch_scale": fs, "write_scale": ws, "kernels": kernels}
+        with open(a.out_json, "w") as f:
+            json.dump(res, f, indent=1)
+            f.write("\n")
+        md = [f"# {a.title}", "", "Command (each counter in a run of its own):", "", "```",
+              a.command, "```", "",
+              f"FETCH_SIZE and WRITE_SIZE per dispatch over the last {n} steps, each scaled so "
+              f"that the run's final 1 GiB copy reads and writes 1 GiB (FETCH_SIZE x{fs:.3f}, "
+              f"WRITE_SIZE x{ws:.3f}).", "",
+              f"Per step: {total / 1e6:.1f} MB against {meta['step_algorithmic_bytes'] / 1e6:.1f} MB "
+              f"algorithmic (all weights once plus each layer's KV cache): "
+              f"{total / meta['step_algorithmic_bytes']:.3f}x.", "",
+              "| kernel | calls/step | read MB/call | written MB/call | MB/step |",
+              "|---|---|---|---|---|"]
+        for k in kernels:
+            name = k["kernel"] if len(k["kernel"]) <= 70 else k["kernel"][:67] + "..."
+            md.append(f"| `{name}` | {k['calls_per_step']:.1f} | {k['fetch_bytes_per_call'] / 1e6:.3f} | "
+                      f"{k['write_bytes_per_call'] / 1e6:.3f} | {k['bytes_per_step'] / 1e6:.1f} |")
+        with open(a.out_md, "w") as f:
+            f.write("\n".join(md) + "\n")
+        print(json.dumps({k: v for k, v in res.items() if k != "kernels"}))
+        return
     if a.cmd == "matrix":
         meta = _meta(a.meta)
         per = matrix(a.pmc, a.kernel, meta.get("attn_algorithmic_flops"))
