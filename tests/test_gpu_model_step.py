@@ -303,7 +303,7 @@ def test_bf16_wide_step_matches_oracle_replay():
     _states_equal(st2, replay)
 
 
-@pytest.mark.parametrize("S", [8, 5])
+@pytest.mark.parametrize("S", [8, 5, 3, 1])
 def test_bf16_ar_steps_match_oracle_replay(S):
     """Greedy AR steps of a two-layer bf16 model (one row per sequence)
     through the few-row decode GEMM paths: Q|K|V of 32/4 heads of 64 in
