@@ -303,7 +303,7 @@ def test_bf16_wide_step_matches_oracle_replay():
     _states_equal(st2, replay)
 
 
-@pytest.mark.parametrize("S", [8, 5, 3, 1])
+@pytest.mark.parametrize("S", [8, 5, 3, 1, 12, 20])
 def test_bf16_ar_steps_match_oracle_replay(S):
     """Greedy AR steps of a two-layer bf16 model (one row per sequence)
     through the few-row decode GEMM paths: Q|K|V of 32/4 heads of 64 in
@@ -313,8 +313,10 @@ def test_bf16_ar_steps_match_oracle_replay(S):
     wide) with its fused top-1. Three steps in a row: logits close to the
     float64 oracle on the same state; the top-1 of the fused LM-head
     epilogue equals the top-1 of the logits; the commit replayed through the
-    oracle bit for bit, which also keeps both sides on the same state."""
-    L = [41, 77, 130, 199, 256, 301, 350, 397][:S]
+    oracle bit for bit, which also keeps both sides on the same state.
+    12 and 20 sequences: the whole-line launches copy every row of A (the
+    LM head still only the first 16 at 12); 20 rows, no first-rows copies."""
+    L = ([41, 77, 130, 199, 256, 301, 350, 397] + [60 + 37 * i for i in range(12)])[:S]
     w = synth.make_model_weights(13, 8200, 256, 32, 4, 64, 2, 2304, std=0.08)
     pools = [synth.make_attn_inputs(13 + 100 * l, S, L, 16, 16, 32, 4, 64, "bf16", std=0.5,
                                     scatter=True, extra_pages=64) for l in range(2)]
