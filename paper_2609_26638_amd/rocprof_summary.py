@@ -21,6 +21,10 @@
   ``steps`` steps (each starts with the marker kernel; the steps end at the
   run's final 1 GiB copy), calibrated against that copy as in ``traffic``; written as JSON (with the
   kernel-source hash the bench compares against) and as a markdown table.
+* ``step-times``: per-kernel durations over the same step window, from a
+  ``--kernel-trace`` run of ``bench.py --workload decoder-stack
+  --profile-stack MODE``: calls and average microseconds per step, and the
+  step's span and busy time.
 * ``matrix``: matrix-core and vector-ALU use of one kernel from a ``--pmc``
   run with GRBM_GUI_ACTIVE, SQ_VALU_MFMA_BUSY_CYCLES, SQ_VALU_MFMA_COEXEC_CYCLES,
   SQ_ACTIVE_INST_VALU and SQ_INSTS_VALU_MFMA_MOPS_BF16: the clock (GPU busy
@@ -153,18 +157,42 @@ def steps(fetch_dir, write_dir, marker, n_steps, copy_bytes):
         if not copies:
             raise ValueError(f"{counter}: no calibration copy")
         scale = copy_bytes / (max(copies) * 1024.0)
-        marks = [i for i, (n, _) in enumerate(disp) if marker in n]
+        # the steps end at the calibration copy (the largest one; the
+        # runtime's small copies for host reads come after it)
+        end = max((i for i, (n, _) in enumerate(disp) if "copyBuffer" in n), key=lambda i: disp[i][1])
+        marks = [i for i, (n, _) in enumerate(disp[:end]) if marker in n]
         if len(marks) < n_steps:
             raise ValueError(f"{counter}: {len(marks)} steps found, {n_steps} asked")
         agg = collections.OrderedDict()
-        for n, v in disp[marks[-n_steps]:]:
-            if "copyBuffer" in n:
-                break                      # the steps end at the calibration copy
+        for n, v in disp[marks[-n_steps]:end]:
             e = agg.setdefault(n, [0, 0.0])
             e[0] += 1
             e[1] += v * 1024.0 * scale
         out[counter] = (scale, agg)
     return out
+
+
+def step_times(trace_dir, marker, n_steps):
+    """Kernel-trace durations of the last n_steps steps before the calibration
+    copy: (span_us, [(kernel, calls, total_us)] by total time)."""
+    rows = sorted(_rows(trace_dir, "kernel_trace.csv"), key=lambda r: int(r["Start_Timestamp"]))
+    # up to the calibration copy: the longest copy (the runtime's small copies
+    # for host reads come after it)
+    dur = lambda r: int(r["End_Timestamp"]) - int(r["Start_Timestamp"])
+    copies = [i for i, r in enumerate(rows) if "copyBuffer" in r["Kernel_Name"]]
+    if copies:
+        rows = rows[:max(copies, key=lambda i: dur(rows[i]))]
+    marks = [i for i, r in enumerate(rows) if marker in r["Kernel_Name"]]
+    if len(marks) < n_steps:
+        raise ValueError(f"{len(marks)} steps found, {n_steps} asked")
+    sel = rows[marks[-n_steps]:]
+    agg = collections.OrderedDict()
+    for r in sel:
+        e = agg.setdefault(r["Kernel_Name"], [0, 0.0])
+        e[0] += 1
+        e[1] += (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+    span = (int(sel[-1]["End_Timestamp"]) - int(sel[0]["Start_Timestamp"])) / 1e3
+    return span, sorted(((k, c, t) for k, (c, t) in agg.items()), key=lambda x: -x[2])
 
 
 def per_dispatch_instances(counter_dir):
@@ -236,6 +264,12 @@ def main():
     st.add_argument("--command", required=True)
     st.add_argument("--out-json", required=True)
     st.add_argument("--out-md", required=True)
+    tt = sub.add_parser("step-times")
+    tt.add_argument("--trace", required=True, help="output directory of the --kernel-trace run")
+    tt.add_argument("--meta", required=True, help="the JSON line bench.py --profile-stack printed")
+    tt.add_argument("--title", required=True)
+    tt.add_argument("--command", required=True)
+    tt.add_argument("--out", required=True)
     m = sub.add_parser("matrix")
     m.add_argument("--pmc", required=True, help="output directory of the --pmc run")
     m.add_argument("--meta", required=True, help="the JSON line bench.py --profile-attn printed")
@@ -243,6 +277,25 @@ def main():
     m.add_argument("--command", required=True)
     m.add_argument("--out", required=True)
     a = ap.parse_args()
+    if a.cmd == "step-times":
+        meta = _meta(a.meta, "profile_stack")
+        n = meta["steps"]
+        span, ks = step_times(a.trace, meta["marker"], n)
+        busy = sum(t for _, _, t in ks) / n
+        md = [f"# {a.title}", "", "Command:", "", "```", a.command, "```", "",
+              f"Kernel-trace durations over the last {n} steps (each starts with "
+              f"`{meta['marker']}`; the run ends with a calibration copy, outside the steps). "
+              f"Per step: {span / n:.1f} us from the first launch's start to the last one's end "
+              f"under the tracer, {busy:.1f} us of kernel time, {sum(c for _, c, _ in ks) / n:.0f} "
+              "launches.", "",
+              "| kernel | calls/step | avg us | us/step |", "|---|---|---|---|"]
+        for k, c, t in ks:
+            name = k if len(k) <= 70 else k[:67] + "..."
+            md.append(f"| `{name}` | {c / n:.1f} | {t / c:.2f} | {t / n:.1f} |")
+        with open(a.out, "w") as f:
+            f.write("\n".join(md) + "\n")
+        print(f"span/step {span / n:.1f} us, busy/step {busy:.1f} us")
+        return
     if a.cmd == "steps":
         meta = _meta(a.meta, "profile_stack")
         n = meta["steps"]

@@ -28,12 +28,14 @@ def _write_counters(d, counter, dispatches):
 
 
 def _stack_run(fetch_scale_kib):
-    """Two warmup steps and three measured steps of two kernels, a fill of
-    the calibration buffer before them, a stray kernel after the copy."""
+    """Two warmup steps and three measured steps of three kernels, a fill of
+    the calibration buffer and a small runtime copy (a host read) before
+    them, a kernel and another small copy after the calibration copy."""
     step = [("embed_rows_kernel", [1.0]), ("gemm_ws_kernel", [10.0, 10.0]),
             ("attn_bf16_kernel", [4.0])]
-    return ([("fill_kernel", [999.0])] + step * 5 +
-            [("__amd_rocclr_copyBuffer", [fetch_scale_kib]), ("reduce_kernel", [7.0])])
+    return ([("fill_kernel", [999.0])] + step * 2 + [("__amd_rocclr_copyBuffer", [0.5])] +
+            step * 3 + [("__amd_rocclr_copyBuffer", [fetch_scale_kib]), ("reduce_kernel", [7.0]),
+                        ("__amd_rocclr_copyBuffer", [0.5])])
 
 
 def test_traffic_calibrates_against_the_copy(tmp_path):
@@ -86,6 +88,27 @@ def test_steps_command_writes_json_and_table(tmp_path):
     assert res["src_hash"] == "abc"
     assert [k["kernel"] for k in res["kernels"]][0] == "gemm_ws_kernel"
     assert "| `gemm_ws_kernel` | 1.0 |" in md.read_text()
+
+
+def test_step_times_window(tmp_path):
+    d = tmp_path / "t"
+    os.makedirs(d)
+    # (kernel, start us, duration us): warmup step, copy for a host read,
+    # two measured steps, the calibration copy, a later small copy
+    seq = [("embed_rows_kernel", 0, 1), ("gemm_ws_kernel", 2, 5),
+           ("__amd_rocclr_copyBuffer", 10, 1),
+           ("embed_rows_kernel", 20, 1), ("gemm_ws_kernel", 22, 5),
+           ("embed_rows_kernel", 30, 1), ("gemm_ws_kernel", 32, 7),
+           ("__amd_rocclr_copyBuffer", 50, 400), ("__amd_rocclr_copyBuffer", 460, 2)]
+    with open(d / "run_kernel_trace.csv", "w", newline="") as f:
+        w = csv.writer(f)
+        w.writerow(["Kernel_Name", "Start_Timestamp", "End_Timestamp"])
+        for name, t, dt in seq:
+            w.writerow([name, t * 1000, (t + dt) * 1000])
+    span, ks = rs.step_times(str(d), "embed_rows", 2)
+    assert span == pytest.approx(19.0)                 # 20 us .. 39 us
+    assert ks[0] == ("gemm_ws_kernel", 2, pytest.approx(12.0))
+    assert [k for k, _, _ in ks] == ["gemm_ws_kernel", "embed_rows_kernel"]
 
 
 def test_source_hashes_ignore_comments():
