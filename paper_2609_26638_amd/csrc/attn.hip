@@ -738,11 +738,16 @@ __global__ void __launch_bounds__(NW * 64, 1) attn_bf16_kernel(AttnParams p) {
     __syncthreads();
     // The count-in is a release (the partials written by every thread of the
     // workgroup, ordered before it by the barrier, become visible at agent
-    // scope first) and an acquire (the last workgroup's loads below see every
-    // other workgroup's partials; the barrier extends it to all its threads).
-    if (tid == 0)
-      s_flag[0] = (__hip_atomic_fetch_add(&p.counters[it], 1, __ATOMIC_ACQ_REL,
-                                          __HIP_MEMORY_SCOPE_AGENT) == nseg - 1);
+    // scope first); the count-ins form one release sequence, so the last
+    // workgroup's acquire fence after its own count-in makes every other
+    // workgroup's partials visible to its loads below (the barrier extends it
+    // to all its threads).  Only that workgroup pays for the acquire.
+    if (tid == 0) {
+      const bool last = __hip_atomic_fetch_add(&p.counters[it], 1, __ATOMIC_RELEASE,
+                                               __HIP_MEMORY_SCOPE_AGENT) == nseg - 1;
+      if (last) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+      s_flag[0] = last;
+    }
     __syncthreads();
     if (!s_flag[0]) continue;
     if (tid == 0) __hip_atomic_store(&p.counters[it], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -1268,9 +1273,14 @@ __global__ void __launch_bounds__(NP * 128, 1) attn_bf16_pc_kernel(AttnParams p)
         }
         wait_vmcnt<0>();
         __syncthreads();                                     // F2
-        if (tid == 0)
-          s_flag[0] = (__hip_atomic_fetch_add(&p.counters[it], 1, __ATOMIC_ACQ_REL,
-                                              __HIP_MEMORY_SCOPE_AGENT) == nseg - 1);
+        // release count-in; the acquire fence only in the last workgroup
+        // (the count-ins form one release sequence)
+        if (tid == 0) {
+          const bool last = __hip_atomic_fetch_add(&p.counters[it], 1, __ATOMIC_RELEASE,
+                                                   __HIP_MEMORY_SCOPE_AGENT) == nseg - 1;
+          if (last) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+          s_flag[0] = last;
+        }
         __syncthreads();                                     // F3
         if (s_flag[0]) {
           if (tid == 0) __hip_atomic_store(&p.counters[it], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
