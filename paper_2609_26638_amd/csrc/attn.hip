@@ -37,11 +37,12 @@
 //     workgroup takes an equal contiguous share, so the grid finishes together
 //     whatever the length mix; only shares that split an item publish
 //     partials.
-//   A split item's partials ((m, l) in fp32; O in fp32, or as O/l in bf16 in
-//   the producer/consumer kernel) are merged in segment order by the last
-//   workgroup to count in; the count-in is an agent-scope acquire-release
-//   atomic add on the item's counter, which orders every workgroup's partial
-//   stores before the merging workgroup's loads.
+//   A split item's partials ((m, l) in fp32; O/l in bf16) are merged in
+//   segment order by the last workgroup to count in; the count-in is an
+//   agent-scope release atomic add on the item's counter, and the workgroup
+//   that counts in last takes an agent-scope acquire fence: the count-ins
+//   form one release sequence, so every workgroup's partial stores are
+//   ordered before the merging workgroup's loads.
 //
 // fp32 path: a plain per-(sequence, row, head) workgroup, fp32 throughout.
 #include <math.h>
