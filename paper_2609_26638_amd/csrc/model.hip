@@ -34,13 +34,41 @@ template <typename T> __device__ __forceinline__ T from_f(float v);
 template <> __device__ __forceinline__ float from_f<float>(float v) { return v; }
 template <> __device__ __forceinline__ __bf16 from_f<__bf16>(float v) { return (__bf16)v; }
 
-// x[m, :] = embed[token(m), :] (fp32 residual stream)
+// The RMS norm of a row held in registers by a 256-thread workgroup:
+// thread t holds elements 8t .. 8t+7 (xa, xb; zeros where t >= H/8 = nrun),
+// and writes them normalized (H/8 <= 256).  rmsnorm_kernel's arithmetic for
+// such a row; shared so that every caller gets the same bits.
+template <typename T>
+__device__ __forceinline__ void rms_row_held(f32x4 xa, f32x4 xb, const T* __restrict__ g, int H,
+                                             float eps, T* __restrict__ orow, float* red) {
+  const int t = threadIdx.x;
+  float ss = 0.f;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) ss = fmaf(xa[e], xa[e], ss);
+#pragma unroll
+  for (int e = 0; e < 4; ++e) ss = fmaf(xb[e], xb[e], ss);
+  for (int off = 32; off > 0; off >>= 1) ss += __shfl_xor(ss, off);
+  if ((t & 63) == 0) red[t >> 6] = ss;
+  __syncthreads();
+  const float tot = (red[0] + red[1]) + (red[2] + red[3]);
+  const float inv = 1.0f / sqrtf(tot / (float)H + eps);
+  if (t < H / 8) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+      orow[8 * t + e] = from_f<T>((e < 4 ? xa[e] : xb[e - 4]) * inv * to_f(g[8 * t + e]));
+  }
+}
+
+// x[m, :] = embed[token(m), :] (fp32 residual stream); with `h` set (bf16,
+// H <= 2048, 256 threads) also h[m, :] = the RMS norm of that row with gain
+// g0 (rms_row_held: the first layer's norm, bit for bit, without a launch)
 template <typename T>
 __global__ void embed_rows_kernel(const T* __restrict__ embed, int H, int vocab, int R, int n_causal,
                                   const int32_t* __restrict__ boundary,
                                   const int32_t* __restrict__ draft, int draft_width,
                                   const int32_t* __restrict__ block, int block_stride,
-                                  float* __restrict__ x) {
+                                  float* __restrict__ x, const T* __restrict__ g0 = nullptr,
+                                  float eps = 0.f, T* __restrict__ h = nullptr) {
   const int mrow = blockIdx.x;
   const int s = mrow / R, r = mrow - s * R;
   int tok = vocab;  // [M]
@@ -50,6 +78,21 @@ __global__ void embed_rows_kernel(const T* __restrict__ embed, int H, int vocab,
   const T* e = embed + (size_t)tok * H;
   float* xr = x + (size_t)mrow * H;
   if constexpr (sizeof(T) == 2) {
+    if (h) {
+      // one run of 8 per thread, kept in registers for the norm
+      __shared__ float red[4];
+      const int t = threadIdx.x;
+      f32x4 xa = f32x4{0.f, 0.f, 0.f, 0.f}, xb = xa;
+      if (t < H / 8) {
+        const bf16x8 v = *(const bf16x8*)(e + 8 * t);
+        xa = f32x4{(float)v[0], (float)v[1], (float)v[2], (float)v[3]};
+        xb = f32x4{(float)v[4], (float)v[5], (float)v[6], (float)v[7]};
+        *(f32x4*)(xr + 8 * t) = xa;
+        *(f32x4*)(xr + 8 * t + 4) = xb;
+      }
+      rms_row_held<T>(xa, xb, g0, H, eps, h + (size_t)mrow * H, red);
+      return;
+    }
     // runs of 8 (H is a multiple of 16): one 16-byte read, two 16-byte writes
     for (int c = threadIdx.x; c < H / 8; c += blockDim.x) {
       const bf16x8 v = *(const bf16x8*)(e + 8 * c);
@@ -151,27 +194,23 @@ __global__ void __launch_bounds__(256) rmsnorm_kernel(const float* __restrict__ 
   const float* xr = x + (size_t)mrow * H;
   T* orow = out + (size_t)mrow * H;
   const int nrun = H / 8;
-  float ss = 0.f;
-  const bool held = nrun <= 256;
-  const bool live = t < nrun;
-  f32x4 xa = f32x4{0.f, 0.f, 0.f, 0.f}, xb = xa;
-  if (held) {
-    if (live) {
+  if (nrun <= 256) {
+    // the row in one pass, loaded before the reduction
+    f32x4 xa = f32x4{0.f, 0.f, 0.f, 0.f}, xb = xa;
+    if (t < nrun) {
       xa = *(const f32x4*)(xr + 8 * t);
       xb = *(const f32x4*)(xr + 8 * t + 4);
     }
+    rms_row_held<T>(xa, xb, g, H, eps, orow, red);
+    return;
+  }
+  float ss = 0.f;
+  for (int c = t; c < nrun; c += 256) {
+    const f32x4 a = *(const f32x4*)(xr + 8 * c), b = *(const f32x4*)(xr + 8 * c + 4);
 #pragma unroll
-    for (int e = 0; e < 4; ++e) ss = fmaf(xa[e], xa[e], ss);
+    for (int e = 0; e < 4; ++e) ss = fmaf(a[e], a[e], ss);
 #pragma unroll
-    for (int e = 0; e < 4; ++e) ss = fmaf(xb[e], xb[e], ss);
-  } else {
-    for (int c = t; c < nrun; c += 256) {
-      const f32x4 a = *(const f32x4*)(xr + 8 * c), b = *(const f32x4*)(xr + 8 * c + 4);
-#pragma unroll
-      for (int e = 0; e < 4; ++e) ss = fmaf(a[e], a[e], ss);
-#pragma unroll
-      for (int e = 0; e < 4; ++e) ss = fmaf(b[e], b[e], ss);
-    }
+    for (int e = 0; e < 4; ++e) ss = fmaf(b[e], b[e], ss);
   }
   for (int off = 32; off > 0; off >>= 1) ss += __shfl_xor(ss, off);
   if ((t & 63) == 0) red[t >> 6] = ss;
@@ -179,11 +218,7 @@ __global__ void __launch_bounds__(256) rmsnorm_kernel(const float* __restrict__ 
   const float tot = (red[0] + red[1]) + (red[2] + red[3]);
   const float inv = 1.0f / sqrtf(tot / (float)H + eps);
   for (int c = t; c < nrun; c += 256) {
-    f32x4 a = xa, b = xb;
-    if (!held) {
-      a = *(const f32x4*)(xr + 8 * c);
-      b = *(const f32x4*)(xr + 8 * c + 4);
-    }
+    const f32x4 a = *(const f32x4*)(xr + 8 * c), b = *(const f32x4*)(xr + 8 * c + 4);
 #pragma unroll
     for (int e = 0; e < 8; ++e)
       orow[8 * c + e] = from_f<T>((e < 4 ? a[e] : b[e - 4]) * inv * to_f(g[8 * c + e]));
@@ -1740,9 +1775,10 @@ static int lm_head_top1(const dvs_model* m, const StepLayout& L, char* ws, const
 // The decoder stack on the rows in x (fp32, [M, hidden]); leaves the final
 // RMSNorm output in h.  The window is (n_causal, n_mask) rows per sequence.
 template <typename T>
+// first_norm_done: the embedding launch already wrote layer 0's norm to h
 static int forward_layers(const dvs_model* m, const dvs_state* st, int n_causal, int n_mask,
                           int chunk_keys, const StepLayout& L, char* ws, hipStream_t stream,
-                          int group = 0) {
+                          int group = 0, bool first_norm_done = false) {
   const int S = st->S, R = n_causal + n_mask, M = S * R;
   const int H = m->hidden, D = m->head_dim, Hq = m->n_heads, Hkv = m->n_kv_heads;
   const int dt = m->dtype;
@@ -1775,8 +1811,9 @@ static int forward_layers(const dvs_model* m, const dvs_state* st, int n_causal,
   }
   for (int l = 0; l < m->n_layers; ++l) {
     const dvs_layer& ly = m->layers[l];
-    hipLaunchKernelGGL(rmsnorm_kernel<T>, dim3(M), dim3(256), 0, stream, x, (const T*)ly.g_attn, H,
-                       m->rms_eps, h);
+    if (l > 0 || !first_norm_done)
+      hipLaunchKernelGGL(rmsnorm_kernel<T>, dim3(M), dim3(256), 0, stream, x, (const T*)ly.g_attn, H,
+                         m->rms_eps, h);
     if (use_ws(dt, M, H)) {
       // Q, K and V in one launch (the same splits as three separate calls)
       GemmArgs g{};
@@ -1848,12 +1885,18 @@ static int run_step(const dvs_model* m, const dvs_state* st, int n_causal, int n
   float* logits = logits_out ? logits_out : (float*)(ws + L.logits);
   int32_t* am = argmax_out ? argmax_out : (int32_t*)(ws + L.am);
   int32_t* acc = accept_out ? accept_out : (int32_t*)(ws + L.acc);
+  // bf16 rows of at most 2048: the embedding launch also writes layer 0's
+  // norm (rms_row_held, the same bits as the norm launch it replaces)
+  const bool embed_norm = m->dtype == DVS_BF16 && m->hidden <= 2048;
   hipLaunchKernelGGL(embed_rows_kernel<T>, dim3(M), dim3(256), 0, stream, (const T*)m->embed,
                      m->hidden, m->vocab, R, n_causal, st->boundary, st->draft, st->draft_width,
-                     nullptr, 0, (float*)(ws + L.x));
+                     nullptr, 0, (float*)(ws + L.x),
+                     embed_norm ? (const T*)m->layers[0].g_attn : nullptr, m->rms_eps,
+                     embed_norm ? (T*)(ws + L.h) : nullptr);
   int rc;
   if ((rc = launch_status("draft_verify_step(embed)"))) return rc;
-  if ((rc = forward_layers<T>(m, st, n_causal, n_mask, chunk_keys, L, ws, stream, group))) return rc;
+  if ((rc = forward_layers<T>(m, st, n_causal, n_mask, chunk_keys, L, ws, stream, group, embed_norm)))
+    return rc;
   if (!logits_out && use_ws(m->dtype, M, m->hidden)) {
     // top-1 in the LM head's epilogue: the logits never reach memory
     if ((rc = lm_head_top1(m, L, ws, ws + L.h, M, am, st->err_word, stream))) return rc;
